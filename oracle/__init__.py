@@ -1,0 +1,144 @@
+"""The CPU oracle for MiCRO's per-worker sparsify step -- TEST INFRASTRUCTURE ONLY.
+
+Only tests/, __graft_entry__.smoke() and bench.py's cpu_baseline leg may import
+this package.  It wraps oracle/libmicro_oracle.so (plain single-threaded C, see
+micro_oracle.h) through ctypes and works on host numpy arrays.  It shares no
+code with the GPU library.
+"""
+import ctypes
+import os
+
+import numpy as np
+
+from .build import LIB, build_oracle
+
+PROPORTIONAL = 0
+FIXED_STEP = 1
+
+
+class Rule(ctypes.Structure):
+    _fields_ = [("kind", ctypes.c_int32), ("beta", ctypes.c_double),
+                ("lo", ctypes.c_double), ("hi", ctypes.c_double),
+                ("alpha", ctypes.c_double)]
+
+
+_lib = None
+
+
+def lib():
+    """Loads the oracle library, building it first if it is absent."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB):
+            build_oracle()
+        L = ctypes.CDLL(LIB)
+        i64p = ctypes.POINTER(ctypes.c_int64)
+        L.micro_oracle_default_rule.argtypes = [ctypes.POINTER(Rule)]
+        L.micro_oracle_default_rule.restype = None
+        L.micro_oracle_partition.argtypes = [ctypes.c_int64, ctypes.c_int32,
+                                             ctypes.c_int32, i64p, i64p]
+        L.micro_oracle_partition.restype = ctypes.c_int
+        L.micro_oracle_select.argtypes = [ctypes.c_void_p, ctypes.c_void_p,
+                                          ctypes.c_int64, ctypes.c_int64,
+                                          ctypes.c_double, ctypes.c_void_p,
+                                          ctypes.c_void_p]
+        L.micro_oracle_select.restype = ctypes.c_int64
+        L.micro_oracle_estimate.argtypes = [ctypes.POINTER(Rule), ctypes.c_double,
+                                            ctypes.c_int64, ctypes.c_int64,
+                                            ctypes.c_double]
+        L.micro_oracle_estimate.restype = ctypes.c_double
+        L.micro_oracle_step.argtypes = [ctypes.c_void_p, ctypes.c_void_p,
+                                        ctypes.c_int64, ctypes.c_int32,
+                                        ctypes.c_int32, ctypes.c_double,
+                                        ctypes.POINTER(Rule),
+                                        ctypes.POINTER(ctypes.c_double),
+                                        ctypes.c_void_p, ctypes.c_void_p, i64p]
+        L.micro_oracle_step.restype = ctypes.c_int
+        _lib = L
+    return _lib
+
+
+def default_rule():
+    r = Rule()
+    lib().micro_oracle_default_rule(ctypes.byref(r))
+    return r
+
+
+def make_rule(kind=PROPORTIONAL, beta=None, lo=None, hi=None, alpha=None):
+    r = default_rule()
+    r.kind = kind
+    if beta is not None:
+        r.beta = beta
+    if lo is not None:
+        r.lo = lo
+    if hi is not None:
+        r.hi = hi
+    if alpha is not None:
+        r.alpha = alpha
+    return r
+
+
+def partition(n_total, rank, world):
+    """Sec. 4.1 partition bounds; returns (start, length)."""
+    s, n = ctypes.c_int64(), ctypes.c_int64()
+    rc = lib().micro_oracle_partition(n_total, rank, world, ctypes.byref(s),
+                                      ctypes.byref(n))
+    if rc != 0:
+        raise ValueError("invalid partition arguments")
+    return s.value, n.value
+
+
+def _f32(a, name):
+    if not (isinstance(a, np.ndarray) and a.dtype == np.float32
+            and a.flags.c_contiguous):
+        raise TypeError(f"{name} must be a C-contiguous float32 numpy array")
+    return a
+
+
+def select(grad, residual, start, length, theta):
+    """Sec. 4.2 selection over [start, start+length); residual is updated in
+    place.  Returns (idx int32[k], val float32[k])."""
+    _f32(grad, "grad")
+    _f32(residual, "residual")
+    if start < 0 or length < 0 or start + length > min(grad.size, residual.size):
+        raise ValueError("range outside the arrays")
+    out_idx = np.empty(max(length, 1), dtype=np.int32)
+    out_val = np.empty(max(length, 1), dtype=np.float32)
+    k = lib().micro_oracle_select(grad.ctypes.data, residual.ctypes.data, start,
+                                  length, float(theta), out_idx.ctypes.data,
+                                  out_val.ctypes.data)
+    return out_idx[:k].copy(), out_val[:k].copy()
+
+
+def estimate(density, part_len, k, theta, rule=None):
+    """Sec. 4.3 threshold update; returns the next threshold (a Python float)."""
+    r = rule if rule is not None else default_rule()
+    return lib().micro_oracle_estimate(ctypes.byref(r), float(density),
+                                       int(part_len), int(k), float(theta))
+
+
+def step(grad, residual, rank, world, density, theta, rule=None, out=None):
+    """One worker, one iteration.  residual (full length) is updated in place.
+    Returns (idx, val, k, theta_next); idx/val are views into `out` buffers
+    (allocated here when `out` is None) of length k."""
+    _f32(grad, "grad")
+    _f32(residual, "residual")
+    n_total = grad.size
+    if residual.size != n_total:
+        raise ValueError("grad and residual lengths differ")
+    _, length = partition(n_total, rank, world)
+    if out is None:
+        out = (np.empty(max(length, 1), np.int32), np.empty(max(length, 1), np.float32))
+    out_idx, out_val = out
+    if out_idx.size < length or out_val.size < length:
+        raise ValueError("output buffers smaller than the partition")
+    r = rule if rule is not None else default_rule()
+    th = ctypes.c_double(float(theta))
+    k = ctypes.c_int64()
+    rc = lib().micro_oracle_step(grad.ctypes.data, residual.ctypes.data, n_total,
+                                 rank, world, float(density), ctypes.byref(r),
+                                 ctypes.byref(th), out_idx.ctypes.data,
+                                 out_val.ctypes.data, ctypes.byref(k))
+    if rc != 0:
+        raise ValueError("invalid oracle step arguments")
+    return out_idx[:k.value], out_val[:k.value], k.value, th.value

@@ -1,0 +1,115 @@
+/*
+ * micro_oracle.c -- TEST INFRASTRUCTURE ONLY: the plain CPU oracle for
+ * MiCRO's per-worker sparsify step (arXiv 2310.00967).  See micro_oracle.h
+ * for what each function follows.  Deliberately a straight loop: no SIMD, no
+ * threads, no blocking, no reordering.  Compile with -O2 -ffp-contract=off,
+ * never with -ffast-math.
+ */
+#include "micro_oracle.h"
+
+#include <math.h>
+#include <stddef.h>
+
+void micro_oracle_default_rule(micro_oracle_rule *rule)
+{
+    rule->kind = MICRO_ORACLE_PROPORTIONAL;
+    rule->beta = 0.1;
+    rule->lo = 0.5;
+    rule->hi = 2.0;
+    rule->alpha = 0.05;
+}
+
+/* Sec. 4.1: the flattened gradient is divided into n equal contiguous ranges;
+ * when n does not divide N, the floor split makes the lengths differ by at
+ * most one and the ranges still tile [0, N) exactly. */
+int micro_oracle_partition(int64_t n_total, int32_t rank, int32_t world,
+                           int64_t *start, int64_t *len)
+{
+    if (world < 1 || rank < 0 || rank >= world || n_total < 0)
+        return -1;
+    int64_t s = ((int64_t)rank * n_total) / (int64_t)world;
+    int64_t e = ((int64_t)rank * n_total + n_total) / (int64_t)world;
+    *start = s;
+    *len = e - s;
+    return 0;
+}
+
+/* Sec. 4.2 and Algorithm 1: every element of the worker's own partition is
+ * inspected.  The error-feedback accumulation adds the new gradient to the
+ * local error (Sec. 2); an element whose accumulated magnitude reaches the
+ * threshold is selected, its accumulated value is what the worker contributes,
+ * and its local error restarts from zero; an unselected element keeps its
+ * accumulated value as the next local error. */
+int64_t micro_oracle_select(const float *grad, float *residual, int64_t start,
+                            int64_t len, double theta, int32_t *out_idx,
+                            float *out_val)
+{
+    int64_t k = 0;
+    for (int64_t j = start; j < start + len; ++j) {
+        float acc = grad[j] + residual[j];
+        double mag = (double)fabsf(acc);
+        if (mag >= theta) {
+            out_idx[k] = (int32_t)j;
+            out_val[k] = acc;
+            k = k + 1;
+            residual[j] = 0.0f;
+        } else {
+            residual[j] = acc;
+        }
+    }
+    return k;
+}
+
+/* Sec. 4.3: the threshold of the next iteration is derived from the target
+ * count k* and the count actually selected.  The paper states only that the
+ * update inspects whether the selected count exceeds the target and assigns an
+ * adjusted threshold; the proportional reading scales the threshold by one
+ * plus beta times the signed relative compression ratio error, clamped to
+ * [lo, hi]; the fixed-step reading moves it by a factor 1 +/- alpha. */
+double micro_oracle_estimate(const micro_oracle_rule *rule, double density,
+                             int64_t part_len, int64_t k, double theta)
+{
+    if (part_len == 0)
+        return theta;
+    double target = density * (double)part_len;
+    double selected = (double)k;
+    if (rule->kind == MICRO_ORACLE_FIXED_STEP) {
+        if (selected > target)
+            return theta * (1.0 + rule->alpha);
+        if (selected < target)
+            return theta * (1.0 - rule->alpha);
+        return theta;
+    }
+    double rel_err = (selected - target) / target;
+    double scale = rule->beta * rel_err;
+    scale = 1.0 + scale;
+    if (scale < rule->lo)
+        scale = rule->lo;
+    if (scale > rule->hi)
+        scale = rule->hi;
+    return theta * scale;
+}
+
+int micro_oracle_step(const float *grad, float *residual, int64_t n_total,
+                      int32_t rank, int32_t world, double density,
+                      const micro_oracle_rule *rule, double *theta,
+                      int32_t *out_idx, float *out_val, int64_t *k)
+{
+    int64_t start = 0, len = 0;
+    if (grad == NULL || residual == NULL || rule == NULL || theta == NULL ||
+        k == NULL)
+        return -1;
+    if (micro_oracle_partition(n_total, rank, world, &start, &len) != 0)
+        return -1;
+    if (!(density > 0.0 && density <= 1.0))
+        return -1;
+    if (!(*theta > 0.0) || isinf(*theta))
+        return -1;
+    if (len > 0 && (out_idx == NULL || out_val == NULL))
+        return -1;
+    int64_t selected = micro_oracle_select(grad, residual, start, len, *theta,
+                                           out_idx, out_val);
+    *theta = micro_oracle_estimate(rule, density, len, selected, *theta);
+    *k = selected;
+    return 0;
+}

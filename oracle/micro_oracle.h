@@ -1,0 +1,96 @@
+/*
+ * micro_oracle.h -- the CPU oracle for MiCRO's per-worker sparsify step.
+ *
+ * TEST INFRASTRUCTURE ONLY.  This is a plain, slow, single-threaded C
+ * implementation of what one worker computes in one iteration of MiCRO
+ * (Yoon & Oh, "MiCRO: Near-Zero Cost Gradient Sparsification for Scaling and
+ * Accelerating Distributed DNN Training", arXiv 2310.00967).  Only the tests,
+ * the smoke check and the benchmark's CPU-baseline leg may load it.  It shares
+ * no code, header or constant with the GPU library, and the GPU library never
+ * calls it.
+ *
+ * What each function follows:
+ *   micro_oracle_partition  Sec. 4.1 (coarse-grained partitioning): n equal
+ *                           contiguous ranges of the flattened gradient.
+ *   micro_oracle_select     Sec. 4.2 (exclusive gradient selection) and
+ *                           Algorithm 1 (error-feedback accumulation, selection
+ *                           in the worker's own partition, gathering the
+ *                           accumulated values, zeroing the selected entries
+ *                           and carrying the rest as the next local error),
+ *                           with error feedback as described in Sec. 2.
+ *   micro_oracle_estimate   Sec. 4.3 (compression ratio error minimisation by
+ *                           threshold scaling) and the Estimate step of
+ *                           Algorithm 1.  The paper gives no formula; the
+ *                           reading implemented here is a memoryless
+ *                           multiplicative scaling by the signed relative
+ *                           compression ratio error, clamped.  Its form is
+ *                           pinned by properties (direction, fixed point,
+ *                           clamps, convergence of the density); the constants
+ *                           beta, lo, hi and alpha are "parity unpinned"
+ *                           against the paper, which prints none.
+ *   micro_oracle_step       one worker, one iteration: the three above.
+ *
+ * Precision: the accumulation is one binary32 addition (round to nearest even,
+ * no fused multiply-add, subnormals kept); the threshold test compares the
+ * magnitude, widened to binary64, against the binary64 threshold with ">=";
+ * the threshold update is binary64 arithmetic.  Build with -ffp-contract=off
+ * and without -ffast-math.
+ */
+#ifndef MICRO_ORACLE_H
+#define MICRO_ORACLE_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* Threshold update rules of the oracle (Sec. 4.3 readings). */
+#define MICRO_ORACLE_PROPORTIONAL 0 /* theta * clamp(1 + beta*(k-k*)/k*, lo, hi) */
+#define MICRO_ORACLE_FIXED_STEP 1   /* theta * (1 +/- alpha) by the sign of k-k* */
+
+typedef struct micro_oracle_rule {
+    int32_t kind;
+    double beta;
+    double lo;
+    double hi;
+    double alpha;
+} micro_oracle_rule;
+
+/* Fills the default rule: proportional, beta 0.1, clamp [0.5, 2], alpha 0.05. */
+void micro_oracle_default_rule(micro_oracle_rule *rule);
+
+/* Sec. 4.1.  Partition `rank` of `world` over [0, n_total): start = floor(rank*N/n),
+ * end = floor((rank+1)*N/n).  Returns 0, or -1 for world < 1, rank outside
+ * [0, world) or n_total < 0. */
+int micro_oracle_partition(int64_t n_total, int32_t rank, int32_t world,
+                           int64_t *start, int64_t *len);
+
+/* Sec. 4.2 and Algorithm 1.  For j = start .. start+len-1 in increasing order:
+ * acc = grad[j] + residual[j]; if |acc| >= theta, append (j, acc) to the
+ * output lists and set residual[j] = +0; otherwise residual[j] = acc.
+ * Returns the number k of appended pairs.  out_idx and out_val must hold len
+ * entries.  Indices are global positions in the flattened vector. */
+int64_t micro_oracle_select(const float *grad, float *residual, int64_t start,
+                            int64_t len, double theta, int32_t *out_idx,
+                            float *out_val);
+
+/* Sec. 4.3.  Returns the next threshold from the target count
+ * k* = density * part_len, the selected count k and the current threshold.
+ * part_len == 0 returns theta unchanged. */
+double micro_oracle_estimate(const micro_oracle_rule *rule, double density,
+                             int64_t part_len, int64_t k, double theta);
+
+/* One worker, one iteration: partition, select, estimate.  theta is in/out;
+ * *k receives the selected count.  Returns 0, or -1 on invalid arguments
+ * (in which case nothing is written). */
+int micro_oracle_step(const float *grad, float *residual, int64_t n_total,
+                      int32_t rank, int32_t world, double density,
+                      const micro_oracle_rule *rule, double *theta,
+                      int32_t *out_idx, float *out_val, int64_t *k);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* MICRO_ORACLE_H */
