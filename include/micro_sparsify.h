@@ -1,0 +1,164 @@
+/*
+ * micro_sparsify.h -- C ABI of the MI355X (gfx950) implementation of MiCRO's
+ * per-worker gradient sparsification step (Yoon & Oh, arXiv 2310.00967).
+ *
+ * One call of micro_sparsify_step is one worker's share of one iteration of
+ * the paper's Algorithm 1, restricted to the worker's own partition:
+ *
+ *   Sec. 4.1  partition:  [s, e) = [floor(r*N/n), floor((r+1)*N/n))
+ *   Sec. 2    error feedback accumulation:  acc_j = grad_j + residual_j
+ *             (one binary32 addition, round to nearest even, no fused
+ *             multiply-add, subnormals kept)
+ *   Sec. 4.2  exclusive selection:  j is selected iff |acc_j| >= theta
+ *             (the binary32 magnitude compared with the binary64 threshold)
+ *   Alg. 1    the selected pairs (j, acc_j), in increasing j, go to
+ *             out_idx / out_val; residual_j becomes +0 where j is selected
+ *             and acc_j elsewhere in [s, e)
+ *   Sec. 4.3  threshold scaling:  theta <- Estimate(d * P, k, theta), in
+ *             binary64 on the host from the selected count k
+ *
+ * Every function is extern "C", takes plain pointers and sizes, and reports
+ * failure through micro_status; no C++ exception crosses the ABI.  Pointers
+ * documented as "device" are HIP device addresses on the device that was
+ * current when the context was created; "host" pointers are ordinary host
+ * memory.  The caller owns every buffer it passes.
+ */
+#ifndef MICRO_SPARSIFY_H
+#define MICRO_SPARSIFY_H
+
+#include <stdint.h>
+
+#if defined(__GNUC__)
+#define MICRO_API __attribute__((visibility("default")))
+#else
+#define MICRO_API
+#endif
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef struct micro_ctx micro_ctx; /* opaque, owned by the library */
+
+typedef enum micro_status {
+    MICRO_OK = 0,
+    MICRO_EINVAL = 1,    /* an argument is invalid; nothing was modified        */
+    MICRO_ECAPACITY = 2, /* a size exceeds what the context was created for     */
+    MICRO_ERANGE = 3,    /* n_total does not fit int32 global indices           */
+    MICRO_ENOMEM = 4,    /* a device or pinned host allocation failed           */
+    MICRO_EHIP = 5       /* a HIP runtime call failed (see micro_last_error)    */
+} micro_status;
+
+/* Threshold update rules (readings of Sec. 4.3, which gives no formula). */
+#define MICRO_RULE_PROPORTIONAL 0 /* theta * clamp(1 + beta*(k - k*)/k*, lo, hi) */
+#define MICRO_RULE_FIXED_STEP 1   /* theta * (1 + alpha) if k > k*,
+                                     theta * (1 - alpha) if k < k*, else theta   */
+
+/* Kernel variants. */
+#define MICRO_VARIANT_AUTO 0
+#define MICRO_VARIANT_SINGLE_PASS 1 /* one fused pass, decoupled look-back   */
+
+/* Flags. */
+#define MICRO_FLAG_TIME_KERNEL 1 /* record HIP events around each launch so
+                                    micro_sparsify_last_kernel_ms can report it */
+
+typedef struct micro_config {
+    int32_t rule;    /* MICRO_RULE_*                                  (default 0)    */
+    double beta;     /* proportional gain                             (default 0.1)  */
+    double lo, hi;   /* clamp of the proportional scale factor        (0.5, 2.0)     */
+    double alpha;    /* fixed-step size                               (default 0.05) */
+    int32_t variant; /* MICRO_VARIANT_*                               (default 0)    */
+    int32_t flags;   /* MICRO_FLAG_*                                  (default 0)    */
+} micro_config;
+
+/* Fills *cfg with the defaults listed above. */
+MICRO_API void micro_config_default(micro_config *cfg);
+
+/*
+ * Creates a context for flattened gradient vectors of n_total fp32 values on
+ * the current HIP device, enqueuing all work on `hip_stream` (a hipStream_t;
+ * NULL means the null stream).  cfg == NULL selects the defaults.
+ * The context owns a small device scratch area (one 64-bit status word per
+ * tile of the largest partition plus a tile ticket counter) and one pinned
+ * host word for the selected count; it never owns the caller's buffers.
+ * Returns MICRO_EINVAL (ctx NULL, n_total < 0, bad cfg), MICRO_ERANGE
+ * (n_total > INT32_MAX: indices are int32), MICRO_EHIP (no usable device) or
+ * MICRO_ENOMEM.  On failure *ctx is set to NULL.
+ */
+MICRO_API micro_status micro_sparsify_init(micro_ctx **ctx, int64_t n_total,
+                                 void *hip_stream, const micro_config *cfg);
+
+/*
+ * One worker's sparsify step on partition `rank` of `world` (the paper's
+ * cyclic partition number: the caller rotates it).
+ *   grad      device, n_total fp32, read only; only [s, e) is read.
+ *   residual  device, n_total fp32, in/out: the local error; only [s, e) is
+ *             read and written, everything outside is untouched.
+ *   rank, world  0 <= rank < world, world >= 1.
+ *   density   the user-set density d, 0 < d <= 1; the target count is d*P.
+ *   theta     host, in/out: the threshold of this step in, the threshold of
+ *             the next step out.  Must be finite and > 0.
+ *   out_idx   device int32, capacity >= P = e - s: the first k entries
+ *             receive the selected global indices, strictly increasing.
+ *   out_val   device fp32, capacity >= P: the first k entries receive acc
+ *             at those indices.
+ *   k         host out: the selected count.
+ * The buffers grad[s,e), residual[s,e), out_idx[0,P) and out_val[0,P) must
+ * not overlap.  grad and residual must be 4-byte aligned; the fastest path
+ * needs them to share the same 16-byte phase.
+ * The call is synchronous: it returns after the device work has finished and
+ * theta has been updated.  Empty partitions (P == 0) return MICRO_OK with
+ * k = 0 and theta unchanged.  Invalid arguments return MICRO_EINVAL before
+ * any device work, with nothing modified.  A HIP failure returns MICRO_EHIP;
+ * the outputs and the residual slice are then unspecified.
+ * One context must not be used from two threads at once.
+ */
+MICRO_API micro_status micro_sparsify_step(micro_ctx *ctx, const float *grad,
+                                 float *residual, int32_t rank, int32_t world,
+                                 double density, double *theta,
+                                 int32_t *out_idx, float *out_val, int64_t *k);
+
+/* Sec. 4.1 partition bounds (pure host arithmetic, no device needed):
+ * *start = floor(rank*n_total/world), *len = floor((rank+1)*n_total/world)
+ * - *start.  Returns MICRO_EINVAL for world < 1, rank outside [0, world),
+ * n_total < 0 or NULL outputs. */
+MICRO_API micro_status micro_partition(int64_t n_total, int32_t rank, int32_t world,
+                             int64_t *start, int64_t *len);
+
+/* Sec. 4.3 threshold update as the step applies it (pure host arithmetic):
+ * *theta <- Estimate(density * part_len, k, *theta) under cfg (NULL =
+ * defaults).  part_len == 0 leaves *theta unchanged.  Returns MICRO_EINVAL
+ * for NULL theta, part_len < 0, k outside [0, part_len] or density outside
+ * (0, 1]. */
+MICRO_API micro_status micro_estimate_threshold(const micro_config *cfg, double density,
+                                      int64_t part_len, int64_t k,
+                                      double *theta);
+
+/* The fp32 threshold the device compares with: the smallest binary32 value
+ * >= theta (+inf when theta exceeds FLT_MAX).  For every binary32 x,
+ * x >= *theta_f  <=>  (double)x >= theta, so the device's binary32 compare
+ * selects exactly what the binary64 definition selects.  Returns
+ * MICRO_EINVAL for NULL output or theta not finite and > 0. */
+MICRO_API micro_status micro_threshold_f32(double theta, float *theta_f);
+
+/* Device time of the last step's kernel launch(es) in milliseconds, from HIP
+ * events on the context's stream.  Needs MICRO_FLAG_TIME_KERNEL at init;
+ * returns MICRO_EINVAL otherwise or before the first timed step. */
+MICRO_API micro_status micro_sparsify_last_kernel_ms(const micro_ctx *ctx, float *ms);
+
+/* Message of the last failure on ctx (or of the last failed init when ctx is
+ * NULL); never NULL. */
+MICRO_API const char *micro_last_error(const micro_ctx *ctx);
+
+/* Static name of a status code. */
+MICRO_API const char *micro_status_string(micro_status status);
+
+/* Releases the context's scratch; NULL is a no-op.  Waits for the context's
+ * stream first. */
+MICRO_API void micro_sparsify_free(micro_ctx *ctx);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* MICRO_SPARSIFY_H */

@@ -1,0 +1,100 @@
+"""MiCRO's per-worker gradient sparsification step on MI355X (gfx950).
+
+    sp = Sparsifier(n_total)                       # on torch's current device/stream
+    k, theta, idx, val = sp.step(grad, residual, rank, world, density, theta)
+
+`grad` and `residual` are contiguous float32 device tensors of n_total values;
+`residual` is updated in place over the rank's partition only; `idx`/`val`
+are views of the first k entries of preallocated output tensors.  Every step
+runs in the HIP library behind include/micro_sparsify.h; PyTorch only
+provides device memory and the stream.
+"""
+from . import _lib
+from ._lib import (MICRO_FLAG_TIME_KERNEL, MICRO_RULE_FIXED_STEP, MICRO_RULE_PROPORTIONAL,
+                   MICRO_VARIANT_AUTO, MICRO_VARIANT_SINGLE_PASS, MicroError, default_config,
+                   micro_estimate_threshold, micro_partition, micro_threshold_f32)
+
+__all__ = ["Sparsifier", "MicroError", "default_config", "micro_partition",
+           "micro_estimate_threshold", "micro_threshold_f32", "MICRO_RULE_PROPORTIONAL",
+           "MICRO_RULE_FIXED_STEP", "MICRO_VARIANT_AUTO", "MICRO_VARIANT_SINGLE_PASS",
+           "MICRO_FLAG_TIME_KERNEL"]
+
+
+class Sparsifier:
+    """One context of the C library bound to a torch device and stream."""
+
+    def __init__(self, n_total, device=None, stream=None, rule=MICRO_RULE_PROPORTIONAL, beta=None,
+                 lo=None, hi=None, alpha=None, variant=MICRO_VARIANT_AUTO, time_kernel=False):
+        import torch
+        if not torch.cuda.is_available():
+            raise RuntimeError("Sparsifier needs a HIP device")
+        dev = torch.device(device) if device is not None else torch.device("cuda")
+        if dev.index is None:
+            dev = torch.device("cuda", torch.cuda.current_device())
+        self.device = dev
+        self.n_total = int(n_total)
+        cfg = default_config()
+        cfg.rule = rule
+        for name, v in (("beta", beta), ("lo", lo), ("hi", hi), ("alpha", alpha)):
+            if v is not None:
+                setattr(cfg, name, float(v))
+        cfg.variant = variant
+        cfg.flags = MICRO_FLAG_TIME_KERNEL if time_kernel else 0
+        self.config = cfg
+        with torch.cuda.device(self.device):
+            self.stream = stream if stream is not None else torch.cuda.current_stream(self.device)
+            self._ctx = _lib.micro_sparsify_init(self.n_total, self.stream.cuda_stream, cfg)
+        self._out_idx = None
+        self._out_val = None
+
+    def close(self):
+        if getattr(self, "_ctx", None) is not None:
+            _lib.micro_sparsify_free(self._ctx)
+            self._ctx = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+    def partition(self, rank, world):
+        return micro_partition(self.n_total, rank, world)
+
+    def outputs(self, capacity):
+        """Preallocated (out_idx int32, out_val float32) of at least `capacity`."""
+        import torch
+        if self._out_idx is None or self._out_idx.numel() < capacity:
+            n = max(1, int(capacity))
+            self._out_idx = torch.empty(n, dtype=torch.int32, device=self.device)
+            self._out_val = torch.empty(n, dtype=torch.float32, device=self.device)
+        return self._out_idx, self._out_val
+
+    def _check(self, t, name, dtype):
+        import torch
+        if not isinstance(t, torch.Tensor) or t.device != self.device or t.dtype != dtype \
+                or not t.is_contiguous():
+            raise TypeError(f"{name} must be a contiguous {dtype} tensor on {self.device}")
+
+    def step(self, grad, residual, rank, world, density, theta, out_idx=None, out_val=None):
+        """One sparsify step; returns (k, theta_next, idx[:k], val[:k])."""
+        import torch
+        if self._ctx is None:
+            raise RuntimeError("Sparsifier is closed")
+        self._check(grad, "grad", torch.float32)
+        self._check(residual, "residual", torch.float32)
+        if grad.numel() != self.n_total or residual.numel() != self.n_total:
+            raise ValueError(f"grad and residual must hold {self.n_total} values")
+        _, length = self.partition(rank, world)
+        if out_idx is None or out_val is None:
+            out_idx, out_val = self.outputs(length)
+        self._check(out_idx, "out_idx", torch.int32)
+        self._check(out_val, "out_val", torch.float32)
+        if out_idx.numel() < length or out_val.numel() < length:
+            raise ValueError(f"output capacity below the partition length {length}")
+        k, th = _lib.micro_sparsify_step(self._ctx, grad.data_ptr(), residual.data_ptr(), rank, world,
+                                         density, theta, out_idx.data_ptr(), out_val.data_ptr())
+        return k, th, out_idx[:k], out_val[:k]
+
+    def last_kernel_ms(self):
+        return _lib.micro_sparsify_last_kernel_ms(self._ctx)

@@ -1,0 +1,364 @@
+// Host side of the C ABI declared in include/micro_sparsify.h: argument
+// validation, the Sec. 4.1 partition, the binary32 form of the threshold,
+// kernel launch, the selected-count readback and the Sec. 4.3 threshold
+// update in binary64.  Compiled with -ffp-contract=off.
+#include "micro_sparsify.h"
+
+#include <hip/hip_runtime.h>
+
+#include <cmath>
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+#include <limits>
+#include <new>
+#include <string>
+
+#include "sparsify_kernel.h"
+
+struct micro_ctx {
+    int device = -1;
+    int64_t n_total = 0;
+    hipStream_t stream = nullptr;
+    micro_config cfg{};
+    uint64_t* d_status = nullptr;            // tile status words
+    int64_t status_words = 0;
+    unsigned long long* d_ticket = nullptr;  // tile ticket counter
+    int64_t* d_count = nullptr;              // selected count of the last launch
+    int64_t* h_count = nullptr;              // pinned host copy
+    uint32_t epoch = 0;                      // epoch of the last launch
+    bool needs_reset = false;                // scratch state unknown after a failure
+    hipEvent_t ev_start = nullptr, ev_stop = nullptr;
+    bool have_timing = false;
+    std::string last_error;
+};
+
+namespace {
+
+thread_local std::string g_init_error = "no error";
+
+void set_error(micro_ctx* ctx, const char* fmt, ...) {
+    char buf[512];
+    va_list ap;
+    va_start(ap, fmt);
+    std::vsnprintf(buf, sizeof buf, fmt, ap);
+    va_end(ap);
+    if (ctx)
+        ctx->last_error = buf;
+    else
+        g_init_error = buf;
+}
+
+micro_status hip_fail(micro_ctx* ctx, hipError_t err, const char* what) {
+    set_error(ctx, "%s failed: %s", what, hipGetErrorString(err));
+    if (ctx) ctx->needs_reset = true;
+    return MICRO_EHIP;
+}
+
+bool config_valid(const micro_config& c) {
+    if (c.rule != MICRO_RULE_PROPORTIONAL && c.rule != MICRO_RULE_FIXED_STEP) return false;
+    if (!std::isfinite(c.beta) || c.beta < 0.0) return false;
+    if (!std::isfinite(c.lo) || !std::isfinite(c.hi) || !(c.lo > 0.0) || !(c.hi >= c.lo)) return false;
+    if (!std::isfinite(c.alpha) || c.alpha < 0.0 || !(c.alpha < 1.0)) return false;
+    if (c.variant != MICRO_VARIANT_AUTO && c.variant != MICRO_VARIANT_SINGLE_PASS) return false;
+    if ((c.flags & ~MICRO_FLAG_TIME_KERNEL) != 0) return false;
+    return true;
+}
+
+bool density_valid(double d) { return d > 0.0 && d <= 1.0; }
+
+bool theta_valid(double t) { return std::isfinite(t) && t > 0.0; }
+
+// Sec. 4.3 threshold scaling (the reading of the paper's Estimate): the
+// target count is d * P; the proportional rule multiplies the threshold by
+// 1 + beta * (k - target) / target clamped to [lo, hi]; the fixed-step rule
+// by 1 + alpha or 1 - alpha according to the sign of k - target.  Each
+// operation is one IEEE binary64 rounding, in this order.
+double next_threshold(const micro_config& c, double density, int64_t part_len, int64_t k,
+                      double theta) {
+    if (part_len == 0) return theta;
+    const double target = density * static_cast<double>(part_len);
+    const double got = static_cast<double>(k);
+    if (c.rule == MICRO_RULE_FIXED_STEP) {
+        if (got > target) return theta * (1.0 + c.alpha);
+        if (got < target) return theta * (1.0 - c.alpha);
+        return theta;
+    }
+    const double relative_error = (got - target) / target;
+    const double gain = c.beta * relative_error;
+    double factor = 1.0 + gain;
+    if (factor < c.lo) factor = c.lo;
+    if (factor > c.hi) factor = c.hi;
+    return theta * factor;
+}
+
+float threshold_as_f32(double theta) {
+    float f = static_cast<float>(theta);  // round to nearest
+    if (static_cast<double>(f) < theta) f = std::nextafter(f, std::numeric_limits<float>::infinity());
+    return f;
+}
+
+bool ranges_overlap(const void* a, size_t an, const void* b, size_t bn) {
+    const uintptr_t a0 = reinterpret_cast<uintptr_t>(a), b0 = reinterpret_cast<uintptr_t>(b);
+    return a0 < b0 + bn && b0 < a0 + an;
+}
+
+micro_status reset_scratch(micro_ctx* ctx) {
+    hipError_t e = hipMemsetAsync(ctx->d_status, 0, sizeof(uint64_t) * ctx->status_words, ctx->stream);
+    if (e == hipSuccess) e = hipMemsetAsync(ctx->d_ticket, 0, sizeof(unsigned long long), ctx->stream);
+    if (e == hipSuccess) e = hipStreamSynchronize(ctx->stream);
+    if (e != hipSuccess) return hip_fail(ctx, e, "scratch reset");
+    ctx->epoch = 0;
+    ctx->needs_reset = false;
+    return MICRO_OK;
+}
+
+void release(micro_ctx* ctx) {
+    if (!ctx) return;
+    if (ctx->stream || ctx->d_status) (void)hipStreamSynchronize(ctx->stream);
+    if (ctx->ev_start) (void)hipEventDestroy(ctx->ev_start);
+    if (ctx->ev_stop) (void)hipEventDestroy(ctx->ev_stop);
+    if (ctx->d_status) (void)hipFree(ctx->d_status);
+    if (ctx->d_ticket) (void)hipFree(ctx->d_ticket);
+    if (ctx->d_count) (void)hipFree(ctx->d_count);
+    if (ctx->h_count) (void)hipHostFree(ctx->h_count);
+    delete ctx;
+}
+
+}  // namespace
+
+extern "C" {
+
+void micro_config_default(micro_config* cfg) {
+    if (!cfg) return;
+    cfg->rule = MICRO_RULE_PROPORTIONAL;
+    cfg->beta = 0.1;
+    cfg->lo = 0.5;
+    cfg->hi = 2.0;
+    cfg->alpha = 0.05;
+    cfg->variant = MICRO_VARIANT_AUTO;
+    cfg->flags = 0;
+}
+
+micro_status micro_partition(int64_t n_total, int32_t rank, int32_t world, int64_t* start,
+                             int64_t* len) {
+    if (!start || !len || world < 1 || rank < 0 || rank >= world || n_total < 0)
+        return MICRO_EINVAL;
+    // Sec. 4.1: equal contiguous ranges; the floor split keeps lengths within
+    // one of each other when world does not divide n_total.  rank * n_total
+    // stays below 2^62 for n_total < 2^31.
+    const int64_t s = (static_cast<int64_t>(rank) * n_total) / world;
+    const int64_t e = (static_cast<int64_t>(rank + 1) * n_total) / world;
+    *start = s;
+    *len = e - s;
+    return MICRO_OK;
+}
+
+micro_status micro_estimate_threshold(const micro_config* cfg, double density, int64_t part_len,
+                                      int64_t k, double* theta) {
+    micro_config c;
+    micro_config_default(&c);
+    if (cfg) c = *cfg;
+    if (!theta || !config_valid(c) || !density_valid(density) || part_len < 0 || k < 0 ||
+        k > part_len)
+        return MICRO_EINVAL;
+    *theta = next_threshold(c, density, part_len, k, *theta);
+    return MICRO_OK;
+}
+
+micro_status micro_threshold_f32(double theta, float* theta_f) {
+    if (!theta_f || !theta_valid(theta)) return MICRO_EINVAL;
+    *theta_f = threshold_as_f32(theta);
+    return MICRO_OK;
+}
+
+micro_status micro_sparsify_init(micro_ctx** out, int64_t n_total, void* hip_stream,
+                                 const micro_config* cfg) {
+    if (!out) {
+        set_error(nullptr, "ctx output pointer is NULL");
+        return MICRO_EINVAL;
+    }
+    *out = nullptr;
+    micro_config c;
+    micro_config_default(&c);
+    if (cfg) c = *cfg;
+    if (n_total < 0 || !config_valid(c)) {
+        set_error(nullptr, "invalid n_total or configuration");
+        return MICRO_EINVAL;
+    }
+    if (n_total > std::numeric_limits<int32_t>::max()) {
+        set_error(nullptr, "n_total %lld exceeds the int32 index range",
+                  static_cast<long long>(n_total));
+        return MICRO_ERANGE;
+    }
+    int count = 0;
+    hipError_t e = hipGetDeviceCount(&count);
+    if (e != hipSuccess || count < 1) {
+        set_error(nullptr, "no HIP device available (%s)",
+                  e == hipSuccess ? "device count is 0" : hipGetErrorString(e));
+        return MICRO_EHIP;
+    }
+    micro_ctx* ctx = new (std::nothrow) micro_ctx;
+    if (!ctx) {
+        set_error(nullptr, "out of host memory");
+        return MICRO_ENOMEM;
+    }
+    ctx->n_total = n_total;
+    ctx->stream = static_cast<hipStream_t>(hip_stream);
+    ctx->cfg = c;
+    if ((e = hipGetDevice(&ctx->device)) != hipSuccess) {
+        set_error(nullptr, "hipGetDevice failed: %s", hipGetErrorString(e));
+        release(ctx);
+        return MICRO_EHIP;
+    }
+    // One status word per tile of the largest possible partition (the whole
+    // vector), plus one tile for the alignment of the first tile.
+    ctx->status_words = n_total / micro::kTileElems + 2;
+    if (hipMalloc(&ctx->d_status, sizeof(uint64_t) * ctx->status_words) != hipSuccess ||
+        hipMalloc(&ctx->d_ticket, sizeof(unsigned long long)) != hipSuccess ||
+        hipMalloc(&ctx->d_count, sizeof(int64_t)) != hipSuccess ||
+        hipHostMalloc(&ctx->h_count, sizeof(int64_t), hipHostMallocDefault) != hipSuccess) {
+        set_error(nullptr, "device or pinned host allocation failed");
+        release(ctx);
+        return MICRO_ENOMEM;
+    }
+    if (c.flags & MICRO_FLAG_TIME_KERNEL) {
+        if ((e = hipEventCreate(&ctx->ev_start)) != hipSuccess ||
+            (e = hipEventCreate(&ctx->ev_stop)) != hipSuccess) {
+            set_error(nullptr, "hipEventCreate failed: %s", hipGetErrorString(e));
+            release(ctx);
+            return MICRO_EHIP;
+        }
+    }
+    if (reset_scratch(ctx) != MICRO_OK) {
+        set_error(nullptr, "%s", ctx->last_error.c_str());
+        release(ctx);
+        return MICRO_EHIP;
+    }
+    *out = ctx;
+    return MICRO_OK;
+}
+
+micro_status micro_sparsify_step(micro_ctx* ctx, const float* grad, float* residual, int32_t rank,
+                                 int32_t world, double density, double* theta, int32_t* out_idx,
+                                 float* out_val, int64_t* k) {
+    if (!ctx) {
+        set_error(nullptr, "ctx is NULL");
+        return MICRO_EINVAL;
+    }
+    if (!grad || !residual || !theta || !out_idx || !out_val || !k) {
+        set_error(ctx, "NULL pointer argument");
+        return MICRO_EINVAL;
+    }
+    int64_t start = 0, len = 0;
+    if (micro_partition(ctx->n_total, rank, world, &start, &len) != MICRO_OK) {
+        set_error(ctx, "invalid rank %d / world %d", rank, world);
+        return MICRO_EINVAL;
+    }
+    if (!density_valid(density)) {
+        set_error(ctx, "density %g outside (0, 1]", density);
+        return MICRO_EINVAL;
+    }
+    if (!theta_valid(*theta)) {
+        set_error(ctx, "threshold %g is not finite and positive", *theta);
+        return MICRO_EINVAL;
+    }
+    const uintptr_t misaligned = (reinterpret_cast<uintptr_t>(grad) | reinterpret_cast<uintptr_t>(residual) |
+                                  reinterpret_cast<uintptr_t>(out_idx) | reinterpret_cast<uintptr_t>(out_val)) & 3u;
+    if (misaligned) {
+        set_error(ctx, "buffers must be 4-byte aligned");
+        return MICRO_EINVAL;
+    }
+    const size_t pb = static_cast<size_t>(len) * sizeof(float);
+    const void* regions[4] = {grad + start, residual + start, out_idx, out_val};
+    for (int i = 0; i < 4; ++i)
+        for (int j = i + 1; j < 4; ++j)
+            if (len > 0 && ranges_overlap(regions[i], pb, regions[j], pb)) {
+                set_error(ctx, "grad, residual and output ranges overlap");
+                return MICRO_EINVAL;
+            }
+    if (len == 0) {  // empty partition: nothing selected, threshold unchanged
+        *k = 0;
+        return MICRO_OK;
+    }
+    if (ctx->needs_reset) {
+        micro_status s = reset_scratch(ctx);
+        if (s != MICRO_OK) return s;
+    }
+    if (ctx->epoch >= micro::kMaxEpoch) {  // epoch field would wrap: clear the status words
+        micro_status s = reset_scratch(ctx);
+        if (s != MICRO_OK) return s;
+    }
+    const bool vec4 = ((reinterpret_cast<uintptr_t>(grad) ^ reinterpret_cast<uintptr_t>(residual)) & 15u) == 0;
+    micro::LaunchArgs a{};
+    a.grad = grad;
+    a.residual = residual;
+    a.out_idx = out_idx;
+    a.out_val = out_val;
+    a.start = start;
+    a.end = start + len;
+    a.base = micro::tile_base_for(grad, start, vec4);
+    a.theta_f = threshold_as_f32(*theta);
+    a.status = ctx->d_status;
+    a.ticket = ctx->d_ticket;
+    a.epoch = ctx->epoch + 1;
+    const int64_t tiles = (a.end - a.base + micro::kTileElems - 1) / micro::kTileElems;
+    if (tiles > ctx->status_words) {
+        set_error(ctx, "partition needs %lld tiles, scratch holds %lld", static_cast<long long>(tiles),
+                  static_cast<long long>(ctx->status_words));
+        return MICRO_ECAPACITY;
+    }
+    a.num_tiles = static_cast<uint32_t>(tiles);
+    a.count_out = ctx->d_count;
+
+    hipError_t e;
+    const bool timed = (ctx->cfg.flags & MICRO_FLAG_TIME_KERNEL) != 0;
+    if (timed && (e = hipEventRecord(ctx->ev_start, ctx->stream)) != hipSuccess)
+        return hip_fail(ctx, e, "hipEventRecord");
+    ctx->epoch = a.epoch;
+    if ((e = micro::launch_sparsify(a, vec4, ctx->stream)) != hipSuccess)
+        return hip_fail(ctx, e, "sparsify kernel launch");
+    if (timed && (e = hipEventRecord(ctx->ev_stop, ctx->stream)) != hipSuccess)
+        return hip_fail(ctx, e, "hipEventRecord");
+    if ((e = hipMemcpyAsync(ctx->h_count, ctx->d_count, sizeof(int64_t), hipMemcpyDeviceToHost,
+                            ctx->stream)) != hipSuccess)
+        return hip_fail(ctx, e, "count readback");
+    if ((e = hipStreamSynchronize(ctx->stream)) != hipSuccess)
+        return hip_fail(ctx, e, "hipStreamSynchronize");
+    const int64_t selected = *ctx->h_count;
+    if (selected < 0 || selected > len) {
+        set_error(ctx, "device reported %lld selected of %lld", static_cast<long long>(selected),
+                  static_cast<long long>(len));
+        ctx->needs_reset = true;
+        return MICRO_EHIP;
+    }
+    ctx->have_timing = timed;
+    *k = selected;
+    *theta = next_threshold(ctx->cfg, density, len, selected, *theta);
+    return MICRO_OK;
+}
+
+micro_status micro_sparsify_last_kernel_ms(const micro_ctx* ctx, float* ms) {
+    if (!ctx || !ms || !ctx->have_timing) return MICRO_EINVAL;
+    return hipEventElapsedTime(ms, ctx->ev_start, ctx->ev_stop) == hipSuccess ? MICRO_OK : MICRO_EHIP;
+}
+
+const char* micro_last_error(const micro_ctx* ctx) {
+    return ctx ? ctx->last_error.c_str() : g_init_error.c_str();
+}
+
+const char* micro_status_string(micro_status s) {
+    switch (s) {
+        case MICRO_OK: return "MICRO_OK";
+        case MICRO_EINVAL: return "MICRO_EINVAL";
+        case MICRO_ECAPACITY: return "MICRO_ECAPACITY";
+        case MICRO_ERANGE: return "MICRO_ERANGE";
+        case MICRO_ENOMEM: return "MICRO_ENOMEM";
+        case MICRO_EHIP: return "MICRO_EHIP";
+    }
+    return "MICRO_UNKNOWN";
+}
+
+void micro_sparsify_free(micro_ctx* ctx) { release(ctx); }
+
+}  // extern "C"

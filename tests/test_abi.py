@@ -1,0 +1,196 @@
+"""The C ABI: exported symbols, host-only helpers and argument validation.
+
+CPU tests load the library and call only what needs no device; the GPU tests
+at the end check that invalid arguments are refused before any device work.
+"""
+import ctypes
+import math
+import os
+import re
+
+import numpy as np
+import pytest
+
+import oracle
+from paper_2310_00967_amd import _lib
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "micro_sparsify.h")
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    return sorted(set(re.findall(r"MICRO_API\s+[\w\s\*]*?\b(micro_\w+)\s*\(", text)))
+
+
+def test_header_declares_the_boundary():
+    names = declared_functions()
+    for required in ["micro_sparsify_init", "micro_sparsify_step", "micro_sparsify_free",
+                     "micro_partition", "micro_last_error"]:
+        assert required in names
+    assert set(names) == set(_lib.SIGNATURES)
+
+
+def test_library_exports_every_declared_symbol():
+    lib = _lib.load()
+    for name in declared_functions():
+        assert hasattr(lib, name), name
+
+
+def test_library_exports_nothing_else():
+    import subprocess
+    out = subprocess.run(["nm", "-D", "--defined-only", _lib.LIB_PATH], capture_output=True,
+                         text=True, check=True).stdout
+    exported = {ln.split()[-1] for ln in out.splitlines() if " T " in ln}
+    micro_syms = {s for s in exported if s.startswith("micro_")}
+    assert micro_syms == set(declared_functions())
+
+
+def test_partition_matches_oracle():
+    rng = np.random.default_rng(0)
+    cases = [(0, 0, 1), (7, 3, 16), (11_689_512, 15, 16), (335_141_888, 3, 8), (2**31 - 1, 6, 7)]
+    for _ in range(300):
+        w = int(rng.integers(1, 70))
+        cases.append((int(rng.integers(0, 2**31)), int(rng.integers(0, w)), w))
+    for n, r, w in cases:
+        assert _lib.micro_partition(n, r, w) == oracle.partition(n, r, w)
+
+
+def test_partition_rejects_bad_arguments():
+    for args in [(10, -1, 4), (10, 4, 4), (10, 0, 0), (-1, 0, 1)]:
+        with pytest.raises(_lib.MicroError) as e:
+            _lib.micro_partition(*args)
+        assert e.value.status == _lib.MICRO_EINVAL
+
+
+@pytest.mark.parametrize("kind", [0, 1])
+def test_threshold_update_matches_oracle(kind):
+    """The library's own binary64 update equals the oracle's independently
+    written one bit for bit."""
+    rng = np.random.default_rng(kind + 1)
+    cfg = _lib.default_config()
+    cfg.rule = kind
+    rule = oracle.make_rule(kind)
+    for _ in range(20000):
+        P = int(rng.integers(0, 2**31))
+        k = int(rng.integers(0, P + 1)) if P else 0
+        d = float(rng.choice([1e-3, 1e-2, 0.1, 1.0, float(rng.uniform(1e-6, 1))]))
+        th = float(np.exp(rng.uniform(-40, 20)))
+        assert _lib.micro_estimate_threshold(d, P, k, th, cfg) == oracle.estimate(d, P, k, th, rule)
+
+
+def test_threshold_update_rejects_bad_arguments():
+    for args in [(0.0, 10, 1, 1.0), (1.5, 10, 1, 1.0), (float("nan"), 10, 1, 1.0),
+                 (0.1, -1, 0, 1.0), (0.1, 10, 11, 1.0), (0.1, 10, -1, 1.0)]:
+        with pytest.raises(_lib.MicroError):
+            _lib.micro_estimate_threshold(*args)
+
+
+def test_threshold_f32_is_the_smallest_float_not_below_theta():
+    rng = np.random.default_rng(4)
+    thetas = [2.33, 1.0, 0.1, 1e-45, 1e-40, 3.4028234663852886e38, 3.5e38, 1e300,
+              float(np.float32(2.33)), np.nextafter(float(np.float32(2.33)), 0.0)]
+    thetas += list(np.exp(rng.uniform(-100, 88, 20000)))
+    for th in thetas:
+        f = np.float32(_lib.micro_threshold_f32(float(th)))
+        if math.isinf(f):
+            assert th > float(np.finfo(np.float32).max)
+            continue
+        assert float(f) >= th
+        below = np.nextafter(f, np.float32(0))
+        assert float(below) < th
+
+
+def test_threshold_f32_compare_equals_double_compare():
+    """x >= theta_f over binary32 selects exactly x >= theta over binary64."""
+    rng = np.random.default_rng(8)
+    xs = np.abs(rng.standard_normal(200000).astype(np.float32))
+    for th in [float(xs[3]), float(np.nextafter(float(xs[3]), 10.0)), 0.37, 1.2345678901234]:
+        f = np.float32(_lib.micro_threshold_f32(th))
+        assert np.array_equal(xs >= f, xs.astype(np.float64) >= th)
+
+
+def test_threshold_f32_rejects_bad_values():
+    for th in [0.0, -1.0, float("inf"), float("nan")]:
+        with pytest.raises(_lib.MicroError):
+            _lib.micro_threshold_f32(th)
+
+
+def test_status_strings():
+    assert _lib.status_string(_lib.MICRO_EINVAL) == "MICRO_EINVAL"
+    assert _lib.status_string(99) == "MICRO_UNKNOWN"
+
+
+def test_init_argument_errors_without_device_work():
+    lib = _lib.load()
+    ctx = ctypes.c_void_p(1)
+    assert lib.micro_sparsify_init(None, 10, None, None) == _lib.MICRO_EINVAL
+    assert lib.micro_sparsify_init(ctypes.byref(ctx), -1, None, None) == _lib.MICRO_EINVAL
+    assert ctx.value is None
+    assert lib.micro_sparsify_init(ctypes.byref(ctx), 2**31, None, None) == _lib.MICRO_ERANGE
+    assert "int32" in _lib.last_error()
+    bad = _lib.default_config()
+    bad.lo = 3.0  # lo > hi
+    assert lib.micro_sparsify_init(ctypes.byref(ctx), 10, None, ctypes.byref(bad)) == _lib.MICRO_EINVAL
+    bad = _lib.default_config()
+    bad.rule = 7
+    assert lib.micro_sparsify_init(ctypes.byref(ctx), 10, None, ctypes.byref(bad)) == _lib.MICRO_EINVAL
+
+
+def test_step_with_null_context_is_rejected():
+    lib = _lib.load()
+    th = ctypes.c_double(1.0)
+    k = ctypes.c_int64(-7)
+    st = lib.micro_sparsify_step(None, None, None, 0, 1, 0.1, ctypes.byref(th), None, None, ctypes.byref(k))
+    assert st == _lib.MICRO_EINVAL
+    assert th.value == 1.0 and k.value == -7
+
+
+def test_init_without_device_reports_hip_error():
+    import torch
+    if torch.cuda.is_available():
+        pytest.skip("a device is present")
+    lib = _lib.load()
+    ctx = ctypes.c_void_p()
+    assert lib.micro_sparsify_init(ctypes.byref(ctx), 100, None, None) == _lib.MICRO_EHIP
+    assert ctx.value is None
+    assert "device" in _lib.last_error()
+
+
+@pytest.mark.gpu
+def test_step_validation_on_device():
+    import torch
+    import paper_2310_00967_amd as micro
+    N = 1000
+    sp = micro.Sparsifier(N, device="cuda")
+    lib = _lib.load()
+    g = torch.randn(N, device="cuda")
+    r = torch.randn(N, device="cuda")
+    r0 = r.clone()
+    oi = torch.full((N,), -1, dtype=torch.int32, device="cuda")
+    ov = torch.full((N,), -1.0, device="cuda")
+
+    def call(grad=g.data_ptr(), res=r.data_ptr(), rank=0, world=1, d=0.1, theta=1.0,
+             idx=oi.data_ptr(), val=ov.data_ptr()):
+        th = ctypes.c_double(theta)
+        k = ctypes.c_int64(-7)
+        st = lib.micro_sparsify_step(sp._ctx, ctypes.c_void_p(grad), ctypes.c_void_p(res), rank, world,
+                                     d, ctypes.byref(th), ctypes.c_void_p(idx), ctypes.c_void_p(val),
+                                     ctypes.byref(k))
+        return st, th.value, k.value
+
+    bad = [dict(grad=0), dict(res=0), dict(idx=0), dict(val=0), dict(rank=-1), dict(rank=1),
+           dict(world=0), dict(d=0.0), dict(d=2.0), dict(d=float("nan")), dict(theta=0.0),
+           dict(theta=-1.0), dict(theta=float("inf")), dict(theta=float("nan")),
+           dict(res=g.data_ptr()), dict(idx=r.data_ptr()), dict(val=oi.data_ptr()),
+           dict(grad=g.data_ptr() + 2)]
+    for kw in bad:
+        st, th, k = call(**kw)
+        assert st == _lib.MICRO_EINVAL, kw
+        assert k == -7 and (th == kw.get("theta", 1.0) or math.isnan(th))
+    torch.cuda.synchronize()
+    assert torch.equal(r, r0)
+    assert bool((oi == -1).all()) and bool((ov == -1.0).all())
+    st, th, k = call()
+    assert st == _lib.MICRO_OK and k >= 0
+    sp.close()

@@ -1,0 +1,227 @@
+"""Bit-exact parity of the HIP path with the CPU oracle (GPU).
+
+Every call goes through the C ABI (include/micro_sparsify.h) via the ctypes
+binding.  Indices, values, the selected count, the next threshold and the
+residual must equal the oracle's bit for bit; the tolerance is zero.
+"""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import paper_2310_00967_amd as micro
+from paper_2310_00967_amd import synth
+
+from gpu_harness import ParityRun, first_mismatch, note
+
+pytestmark = pytest.mark.gpu
+
+DEV = "cuda"
+
+
+@pytest.mark.parametrize("name,density,steps", [
+    ("toy", 0.01, 20),
+    ("resnet18", 0.01, 100),
+    ("resnet50", 0.001, 100),
+    ("bert_large", 0.01, 50),
+])
+def test_workload_parity(name, density, steps):
+    note(f"parity {name} d={density} steps={steps}")
+    run = ParityRun(synth.get(name), density, DEV)
+    try:
+        run.run(steps)
+    finally:
+        run.close()
+
+
+@pytest.mark.parametrize("density", [0.001, 0.01])
+def test_gpt_parity(density):
+    """The 1.3B-value GPT gradient as one partition (world 1), 20 steps."""
+    note(f"parity gpt_1p3b d={density}")
+    run = ParityRun(synth.get("gpt_1p3b"), density, DEV)
+    try:
+        run.run(20)
+    finally:
+        run.close()
+
+
+# ---------------------------------------------------------------------------
+# edge cases and ragged sizes (small inputs, oracle finishes instantly)
+# ---------------------------------------------------------------------------
+
+def gpu_vs_oracle(g, res, rank, world, density, theta, phase_shift=0, sp=None):
+    """One call on both sides; g/res are host float32 arrays.  phase_shift != 0
+    places grad at a different 16-byte phase than residual (scalar-load kernel)."""
+    N = g.size
+    sp = sp or micro.Sparsifier(N, device=DEV)
+    gbuf = torch.empty(N + 4, dtype=torch.float32, device=DEV)
+    g_dev = gbuf[phase_shift:phase_shift + N]
+    g_dev.copy_(torch.from_numpy(g))
+    r_dev = torch.from_numpy(res).to(DEV)
+    s, ln = oracle.partition(N, rank, world)
+    sentinel = -12345
+    out_idx = torch.full((max(1, ln) + 8,), sentinel, dtype=torch.int32, device=DEV)
+    out_val = torch.full((max(1, ln) + 8,), float(sentinel), dtype=torch.float32, device=DEV)
+    k, th, idx, val = sp.step(g_dev, r_dev, rank, world, density, theta, out_idx, out_val)
+    r_or = res.copy()
+    o_idx, o_val, k_or, th_or = oracle.step(g, r_or, rank, world, density, theta)
+    assert k == k_or
+    assert th == th_or
+    assert np.array_equal(idx.cpu().numpy(), o_idx)
+    v = val.cpu().numpy()
+    nan_ok = np.isnan(v) & np.isnan(o_val)
+    assert np.array_equal(v.view(np.uint32)[~nan_ok], o_val.view(np.uint32)[~nan_ok])
+    rg = r_dev.cpu().numpy()
+    nan_ok = np.isnan(rg) & np.isnan(r_or)
+    assert np.array_equal(rg.view(np.uint32)[~nan_ok], r_or.view(np.uint32)[~nan_ok])
+    # nothing written past k
+    assert np.all(out_idx.cpu().numpy()[k:] == sentinel)
+    assert np.all(out_val.cpu().numpy()[k:] == float(sentinel))
+    return k
+
+
+@pytest.mark.parametrize("N,world,rank", [
+    (1, 1, 0), (3, 1, 0), (4095, 1, 0), (4096, 1, 0), (4097, 1, 0), (4099, 3, 1),
+    (12289, 3, 2), (40000, 7, 6), (100003, 16, 5), (262144 + 5, 4, 3), (1000, 2000, 1999),
+])
+@pytest.mark.parametrize("phase_shift", [0, 1])
+@pytest.mark.parametrize("regime", ["sparse", "all", "none"])
+def test_ragged_and_degenerate(N, world, rank, phase_shift, regime):
+    rng = np.random.default_rng(N + world + rank)
+    g = rng.standard_normal(N).astype(np.float32)
+    res = (rng.standard_normal(N) * 0.7).astype(np.float32)
+    theta = {"sparse": 2.4, "all": 1e-30, "none": 1e30}[regime]
+    k = gpu_vs_oracle(g, res, rank, world, 0.01, theta, phase_shift)
+    _, ln = oracle.partition(N, rank, world)
+    if regime == "all":
+        assert k == ln
+    if regime == "none":
+        assert k == 0
+
+
+@pytest.mark.parametrize("seed", range(12))
+def test_fuzz_sizes_and_starts(seed):
+    """Random N, world and rank: every start phase modulo 4, ragged tails,
+    selection fractions from 0% to 100%."""
+    rng = np.random.default_rng(1000 + seed)
+    N = int(rng.integers(1, 3_000_000))
+    world = int(rng.integers(1, 17))
+    rank = int(rng.integers(0, world))
+    g = (rng.standard_normal(N) * rng.uniform(0.1, 3)).astype(np.float32)
+    res = (rng.standard_normal(N) * rng.uniform(0.0, 2)).astype(np.float32)
+    theta = float(np.exp(rng.uniform(-4, 2.5)))
+    gpu_vs_oracle(g, res, rank, world, float(rng.choice([0.001, 0.01, 0.1])), theta,
+                  phase_shift=int(rng.integers(0, 4)))
+
+
+def test_ieee_specials_and_threshold_boundaries():
+    f = np.float32
+    tiny = f(2.0) ** -149
+    base = np.array([np.nan, np.inf, -np.inf, -0.0, 0.0, tiny, 1.0, -1.0, tiny, 3.0], dtype=np.float32)
+    g = np.tile(base, 1000)
+    res = np.tile(np.array([0.0, 0.0, 0.0, -0.0, 0.0, tiny, 0.0, 0.0, -tiny, np.nan], np.float32), 1000)
+    gpu_vs_oracle(g, res, 0, 1, 0.5, float(f(2.0) ** -148))
+    gpu_vs_oracle(g, res, 0, 1, 0.5, float(f(2.0) ** -148), phase_shift=3)
+    # thresholds at, and between, binary32 magnitudes
+    rng = np.random.default_rng(5)
+    g = rng.standard_normal(50_000).astype(np.float32)
+    res = np.zeros_like(g)
+    a = float(np.sort(np.abs(g))[-500])
+    for theta in [a, np.nextafter(a, np.inf), np.nextafter(a, 0.0),
+                  float(np.nextafter(np.float32(a), np.float32(np.inf))), a * (1 + 1e-12)]:
+        gpu_vs_oracle(g, res, 0, 1, 0.01, float(theta))
+    # threshold above FLT_MAX: only infinities are selected
+    g[::97] = np.inf
+    k = gpu_vs_oracle(g, res, 0, 1, 0.01, 1e39)
+    assert k == g[::97].size
+
+
+def test_subnormals_are_not_flushed():
+    tiny = np.float32(2.0) ** -149
+    N = 70_000
+    g = np.full(N, tiny, np.float32)
+    res = np.full(N, tiny, np.float32)
+    k = gpu_vs_oracle(g, res, 0, 1, 0.5, float(np.float32(2.0) ** -148))
+    assert k == N
+
+
+def test_deterministic_under_repetition():
+    """The look-back must give the same bits every time (20 repetitions)."""
+    N = 4_000_037
+    rng = np.random.default_rng(9)
+    g = torch.from_numpy(rng.standard_normal(N).astype(np.float32)).to(DEV)
+    res0 = torch.from_numpy((rng.standard_normal(N) * 0.5).astype(np.float32)).to(DEV)
+    sp = micro.Sparsifier(N, device=DEV)
+    ref = None
+    for _ in range(20):
+        res = res0.clone()
+        k, th, idx, val = sp.step(g, res, 1, 3, 0.01, 2.0)
+        cur = (k, th, idx.cpu().numpy().copy(), val.cpu().numpy().copy(), res.cpu().numpy())
+        if ref is None:
+            ref = cur
+        else:
+            assert cur[0] == ref[0] and cur[1] == ref[1]
+            assert np.array_equal(cur[2], ref[2])
+            assert first_mismatch(cur[3], ref[3]) < 0
+            assert first_mismatch(cur[4], ref[4]) < 0
+    sp.close()
+
+
+def test_every_rank_of_a_world_and_disjointness():
+    """Sweeping every rank with one threshold reproduces the unpartitioned
+    filter (partition invariance) with pairwise disjoint outputs."""
+    N = 1_000_003
+    rng = np.random.default_rng(21)
+    g = rng.standard_normal(N).astype(np.float32)
+    res = np.zeros(N, np.float32)
+    g_dev = torch.from_numpy(g).to(DEV)
+    r_dev = torch.zeros(N, dtype=torch.float32, device=DEV)
+    sp = micro.Sparsifier(N, device=DEV)
+    idx_all = []
+    for r in range(16):
+        k, th, idx, val = sp.step(g_dev, r_dev, r, 16, 0.01, 2.5)
+        idx_all.append(idx.cpu().numpy().copy())
+    whole_idx, _ = oracle.select(g, res, 0, N, 2.5)
+    cat = np.concatenate(idx_all)
+    assert np.array_equal(cat, whole_idx)
+    assert np.unique(cat).size == cat.size
+    assert first_mismatch(r_dev.cpu().numpy(), res) < 0
+    sp.close()
+
+
+def test_checkpoint_resume_matches_straight_run():
+    w = synth.get("toy")
+    N = w.n_total
+    gs = [synth.gradient(w, t, DEV) for t in range(6)]
+
+    def run(sp, res, th, ts):
+        out = []
+        for t in ts:
+            k, th, idx, val = sp.step(gs[t], res, 0, w.world, 0.01, th)
+            out.append((k, th, idx.cpu().numpy().copy(), val.cpu().numpy().copy()))
+        return out, th
+
+    sp = micro.Sparsifier(N, device=DEV)
+    res_a = torch.zeros(N, device=DEV)
+    straight, _ = run(sp, res_a, 2.33, range(6))
+    res_b = torch.zeros(N, device=DEV)
+    first, th_b = run(sp, res_b, 2.33, range(3))
+    saved = res_b.cpu().clone()
+    sp.close()
+    sp2 = micro.Sparsifier(N, device=DEV)      # a fresh context resumes
+    res_c = saved.to(DEV)
+    resumed, _ = run(sp2, res_c, th_b, range(3, 6))
+    for a, b in zip(straight, first + resumed):
+        assert a[0] == b[0] and a[1] == b[1]
+        assert np.array_equal(a[2], b[2]) and np.array_equal(a[3].view(np.uint32), b[3].view(np.uint32))
+    assert first_mismatch(res_a.cpu().numpy(), res_c.cpu().numpy()) < 0
+    sp2.close()
+
+
+def test_fixed_step_rule_matches_oracle():
+    w = synth.get("toy")
+    run = ParityRun(w, 0.01, DEV, rule_kind=oracle.FIXED_STEP)
+    try:
+        run.run(6, verbose=False)
+    finally:
+        run.close()
