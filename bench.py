@@ -118,7 +118,7 @@ class Run:
         cap = max(ln for _, ln in self.bounds.values())
         self.out_idx, self.out_val = sp.outputs(cap)
         self.t = 0
-        self.log = []   # (rank, P, k, kernel_ms)
+        self.log = []   # (rank, P, k, kernel_ms, tiles redone by the gather pass)
 
     def step(self, timed):
         g = self.pool[self.t % len(self.pool)]
@@ -127,10 +127,8 @@ class Run:
             k, th, _, _ = self.sp.step(g, self.res, r, self.w.world, self.d, self.theta[r],
                                        self.out_idx, self.out_val)
             self.theta[r] = th
-            if timed:
-                self.log.append((r, ln, k, self.sp.last_kernel_ms()))
-            else:
-                self.log.append((r, ln, k, None))
+            kernel_ms, redone, _ = self.sp.last_stats()
+            self.log.append((r, ln, k, kernel_ms if timed else None, redone))
         self.t += 1
 
 
@@ -162,6 +160,7 @@ def measure(w, density, pool, sp, micro, warmup, steps):
         "launches": len(timed),
         "alg_bytes_per_launch": alg_bytes / len(timed),
         "k_avg": sum(x[2] for x in timed) / len(timed),
+        "redone_tiles": sum(x[4] for x in timed),
         "density_error_last_half": sum(half) / len(half),
         "theta0": run.theta0,
         "theta_final": run.theta,
@@ -285,9 +284,10 @@ def main():
             "unit": "GB/s",
             "frac": main_res["kernel_gbs"] / HBM_PEAK_GBS,
             "traffic": traffic,
-            "kernel": "sparsify_kernel<4,4>",
+            "kernel": "stream_kernel<4,1> + gather_kernel<4,1>",
             "kernel_ms_avg": main_res["kernel_ms_avg"],
             "alg_bytes_per_launch": main_res["alg_bytes_per_launch"],
+            "redone_tiles_timed": main_res["redone_tiles"],
         },
         "cpu_baseline": cpu,
         "extra": extra,

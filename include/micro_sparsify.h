@@ -54,9 +54,15 @@ typedef enum micro_status {
 #define MICRO_RULE_FIXED_STEP 1   /* theta * (1 + alpha) if k > k*,
                                      theta * (1 - alpha) if k < k*, else theta   */
 
-/* Kernel variants. */
-#define MICRO_VARIANT_AUTO 0
-#define MICRO_VARIANT_SINGLE_PASS 1 /* one fused pass, decoupled look-back   */
+/* Kernel schedules (both compute the same result). */
+#define MICRO_VARIANT_AUTO 0   /* the fastest measured schedule: STAGED          */
+#define MICRO_VARIANT_TICKET 1 /* one pass; tiles from a ticket counter, each
+                                  tile's offset by decoupled look-back           */
+#define MICRO_VARIANT_STAGED 2 /* a streaming pass that stages each tile's pairs
+                                  (no inter-workgroup waits), then a gather pass
+                                  that places them (look-back per chunk of a
+                                  million values); scratch of about 2 bytes per
+                                  value of the vector                            */
 
 /* Flags. */
 #define MICRO_FLAG_TIME_KERNEL 1 /* record HIP events around each launch so
@@ -71,6 +77,16 @@ typedef struct micro_config {
     int32_t flags;   /* MICRO_FLAG_*                                  (default 0)    */
 } micro_config;
 
+/* What the last micro_sparsify_step on a context did. */
+typedef struct micro_step_stats {
+    float kernel_ms;        /* device time of its kernels from HIP events
+                               (MICRO_FLAG_TIME_KERNEL), else -1               */
+    int64_t redone_tiles;   /* STAGED: 1024-value tiles with more selected
+                               values than their staging slot holds (256),
+                               processed by the gather pass instead            */
+    int32_t variant;        /* MICRO_VARIANT_TICKET or MICRO_VARIANT_STAGED    */
+} micro_step_stats;
+
 /* Fills *cfg with the defaults listed above. */
 MICRO_API void micro_config_default(micro_config *cfg);
 
@@ -78,9 +94,10 @@ MICRO_API void micro_config_default(micro_config *cfg);
  * Creates a context for flattened gradient vectors of n_total fp32 values on
  * the current HIP device, enqueuing all work on `hip_stream` (a hipStream_t;
  * NULL means the null stream).  cfg == NULL selects the defaults.
- * The context owns a small device scratch area (one 64-bit status word per
- * tile of the largest partition plus a tile ticket counter) and one pinned
- * host word for the selected count; it never owns the caller's buffers.
+ * The context owns its device scratch (STAGED: a 256-pair staging slot and a
+ * count per 1024 values of the vector plus look-back words, about 2 bytes per
+ * value; TICKET: one look-back word per 4096 values) and a pinned host word
+ * for the selected count; it never owns the caller's buffers.
  * Returns MICRO_EINVAL (ctx NULL, n_total < 0, bad cfg), MICRO_ERANGE
  * (n_total > INT32_MAX: indices are int32), MICRO_EHIP (no usable device) or
  * MICRO_ENOMEM.  On failure *ctx is set to NULL.
@@ -141,10 +158,10 @@ MICRO_API micro_status micro_estimate_threshold(const micro_config *cfg, double 
  * MICRO_EINVAL for NULL output or theta not finite and > 0. */
 MICRO_API micro_status micro_threshold_f32(double theta, float *theta_f);
 
-/* Device time of the last step's kernel launch(es) in milliseconds, from HIP
- * events on the context's stream.  Needs MICRO_FLAG_TIME_KERNEL at init;
- * returns MICRO_EINVAL otherwise or before the first timed step. */
-MICRO_API micro_status micro_sparsify_last_kernel_ms(const micro_ctx *ctx, float *ms);
+/* Copies the statistics of the last step on ctx (zeroes and kernel_ms = -1
+ * before the first step or without MICRO_FLAG_TIME_KERNEL).  Returns
+ * MICRO_EINVAL for NULL arguments. */
+MICRO_API micro_status micro_sparsify_last_stats(const micro_ctx *ctx, micro_step_stats *stats);
 
 /* Message of the last failure on ctx (or of the last failed init when ctx is
  * NULL); never NULL. */

@@ -11,12 +11,12 @@ provides device memory and the stream.
 """
 from . import _lib
 from ._lib import (MICRO_FLAG_TIME_KERNEL, MICRO_RULE_FIXED_STEP, MICRO_RULE_PROPORTIONAL,
-                   MICRO_VARIANT_AUTO, MICRO_VARIANT_SINGLE_PASS, MicroError, default_config,
+                   MICRO_VARIANT_AUTO, MICRO_VARIANT_STAGED, MICRO_VARIANT_TICKET, MicroError, default_config,
                    micro_estimate_threshold, micro_partition, micro_threshold_f32)
 
 __all__ = ["Sparsifier", "MicroError", "default_config", "micro_partition",
            "micro_estimate_threshold", "micro_threshold_f32", "MICRO_RULE_PROPORTIONAL",
-           "MICRO_RULE_FIXED_STEP", "MICRO_VARIANT_AUTO", "MICRO_VARIANT_SINGLE_PASS",
+           "MICRO_RULE_FIXED_STEP", "MICRO_VARIANT_AUTO", "MICRO_VARIANT_TICKET", "MICRO_VARIANT_STAGED",
            "MICRO_FLAG_TIME_KERNEL"]
 
 
@@ -96,5 +96,10 @@ class Sparsifier:
                                          density, theta, out_idx.data_ptr(), out_val.data_ptr())
         return k, th, out_idx[:k], out_val[:k]
 
+    def last_stats(self):
+        """(kernel_ms, redone_tiles, variant) of the last step."""
+        st = _lib.micro_sparsify_last_stats(self._ctx)
+        return st.kernel_ms, st.redone_tiles, st.variant
+
     def last_kernel_ms(self):
-        return _lib.micro_sparsify_last_kernel_ms(self._ctx)
+        return self.last_stats()[0]

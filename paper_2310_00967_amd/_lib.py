@@ -12,7 +12,7 @@ LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libmicro_sp
 
 MICRO_OK, MICRO_EINVAL, MICRO_ECAPACITY, MICRO_ERANGE, MICRO_ENOMEM, MICRO_EHIP = range(6)
 MICRO_RULE_PROPORTIONAL, MICRO_RULE_FIXED_STEP = 0, 1
-MICRO_VARIANT_AUTO, MICRO_VARIANT_SINGLE_PASS = 0, 1
+MICRO_VARIANT_AUTO, MICRO_VARIANT_TICKET, MICRO_VARIANT_STAGED = 0, 1, 2
 MICRO_FLAG_TIME_KERNEL = 1
 
 # Every function the header declares, with (restype, argtypes).
@@ -25,6 +25,11 @@ class micro_config(ctypes.Structure):
     _fields_ = [("rule", ctypes.c_int32), ("beta", ctypes.c_double), ("lo", ctypes.c_double),
                 ("hi", ctypes.c_double), ("alpha", ctypes.c_double), ("variant", ctypes.c_int32),
                 ("flags", ctypes.c_int32)]
+
+
+class micro_step_stats(ctypes.Structure):
+    _fields_ = [("kernel_ms", ctypes.c_float), ("redone_tiles", ctypes.c_int64),
+                ("variant", ctypes.c_int32)]
 
 
 _cfgp = ctypes.POINTER(micro_config)
@@ -40,7 +45,7 @@ SIGNATURES = {
     "micro_estimate_threshold": (ctypes.c_int, [_cfgp, ctypes.c_double, ctypes.c_int64,
                                                 ctypes.c_int64, _dblp]),
     "micro_threshold_f32": (ctypes.c_int, [ctypes.c_double, _fltp]),
-    "micro_sparsify_last_kernel_ms": (ctypes.c_int, [ctypes.c_void_p, _fltp]),
+    "micro_sparsify_last_stats": (ctypes.c_int, [ctypes.c_void_p, ctypes.POINTER(micro_step_stats)]),
     "micro_last_error": (ctypes.c_char_p, [ctypes.c_void_p]),
     "micro_status_string": (ctypes.c_char_p, [ctypes.c_int]),
     "micro_sparsify_free": (None, [ctypes.c_void_p]),
@@ -131,10 +136,10 @@ def micro_sparsify_step(ctx, grad_ptr, residual_ptr, rank, world, density, theta
     return k.value, th.value
 
 
-def micro_sparsify_last_kernel_ms(ctx):
-    ms = ctypes.c_float()
-    check(load().micro_sparsify_last_kernel_ms(ctx, ctypes.byref(ms)), ctx)
-    return ms.value
+def micro_sparsify_last_stats(ctx):
+    st = micro_step_stats()
+    check(load().micro_sparsify_last_stats(ctx, ctypes.byref(st)), ctx)
+    return st
 
 
 def micro_sparsify_free(ctx):

@@ -21,15 +21,26 @@ struct micro_ctx {
     int64_t n_total = 0;
     hipStream_t stream = nullptr;
     micro_config cfg{};
-    uint64_t* d_status = nullptr;            // tile status words
-    int64_t status_words = 0;
-    unsigned long long* d_ticket = nullptr;  // tile ticket counter
-    int64_t* d_count = nullptr;              // selected count of the last launch
-    int64_t* h_count = nullptr;              // pinned host copy
+    bool staged = true;                      // staged schedule, else ticket
+    int64_t tile_capacity = 0;               // tiles of the largest partition
+    // staged schedule: tile counts, staged pairs, chunk look-back words
+    uint32_t* d_tile_counts = nullptr;
+    uint32_t* d_tile_excl = nullptr;
+    uint32_t* d_piece_start = nullptr;
+    int64_t piece_capacity = 0;
+    int32_t* d_stage_idx = nullptr;
+    float* d_stage_val = nullptr;
+    uint64_t* d_chunk_status = nullptr;
+    int64_t chunk_capacity = 0;
+    // ticket schedule: tile look-back words
+    uint64_t* d_status = nullptr;
+    unsigned long long* d_tickets = nullptr; // [0] tile ticket, [1] chunk ticket
+    int64_t* d_count = nullptr;              // [0] selected count, [1] flagged tiles
+    int64_t* h_count = nullptr;              // pinned host copy of d_count
     uint32_t epoch = 0;                      // epoch of the last launch
     bool needs_reset = false;                // scratch state unknown after a failure
-    hipEvent_t ev_start = nullptr, ev_stop = nullptr;
-    bool have_timing = false;
+    hipEvent_t ev[2] = {nullptr, nullptr};
+    micro_step_stats stats{};
     std::string last_error;
 };
 
@@ -60,7 +71,9 @@ bool config_valid(const micro_config& c) {
     if (!std::isfinite(c.beta) || c.beta < 0.0) return false;
     if (!std::isfinite(c.lo) || !std::isfinite(c.hi) || !(c.lo > 0.0) || !(c.hi >= c.lo)) return false;
     if (!std::isfinite(c.alpha) || c.alpha < 0.0 || !(c.alpha < 1.0)) return false;
-    if (c.variant != MICRO_VARIANT_AUTO && c.variant != MICRO_VARIANT_SINGLE_PASS) return false;
+    if (c.variant != MICRO_VARIANT_AUTO && c.variant != MICRO_VARIANT_TICKET &&
+        c.variant != MICRO_VARIANT_STAGED)
+        return false;
     if ((c.flags & ~MICRO_FLAG_TIME_KERNEL) != 0) return false;
     return true;
 }
@@ -104,8 +117,12 @@ bool ranges_overlap(const void* a, size_t an, const void* b, size_t bn) {
 }
 
 micro_status reset_scratch(micro_ctx* ctx) {
-    hipError_t e = hipMemsetAsync(ctx->d_status, 0, sizeof(uint64_t) * ctx->status_words, ctx->stream);
-    if (e == hipSuccess) e = hipMemsetAsync(ctx->d_ticket, 0, sizeof(unsigned long long), ctx->stream);
+    hipError_t e = hipMemsetAsync(ctx->d_tickets, 0, 2 * sizeof(unsigned long long), ctx->stream);
+    if (e == hipSuccess) e = hipMemsetAsync(ctx->d_count, 0, 2 * sizeof(int64_t), ctx->stream);
+    if (e == hipSuccess && ctx->d_status)
+        e = hipMemsetAsync(ctx->d_status, 0, sizeof(uint64_t) * ctx->tile_capacity, ctx->stream);
+    if (e == hipSuccess && ctx->d_chunk_status)
+        e = hipMemsetAsync(ctx->d_chunk_status, 0, sizeof(uint64_t) * ctx->chunk_capacity, ctx->stream);
     if (e == hipSuccess) e = hipStreamSynchronize(ctx->stream);
     if (e != hipSuccess) return hip_fail(ctx, e, "scratch reset");
     ctx->epoch = 0;
@@ -115,12 +132,14 @@ micro_status reset_scratch(micro_ctx* ctx) {
 
 void release(micro_ctx* ctx) {
     if (!ctx) return;
-    if (ctx->stream || ctx->d_status) (void)hipStreamSynchronize(ctx->stream);
-    if (ctx->ev_start) (void)hipEventDestroy(ctx->ev_start);
-    if (ctx->ev_stop) (void)hipEventDestroy(ctx->ev_stop);
-    if (ctx->d_status) (void)hipFree(ctx->d_status);
-    if (ctx->d_ticket) (void)hipFree(ctx->d_ticket);
-    if (ctx->d_count) (void)hipFree(ctx->d_count);
+    if (ctx->device >= 0) (void)hipStreamSynchronize(ctx->stream);
+    for (hipEvent_t ev : ctx->ev)
+        if (ev) (void)hipEventDestroy(ev);
+    void* device_buffers[] = {ctx->d_tile_counts, ctx->d_tile_excl, ctx->d_piece_start, ctx->d_stage_idx,
+                              ctx->d_stage_val, ctx->d_chunk_status, ctx->d_status, ctx->d_tickets,
+                              ctx->d_count};
+    for (void* p : device_buffers)
+        if (p) (void)hipFree(p);
     if (ctx->h_count) (void)hipHostFree(ctx->h_count);
     delete ctx;
 }
@@ -211,25 +230,44 @@ micro_status micro_sparsify_init(micro_ctx** out, int64_t n_total, void* hip_str
         release(ctx);
         return MICRO_EHIP;
     }
-    // One status word per tile of the largest possible partition (the whole
-    // vector), plus one tile for the alignment of the first tile.
-    ctx->status_words = n_total / micro::kTileElems + 2;
-    if (hipMalloc(&ctx->d_status, sizeof(uint64_t) * ctx->status_words) != hipSuccess ||
-        hipMalloc(&ctx->d_ticket, sizeof(unsigned long long)) != hipSuccess ||
-        hipMalloc(&ctx->d_count, sizeof(int64_t)) != hipSuccess ||
-        hipHostMalloc(&ctx->h_count, sizeof(int64_t), hipHostMallocDefault) != hipSuccess) {
+    // Scratch sized for the largest possible partition (the whole vector),
+    // plus one tile for the alignment of the first tile.
+    ctx->staged = c.variant != MICRO_VARIANT_TICKET;
+    bool ok = hipMalloc(&ctx->d_tickets, 2 * sizeof(unsigned long long)) == hipSuccess &&
+              hipMalloc(&ctx->d_count, 2 * sizeof(int64_t)) == hipSuccess &&
+              hipHostMalloc(&ctx->h_count, 2 * sizeof(int64_t), hipHostMallocDefault) == hipSuccess;
+    if (ok && ctx->staged) {
+        ctx->tile_capacity = n_total / micro::kStreamTile + 2;
+        ctx->chunk_capacity = ctx->tile_capacity / micro::kChunkTiles + 2;
+        ctx->piece_capacity = n_total / micro::kPieceSize + 2;
+        const size_t stage = static_cast<size_t>(ctx->tile_capacity) * micro::kStageCap;
+        ok = hipMalloc(&ctx->d_tile_counts, sizeof(uint32_t) * ctx->tile_capacity) == hipSuccess &&
+             hipMalloc(&ctx->d_tile_excl, sizeof(uint32_t) * ctx->tile_capacity) == hipSuccess &&
+             hipMalloc(&ctx->d_piece_start, sizeof(uint32_t) * ctx->piece_capacity) == hipSuccess &&
+             hipMalloc(&ctx->d_stage_idx, sizeof(int32_t) * stage) == hipSuccess &&
+             hipMalloc(&ctx->d_stage_val, sizeof(float) * stage) == hipSuccess &&
+             hipMalloc(&ctx->d_chunk_status, sizeof(uint64_t) * ctx->chunk_capacity) == hipSuccess;
+    } else if (ok) {
+        ctx->tile_capacity = n_total / micro::kTicketTile + 2;
+        ok = hipMalloc(&ctx->d_status, sizeof(uint64_t) * ctx->tile_capacity) == hipSuccess;
+    }
+    if (!ok) {
         set_error(nullptr, "device or pinned host allocation failed");
         release(ctx);
         return MICRO_ENOMEM;
     }
     if (c.flags & MICRO_FLAG_TIME_KERNEL) {
-        if ((e = hipEventCreate(&ctx->ev_start)) != hipSuccess ||
-            (e = hipEventCreate(&ctx->ev_stop)) != hipSuccess) {
-            set_error(nullptr, "hipEventCreate failed: %s", hipGetErrorString(e));
-            release(ctx);
-            return MICRO_EHIP;
+        for (hipEvent_t& ev : ctx->ev) {
+            if ((e = hipEventCreate(&ev)) != hipSuccess) {
+                set_error(nullptr, "hipEventCreate failed: %s", hipGetErrorString(e));
+                release(ctx);
+                return MICRO_EHIP;
+            }
         }
     }
+    ctx->stats.kernel_ms = -1.0f;
+    ctx->stats.redone_tiles = 0;
+    ctx->stats.variant = ctx->staged ? MICRO_VARIANT_STAGED : MICRO_VARIANT_TICKET;
     if (reset_scratch(ctx) != MICRO_OK) {
         set_error(nullptr, "%s", ctx->last_error.c_str());
         release(ctx);
@@ -290,6 +328,7 @@ micro_status micro_sparsify_step(micro_ctx* ctx, const float* grad, float* resid
         if (s != MICRO_OK) return s;
     }
     const bool vec4 = ((reinterpret_cast<uintptr_t>(grad) ^ reinterpret_cast<uintptr_t>(residual)) & 15u) == 0;
+    const int64_t tile_elems = ctx->staged ? micro::kStreamTile : micro::kTicketTile;
     micro::LaunchArgs a{};
     a.grad = grad;
     a.residual = residual;
@@ -299,48 +338,67 @@ micro_status micro_sparsify_step(micro_ctx* ctx, const float* grad, float* resid
     a.end = start + len;
     a.base = micro::tile_base_for(grad, start, vec4);
     a.theta_f = threshold_as_f32(*theta);
-    a.status = ctx->d_status;
-    a.ticket = ctx->d_ticket;
     a.epoch = ctx->epoch + 1;
-    const int64_t tiles = (a.end - a.base + micro::kTileElems - 1) / micro::kTileElems;
-    if (tiles > ctx->status_words) {
+    const int64_t tiles = (a.end - a.base + tile_elems - 1) / tile_elems;
+    const int64_t chunks = (tiles + micro::kChunkTiles - 1) / micro::kChunkTiles;
+    if (tiles > ctx->tile_capacity || (ctx->staged && chunks > ctx->chunk_capacity)) {
         set_error(ctx, "partition needs %lld tiles, scratch holds %lld", static_cast<long long>(tiles),
-                  static_cast<long long>(ctx->status_words));
+                  static_cast<long long>(ctx->tile_capacity));
         return MICRO_ECAPACITY;
     }
     a.num_tiles = static_cast<uint32_t>(tiles);
     a.count_out = ctx->d_count;
+    a.tile_counts = ctx->d_tile_counts;
+    a.tile_excl = ctx->d_tile_excl;
+    a.piece_start = ctx->d_piece_start;
+    {
+        // at most ceil(P / kPieceSize) output pieces; up to four workgroups per
+        // compute unit of an MI355X
+        const int64_t pieces = (len + micro::kPieceSize - 1) / micro::kPieceSize;
+        a.move_blocks = static_cast<uint32_t>(pieces < 1024 ? pieces : 1024);
+    }
+    a.stage_idx = ctx->d_stage_idx;
+    a.stage_val = ctx->d_stage_val;
+    a.num_chunks = static_cast<uint32_t>(chunks);
+    a.chunk_status = ctx->d_chunk_status;
+    a.chunk_ticket = &ctx->d_tickets[1];
+    a.status = ctx->d_status;
+    a.ticket = &ctx->d_tickets[0];
 
     hipError_t e;
     const bool timed = (ctx->cfg.flags & MICRO_FLAG_TIME_KERNEL) != 0;
-    if (timed && (e = hipEventRecord(ctx->ev_start, ctx->stream)) != hipSuccess)
+    ctx->stats.kernel_ms = -1.0f;
+    ctx->stats.redone_tiles = 0;
+    if (timed && (e = hipEventRecord(ctx->ev[0], ctx->stream)) != hipSuccess)
         return hip_fail(ctx, e, "hipEventRecord");
     ctx->epoch = a.epoch;
-    if ((e = micro::launch_sparsify(a, vec4, ctx->stream)) != hipSuccess)
-        return hip_fail(ctx, e, "sparsify kernel launch");
-    if (timed && (e = hipEventRecord(ctx->ev_stop, ctx->stream)) != hipSuccess)
+    e = ctx->staged ? micro::launch_staged(a, vec4, ctx->stream) : micro::launch_ticket(a, vec4, ctx->stream);
+    if (e != hipSuccess) return hip_fail(ctx, e, "sparsify kernel launch");
+    if (timed && (e = hipEventRecord(ctx->ev[1], ctx->stream)) != hipSuccess)
         return hip_fail(ctx, e, "hipEventRecord");
-    if ((e = hipMemcpyAsync(ctx->h_count, ctx->d_count, sizeof(int64_t), hipMemcpyDeviceToHost,
+    if ((e = hipMemcpyAsync(ctx->h_count, ctx->d_count, 2 * sizeof(int64_t), hipMemcpyDeviceToHost,
                             ctx->stream)) != hipSuccess)
         return hip_fail(ctx, e, "count readback");
-    if ((e = hipStreamSynchronize(ctx->stream)) != hipSuccess)
-        return hip_fail(ctx, e, "hipStreamSynchronize");
-    const int64_t selected = *ctx->h_count;
+    if ((e = hipStreamSynchronize(ctx->stream)) != hipSuccess) return hip_fail(ctx, e, "hipStreamSynchronize");
+    const int64_t selected = ctx->h_count[0];
     if (selected < 0 || selected > len) {
         set_error(ctx, "device reported %lld selected of %lld", static_cast<long long>(selected),
                   static_cast<long long>(len));
         ctx->needs_reset = true;
         return MICRO_EHIP;
     }
-    ctx->have_timing = timed;
+    if (timed && (e = hipEventElapsedTime(&ctx->stats.kernel_ms, ctx->ev[0], ctx->ev[1])) != hipSuccess)
+        return hip_fail(ctx, e, "hipEventElapsedTime");
+    ctx->stats.redone_tiles = ctx->staged ? ctx->h_count[1] : 0;
     *k = selected;
     *theta = next_threshold(ctx->cfg, density, len, selected, *theta);
     return MICRO_OK;
 }
 
-micro_status micro_sparsify_last_kernel_ms(const micro_ctx* ctx, float* ms) {
-    if (!ctx || !ms || !ctx->have_timing) return MICRO_EINVAL;
-    return hipEventElapsedTime(ms, ctx->ev_start, ctx->ev_stop) == hipSuccess ? MICRO_OK : MICRO_EHIP;
+micro_status micro_sparsify_last_stats(const micro_ctx* ctx, micro_step_stats* stats) {
+    if (!ctx || !stats) return MICRO_EINVAL;
+    *stats = ctx->stats;
+    return MICRO_OK;
 }
 
 const char* micro_last_error(const micro_ctx* ctx) {

@@ -7,16 +7,25 @@
 
 namespace micro {
 
-// Elements per tile; the same for every kernel variant so one status array
-// sized for the largest partition serves all of them.
-constexpr int kTileElems = 4096;
+// Staged schedule: values per stream tile (one 256-thread workgroup), staged
+// pairs per tile, tiles per scan chunk (one 256-thread workgroup), output
+// pairs per move piece.
+constexpr int kStreamTile = 1024;
+constexpr int kStreamBlock = 256;
+constexpr uint32_t kStageCap = 256;
+constexpr int kChunkTiles = 1024;
+constexpr int kScanBlock = 256;
+constexpr int kPieceSize = 2048;   // output pairs per move piece
+constexpr int kMoveBlock = 256;
+// Ticket schedule: values per tile (256 threads, four dwordx4 per lane).
+constexpr int kTicketTile = 4096;
 
-// Bits of a tile status word (one 64-bit word per tile):
-//   [0, 32)  count: the tile's own selected count (aggregate) or the
-//            inclusive prefix of selected counts through this tile
+// Bits of a look-back status word (one 64-bit word per tile or chunk):
+//   [0, 32)  count: the item's own selected count (aggregate) or the
+//            inclusive prefix of selected counts through this item
 //   [32, 34) flag: 1 = aggregate published, 2 = inclusive prefix published
 //   [34, 64) epoch of the launch that wrote it; words of older launches
-//            read as "not yet published", so the array is never cleared
+//            read as "not yet published", so the arrays are never cleared
 //            between launches
 constexpr int kEpochShift = 34;
 constexpr uint32_t kMaxEpoch = (1u << 30) - 1;
@@ -28,24 +37,33 @@ struct LaunchArgs {
     float* out_val;         // device, P entries
     int64_t start;          // partition [start, end)
     int64_t end;
-    int64_t base;           // global index of tile 0's first element (<= start)
+    int64_t base;           // global index of tile 0's first value (<= start)
     float theta_f;          // smallest binary32 >= theta
-    uint64_t* status;       // device, >= num_tiles words
-    unsigned long long* ticket;  // device tile ticket counter: 0 at launch,
-                                 // reset to 0 by the workgroup that draws the
-                                 // last ticket
     uint32_t epoch;         // 1 .. kMaxEpoch
-    uint32_t num_tiles;
-    int64_t* count_out;     // device word: receives the selected count
+    uint32_t num_tiles;     // tiles covering [base, end)
+    int64_t* count_out;     // device: [0] selected count, [1] flagged tiles (redone by the scan kernel)
+    // staged schedule
+    uint32_t* tile_counts;  // num_tiles counts (bit 31: tile left to the scan kernel)
+    uint32_t* tile_excl;    // num_tiles output offsets (bit 31: flagged tile)
+    uint32_t* piece_start;  // >= ceil(P / kPieceSize) tiles where output pieces start
+    uint32_t move_blocks;   // workgroups of the move kernel
+    int32_t* stage_idx;     // num_tiles * kStageCap staged indices
+    float* stage_val;       // num_tiles * kStageCap staged values
+    uint32_t num_chunks;    // ceil(num_tiles / kChunkTiles)
+    uint64_t* chunk_status;             // >= num_chunks look-back words
+    unsigned long long* chunk_ticket;   // 0 at launch, rearmed by the kernel
+    // ticket schedule
+    uint64_t* status;                   // >= num_tiles look-back words
+    unsigned long long* ticket;         // 0 at launch, rearmed by the kernel
 };
 
-// Chooses the vectorised (dwordx4) kernel when grad and residual share their
-// 16-byte phase, else the scalar-load kernel; `base` must be set accordingly
-// (see tile_base_for).  Returns the launch status.
-hipError_t launch_sparsify(const LaunchArgs& args, bool vec4, hipStream_t stream);
-
-// Global index of tile 0's first element: the start rounded down so that
-// grad + base is 16-byte aligned (vectorised kernel), or the start itself.
+// Global index of tile 0's first value: the start rounded down so that
+// grad + base is 16-byte aligned (vectorised kernels), or the start.
 int64_t tile_base_for(const float* grad, int64_t start, bool vec4);
+
+// vec4: grad and residual share their 16-byte phase (dwordx4 kernels), else
+// the scalar-load kernels.  Each returns the launch status.
+hipError_t launch_staged(const LaunchArgs& args, bool vec4, hipStream_t stream);
+hipError_t launch_ticket(const LaunchArgs& args, bool vec4, hipStream_t stream);
 
 }  // namespace micro

@@ -1,32 +1,52 @@
-// gfx950 kernel of MiCRO's per-worker sparsify step (arXiv 2310.00967).
+// gfx950 kernels of MiCRO's per-worker sparsify step (arXiv 2310.00967).
 //
-// One launch streams a worker's partition [start, end) once (Sec. 4.1,
-// Sec. 4.2): every workgroup takes the next tile by ticket, reads grad and
-// residual (dwordx4 per lane), forms acc = grad + residual (Sec. 2, error
-// feedback), tests |acc| >= theta_f, writes residual = selected ? +0 : acc
-// (Algorithm 1, reset and carry of the local error) and compacts the selected
-// (index, acc) pairs in index order (Algorithm 1, selection and gathering).
+// The step streams a worker's partition [start, end) once (Sec. 4.1,
+// Sec. 4.2): grad and residual are read (dwordx4 per lane), acc = grad +
+// residual is formed (Sec. 2, error feedback), |acc| is tested against
+// theta_f, the residual is written back as selected ? +0 : acc (Algorithm 1,
+// reset and carry of the local error), and the selected (index, acc) pairs
+// are written in index order (Algorithm 1, selection and gathering of the
+// accumulated values).
 //
-// Order-preserving compaction, all in one pass:
+// Order-preserving compaction in the same pass:
 //   * per wavefront row: one ballot per element slot and mbcnt give each
-//     lane's rank among the selected elements before it in the row;
+//     lane's rank among the selected values before it in the row;
 //   * per workgroup: the wavefront row totals go through LDS, giving each
 //     row's offset inside the tile and the tile's count;
 //   * across workgroups: decoupled look-back over one 64-bit status word per
 //     tile (count | flag | epoch).  Wavefront 0 inspects 64 predecessors per
-//     round with agent-scope atomic loads, so a tile rarely waits longer than
-//     one round trip through the coherent memory level shared by all XCDs.
-// Tiles are claimed in increasing order through a ticket counter, so a tile
-// only ever waits for tiles claimed earlier by workgroups that are already
-// running: the look-back always makes progress.
+//     round with agent-scope atomic loads, which read the memory level shared
+//     by all XCDs.  The count and its flag share one word, so relaxed atomics
+//     suffice: a reader sees either the whole published word or an older one.
+//
+// Staged schedule (default), three kernels; no workgroup of the first and the
+//   last ever waits for another:
+//   stream_kernel: one 1024-value tile per 256-thread workgroup, one dwordx4
+//     per lane and stream, every HBM stream non-temporal.  It ranks the tile's
+//     selected values, writes the residual, packs the pairs in LDS and writes
+//     them with coalesced stores to the tile's staging slot (kStageCap pairs),
+//     then stores the tile's count.  A tile with more than kStageCap selected
+//     values is left untouched and flagged.
+//   scan_kernel: one workgroup per chunk of kChunkTiles tiles, in ticket
+//     order: a scan of the chunk's tile counts and a decoupled look-back over
+//     chunk status words give every tile its output offset; it records where
+//     each output piece starts and processes the flagged tiles.  One ticket
+//     and one look-back per million values keep the cross-XCD round trips
+//     off the streaming pass.
+//   move_kernel: a fixed grid moves the staged pairs to their final places in
+//     equal pieces of the output, whatever the clustering of the selection.
+//   HBM traffic beyond the 12 bytes per value of the stream: 16 bytes per
+//   selected value (staged write and read) and 8 bytes per 1024 values.
+// Ticket schedule (variant 1): a single pass; tiles are drawn from a ticket
+//   counter in increasing order, so a tile only waits for tiles claimed by
+//   running workgroups; the per-tile ticket and look-back round trips cost
+//   bandwidth.
 #include "sparsify_kernel.h"
 
 namespace micro {
 namespace {
 
-constexpr int kBlock = 256;
 constexpr int kWaveSize = 64;
-constexpr int kWaves = kBlock / kWaveSize;
 
 constexpr uint64_t kCountMask = 0xffffffffull;
 constexpr uint64_t kFlagAggregate = 1ull << 32;
@@ -54,25 +74,19 @@ __device__ __forceinline__ void store_status(uint64_t* p, uint64_t v) {
     __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
-// Executed by all 64 lanes of one wavefront.  Publishes the tile's aggregate,
-// sums predecessors back to the nearest inclusive prefix, publishes the
-// tile's inclusive prefix and returns the exclusive prefix (uniform).
-// The count and its flag share one 64-bit word, so relaxed atomics suffice:
-// a reader either sees the whole published word or an older one.
-__device__ uint32_t decoupled_lookback(uint64_t* status, uint32_t tile, uint32_t epoch,
-                                       uint32_t tile_count, int lane) {
+// Look-back by all 64 lanes of one wavefront over the status words of the
+// items (tiles or chunks) before `item`: sums their counts back to the nearest
+// inclusive prefix and returns the exclusive prefix (uniform).  Callers draw
+// their items from a ticket counter, so every earlier item belongs to a
+// running workgroup that publishes its count without waiting for later ones:
+// the retries end.
+__device__ uint32_t lookback(const uint64_t* status, uint32_t item, uint32_t epoch, int lane) {
     const uint64_t tag = static_cast<uint64_t>(epoch) << kEpochShift;
-    if (tile == 0) {
-        if (lane == 0) store_status(&status[0], tag | kFlagInclusive | tile_count);
-        return 0;
-    }
-    if (lane == 0) store_status(&status[tile], tag | kFlagAggregate | tile_count);
-
     uint32_t exclusive = 0;
-    int64_t top = static_cast<int64_t>(tile) - 1;
+    int64_t top = static_cast<int64_t>(item) - 1;
     for (;;) {
         const int64_t p = top - lane;
-        // Positions before tile 0 read as an inclusive prefix of zero; tile 0
+        // Positions before item 0 read as an inclusive prefix of zero; item 0
         // itself always publishes an inclusive word, so they are only reached
         // once every real predecessor in the window is published.
         const uint64_t w = (p >= 0) ? load_status(&status[p]) : (tag | kFlagInclusive);
@@ -88,166 +102,556 @@ __device__ uint32_t decoupled_lookback(uint64_t* status, uint32_t tile, uint32_t
         }
         const uint32_t v = ((need >> lane) & 1ull) ? static_cast<uint32_t>(w & kCountMask) : 0u;
         exclusive += wave_sum(v);
-        if (inc_mask) break;
+        if (inc_mask) return exclusive;
         top -= kWaveSize;
     }
-    if (lane == 0) store_status(&status[tile], tag | kFlagInclusive | (exclusive + tile_count));
-    return exclusive;
 }
 
-// VEC consecutive elements per lane per row, ROWS rows per tile; element
-// (row, thread, c) of a tile sits at tile_base + (row * kBlock + thread) * VEC + c,
-// which is also its order in the compacted output.
+// Values of one tile in registers: LANES threads, ROWS rows of VEC consecutive
+// values per lane; value (row, lane, c) sits at
+// base + (row * LANES + lane) * VEC + c, which is also its output order.
+template <int VEC, int ROWS, int LANES>
+struct Tile {
+    static constexpr int kElems = VEC * ROWS * LANES;
+    int64_t base;
+    bool interior;       // the whole tile lies inside [start, end)
+    float v[ROWS][VEC];  // grad, then acc
+    float e[ROWS][VEC];  // residual
+};
+
+template <int VEC, int ROWS, int LANES>
+__device__ __forceinline__ int64_t elem_index(const Tile<VEC, ROWS, LANES>& t, int r, int lane, int c) {
+    return t.base + static_cast<int64_t>(r * LANES + lane) * VEC + c;
+}
+
+// Issues every load of tile number `tile`.  Interior tiles use dwordx4
+// (VEC == 4, 16-byte aligned by the choice of base) or dword loads,
+// non-temporal when NT (each value is read once); tiles that cross start or
+// end load element by element inside [start, end) and read 0 elsewhere.
+template <int VEC, int ROWS, int LANES, bool NT>
+__device__ __forceinline__ void load_tile(const LaunchArgs& a, uint32_t tile, int lane,
+                                          Tile<VEC, ROWS, LANES>& t) {
+    using T = Tile<VEC, ROWS, LANES>;
+    t.base = a.base + static_cast<int64_t>(tile) * T::kElems;
+    t.interior = t.base >= a.start && t.base + T::kElems <= a.end;
+    if (t.interior) {
+        if constexpr (VEC == 4) {
+#pragma unroll
+            for (int r = 0; r < ROWS; ++r) {
+                const f32x4* p = reinterpret_cast<const f32x4*>(a.grad + elem_index(t, r, lane, 0));
+                const f32x4 x = __builtin_nontemporal_load(p);
+#pragma unroll
+                for (int c = 0; c < 4; ++c) t.v[r][c] = x[c];
+            }
+#pragma unroll
+            for (int r = 0; r < ROWS; ++r) {
+                const f32x4* p = reinterpret_cast<const f32x4*>(a.residual + elem_index(t, r, lane, 0));
+                const f32x4 x = NT ? __builtin_nontemporal_load(p) : *p;
+#pragma unroll
+                for (int c = 0; c < 4; ++c) t.e[r][c] = x[c];
+            }
+        } else {
+#pragma unroll
+            for (int r = 0; r < ROWS; ++r)
+#pragma unroll
+                for (int c = 0; c < VEC; ++c)
+                    t.v[r][c] = __builtin_nontemporal_load(a.grad + elem_index(t, r, lane, c));
+#pragma unroll
+            for (int r = 0; r < ROWS; ++r)
+#pragma unroll
+                for (int c = 0; c < VEC; ++c) {
+                    const float* p = a.residual + elem_index(t, r, lane, c);
+                    t.e[r][c] = NT ? __builtin_nontemporal_load(p) : *p;
+                }
+        }
+    } else {
+#pragma unroll
+        for (int r = 0; r < ROWS; ++r) {
+#pragma unroll
+            for (int c = 0; c < VEC; ++c) {
+                const int64_t i = elem_index(t, r, lane, c);
+                const bool inside = i >= a.start && i < a.end;
+                t.v[r][c] = inside ? a.grad[i] : 0.0f;
+                t.e[r][c] = inside ? a.residual[i] : 0.0f;
+            }
+        }
+    }
+}
+
+// acc = grad + residual (one binary32 add) and the threshold test; values
+// outside [start, end) are never selected.  Leaves acc in t.v and returns the
+// lane's selection bits: bit r * VEC + c for value (r, lane, c).
+template <int VEC, int ROWS, int LANES>
+__device__ __forceinline__ uint32_t compute_tile(const LaunchArgs& a, int lane, Tile<VEC, ROWS, LANES>& t) {
+    static_assert(VEC * ROWS <= 32, "selection bits");
+    uint32_t sel = 0;
+#pragma unroll
+    for (int r = 0; r < ROWS; ++r)
+#pragma unroll
+        for (int c = 0; c < VEC; ++c) {
+            const float acc = t.v[r][c] + t.e[r][c];
+            t.v[r][c] = acc;
+            bool s = __builtin_fabsf(acc) >= a.theta_f;
+            if (!t.interior) {
+                const int64_t i = elem_index(t, r, lane, c);
+                s = s && i >= a.start && i < a.end;
+            }
+            sel |= static_cast<uint32_t>(s) << (r * VEC + c);
+        }
+    return sel;
+}
+
+template <int VEC>
+__device__ __forceinline__ bool selected(uint32_t sel, int r, int c) {
+    return (sel >> (r * VEC + c)) & 1u;
+}
+
+// residual = selected ? +0 : acc, inside [start, end) only.
+template <int VEC, int ROWS, int LANES, bool NT>
+__device__ __forceinline__ void store_residual(const LaunchArgs& a, int lane, const Tile<VEC, ROWS, LANES>& t,
+                                               uint32_t sel) {
+    if (t.interior) {
+        if constexpr (VEC == 4) {
+#pragma unroll
+            for (int r = 0; r < ROWS; ++r) {
+                f32x4 out;
+#pragma unroll
+                for (int c = 0; c < 4; ++c) out[c] = selected<4>(sel, r, c) ? 0.0f : t.v[r][c];
+                f32x4* p = reinterpret_cast<f32x4*>(a.residual + elem_index(t, r, lane, 0));
+                if (NT)
+                    __builtin_nontemporal_store(out, p);
+                else
+                    *p = out;
+            }
+        } else {
+#pragma unroll
+            for (int r = 0; r < ROWS; ++r)
+#pragma unroll
+                for (int c = 0; c < VEC; ++c) {
+                    float* p = a.residual + elem_index(t, r, lane, c);
+                    const float out = selected<VEC>(sel, r, c) ? 0.0f : t.v[r][c];
+                    if (NT)
+                        __builtin_nontemporal_store(out, p);
+                    else
+                        *p = out;
+                }
+        }
+    } else {
+#pragma unroll
+        for (int r = 0; r < ROWS; ++r)
+#pragma unroll
+            for (int c = 0; c < VEC; ++c) {
+                const int64_t i = elem_index(t, r, lane, c);
+                if (i >= a.start && i < a.end) a.residual[i] = selected<VEC>(sel, r, c) ? 0.0f : t.v[r][c];
+            }
+    }
+}
+
+// Ranks of a wavefront's selected values: lane_rank[r] = number of selected
+// values before the lane's first value of row r among the wavefront's values
+// of that row; row_count[r] = the wavefront's count in row r (uniform).
 template <int VEC, int ROWS>
-__global__ __launch_bounds__(kBlock) void sparsify_kernel(LaunchArgs a) {
-    static_assert(VEC * ROWS * kBlock == kTileElems, "tile size");
+__device__ __forceinline__ void wave_ranks(uint32_t sel, uint32_t (&lane_rank)[ROWS],
+                                           uint32_t (&row_count)[ROWS]) {
+#pragma unroll
+    for (int r = 0; r < ROWS; ++r) {
+        uint32_t below = 0, total = 0;
+#pragma unroll
+        for (int c = 0; c < VEC; ++c) {
+            const uint64_t m = __ballot(selected<VEC>(sel, r, c));
+            below += lanes_below(m);
+            total += static_cast<uint32_t>(__popcll(m));
+        }
+        lane_rank[r] = below;
+        row_count[r] = total;
+    }
+}
+
+// Workgroup-level ranks: each wavefront's row counts go through LDS (the
+// wavefront parts of a row are ordered by wavefront, rows by row);
+// row_base[r] receives this wavefront's offset of row r inside the tile and
+// the tile's count is returned.  Contains one barrier.
+template <int ROWS, int WAVES>
+__device__ __forceinline__ uint32_t tile_ranks(const uint32_t (&row_count)[ROWS], int lane, int wave,
+                                               uint32_t* s_wave_total, uint32_t (&row_base)[ROWS]) {
+    if (lane == 0) {
+#pragma unroll
+        for (int r = 0; r < ROWS; ++r) s_wave_total[r * WAVES + wave] = row_count[r];
+    }
+    __syncthreads();
+    uint32_t running = 0;
+#pragma unroll
+    for (int r = 0; r < ROWS; ++r) {
+#pragma unroll
+        for (int w = 0; w < WAVES; ++w) {
+            const uint32_t v = s_wave_total[r * WAVES + w];
+            if (w == wave) row_base[r] = running;
+            running += v;
+        }
+    }
+    return running;
+}
+
+// Writes the selected (index, acc) pairs: the k-th selected value of row r of
+// this lane goes to position out_base + row_base[r] + lane_rank[r] + k.
+template <int VEC, int ROWS, int LANES>
+__device__ __forceinline__ void scatter_pairs(const LaunchArgs& a, int lane, const Tile<VEC, ROWS, LANES>& t,
+                                              uint32_t sel, uint32_t out_base, const uint32_t (&row_base)[ROWS],
+                                              const uint32_t (&lane_rank)[ROWS]) {
+#pragma unroll
+    for (int r = 0; r < ROWS; ++r) {
+        uint32_t pos = out_base + row_base[r] + lane_rank[r];
+#pragma unroll
+        for (int c = 0; c < VEC; ++c) {
+            if (selected<VEC>(sel, r, c)) {
+                a.out_idx[pos] = static_cast<int32_t>(elem_index(t, r, lane, c));
+                a.out_val[pos] = t.v[r][c];
+                ++pos;
+            }
+        }
+    }
+}
+
+// ---------------------------------------------------------------------------
+// Staged schedule
+// ---------------------------------------------------------------------------
+
+constexpr uint32_t kOverflow = 0x80000000u;
+constexpr int kMoveBatch = 8;      // independent copies in flight per thread
+constexpr int kMoveWindow = 2048;  // tile offsets staged in LDS for one piece
+
+// Draws the workgroup's ticket (thread 0) and rearms the counter when the
+// last ticket of the launch is drawn: every other workgroup of the launch has
+// drawn its ticket by then.
+__device__ __forceinline__ uint32_t draw_ticket(unsigned long long* counter, uint32_t last) {
+    const uint32_t drawn = static_cast<uint32_t>(atomicAdd(counter, 1ull));
+    if (drawn == last) __hip_atomic_store(counter, 0ull, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    return drawn;
+}
+
+template <int VEC, int ROWS>
+__global__ __launch_bounds__(kStreamBlock) void stream_kernel(LaunchArgs a) {
+    constexpr int WAVES = kStreamBlock / kWaveSize;
+    static_assert(VEC * ROWS * kStreamBlock == kStreamTile, "tile size");
+    __shared__ uint32_t s_wave_total[ROWS * WAVES];
+    __shared__ int32_t s_idx[kStageCap];
+    __shared__ float s_val[kStageCap];
+
+    const int tid = threadIdx.x;
+    const int lane = tid & (kWaveSize - 1);
+    const int wave = tid / kWaveSize;
+    const uint32_t tile = blockIdx.x;
+
+    Tile<VEC, ROWS, kStreamBlock> t;
+    uint32_t lane_rank[ROWS], row_count[ROWS], row_base[ROWS];
+    load_tile<VEC, ROWS, kStreamBlock, true>(a, tile, tid, t);
+    const uint32_t sel = compute_tile(a, tid, t);
+    wave_ranks<VEC, ROWS>(sel, lane_rank, row_count);
+    const uint32_t count = tile_ranks<ROWS, WAVES>(row_count, lane, wave, s_wave_total, row_base);
+    if (tile == 0 && tid == 0) a.count_out[1] = 0;  // the scan kernel adds the flagged tiles
+    if (count > kStageCap) {  // uniform: left to scan_kernel, residual untouched
+        if (tid == 0) a.tile_counts[tile] = count | kOverflow;
+        return;
+    }
+    store_residual<VEC, ROWS, kStreamBlock, true>(a, tid, t, sel);
+#pragma unroll
+    for (int r = 0; r < ROWS; ++r) {
+        uint32_t pos = row_base[r] + lane_rank[r];
+#pragma unroll
+        for (int c = 0; c < VEC; ++c) {
+            if (selected<VEC>(sel, r, c)) {
+                s_idx[pos] = static_cast<int32_t>(elem_index(t, r, tid, c));
+                s_val[pos] = t.v[r][c];
+                ++pos;
+            }
+        }
+    }
+    __syncthreads();
+    const size_t slot = static_cast<size_t>(tile) * kStageCap;
+    for (uint32_t j = tid; j < count; j += kStreamBlock) {
+        a.stage_idx[slot + j] = s_idx[j];
+        a.stage_val[slot + j] = s_val[j];
+    }
+    if (tid == 0) a.tile_counts[tile] = count;
+}
+
+// Full processing of one flagged tile by one wavefront with its pairs from
+// position out_base on.  The wavefront walks the tile in the stream kernel's
+// value order: 1024 values as ROWS rows of 64 lanes.
+template <int VEC, int ROWS>
+__device__ void redo_tile(const LaunchArgs& a, uint32_t tile, int lane, uint32_t out_base) {
+    Tile<VEC, ROWS, kWaveSize> t;
+    uint32_t lane_rank[ROWS], row_count[ROWS], row_base[ROWS];
+    load_tile<VEC, ROWS, kWaveSize, false>(a, tile, lane, t);
+    const uint32_t sel = compute_tile(a, lane, t);
+    wave_ranks<VEC, ROWS>(sel, lane_rank, row_count);
+    uint32_t run = 0;
+#pragma unroll
+    for (int r = 0; r < ROWS; ++r) {
+        row_base[r] = run;
+        run += row_count[r];
+    }
+    store_residual<VEC, ROWS, kWaveSize, false>(a, lane, t, sel);
+    scatter_pairs(a, lane, t, sel, out_base, row_base, lane_rank);
+}
+
+// Scan kernel: one workgroup per chunk of kChunkTiles tiles, in ticket order.
+// Scans the chunk's tile counts, finds the chunk's output offset by decoupled
+// look-back over chunk status words, publishes every tile's output offset
+// (bit 31: flagged tile), records for every output piece of kPieceSize pairs
+// the tile where it starts, and processes the chunk's flagged tiles.
+template <int VEC, int ROWS>
+__global__ __launch_bounds__(kScanBlock) void scan_kernel(LaunchArgs a) {
+    constexpr int WAVES = kScanBlock / kWaveSize;
+    constexpr int PER_THREAD = kChunkTiles / kScanBlock;
+    static_assert(PER_THREAD == 4, "one uint4 of counts per thread");
+    __shared__ uint32_t s_chunk, s_exclusive, s_num_flagged;
+    __shared__ uint32_t s_wave_total[WAVES];
+    __shared__ uint32_t s_flagged[kChunkTiles];
+    __shared__ uint32_t s_flagged_base[kChunkTiles];
+
+    const int tid = threadIdx.x;
+    const int lane = tid & (kWaveSize - 1);
+    const int wave = tid / kWaveSize;
+    if (tid == 0) {
+        s_chunk = draw_ticket(a.chunk_ticket, a.num_chunks - 1);
+        s_num_flagged = 0;
+    }
+    __syncthreads();
+    const uint32_t chunk = s_chunk;
+    if (chunk >= a.num_chunks) return;  // only reachable if the counter was not rearmed
+    const uint32_t first_tile = chunk * kChunkTiles + tid * PER_THREAD;
+
+    uint32_t raw[PER_THREAD];
+    if (first_tile + PER_THREAD <= a.num_tiles) {
+        const uint4 v = *reinterpret_cast<const uint4*>(a.tile_counts + first_tile);
+        raw[0] = v.x;
+        raw[1] = v.y;
+        raw[2] = v.z;
+        raw[3] = v.w;
+    } else {
+#pragma unroll
+        for (int i = 0; i < PER_THREAD; ++i) raw[i] = first_tile + i < a.num_tiles ? a.tile_counts[first_tile + i] : 0u;
+    }
+    uint32_t mine = 0;
+#pragma unroll
+    for (int i = 0; i < PER_THREAD; ++i) mine += raw[i] & ~kOverflow;
+    uint32_t x = mine;  // inclusive scan of thread totals inside the wavefront
+#pragma unroll
+    for (int off = 1; off < kWaveSize; off <<= 1) {
+        const uint32_t y = __shfl_up(x, off, kWaveSize);
+        if (lane >= off) x += y;
+    }
+    if (lane == kWaveSize - 1) s_wave_total[wave] = x;
+    __syncthreads();
+    uint32_t before = 0, total = 0;
+#pragma unroll
+    for (int w = 0; w < WAVES; ++w) {
+        if (w < wave) before += s_wave_total[w];
+        total += s_wave_total[w];
+    }
+    if (wave == 0) {
+        const uint64_t tag = static_cast<uint64_t>(a.epoch) << kEpochShift;
+        uint32_t excl = 0;
+        if (chunk == 0) {
+            if (lane == 0) store_status(&a.chunk_status[0], tag | kFlagInclusive | total);
+        } else {
+            if (lane == 0) store_status(&a.chunk_status[chunk], tag | kFlagAggregate | total);
+            excl = lookback(a.chunk_status, chunk, a.epoch, lane);
+            if (lane == 0) store_status(&a.chunk_status[chunk], tag | kFlagInclusive | (excl + total));
+        }
+        if (lane == 0) {
+            s_exclusive = excl;
+            if (chunk == a.num_chunks - 1) a.count_out[0] = static_cast<int64_t>(excl) + total;
+        }
+    }
+    __syncthreads();
+    uint32_t pos = s_exclusive + before + x - mine;  // output offset of my first tile
+    uint32_t offs[PER_THREAD];
+#pragma unroll
+    for (int i = 0; i < PER_THREAD; ++i) {
+        const uint32_t count = raw[i] & ~kOverflow;
+        offs[i] = pos | (raw[i] & kOverflow);
+        // output pieces whose first position falls inside this tile
+        for (uint32_t piece = (pos + kPieceSize - 1) / kPieceSize; piece * kPieceSize < pos + count; ++piece)
+            a.piece_start[piece] = first_tile + i;
+        if (raw[i] & kOverflow) {
+            const uint32_t f = atomicAdd(&s_num_flagged, 1u);
+            s_flagged[f] = first_tile + i;
+            s_flagged_base[f] = pos;
+        }
+        pos += count;
+    }
+    if (first_tile + PER_THREAD <= a.num_tiles) {
+        *reinterpret_cast<uint4*>(a.tile_excl + first_tile) = make_uint4(offs[0], offs[1], offs[2], offs[3]);
+    } else {
+#pragma unroll
+        for (int i = 0; i < PER_THREAD; ++i)
+            if (first_tile + i < a.num_tiles) a.tile_excl[first_tile + i] = offs[i];
+    }
+    __syncthreads();
+    const uint32_t flagged = s_num_flagged;
+    if (tid == 0 && flagged != 0)
+        atomicAdd(reinterpret_cast<unsigned long long*>(&a.count_out[1]), static_cast<unsigned long long>(flagged));
+    for (uint32_t f = wave; f < flagged; f += WAVES)
+        redo_tile<VEC, ROWS * kStreamBlock / kWaveSize>(a, s_flagged[f], lane, s_flagged_base[f]);
+}
+
+// Smallest i in [0, n) with v[i] > x, or n.
+__device__ __forceinline__ uint32_t upper_bound(const uint32_t* v, uint32_t n, uint32_t x) {
+    uint32_t lo = 0, hi = n;
+    while (lo < hi) {
+        const uint32_t mid = (lo + hi) / 2;
+        if (v[mid] > x)
+            hi = mid;
+        else
+            lo = mid + 1;
+    }
+    return lo;
+}
+
+// Move kernel: a fixed grid splits the output [0, k) into pieces of
+// kPieceSize pairs, so the work per workgroup does not depend on where the
+// selected values cluster.  Every position of piece p lies in the tiles from
+// piece_start[p] to piece_start[p + 1] (both recorded by the scan kernel).
+// When that range fits in kMoveWindow tiles their output offsets go to LDS
+// and each position finds its tile there by binary search; a longer range
+// (a piece that spans a run of tiles with nothing selected) is searched in
+// the global offsets directly.  Each position copies its staged pair with a
+// coalesced write; positions of flagged tiles were written by the scan kernel.
+__global__ __launch_bounds__(kMoveBlock) void move_kernel(LaunchArgs a) {
+    __shared__ uint32_t s_off[kMoveWindow];
+    __shared__ uint32_t s_flag_bits[kMoveWindow / 32];
+
+    const int tid = threadIdx.x;
+    const int64_t k = a.count_out[0];
+    const uint32_t pieces = static_cast<uint32_t>((k + kPieceSize - 1) / kPieceSize);
+    for (uint32_t piece = blockIdx.x; piece < pieces; piece += gridDim.x) {
+        const uint32_t lo = piece * kPieceSize;
+        const uint32_t hi = static_cast<uint32_t>(k < int64_t(lo) + kPieceSize ? k : int64_t(lo) + kPieceSize);
+        const uint32_t t_begin = a.piece_start[piece];
+        const uint32_t t_end = piece + 1 < pieces ? a.piece_start[piece + 1] + 1 : a.num_tiles;
+        const uint32_t span = t_end - t_begin;
+        const bool windowed = span <= static_cast<uint32_t>(kMoveWindow);
+        if (windowed) {
+            if (tid < kMoveWindow / 32) s_flag_bits[tid] = 0u;
+            __syncthreads();
+            for (uint32_t i = tid; i < kMoveWindow; i += kMoveBlock) {
+                const uint32_t v = i < span ? a.tile_excl[t_begin + i] : static_cast<uint32_t>(k);
+                s_off[i] = v & ~kOverflow;
+                if (v & kOverflow) atomicOr(&s_flag_bits[i / 32], 1u << (i % 32));
+            }
+            __syncthreads();
+        }
+        for (uint32_t j0 = lo + tid; j0 < hi; j0 += kMoveBlock * kMoveBatch) {
+            size_t src[kMoveBatch];
+            bool live[kMoveBatch];
+#pragma unroll
+            for (int u = 0; u < kMoveBatch; ++u) {
+                const uint32_t j = j0 + u * kMoveBlock;
+                live[u] = j < hi;
+                src[u] = 0;
+                if (live[u]) {
+                    uint32_t tile, first;
+                    bool flagged;
+                    if (windowed) {
+                        const uint32_t q = upper_bound(s_off, kMoveWindow, j) - 1;
+                        tile = t_begin + q;
+                        first = s_off[q];
+                        flagged = (s_flag_bits[q / 32] >> (q % 32)) & 1u;
+                    } else {
+                        uint32_t l = t_begin, h = t_end;  // smallest t with offset > j
+                        while (l < h) {
+                            const uint32_t m = (l + h) / 2;
+                            if ((a.tile_excl[m] & ~kOverflow) > j)
+                                h = m;
+                            else
+                                l = m + 1;
+                        }
+                        tile = l - 1;
+                        const uint32_t v = a.tile_excl[tile];
+                        first = v & ~kOverflow;
+                        flagged = (v & kOverflow) != 0u;
+                    }
+                    live[u] = !flagged;
+                    src[u] = static_cast<size_t>(tile) * kStageCap + (j - first);
+                }
+            }
+            int32_t idx[kMoveBatch];
+            float val[kMoveBatch];
+#pragma unroll
+            for (int u = 0; u < kMoveBatch; ++u) {
+                if (live[u]) {
+                    idx[u] = a.stage_idx[src[u]];
+                    val[u] = a.stage_val[src[u]];
+                }
+            }
+#pragma unroll
+            for (int u = 0; u < kMoveBatch; ++u) {
+                if (live[u]) {
+                    const uint32_t j = j0 + u * kMoveBlock;
+                    a.out_idx[j] = idx[u];
+                    a.out_val[j] = val[u];
+                }
+            }
+        }
+        __syncthreads();  // the window is reloaded for the next piece
+    }
+}
+
+// ---------------------------------------------------------------------------
+// Ticket schedule (variant 1)
+// ---------------------------------------------------------------------------
+
+constexpr int kTicketBlock = 256;
+
+template <int VEC, int ROWS>
+__global__ __launch_bounds__(kTicketBlock) void ticket_kernel(LaunchArgs a) {
+    constexpr int WAVES = kTicketBlock / kWaveSize;
+    static_assert(VEC * ROWS * kTicketBlock == kTicketTile, "tile size");
     __shared__ uint32_t s_tile;
     __shared__ uint32_t s_exclusive;
-    __shared__ uint32_t s_wave_total[ROWS * kWaves];
+    __shared__ uint32_t s_wave_total[ROWS * WAVES];
 
     const int tid = threadIdx.x;
     const int lane = tid & (kWaveSize - 1);
     const int wave = tid / kWaveSize;
 
     if (tid == 0) {
-        const uint32_t t = static_cast<uint32_t>(atomicAdd(a.ticket, 1ull));
+        const uint32_t drawn = static_cast<uint32_t>(atomicAdd(a.ticket, 1ull));
         // Every other workgroup of this launch has drawn its ticket before the
         // last one is drawn, so the counter can be rearmed for the next launch.
-        if (t == a.num_tiles - 1) __hip_atomic_store(a.ticket, 0ull, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-        s_tile = t;
+        if (drawn == a.num_tiles - 1) __hip_atomic_store(a.ticket, 0ull, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        s_tile = drawn;
     }
     __syncthreads();
     const uint32_t tile = s_tile;
     if (tile >= a.num_tiles) return;  // only reachable if the counter was not rearmed
-    const int64_t tile_base = a.base + static_cast<int64_t>(tile) * kTileElems;
-    const bool interior = tile_base >= a.start && tile_base + kTileElems <= a.end;
 
-    float acc[ROWS][VEC];
-    bool sel[ROWS][VEC];
-
-    if (interior) {
-        // All loads of the tile are issued before any residual store, so each
-        // lane keeps 2 * ROWS * VEC * 4 bytes in flight.
-        if constexpr (VEC == 4) {
-            f32x4 g[ROWS], e[ROWS];
-#pragma unroll
-            for (int r = 0; r < ROWS; ++r) {
-                const int64_t i = tile_base + static_cast<int64_t>(r * kBlock + tid) * VEC;
-                g[r] = __builtin_nontemporal_load(reinterpret_cast<const f32x4*>(a.grad + i));
-            }
-#pragma unroll
-            for (int r = 0; r < ROWS; ++r) {
-                const int64_t i = tile_base + static_cast<int64_t>(r * kBlock + tid) * VEC;
-                e[r] = *reinterpret_cast<const f32x4*>(a.residual + i);
-            }
-#pragma unroll
-            for (int r = 0; r < ROWS; ++r) {
-                const int64_t i = tile_base + static_cast<int64_t>(r * kBlock + tid) * VEC;
-                f32x4 out;
-#pragma unroll
-                for (int c = 0; c < 4; ++c) {
-                    acc[r][c] = g[r][c] + e[r][c];
-                    sel[r][c] = __builtin_fabsf(acc[r][c]) >= a.theta_f;
-                    out[c] = sel[r][c] ? 0.0f : acc[r][c];
-                }
-                *reinterpret_cast<f32x4*>(a.residual + i) = out;
-            }
-        } else {
-            float g[ROWS][VEC], e[ROWS][VEC];
-#pragma unroll
-            for (int r = 0; r < ROWS; ++r)
-#pragma unroll
-                for (int c = 0; c < VEC; ++c)
-                    g[r][c] = __builtin_nontemporal_load(
-                        a.grad + tile_base + static_cast<int64_t>(r * kBlock + tid) * VEC + c);
-#pragma unroll
-            for (int r = 0; r < ROWS; ++r)
-#pragma unroll
-                for (int c = 0; c < VEC; ++c)
-                    e[r][c] = a.residual[tile_base + static_cast<int64_t>(r * kBlock + tid) * VEC + c];
-#pragma unroll
-            for (int r = 0; r < ROWS; ++r) {
-#pragma unroll
-                for (int c = 0; c < VEC; ++c) {
-                    const int64_t i = tile_base + static_cast<int64_t>(r * kBlock + tid) * VEC + c;
-                    acc[r][c] = g[r][c] + e[r][c];
-                    sel[r][c] = __builtin_fabsf(acc[r][c]) >= a.theta_f;
-                    a.residual[i] = sel[r][c] ? 0.0f : acc[r][c];
-                }
-            }
-        }
-    } else {
-        // First or last tile of the partition: per-element guards.
-#pragma unroll
-        for (int r = 0; r < ROWS; ++r) {
-#pragma unroll
-            for (int c = 0; c < VEC; ++c) {
-                const int64_t i = tile_base + static_cast<int64_t>(r * kBlock + tid) * VEC + c;
-                const bool inside = i >= a.start && i < a.end;
-                acc[r][c] = 0.0f;
-                sel[r][c] = false;
-                if (inside) {
-                    acc[r][c] = a.grad[i] + a.residual[i];
-                    sel[r][c] = __builtin_fabsf(acc[r][c]) >= a.theta_f;
-                    a.residual[i] = sel[r][c] ? 0.0f : acc[r][c];
-                }
-            }
-        }
-    }
-
-    // Rank of each lane's first selected element inside its wavefront row,
-    // and the row totals of every wavefront.
-    uint32_t lane_rank[ROWS];
-#pragma unroll
-    for (int r = 0; r < ROWS; ++r) {
-        uint32_t below = 0, total = 0;
-#pragma unroll
-        for (int c = 0; c < VEC; ++c) {
-            const uint64_t m = __ballot(sel[r][c]);
-            below += lanes_below(m);
-            total += static_cast<uint32_t>(__popcll(m));
-        }
-        lane_rank[r] = below;
-        if (lane == 0) s_wave_total[r * kWaves + wave] = total;
-    }
-    __syncthreads();
-
-    uint32_t row_offset[ROWS];
-    uint32_t running = 0;
-#pragma unroll
-    for (int r = 0; r < ROWS; ++r) {
-#pragma unroll
-        for (int w = 0; w < kWaves; ++w) {
-            const uint32_t v = s_wave_total[r * kWaves + w];
-            if (w == wave) row_offset[r] = running;
-            running += v;
-        }
-    }
-    const uint32_t tile_count = running;
-
+    Tile<VEC, ROWS, kTicketBlock> t;
+    uint32_t lane_rank[ROWS], row_count[ROWS], row_base[ROWS];
+    load_tile<VEC, ROWS, kTicketBlock, false>(a, tile, tid, t);
+    const uint32_t sel = compute_tile(a, tid, t);
+    store_residual<VEC, ROWS, kTicketBlock, false>(a, tid, t, sel);
+    wave_ranks<VEC, ROWS>(sel, lane_rank, row_count);
+    const uint32_t count = tile_ranks<ROWS, WAVES>(row_count, lane, wave, s_wave_total, row_base);
     if (wave == 0) {
-        const uint32_t excl = decoupled_lookback(a.status, tile, a.epoch, tile_count, lane);
+        const uint64_t tag = static_cast<uint64_t>(a.epoch) << kEpochShift;
+        uint32_t excl = 0;
+        if (tile == 0) {
+            if (lane == 0) store_status(&a.status[0], tag | kFlagInclusive | count);
+        } else {
+            if (lane == 0) store_status(&a.status[tile], tag | kFlagAggregate | count);
+            excl = lookback(a.status, tile, a.epoch, lane);
+            if (lane == 0) store_status(&a.status[tile], tag | kFlagInclusive | (excl + count));
+        }
         if (lane == 0) {
             s_exclusive = excl;
-            if (tile == a.num_tiles - 1) *a.count_out = static_cast<int64_t>(excl) + tile_count;
+            if (tile == a.num_tiles - 1) a.count_out[0] = static_cast<int64_t>(excl) + count;
         }
     }
     __syncthreads();
-    const uint32_t exclusive = s_exclusive;
-
-#pragma unroll
-    for (int r = 0; r < ROWS; ++r) {
-        uint32_t pos = exclusive + row_offset[r] + lane_rank[r];
-#pragma unroll
-        for (int c = 0; c < VEC; ++c) {
-            if (sel[r][c]) {
-                const int64_t i = tile_base + static_cast<int64_t>(r * kBlock + tid) * VEC + c;
-                a.out_idx[pos] = static_cast<int32_t>(i);
-                a.out_val[pos] = acc[r][c];
-                ++pos;
-            }
-        }
-    }
+    scatter_pairs(a, tid, t, sel, s_exclusive, row_base, lane_rank);
 }
 
 }  // namespace
@@ -258,12 +662,25 @@ int64_t tile_base_for(const float* grad, int64_t start, bool vec4) {
     return start - static_cast<int64_t>((addr & 15u) / sizeof(float));
 }
 
-hipError_t launch_sparsify(const LaunchArgs& args, bool vec4, hipStream_t stream) {
-    const dim3 grid(args.num_tiles), block(kBlock);
+hipError_t launch_staged(const LaunchArgs& args, bool vec4, hipStream_t stream) {
+    const dim3 grid_stream(args.num_tiles), grid_scan(args.num_chunks), grid_move(args.move_blocks);
+    if (vec4) {
+        hipLaunchKernelGGL((stream_kernel<4, 1>), grid_stream, dim3(kStreamBlock), 0, stream, args);
+        hipLaunchKernelGGL((scan_kernel<4, 1>), grid_scan, dim3(kScanBlock), 0, stream, args);
+    } else {
+        hipLaunchKernelGGL((stream_kernel<1, 4>), grid_stream, dim3(kStreamBlock), 0, stream, args);
+        hipLaunchKernelGGL((scan_kernel<1, 4>), grid_scan, dim3(kScanBlock), 0, stream, args);
+    }
+    hipLaunchKernelGGL(move_kernel, grid_move, dim3(kMoveBlock), 0, stream, args);
+    return hipGetLastError();
+}
+
+hipError_t launch_ticket(const LaunchArgs& args, bool vec4, hipStream_t stream) {
+    const dim3 grid(args.num_tiles), block(kTicketBlock);
     if (vec4)
-        hipLaunchKernelGGL((sparsify_kernel<4, 4>), grid, block, 0, stream, args);
+        hipLaunchKernelGGL((ticket_kernel<4, 4>), grid, block, 0, stream, args);
     else
-        hipLaunchKernelGGL((sparsify_kernel<1, 16>), grid, block, 0, stream, args);
+        hipLaunchKernelGGL((ticket_kernel<1, 16>), grid, block, 0, stream, args);
     return hipGetLastError();
 }
 

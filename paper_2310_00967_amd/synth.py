@@ -225,14 +225,28 @@ def gradient(w, t, device="cpu", out=None):
 
 def calibrate_theta0(g, start, end, density):
     """Initial threshold: the K-th largest magnitude in g[start:end),
-    K = max(1, floor(density * P)), as a Python float (exact widening)."""
+    K = max(1, floor(density * P)), as a Python float (exact widening).
+
+    Found by bisection over the bit patterns of non-negative binary32 values,
+    which order like the integers: the largest x with #{|g| >= x} >= K is the
+    K-th largest magnitude.  31 counting passes on the tensor's device."""
     P = end - start
     if P <= 0:
         return 1.0
     K = max(1, int(math.floor(density * P)))
     mag = g[start:end].abs()
-    val = torch.kthvalue(mag.reshape(-1), P - K + 1).values
-    return float(val.item())
+    lo, hi = 0, 0x7F800000  # +0 .. +inf
+    probe = torch.empty(1, dtype=torch.int32)
+    while lo < hi:
+        mid = (lo + hi + 1) // 2
+        probe[0] = mid
+        x = float(probe.view(torch.float32)[0])
+        if int((mag >= x).sum()) >= K:
+            lo = mid
+        else:
+            hi = mid - 1
+    probe[0] = lo
+    return float(probe.view(torch.float32)[0])
 
 
 def initial_theta(w, g0, start, end, density):

@@ -17,17 +17,25 @@ from gpu_harness import ParityRun, first_mismatch, note
 pytestmark = pytest.mark.gpu
 
 DEV = "cuda"
+STAGED, TICKET = micro.MICRO_VARIANT_STAGED, micro.MICRO_VARIANT_TICKET
+VARIANTS = pytest.mark.parametrize("variant", [STAGED, TICKET], ids=["staged", "ticket"])
 
 
-@pytest.mark.parametrize("name,density,steps", [
-    ("toy", 0.01, 20),
-    ("resnet18", 0.01, 100),
-    ("resnet50", 0.001, 100),
-    ("bert_large", 0.01, 50),
+def make_sparsifier(n, variant):
+    return micro.Sparsifier(n, device=DEV, variant=variant)
+
+
+@pytest.mark.parametrize("name,density,steps,variant", [
+    ("toy", 0.01, 20, STAGED),
+    ("toy", 0.01, 20, TICKET),
+    ("resnet18", 0.01, 100, STAGED),
+    ("resnet50", 0.001, 100, STAGED),
+    ("bert_large", 0.01, 50, STAGED),
+    ("bert_large", 0.01, 10, TICKET),
 ])
-def test_workload_parity(name, density, steps):
-    note(f"parity {name} d={density} steps={steps}")
-    run = ParityRun(synth.get(name), density, DEV)
+def test_workload_parity(name, density, steps, variant):
+    note(f"parity {name} d={density} steps={steps} variant={variant}")
+    run = ParityRun(synth.get(name), density, DEV, variant=variant)
     try:
         run.run(steps)
     finally:
@@ -49,11 +57,11 @@ def test_gpt_parity(density):
 # edge cases and ragged sizes (small inputs, oracle finishes instantly)
 # ---------------------------------------------------------------------------
 
-def gpu_vs_oracle(g, res, rank, world, density, theta, phase_shift=0, sp=None):
+def gpu_vs_oracle(g, res, rank, world, density, theta, phase_shift=0, variant=STAGED):
     """One call on both sides; g/res are host float32 arrays.  phase_shift != 0
-    places grad at a different 16-byte phase than residual (scalar-load kernel)."""
+    places grad at a different 16-byte phase than residual (scalar-load kernels)."""
     N = g.size
-    sp = sp or micro.Sparsifier(N, device=DEV)
+    sp = make_sparsifier(N, variant)
     gbuf = torch.empty(N + 4, dtype=torch.float32, device=DEV)
     g_dev = gbuf[phase_shift:phase_shift + N]
     g_dev.copy_(torch.from_numpy(g))
@@ -77,6 +85,7 @@ def gpu_vs_oracle(g, res, rank, world, density, theta, phase_shift=0, sp=None):
     # nothing written past k
     assert np.all(out_idx.cpu().numpy()[k:] == sentinel)
     assert np.all(out_val.cpu().numpy()[k:] == float(sentinel))
+    sp.close()
     return k
 
 
@@ -86,12 +95,13 @@ def gpu_vs_oracle(g, res, rank, world, density, theta, phase_shift=0, sp=None):
 ])
 @pytest.mark.parametrize("phase_shift", [0, 1])
 @pytest.mark.parametrize("regime", ["sparse", "all", "none"])
-def test_ragged_and_degenerate(N, world, rank, phase_shift, regime):
+@VARIANTS
+def test_ragged_and_degenerate(N, world, rank, phase_shift, regime, variant):
     rng = np.random.default_rng(N + world + rank)
     g = rng.standard_normal(N).astype(np.float32)
     res = (rng.standard_normal(N) * 0.7).astype(np.float32)
     theta = {"sparse": 2.4, "all": 1e-30, "none": 1e30}[regime]
-    k = gpu_vs_oracle(g, res, rank, world, 0.01, theta, phase_shift)
+    k = gpu_vs_oracle(g, res, rank, world, 0.01, theta, phase_shift, variant)
     _, ln = oracle.partition(N, rank, world)
     if regime == "all":
         assert k == ln
@@ -100,7 +110,8 @@ def test_ragged_and_degenerate(N, world, rank, phase_shift, regime):
 
 
 @pytest.mark.parametrize("seed", range(12))
-def test_fuzz_sizes_and_starts(seed):
+@VARIANTS
+def test_fuzz_sizes_and_starts(seed, variant):
     """Random N, world and rank: every start phase modulo 4, ragged tails,
     selection fractions from 0% to 100%."""
     rng = np.random.default_rng(1000 + seed)
@@ -111,17 +122,18 @@ def test_fuzz_sizes_and_starts(seed):
     res = (rng.standard_normal(N) * rng.uniform(0.0, 2)).astype(np.float32)
     theta = float(np.exp(rng.uniform(-4, 2.5)))
     gpu_vs_oracle(g, res, rank, world, float(rng.choice([0.001, 0.01, 0.1])), theta,
-                  phase_shift=int(rng.integers(0, 4)))
+                  phase_shift=int(rng.integers(0, 4)), variant=variant)
 
 
-def test_ieee_specials_and_threshold_boundaries():
+@VARIANTS
+def test_ieee_specials_and_threshold_boundaries(variant):
     f = np.float32
     tiny = f(2.0) ** -149
     base = np.array([np.nan, np.inf, -np.inf, -0.0, 0.0, tiny, 1.0, -1.0, tiny, 3.0], dtype=np.float32)
     g = np.tile(base, 1000)
     res = np.tile(np.array([0.0, 0.0, 0.0, -0.0, 0.0, tiny, 0.0, 0.0, -tiny, np.nan], np.float32), 1000)
-    gpu_vs_oracle(g, res, 0, 1, 0.5, float(f(2.0) ** -148))
-    gpu_vs_oracle(g, res, 0, 1, 0.5, float(f(2.0) ** -148), phase_shift=3)
+    gpu_vs_oracle(g, res, 0, 1, 0.5, float(f(2.0) ** -148), variant=variant)
+    gpu_vs_oracle(g, res, 0, 1, 0.5, float(f(2.0) ** -148), phase_shift=3, variant=variant)
     # thresholds at, and between, binary32 magnitudes
     rng = np.random.default_rng(5)
     g = rng.standard_normal(50_000).astype(np.float32)
@@ -129,29 +141,57 @@ def test_ieee_specials_and_threshold_boundaries():
     a = float(np.sort(np.abs(g))[-500])
     for theta in [a, np.nextafter(a, np.inf), np.nextafter(a, 0.0),
                   float(np.nextafter(np.float32(a), np.float32(np.inf))), a * (1 + 1e-12)]:
-        gpu_vs_oracle(g, res, 0, 1, 0.01, float(theta))
+        gpu_vs_oracle(g, res, 0, 1, 0.01, float(theta), variant=variant)
     # threshold above FLT_MAX: only infinities are selected
     g[::97] = np.inf
-    k = gpu_vs_oracle(g, res, 0, 1, 0.01, 1e39)
+    k = gpu_vs_oracle(g, res, 0, 1, 0.01, 1e39, variant=variant)
     assert k == g[::97].size
 
 
-def test_subnormals_are_not_flushed():
+@VARIANTS
+def test_subnormals_are_not_flushed(variant):
     tiny = np.float32(2.0) ** -149
     N = 70_000
     g = np.full(N, tiny, np.float32)
     res = np.full(N, tiny, np.float32)
-    k = gpu_vs_oracle(g, res, 0, 1, 0.5, float(np.float32(2.0) ** -148))
+    k = gpu_vs_oracle(g, res, 0, 1, 0.5, float(np.float32(2.0) ** -148), variant=variant)
     assert k == N
 
 
-def test_deterministic_under_repetition():
+@pytest.mark.parametrize("phase_shift", [0, 2])
+def test_dense_tiles_redone_by_gather_mixed_with_staged_ones(phase_shift):
+    """Tiles with more selected values than their staging slot holds (256 of
+    1024) are left to the gather pass, which processes them straight into the
+    output; they interleave with staged tiles and with each other, including
+    at the ragged ends and across gather chunks (a million values each)."""
+    rng = np.random.default_rng(77)
+    N = 3 * 1_048_576 + 1234
+    g = rng.standard_normal(N).astype(np.float32)
+    res = np.zeros(N, np.float32)
+    # dense bands (most values selected) of varied lengths and offsets
+    for lo, ln in [(0, 700), (5000, 4096), (70_000, 1), (1_000_001, 300_000),
+                   (2_097_000, 5000), (N - 3000, 3000)]:
+        g[lo:lo + ln] *= 40.0
+    for world, rank in [(1, 0), (3, 1), (7, 6)]:
+        for theta in [3.0, 0.3, 1e-30]:
+            gpu_vs_oracle(g, res, rank, world, 0.01, theta, phase_shift, STAGED)
+    sp = micro.Sparsifier(N, device=DEV, variant=STAGED)
+    g_dev = torch.from_numpy(g).to(DEV)
+    r_dev = torch.zeros(N, dtype=torch.float32, device=DEV)
+    sp.step(g_dev, r_dev, 0, 1, 0.01, 3.0)
+    _, redone, variant = sp.last_stats()
+    assert variant == STAGED and redone > 300
+    sp.close()
+
+
+@VARIANTS
+def test_deterministic_under_repetition(variant):
     """The look-back must give the same bits every time (20 repetitions)."""
     N = 4_000_037
     rng = np.random.default_rng(9)
     g = torch.from_numpy(rng.standard_normal(N).astype(np.float32)).to(DEV)
     res0 = torch.from_numpy((rng.standard_normal(N) * 0.5).astype(np.float32)).to(DEV)
-    sp = micro.Sparsifier(N, device=DEV)
+    sp = make_sparsifier(N, variant)
     ref = None
     for _ in range(20):
         res = res0.clone()
