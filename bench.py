@@ -49,6 +49,8 @@ def parse_args():
                     help="target CPU time of the oracle baseline sample (0 disables)")
     ap.add_argument("--pool-gb", type=float, default=100.0,
                     help="HBM budget for the pre-generated gradient pool")
+    ap.add_argument("--variant", default="staged", choices=["staged", "ticket"],
+                    help="kernel schedule (staged is the library default)")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only run a plain device copy of known size (HBM counter scaling)")
     return ap.parse_args()
@@ -235,7 +237,8 @@ def main():
     n_pool = max(1, min(args.warmup + args.steps, int(args.pool_gb * 1e9 // (4 * w.n_total))))
     pool = [synth.gradient(w, t, "cuda") for t in range(n_pool)]
     torch.cuda.synchronize()
-    sp = micro.Sparsifier(w.n_total, device="cuda", time_kernel=True)
+    variant = micro.MICRO_VARIANT_STAGED if args.variant == "staged" else micro.MICRO_VARIANT_TICKET
+    sp = micro.Sparsifier(w.n_total, device="cuda", time_kernel=True, variant=variant)
 
     main_res = measure(w, head, pool, sp, micro, args.warmup, args.steps)
     extra = {}
@@ -273,6 +276,7 @@ def main():
             "distribution": w.dist,
             "gradient_pool": n_pool,
             "parallelism": "one worker's partition on one GPU",
+            "variant": args.variant,
         },
         "hbm_gbs_wall": main_res["wall_gbs"],
         "hbm_frac_wall": main_res["wall_gbs"] / HBM_PEAK_GBS,
@@ -284,7 +288,8 @@ def main():
             "unit": "GB/s",
             "frac": main_res["kernel_gbs"] / HBM_PEAK_GBS,
             "traffic": traffic,
-            "kernel": "stream_kernel<4,1> + gather_kernel<4,1>",
+            "kernel": ("stream_kernel + scan_kernel + move_kernel (one step, event-timed together)"
+                       if args.variant == "staged" else "ticket_kernel"),
             "kernel_ms_avg": main_res["kernel_ms_avg"],
             "alg_bytes_per_launch": main_res["alg_bytes_per_launch"],
             "redone_tiles_timed": main_res["redone_tiles"],
