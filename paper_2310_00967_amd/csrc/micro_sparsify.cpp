@@ -26,17 +26,17 @@ struct micro_ctx {
     // staged schedule: tile counts, staged pairs, chunk look-back words
     uint32_t* d_tile_counts = nullptr;
     uint32_t* d_tile_excl = nullptr;
-    uint32_t* d_piece_start = nullptr;
-    int64_t piece_capacity = 0;
-    int32_t* d_stage_idx = nullptr;
-    float* d_stage_val = nullptr;
+    uint32_t* d_split_tile = nullptr;
+    int64_t split_capacity = 0;
+    uint2* d_stage = nullptr;                // (index, value bits) pairs
     uint64_t* d_chunk_status = nullptr;
     int64_t chunk_capacity = 0;
     // ticket schedule: tile look-back words
     uint64_t* d_status = nullptr;
     unsigned long long* d_tickets = nullptr; // [0] tile ticket, [1] chunk ticket
     int64_t* d_count = nullptr;              // [0] selected count, [1] flagged tiles
-    int64_t* h_count = nullptr;              // pinned host copy of d_count
+    int64_t* h_count = nullptr;              // mapped pinned host copy of d_count, stored by the kernels
+    int64_t* h_count_dev = nullptr;          // the device's address of h_count
     uint32_t epoch = 0;                      // epoch of the last launch
     bool needs_reset = false;                // scratch state unknown after a failure
     hipEvent_t ev[2] = {nullptr, nullptr};
@@ -135,8 +135,8 @@ void release(micro_ctx* ctx) {
     if (ctx->device >= 0) (void)hipStreamSynchronize(ctx->stream);
     for (hipEvent_t ev : ctx->ev)
         if (ev) (void)hipEventDestroy(ev);
-    void* device_buffers[] = {ctx->d_tile_counts, ctx->d_tile_excl, ctx->d_piece_start, ctx->d_stage_idx,
-                              ctx->d_stage_val, ctx->d_chunk_status, ctx->d_status, ctx->d_tickets,
+    void* device_buffers[] = {ctx->d_tile_counts, ctx->d_tile_excl, ctx->d_split_tile, ctx->d_stage,
+                              ctx->d_chunk_status, ctx->d_status, ctx->d_tickets,
                               ctx->d_count};
     for (void* p : device_buffers)
         if (p) (void)hipFree(p);
@@ -235,17 +235,18 @@ micro_status micro_sparsify_init(micro_ctx** out, int64_t n_total, void* hip_str
     ctx->staged = c.variant != MICRO_VARIANT_TICKET;
     bool ok = hipMalloc(&ctx->d_tickets, 2 * sizeof(unsigned long long)) == hipSuccess &&
               hipMalloc(&ctx->d_count, 2 * sizeof(int64_t)) == hipSuccess &&
-              hipHostMalloc(&ctx->h_count, 2 * sizeof(int64_t), hipHostMallocDefault) == hipSuccess;
+              hipHostMalloc(&ctx->h_count, 2 * sizeof(int64_t), hipHostMallocMapped | hipHostMallocCoherent) ==
+                  hipSuccess &&
+              hipHostGetDevicePointer(reinterpret_cast<void**>(&ctx->h_count_dev), ctx->h_count, 0) == hipSuccess;
     if (ok && ctx->staged) {
         ctx->tile_capacity = n_total / micro::kStreamTile + 2;
         ctx->chunk_capacity = ctx->tile_capacity / micro::kChunkTiles + 2;
-        ctx->piece_capacity = n_total / micro::kPieceSize + 2;
+        ctx->split_capacity = (ctx->tile_capacity + n_total) / micro::kMoveSpan + 2;
         const size_t stage = static_cast<size_t>(ctx->tile_capacity) * micro::kStageCap;
         ok = hipMalloc(&ctx->d_tile_counts, sizeof(uint32_t) * ctx->tile_capacity) == hipSuccess &&
              hipMalloc(&ctx->d_tile_excl, sizeof(uint32_t) * ctx->tile_capacity) == hipSuccess &&
-             hipMalloc(&ctx->d_piece_start, sizeof(uint32_t) * ctx->piece_capacity) == hipSuccess &&
-             hipMalloc(&ctx->d_stage_idx, sizeof(int32_t) * stage) == hipSuccess &&
-             hipMalloc(&ctx->d_stage_val, sizeof(float) * stage) == hipSuccess &&
+             hipMalloc(&ctx->d_split_tile, sizeof(uint32_t) * ctx->split_capacity) == hipSuccess &&
+             hipMalloc(&ctx->d_stage, sizeof(uint2) * stage) == hipSuccess &&
              hipMalloc(&ctx->d_chunk_status, sizeof(uint64_t) * ctx->chunk_capacity) == hipSuccess;
     } else if (ok) {
         ctx->tile_capacity = n_total / micro::kTicketTile + 2;
@@ -348,17 +349,16 @@ micro_status micro_sparsify_step(micro_ctx* ctx, const float* grad, float* resid
     }
     a.num_tiles = static_cast<uint32_t>(tiles);
     a.count_out = ctx->d_count;
+    a.host_count = ctx->h_count_dev;
     a.tile_counts = ctx->d_tile_counts;
     a.tile_excl = ctx->d_tile_excl;
-    a.piece_start = ctx->d_piece_start;
+    a.split_tile = ctx->d_split_tile;
     {
-        // at most ceil(P / kPieceSize) output pieces; up to four workgroups per
-        // compute unit of an MI355X
-        const int64_t pieces = (len + micro::kPieceSize - 1) / micro::kPieceSize;
-        a.move_blocks = static_cast<uint32_t>(pieces < 1024 ? pieces : 1024);
+        // at most ceil((tiles + P) / kMoveSpan) move pieces, whatever k is
+        const int64_t pieces = (tiles + len + micro::kMoveSpan - 1) / micro::kMoveSpan;
+        a.move_blocks = static_cast<uint32_t>(pieces < micro::kMoveGrid ? pieces : micro::kMoveGrid);
     }
-    a.stage_idx = ctx->d_stage_idx;
-    a.stage_val = ctx->d_stage_val;
+    a.stage = ctx->d_stage;
     a.num_chunks = static_cast<uint32_t>(chunks);
     a.chunk_status = ctx->d_chunk_status;
     a.chunk_ticket = &ctx->d_tickets[1];
@@ -372,15 +372,15 @@ micro_status micro_sparsify_step(micro_ctx* ctx, const float* grad, float* resid
     if (timed && (e = hipEventRecord(ctx->ev[0], ctx->stream)) != hipSuccess)
         return hip_fail(ctx, e, "hipEventRecord");
     ctx->epoch = a.epoch;
+    volatile int64_t* host_count = ctx->h_count;  // stored by the last kernel of the step
+    host_count[0] = -1;
+    host_count[1] = -1;
     e = ctx->staged ? micro::launch_staged(a, vec4, ctx->stream) : micro::launch_ticket(a, vec4, ctx->stream);
     if (e != hipSuccess) return hip_fail(ctx, e, "sparsify kernel launch");
     if (timed && (e = hipEventRecord(ctx->ev[1], ctx->stream)) != hipSuccess)
         return hip_fail(ctx, e, "hipEventRecord");
-    if ((e = hipMemcpyAsync(ctx->h_count, ctx->d_count, 2 * sizeof(int64_t), hipMemcpyDeviceToHost,
-                            ctx->stream)) != hipSuccess)
-        return hip_fail(ctx, e, "count readback");
     if ((e = hipStreamSynchronize(ctx->stream)) != hipSuccess) return hip_fail(ctx, e, "hipStreamSynchronize");
-    const int64_t selected = ctx->h_count[0];
+    const int64_t selected = host_count[0];
     if (selected < 0 || selected > len) {
         set_error(ctx, "device reported %lld selected of %lld", static_cast<long long>(selected),
                   static_cast<long long>(len));
@@ -389,7 +389,7 @@ micro_status micro_sparsify_step(micro_ctx* ctx, const float* grad, float* resid
     }
     if (timed && (e = hipEventElapsedTime(&ctx->stats.kernel_ms, ctx->ev[0], ctx->ev[1])) != hipSuccess)
         return hip_fail(ctx, e, "hipEventElapsedTime");
-    ctx->stats.redone_tiles = ctx->staged ? ctx->h_count[1] : 0;
+    ctx->stats.redone_tiles = ctx->staged ? host_count[1] : 0;
     *k = selected;
     *theta = next_threshold(ctx->cfg, density, len, selected, *theta);
     return MICRO_OK;

@@ -8,15 +8,19 @@
 namespace micro {
 
 // Staged schedule: values per stream tile (one 256-thread workgroup), staged
-// pairs per tile, tiles per scan chunk (one 256-thread workgroup), output
-// pairs per move piece.
+// pairs per tile, tiles per scan chunk (one 256-thread workgroup), items per
+// move piece.  The move kernel walks the merged sequence of tiles and output
+// pairs (each tile is one item, followed by one item per selected value of
+// the tile) in pieces of kMoveSpan items, so a piece holds at most kMoveSpan
+// pairs and touches at most kMoveSpan + 1 tiles.
 constexpr int kStreamTile = 1024;
 constexpr int kStreamBlock = 256;
 constexpr uint32_t kStageCap = 256;
 constexpr int kChunkTiles = 1024;
 constexpr int kScanBlock = 256;
-constexpr int kPieceSize = 2048;   // output pairs per move piece
+constexpr int kMoveSpan = 4096;
 constexpr int kMoveBlock = 256;
+constexpr uint32_t kMoveGrid = 2048;  // largest move grid (eight workgroups per compute unit)
 // Ticket schedule: values per tile (256 threads, four dwordx4 per lane).
 constexpr int kTicketTile = 4096;
 
@@ -42,13 +46,13 @@ struct LaunchArgs {
     uint32_t epoch;         // 1 .. kMaxEpoch
     uint32_t num_tiles;     // tiles covering [base, end)
     int64_t* count_out;     // device: [0] selected count, [1] flagged tiles (redone by the scan kernel)
+    int64_t* host_count;    // mapped pinned host memory: the final count_out, stored by the last kernel
     // staged schedule
     uint32_t* tile_counts;  // num_tiles counts (bit 31: tile left to the scan kernel)
     uint32_t* tile_excl;    // num_tiles output offsets (bit 31: flagged tile)
-    uint32_t* piece_start;  // >= ceil(P / kPieceSize) tiles where output pieces start
+    uint32_t* split_tile;   // >= ceil((num_tiles + P) / kMoveSpan) tiles holding each piece's first item
     uint32_t move_blocks;   // workgroups of the move kernel
-    int32_t* stage_idx;     // num_tiles * kStageCap staged indices
-    float* stage_val;       // num_tiles * kStageCap staged values
+    uint2* stage;           // num_tiles * kStageCap staged (index, value bits) pairs
     uint32_t num_chunks;    // ceil(num_tiles / kChunkTiles)
     uint64_t* chunk_status;             // >= num_chunks look-back words
     unsigned long long* chunk_ticket;   // 0 at launch, rearmed by the kernel

@@ -24,17 +24,18 @@
 //   stream_kernel: one 1024-value tile per 256-thread workgroup, one dwordx4
 //     per lane and stream, every HBM stream non-temporal.  It ranks the tile's
 //     selected values, writes the residual, packs the pairs in LDS and writes
-//     them with coalesced stores to the tile's staging slot (kStageCap pairs),
-//     then stores the tile's count.  A tile with more than kStageCap selected
-//     values is left untouched and flagged.
+//     them with coalesced stores to the tile's staging slot (kStageCap
+//     8-byte (index, value) records), then stores the tile's count.  A tile
+//     with more than kStageCap selected values is left untouched and flagged.
 //   scan_kernel: one workgroup per chunk of kChunkTiles tiles, in ticket
 //     order: a scan of the chunk's tile counts and a decoupled look-back over
-//     chunk status words give every tile its output offset; it records where
-//     each output piece starts and processes the flagged tiles.  One ticket
-//     and one look-back per million values keep the cross-XCD round trips
-//     off the streaming pass.
+//     chunk status words give every tile its output offset; it records the
+//     tile where each move piece starts and processes the flagged tiles.
+//     One ticket and one look-back per million values keep the cross-XCD
+//     round trips off the streaming pass.
 //   move_kernel: a fixed grid moves the staged pairs to their final places in
-//     equal pieces of the output, whatever the clustering of the selection.
+//     equal pieces of the merged sequence of tiles and pairs, whatever the
+//     clustering of the selection.
 //   HBM traffic beyond the 12 bytes per value of the stream: 16 bytes per
 //   selected value (staged write and read) and 8 bytes per 1024 values.
 // Ticket schedule (variant 1): a single pass; tiles are drawn from a ticket
@@ -318,7 +319,6 @@ __device__ __forceinline__ void scatter_pairs(const LaunchArgs& a, int lane, con
 
 constexpr uint32_t kOverflow = 0x80000000u;
 constexpr int kMoveBatch = 8;      // independent copies in flight per thread
-constexpr int kMoveWindow = 2048;  // tile offsets staged in LDS for one piece
 
 // Draws the workgroup's ticket (thread 0) and rearms the counter when the
 // last ticket of the launch is drawn: every other workgroup of the launch has
@@ -334,8 +334,7 @@ __global__ __launch_bounds__(kStreamBlock) void stream_kernel(LaunchArgs a) {
     constexpr int WAVES = kStreamBlock / kWaveSize;
     static_assert(VEC * ROWS * kStreamBlock == kStreamTile, "tile size");
     __shared__ uint32_t s_wave_total[ROWS * WAVES];
-    __shared__ int32_t s_idx[kStageCap];
-    __shared__ float s_val[kStageCap];
+    __shared__ uint2 s_pair[kStageCap];  // (index, value bits)
 
     const int tid = threadIdx.x;
     const int lane = tid & (kWaveSize - 1);
@@ -360,8 +359,8 @@ __global__ __launch_bounds__(kStreamBlock) void stream_kernel(LaunchArgs a) {
 #pragma unroll
         for (int c = 0; c < VEC; ++c) {
             if (selected<VEC>(sel, r, c)) {
-                s_idx[pos] = static_cast<int32_t>(elem_index(t, r, tid, c));
-                s_val[pos] = t.v[r][c];
+                s_pair[pos] = make_uint2(static_cast<uint32_t>(elem_index(t, r, tid, c)),
+                                         __float_as_uint(t.v[r][c]));
                 ++pos;
             }
         }
@@ -369,8 +368,7 @@ __global__ __launch_bounds__(kStreamBlock) void stream_kernel(LaunchArgs a) {
     __syncthreads();
     const size_t slot = static_cast<size_t>(tile) * kStageCap;
     for (uint32_t j = tid; j < count; j += kStreamBlock) {
-        a.stage_idx[slot + j] = s_idx[j];
-        a.stage_val[slot + j] = s_val[j];
+        a.stage[slot + j] = s_pair[j];
     }
     if (tid == 0) a.tile_counts[tile] = count;
 }
@@ -398,8 +396,8 @@ __device__ void redo_tile(const LaunchArgs& a, uint32_t tile, int lane, uint32_t
 // Scan kernel: one workgroup per chunk of kChunkTiles tiles, in ticket order.
 // Scans the chunk's tile counts, finds the chunk's output offset by decoupled
 // look-back over chunk status words, publishes every tile's output offset
-// (bit 31: flagged tile), records for every output piece of kPieceSize pairs
-// the tile where it starts, and processes the chunk's flagged tiles.
+// (bit 31: flagged tile), records for every move piece the tile that holds
+// its first item, and processes the chunk's flagged tiles.
 template <int VEC, int ROWS>
 __global__ __launch_bounds__(kScanBlock) void scan_kernel(LaunchArgs a) {
     constexpr int WAVES = kScanBlock / kWaveSize;
@@ -472,9 +470,14 @@ __global__ __launch_bounds__(kScanBlock) void scan_kernel(LaunchArgs a) {
     for (int i = 0; i < PER_THREAD; ++i) {
         const uint32_t count = raw[i] & ~kOverflow;
         offs[i] = pos | (raw[i] & kOverflow);
-        // output pieces whose first position falls inside this tile
-        for (uint32_t piece = (pos + kPieceSize - 1) / kPieceSize; piece * kPieceSize < pos + count; ++piece)
-            a.piece_start[piece] = first_tile + i;
+        // The move piece whose first item falls among this tile's items: the
+        // tile's own item sits at tile + pos in the merged sequence and its
+        // count pairs follow it; count < kMoveSpan, so there is at most one.
+        if (first_tile + i < a.num_tiles) {
+            const uint64_t item = static_cast<uint64_t>(first_tile + i) + pos;
+            const uint64_t m = (item + kMoveSpan - 1) / kMoveSpan;
+            if (m * kMoveSpan < item + 1 + count) a.split_tile[m] = first_tile + i;
+        }
         if (raw[i] & kOverflow) {
             const uint32_t f = atomicAdd(&s_num_flagged, 1u);
             s_flagged[f] = first_tile + i;
@@ -497,52 +500,111 @@ __global__ __launch_bounds__(kScanBlock) void scan_kernel(LaunchArgs a) {
         redo_tile<VEC, ROWS * kStreamBlock / kWaveSize>(a, s_flagged[f], lane, s_flagged_base[f]);
 }
 
-// Smallest i in [0, n) with v[i] > x, or n.
-__device__ __forceinline__ uint32_t upper_bound(const uint32_t* v, uint32_t n, uint32_t x) {
-    uint32_t lo = 0, hi = n;
-    while (lo < hi) {
-        const uint32_t mid = (lo + hi) / 2;
-        if (v[mid] > x)
-            hi = mid;
-        else
-            lo = mid + 1;
-    }
-    return lo;
+// Number of output pairs before item x of the merged sequence, given the tile
+// t whose items contain x and its output offset off: the tile's own item sits
+// at t + off and its pairs follow it.
+__device__ __forceinline__ uint32_t pairs_before(uint64_t x, uint32_t t, uint32_t off) {
+    const uint64_t item = static_cast<uint64_t>(t) + off;
+    return off + (x > item ? static_cast<uint32_t>(x - item - 1) : 0u);
 }
 
-// Move kernel: a fixed grid splits the output [0, k) into pieces of
-// kPieceSize pairs, so the work per workgroup does not depend on where the
-// selected values cluster.  Every position of piece p lies in the tiles from
-// piece_start[p] to piece_start[p + 1] (both recorded by the scan kernel).
-// When that range fits in kMoveWindow tiles their output offsets go to LDS
-// and each position finds its tile there by binary search; a longer range
-// (a piece that spans a run of tiles with nothing selected) is searched in
-// the global offsets directly.  Each position copies its staged pair with a
+// Inclusive running maximum over v[0, n) (n <= kMoveSpan) by the whole
+// workgroup: each thread takes kMovePer consecutive entries.  Contains two
+// barriers; the caller synchronises before the entries are read.
+__device__ __forceinline__ void block_max_scan(uint16_t* v, uint32_t n, int tid, uint32_t* s_wave_max) {
+    constexpr int kMovePer = kMoveSpan / kMoveBlock;
+    const int lane = tid & (kWaveSize - 1);
+    const int wave = tid / kWaveSize;
+    const uint32_t first = static_cast<uint32_t>(tid) * kMovePer;
+    uint32_t run[kMovePer];
+    uint32_t m = 0;
+#pragma unroll
+    for (int i = 0; i < kMovePer; ++i) {
+        const uint32_t x = first + i < n ? v[first + i] : 0u;
+        m = x > m ? x : m;
+        run[i] = m;
+    }
+    uint32_t incl = m;  // inclusive maximum over the threads of the wavefront
+#pragma unroll
+    for (int off = 1; off < kWaveSize; off <<= 1) {
+        const uint32_t y = __shfl_up(incl, off, kWaveSize);
+        if (lane >= off) incl = y > incl ? y : incl;
+    }
+    uint32_t before = __shfl_up(incl, 1, kWaveSize);
+    if (lane == 0) before = 0;
+    if (lane == kWaveSize - 1) s_wave_max[wave] = incl;
+    __syncthreads();
+    for (int w = 0; w < wave; ++w) before = s_wave_max[w] > before ? s_wave_max[w] : before;
+#pragma unroll
+    for (int i = 0; i < kMovePer; ++i)
+        if (first + i < n) v[first + i] = static_cast<uint16_t>(run[i] > before ? run[i] : before);
+    __syncthreads();
+}
+
+// Move kernel: a fixed grid walks the merged sequence of tiles and output
+// pairs in pieces of kMoveSpan items, so every piece costs about the same
+// whatever the clustering of the selection: many pairs from few tiles, or few
+// pairs scattered over many tiles.  Piece m's items lie in the tiles from
+// split_tile[m] to split_tile[m + 1] (recorded by the scan kernel), at most
+// kMoveSpan + 1 of them, and it holds the output positions [lo, hi).  The
+// tiles' output offsets go to LDS; every tile that is the last of its offset
+// (so the one that owns the positions from that offset on) writes its window
+// index at its first position in the piece, and a running maximum fills in the
+// owner of every position.  Each position then copies its staged pair with a
 // coalesced write; positions of flagged tiles were written by the scan kernel.
 __global__ __launch_bounds__(kMoveBlock) void move_kernel(LaunchArgs a) {
-    __shared__ uint32_t s_off[kMoveWindow];
-    __shared__ uint32_t s_flag_bits[kMoveWindow / 32];
+    constexpr uint32_t kWindow = kMoveSpan + 1;
+    constexpr int WAVES = kMoveBlock / kWaveSize;
+    static_assert(kWindow <= 65536, "window indices fit in 16 bits");
+    __shared__ uint32_t s_off[kWindow];
+    __shared__ uint32_t s_flag_bits[(kWindow + 31) / 32];
+    __shared__ uint16_t s_owner[kMoveSpan];
+    __shared__ uint32_t s_wave_max[WAVES];
 
     const int tid = threadIdx.x;
     const int64_t k = a.count_out[0];
-    const uint32_t pieces = static_cast<uint32_t>((k + kPieceSize - 1) / kPieceSize);
-    for (uint32_t piece = blockIdx.x; piece < pieces; piece += gridDim.x) {
-        const uint32_t lo = piece * kPieceSize;
-        const uint32_t hi = static_cast<uint32_t>(k < int64_t(lo) + kPieceSize ? k : int64_t(lo) + kPieceSize);
-        const uint32_t t_begin = a.piece_start[piece];
-        const uint32_t t_end = piece + 1 < pieces ? a.piece_start[piece + 1] + 1 : a.num_tiles;
-        const uint32_t span = t_end - t_begin;
-        const bool windowed = span <= static_cast<uint32_t>(kMoveWindow);
-        if (windowed) {
-            if (tid < kMoveWindow / 32) s_flag_bits[tid] = 0u;
-            __syncthreads();
-            for (uint32_t i = tid; i < kMoveWindow; i += kMoveBlock) {
-                const uint32_t v = i < span ? a.tile_excl[t_begin + i] : static_cast<uint32_t>(k);
-                s_off[i] = v & ~kOverflow;
-                if (v & kOverflow) atomicOr(&s_flag_bits[i / 32], 1u << (i % 32));
-            }
-            __syncthreads();
+    if (blockIdx.x == 0 && tid == 0) {  // the scan kernel has finished both counts
+        a.host_count[0] = k;
+        a.host_count[1] = a.count_out[1];
+    }
+    if (k == 0) return;
+    const uint64_t total = static_cast<uint64_t>(a.num_tiles) + static_cast<uint64_t>(k);
+    const uint32_t pieces = static_cast<uint32_t>((total + kMoveSpan - 1) / kMoveSpan);
+    for (uint32_t m = blockIdx.x; m < pieces; m += gridDim.x) {
+        const uint32_t t0 = a.split_tile[m];
+        const uint32_t t1 = m + 1 < pieces ? a.split_tile[m + 1] : a.num_tiles - 1;
+        // t1 - t0 <= kMoveSpan by construction; the clamp only keeps LDS
+        // accesses inside the window
+        const uint32_t span = t1 - t0 + 1;
+        const uint32_t ntiles = span < kWindow ? span : kWindow;
+        for (uint32_t i = tid; i < (ntiles + 31) / 32; i += kMoveBlock) s_flag_bits[i] = 0u;
+        for (uint32_t i = tid; i < kMoveSpan; i += kMoveBlock) s_owner[i] = 0;
+        __syncthreads();
+        for (uint32_t i = tid; i < ntiles; i += kMoveBlock) {
+            const uint32_t v = a.tile_excl[t0 + i];
+            s_off[i] = v & ~kOverflow;
+            if (v & kOverflow) atomicOr(&s_flag_bits[i / 32], 1u << (i % 32));
         }
+        __syncthreads();
+        const uint64_t x0 = static_cast<uint64_t>(m) * kMoveSpan;
+        const uint64_t x1 = x0 + kMoveSpan < total ? x0 + kMoveSpan : total;
+        const uint32_t lo = pairs_before(x0, t0, s_off[0]);
+        uint32_t hi = x1 == total ? static_cast<uint32_t>(k) : pairs_before(x1, t1, s_off[ntiles - 1]);
+        // lo <= hi <= lo + kMoveSpan and hi <= k hold by construction; the
+        // clamps only keep the accesses below inside their buffers
+        hi = hi < lo ? lo : hi;
+        hi = hi - lo <= static_cast<uint32_t>(kMoveSpan) ? hi : lo + kMoveSpan;
+        hi = static_cast<int64_t>(hi) <= k ? hi : static_cast<uint32_t>(k);
+        hi = hi < lo ? lo : hi;
+        // Tile q owns the positions from its offset up to the next tile's;
+        // only the first tile of the window can start before lo.
+        for (uint32_t q = tid; q < ntiles; q += kMoveBlock) {
+            const uint32_t off = s_off[q];
+            const bool owner = q + 1 == ntiles || s_off[q + 1] != off;
+            if (owner && off < hi) s_owner[(off > lo ? off : lo) - lo] = static_cast<uint16_t>(q);
+        }
+        __syncthreads();
+        block_max_scan(s_owner, hi - lo, tid, s_wave_max);
         for (uint32_t j0 = lo + tid; j0 < hi; j0 += kMoveBlock * kMoveBatch) {
             size_t src[kMoveBatch];
             bool live[kMoveBatch];
@@ -552,46 +614,21 @@ __global__ __launch_bounds__(kMoveBlock) void move_kernel(LaunchArgs a) {
                 live[u] = j < hi;
                 src[u] = 0;
                 if (live[u]) {
-                    uint32_t tile, first;
-                    bool flagged;
-                    if (windowed) {
-                        const uint32_t q = upper_bound(s_off, kMoveWindow, j) - 1;
-                        tile = t_begin + q;
-                        first = s_off[q];
-                        flagged = (s_flag_bits[q / 32] >> (q % 32)) & 1u;
-                    } else {
-                        uint32_t l = t_begin, h = t_end;  // smallest t with offset > j
-                        while (l < h) {
-                            const uint32_t m = (l + h) / 2;
-                            if ((a.tile_excl[m] & ~kOverflow) > j)
-                                h = m;
-                            else
-                                l = m + 1;
-                        }
-                        tile = l - 1;
-                        const uint32_t v = a.tile_excl[tile];
-                        first = v & ~kOverflow;
-                        flagged = (v & kOverflow) != 0u;
-                    }
-                    live[u] = !flagged;
-                    src[u] = static_cast<size_t>(tile) * kStageCap + (j - first);
+                    const uint32_t q = s_owner[j - lo];
+                    live[u] = !((s_flag_bits[q / 32] >> (q % 32)) & 1u);
+                    src[u] = static_cast<size_t>(t0 + q) * kStageCap + (j - s_off[q]);
                 }
             }
-            int32_t idx[kMoveBatch];
-            float val[kMoveBatch];
+            uint2 pair[kMoveBatch];
 #pragma unroll
-            for (int u = 0; u < kMoveBatch; ++u) {
-                if (live[u]) {
-                    idx[u] = a.stage_idx[src[u]];
-                    val[u] = a.stage_val[src[u]];
-                }
-            }
+            for (int u = 0; u < kMoveBatch; ++u)
+                if (live[u]) pair[u] = a.stage[src[u]];
 #pragma unroll
             for (int u = 0; u < kMoveBatch; ++u) {
                 if (live[u]) {
                     const uint32_t j = j0 + u * kMoveBlock;
-                    a.out_idx[j] = idx[u];
-                    a.out_val[j] = val[u];
+                    a.out_idx[j] = static_cast<int32_t>(pair[u].x);
+                    a.out_val[j] = __uint_as_float(pair[u].y);
                 }
             }
         }
@@ -647,7 +684,11 @@ __global__ __launch_bounds__(kTicketBlock) void ticket_kernel(LaunchArgs a) {
         }
         if (lane == 0) {
             s_exclusive = excl;
-            if (tile == a.num_tiles - 1) a.count_out[0] = static_cast<int64_t>(excl) + count;
+            if (tile == a.num_tiles - 1) {
+                a.count_out[0] = static_cast<int64_t>(excl) + count;
+                a.host_count[0] = static_cast<int64_t>(excl) + count;
+                a.host_count[1] = 0;
+            }
         }
     }
     __syncthreads();
