@@ -26,6 +26,7 @@ struct micro_ctx {
     // staged schedule: tile counts, staged pairs, chunk look-back words
     uint32_t* d_tile_counts = nullptr;
     uint32_t* d_tile_excl = nullptr;
+    uint32_t* d_flagged_list = nullptr;
     uint32_t* d_split_tile = nullptr;
     int64_t split_capacity = 0;
     uint2* d_stage = nullptr;                // (index, value bits) pairs
@@ -135,7 +136,7 @@ void release(micro_ctx* ctx) {
     if (ctx->device >= 0) (void)hipStreamSynchronize(ctx->stream);
     for (hipEvent_t ev : ctx->ev)
         if (ev) (void)hipEventDestroy(ev);
-    void* device_buffers[] = {ctx->d_tile_counts, ctx->d_tile_excl, ctx->d_split_tile, ctx->d_stage,
+    void* device_buffers[] = {ctx->d_tile_counts, ctx->d_tile_excl, ctx->d_flagged_list, ctx->d_split_tile, ctx->d_stage,
                               ctx->d_chunk_status, ctx->d_status, ctx->d_tickets,
                               ctx->d_count};
     for (void* p : device_buffers)
@@ -245,6 +246,7 @@ micro_status micro_sparsify_init(micro_ctx** out, int64_t n_total, void* hip_str
         const size_t stage = static_cast<size_t>(ctx->tile_capacity) * micro::kStageCap;
         ok = hipMalloc(&ctx->d_tile_counts, sizeof(uint32_t) * ctx->tile_capacity) == hipSuccess &&
              hipMalloc(&ctx->d_tile_excl, sizeof(uint32_t) * ctx->tile_capacity) == hipSuccess &&
+             hipMalloc(&ctx->d_flagged_list, sizeof(uint32_t) * ctx->tile_capacity) == hipSuccess &&
              hipMalloc(&ctx->d_split_tile, sizeof(uint32_t) * ctx->split_capacity) == hipSuccess &&
              hipMalloc(&ctx->d_stage, sizeof(uint2) * stage) == hipSuccess &&
              hipMalloc(&ctx->d_chunk_status, sizeof(uint64_t) * ctx->chunk_capacity) == hipSuccess;
@@ -352,6 +354,7 @@ micro_status micro_sparsify_step(micro_ctx* ctx, const float* grad, float* resid
     a.host_count = ctx->h_count_dev;
     a.tile_counts = ctx->d_tile_counts;
     a.tile_excl = ctx->d_tile_excl;
+    a.flagged_list = ctx->d_flagged_list;
     a.split_tile = ctx->d_split_tile;
     {
         // at most ceil((tiles + P) / kMoveSpan) move pieces, whatever k is

@@ -45,11 +45,12 @@ struct LaunchArgs {
     float theta_f;          // smallest binary32 >= theta
     uint32_t epoch;         // 1 .. kMaxEpoch
     uint32_t num_tiles;     // tiles covering [base, end)
-    int64_t* count_out;     // device: [0] selected count, [1] flagged tiles (redone by the scan kernel)
+    int64_t* count_out;     // device: [0] selected count, [1] flagged tiles (redone by the move kernel)
     int64_t* host_count;    // mapped pinned host memory: the final count_out, stored by the last kernel
     // staged schedule
     uint32_t* tile_counts;  // num_tiles counts (bit 31: tile left to the scan kernel)
     uint32_t* tile_excl;    // num_tiles output offsets (bit 31: flagged tile)
+    uint32_t* flagged_list; // count_out[1] flagged tiles, in no particular order
     uint32_t* split_tile;   // >= ceil((num_tiles + P) / kMoveSpan) tiles holding each piece's first item
     uint32_t move_blocks;   // workgroups of the move kernel
     uint2* stage;           // num_tiles * kStageCap staged (index, value bits) pairs

@@ -30,12 +30,13 @@
 //   scan_kernel: one workgroup per chunk of kChunkTiles tiles, in ticket
 //     order: a scan of the chunk's tile counts and a decoupled look-back over
 //     chunk status words give every tile its output offset; it records the
-//     tile where each move piece starts and processes the flagged tiles.
+//     tile where each move piece starts and lists the flagged tiles.
 //     One ticket and one look-back per million values keep the cross-XCD
 //     round trips off the streaming pass.
-//   move_kernel: a fixed grid moves the staged pairs to their final places in
-//     equal pieces of the merged sequence of tiles and pairs, whatever the
-//     clustering of the selection.
+//   move_kernel: a fixed grid redoes the flagged tiles (one wavefront each)
+//     and moves the staged pairs to their final places in equal pieces of the
+//     merged sequence of tiles and pairs, whatever the clustering of the
+//     selection.
 //   HBM traffic beyond the 12 bytes per value of the stream: 16 bytes per
 //   selected value (staged write and read) and 8 bytes per 1024 values.
 // Ticket schedule (variant 1): a single pass; tiles are drawn from a ticket
@@ -125,15 +126,16 @@ __device__ __forceinline__ int64_t elem_index(const Tile<VEC, ROWS, LANES>& t, i
     return t.base + static_cast<int64_t>(r * LANES + lane) * VEC + c;
 }
 
-// Issues every load of tile number `tile`.  Interior tiles use dwordx4
-// (VEC == 4, 16-byte aligned by the choice of base) or dword loads,
+// Issues every load of the tile whose first value has global index `base`
+// (a.base plus a multiple of the tile size).  Interior tiles use dwordx4
+// (VEC == 4, 16-byte aligned by the choice of a.base) or dword loads,
 // non-temporal when NT (each value is read once); tiles that cross start or
 // end load element by element inside [start, end) and read 0 elsewhere.
 template <int VEC, int ROWS, int LANES, bool NT>
-__device__ __forceinline__ void load_tile(const LaunchArgs& a, uint32_t tile, int lane,
+__device__ __forceinline__ void load_tile(const LaunchArgs& a, int64_t base, int lane,
                                           Tile<VEC, ROWS, LANES>& t) {
     using T = Tile<VEC, ROWS, LANES>;
-    t.base = a.base + static_cast<int64_t>(tile) * T::kElems;
+    t.base = base;
     t.interior = t.base >= a.start && t.base + T::kElems <= a.end;
     if (t.interior) {
         if constexpr (VEC == 4) {
@@ -343,12 +345,12 @@ __global__ __launch_bounds__(kStreamBlock) void stream_kernel(LaunchArgs a) {
 
     Tile<VEC, ROWS, kStreamBlock> t;
     uint32_t lane_rank[ROWS], row_count[ROWS], row_base[ROWS];
-    load_tile<VEC, ROWS, kStreamBlock, true>(a, tile, tid, t);
+    load_tile<VEC, ROWS, kStreamBlock, true>(a, a.base + static_cast<int64_t>(tile) * kStreamTile, tid, t);
     const uint32_t sel = compute_tile(a, tid, t);
     wave_ranks<VEC, ROWS>(sel, lane_rank, row_count);
     const uint32_t count = tile_ranks<ROWS, WAVES>(row_count, lane, wave, s_wave_total, row_base);
     if (tile == 0 && tid == 0) a.count_out[1] = 0;  // the scan kernel adds the flagged tiles
-    if (count > kStageCap) {  // uniform: left to scan_kernel, residual untouched
+    if (count > kStageCap) {  // uniform: left to the move kernel, residual untouched
         if (tid == 0) a.tile_counts[tile] = count | kOverflow;
         return;
     }
@@ -374,39 +376,47 @@ __global__ __launch_bounds__(kStreamBlock) void stream_kernel(LaunchArgs a) {
 }
 
 // Full processing of one flagged tile by one wavefront with its pairs from
-// position out_base on.  The wavefront walks the tile in the stream kernel's
-// value order: 1024 values as ROWS rows of 64 lanes.
-template <int VEC, int ROWS>
+// position out_base on: the tile's values in index order, 256 at a time (one
+// part in registers keeps the move kernel's register budget).
+template <int VEC>
 __device__ void redo_tile(const LaunchArgs& a, uint32_t tile, int lane, uint32_t out_base) {
-    Tile<VEC, ROWS, kWaveSize> t;
-    uint32_t lane_rank[ROWS], row_count[ROWS], row_base[ROWS];
-    load_tile<VEC, ROWS, kWaveSize, false>(a, tile, lane, t);
-    const uint32_t sel = compute_tile(a, lane, t);
-    wave_ranks<VEC, ROWS>(sel, lane_rank, row_count);
-    uint32_t run = 0;
+    constexpr int ROWS = 4 / VEC;
+    using T = Tile<VEC, ROWS, kWaveSize>;
+    static_assert(kStreamTile % T::kElems == 0, "whole parts");
+    const int64_t tile_base = a.base + static_cast<int64_t>(tile) * kStreamTile;
+    uint32_t run = out_base;
+#pragma unroll 1
+    for (int part = 0; part < kStreamTile / T::kElems; ++part) {
+        T t;
+        uint32_t lane_rank[ROWS], row_count[ROWS], row_base[ROWS];
+        load_tile<VEC, ROWS, kWaveSize, false>(a, tile_base + part * T::kElems, lane, t);
+        const uint32_t sel = compute_tile(a, lane, t);
+        wave_ranks<VEC, ROWS>(sel, lane_rank, row_count);
+        uint32_t sub = 0;
 #pragma unroll
-    for (int r = 0; r < ROWS; ++r) {
-        row_base[r] = run;
-        run += row_count[r];
+        for (int r = 0; r < ROWS; ++r) {
+            row_base[r] = sub;
+            sub += row_count[r];
+        }
+        store_residual<VEC, ROWS, kWaveSize, false>(a, lane, t, sel);
+        scatter_pairs(a, lane, t, sel, run, row_base, lane_rank);
+        run += sub;
     }
-    store_residual<VEC, ROWS, kWaveSize, false>(a, lane, t, sel);
-    scatter_pairs(a, lane, t, sel, out_base, row_base, lane_rank);
 }
 
 // Scan kernel: one workgroup per chunk of kChunkTiles tiles, in ticket order.
 // Scans the chunk's tile counts, finds the chunk's output offset by decoupled
 // look-back over chunk status words, publishes every tile's output offset
 // (bit 31: flagged tile), records for every move piece the tile that holds
-// its first item, and processes the chunk's flagged tiles.
-template <int VEC, int ROWS>
+// its first item, and appends the chunk's flagged tiles to the list that the
+// move kernel redoes.
 __global__ __launch_bounds__(kScanBlock) void scan_kernel(LaunchArgs a) {
     constexpr int WAVES = kScanBlock / kWaveSize;
     constexpr int PER_THREAD = kChunkTiles / kScanBlock;
-    static_assert(PER_THREAD == 4, "one uint4 of counts per thread");
-    __shared__ uint32_t s_chunk, s_exclusive, s_num_flagged;
+    static_assert(PER_THREAD % 4 == 0, "whole uint4s of counts per thread");
+    __shared__ uint32_t s_chunk, s_exclusive, s_num_flagged, s_list_base;
     __shared__ uint32_t s_wave_total[WAVES];
     __shared__ uint32_t s_flagged[kChunkTiles];
-    __shared__ uint32_t s_flagged_base[kChunkTiles];
 
     const int tid = threadIdx.x;
     const int lane = tid & (kWaveSize - 1);
@@ -422,11 +432,14 @@ __global__ __launch_bounds__(kScanBlock) void scan_kernel(LaunchArgs a) {
 
     uint32_t raw[PER_THREAD];
     if (first_tile + PER_THREAD <= a.num_tiles) {
-        const uint4 v = *reinterpret_cast<const uint4*>(a.tile_counts + first_tile);
-        raw[0] = v.x;
-        raw[1] = v.y;
-        raw[2] = v.z;
-        raw[3] = v.w;
+#pragma unroll
+        for (int i = 0; i < PER_THREAD; i += 4) {
+            const uint4 v = *reinterpret_cast<const uint4*>(a.tile_counts + first_tile + i);
+            raw[i] = v.x;
+            raw[i + 1] = v.y;
+            raw[i + 2] = v.z;
+            raw[i + 3] = v.w;
+        }
     } else {
 #pragma unroll
         for (int i = 0; i < PER_THREAD; ++i) raw[i] = first_tile + i < a.num_tiles ? a.tile_counts[first_tile + i] : 0u;
@@ -478,15 +491,14 @@ __global__ __launch_bounds__(kScanBlock) void scan_kernel(LaunchArgs a) {
             const uint64_t m = (item + kMoveSpan - 1) / kMoveSpan;
             if (m * kMoveSpan < item + 1 + count) a.split_tile[m] = first_tile + i;
         }
-        if (raw[i] & kOverflow) {
-            const uint32_t f = atomicAdd(&s_num_flagged, 1u);
-            s_flagged[f] = first_tile + i;
-            s_flagged_base[f] = pos;
-        }
+        if (raw[i] & kOverflow) s_flagged[atomicAdd(&s_num_flagged, 1u)] = first_tile + i;
         pos += count;
     }
     if (first_tile + PER_THREAD <= a.num_tiles) {
-        *reinterpret_cast<uint4*>(a.tile_excl + first_tile) = make_uint4(offs[0], offs[1], offs[2], offs[3]);
+#pragma unroll
+        for (int i = 0; i < PER_THREAD; i += 4)
+            *reinterpret_cast<uint4*>(a.tile_excl + first_tile + i) =
+                make_uint4(offs[i], offs[i + 1], offs[i + 2], offs[i + 3]);
     } else {
 #pragma unroll
         for (int i = 0; i < PER_THREAD; ++i)
@@ -494,10 +506,12 @@ __global__ __launch_bounds__(kScanBlock) void scan_kernel(LaunchArgs a) {
     }
     __syncthreads();
     const uint32_t flagged = s_num_flagged;
-    if (tid == 0 && flagged != 0)
-        atomicAdd(reinterpret_cast<unsigned long long*>(&a.count_out[1]), static_cast<unsigned long long>(flagged));
-    for (uint32_t f = wave; f < flagged; f += WAVES)
-        redo_tile<VEC, ROWS * kStreamBlock / kWaveSize>(a, s_flagged[f], lane, s_flagged_base[f]);
+    if (flagged == 0) return;  // uniform
+    if (tid == 0)
+        s_list_base = static_cast<uint32_t>(atomicAdd(reinterpret_cast<unsigned long long*>(&a.count_out[1]),
+                                                      static_cast<unsigned long long>(flagged)));
+    __syncthreads();
+    for (uint32_t f = tid; f < flagged; f += kScanBlock) a.flagged_list[s_list_base + f] = s_flagged[f];
 }
 
 // Number of output pairs before item x of the merged sequence, given the tile
@@ -551,7 +565,10 @@ __device__ __forceinline__ void block_max_scan(uint16_t* v, uint32_t n, int tid,
 // (so the one that owns the positions from that offset on) writes its window
 // index at its first position in the piece, and a running maximum fills in the
 // owner of every position.  Each position then copies its staged pair with a
-// coalesced write; positions of flagged tiles were written by the scan kernel.
+// coalesced write.  Before its pieces, every workgroup redoes its share of the
+// flagged tiles, so a dense region of the partition costs the whole grid a
+// second pass over it rather than one workgroup a serial one.
+template <int VEC>
 __global__ __launch_bounds__(kMoveBlock) void move_kernel(LaunchArgs a) {
     constexpr uint32_t kWindow = kMoveSpan + 1;
     constexpr int WAVES = kMoveBlock / kWaveSize;
@@ -568,6 +585,14 @@ __global__ __launch_bounds__(kMoveBlock) void move_kernel(LaunchArgs a) {
         a.host_count[1] = a.count_out[1];
     }
     if (k == 0) return;
+    // Flagged tiles first, one wavefront each over the whole grid: the
+    // wavefront recomputes the tile and writes its pairs and residual.
+    const uint32_t flagged = static_cast<uint32_t>(a.count_out[1]);
+    const int lane = tid & (kWaveSize - 1);
+    for (uint32_t f = blockIdx.x * WAVES + tid / kWaveSize; f < flagged; f += gridDim.x * WAVES) {
+        const uint32_t tile = a.flagged_list[f];
+        redo_tile<VEC>(a, tile, lane, a.tile_excl[tile] & ~kOverflow);
+    }
     const uint64_t total = static_cast<uint64_t>(a.num_tiles) + static_cast<uint64_t>(k);
     const uint32_t pieces = static_cast<uint32_t>((total + kMoveSpan - 1) / kMoveSpan);
     for (uint32_t m = blockIdx.x; m < pieces; m += gridDim.x) {
@@ -667,7 +692,7 @@ __global__ __launch_bounds__(kTicketBlock) void ticket_kernel(LaunchArgs a) {
 
     Tile<VEC, ROWS, kTicketBlock> t;
     uint32_t lane_rank[ROWS], row_count[ROWS], row_base[ROWS];
-    load_tile<VEC, ROWS, kTicketBlock, false>(a, tile, tid, t);
+    load_tile<VEC, ROWS, kTicketBlock, false>(a, a.base + static_cast<int64_t>(tile) * kTicketTile, tid, t);
     const uint32_t sel = compute_tile(a, tid, t);
     store_residual<VEC, ROWS, kTicketBlock, false>(a, tid, t, sel);
     wave_ranks<VEC, ROWS>(sel, lane_rank, row_count);
@@ -707,12 +732,13 @@ hipError_t launch_staged(const LaunchArgs& args, bool vec4, hipStream_t stream) 
     const dim3 grid_stream(args.num_tiles), grid_scan(args.num_chunks), grid_move(args.move_blocks);
     if (vec4) {
         hipLaunchKernelGGL((stream_kernel<4, 1>), grid_stream, dim3(kStreamBlock), 0, stream, args);
-        hipLaunchKernelGGL((scan_kernel<4, 1>), grid_scan, dim3(kScanBlock), 0, stream, args);
+        hipLaunchKernelGGL(scan_kernel, grid_scan, dim3(kScanBlock), 0, stream, args);
+        hipLaunchKernelGGL(move_kernel<4>, grid_move, dim3(kMoveBlock), 0, stream, args);
     } else {
         hipLaunchKernelGGL((stream_kernel<1, 4>), grid_stream, dim3(kStreamBlock), 0, stream, args);
-        hipLaunchKernelGGL((scan_kernel<1, 4>), grid_scan, dim3(kScanBlock), 0, stream, args);
+        hipLaunchKernelGGL(scan_kernel, grid_scan, dim3(kScanBlock), 0, stream, args);
+        hipLaunchKernelGGL(move_kernel<1>, grid_move, dim3(kMoveBlock), 0, stream, args);
     }
-    hipLaunchKernelGGL(move_kernel, grid_move, dim3(kMoveBlock), 0, stream, args);
     return hipGetLastError();
 }
 

@@ -159,11 +159,12 @@ def test_subnormals_are_not_flushed(variant):
 
 
 @pytest.mark.parametrize("phase_shift", [0, 2])
-def test_dense_tiles_redone_by_gather_mixed_with_staged_ones(phase_shift):
+def test_dense_tiles_redone_by_move_kernel_mixed_with_staged_ones(phase_shift):
     """Tiles with more selected values than their staging slot holds (256 of
-    1024) are left to the gather pass, which processes them straight into the
-    output; they interleave with staged tiles and with each other, including
-    at the ragged ends and across gather chunks (a million values each)."""
+    1024) are listed by the scan kernel and redone by the move kernel's
+    wavefronts straight into the output; they interleave with staged tiles
+    and with each other, including at the ragged ends and across scan chunks
+    (a million values each); theta = 1e-30 flags every tile."""
     rng = np.random.default_rng(77)
     N = 3 * 1_048_576 + 1234
     g = rng.standard_normal(N).astype(np.float32)
