@@ -54,6 +54,28 @@ def lib():
                                         ctypes.POINTER(ctypes.c_double),
                                         ctypes.c_void_p, ctypes.c_void_p, i64p]
         L.micro_oracle_step.restype = ctypes.c_int
+        L.micro_oracle_cycle.argtypes = [ctypes.c_int64, ctypes.c_int32, ctypes.c_int32]
+        L.micro_oracle_cycle.restype = ctypes.c_int32
+        L.micro_oracle_ef_step.argtypes = [ctypes.c_void_p, ctypes.c_void_p,
+                                           ctypes.c_int64, ctypes.c_int64,
+                                           ctypes.c_int32, ctypes.c_int32,
+                                           ctypes.c_double, ctypes.POINTER(Rule),
+                                           ctypes.POINTER(ctypes.c_double),
+                                           ctypes.c_void_p, ctypes.c_void_p, i64p,
+                                           ctypes.POINTER(ctypes.c_int32)]
+        L.micro_oracle_ef_step.restype = ctypes.c_int
+        L.micro_oracle_accumulate.argtypes = [ctypes.c_void_p, ctypes.c_void_p,
+                                              ctypes.c_int64, ctypes.c_void_p]
+        L.micro_oracle_accumulate.restype = None
+        L.micro_oracle_gather.argtypes = [ctypes.c_void_p, ctypes.c_void_p,
+                                          ctypes.c_int64, ctypes.c_void_p]
+        L.micro_oracle_gather.restype = None
+        L.micro_oracle_zero.argtypes = [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int64]
+        L.micro_oracle_zero.restype = None
+        L.micro_oracle_update.argtypes = [ctypes.c_void_p, ctypes.c_void_p,
+                                          ctypes.c_void_p, ctypes.c_int64,
+                                          ctypes.c_int32]
+        L.micro_oracle_update.restype = ctypes.c_int
         _lib = L
     return _lib
 
@@ -142,3 +164,92 @@ def step(grad, residual, rank, world, density, theta, rule=None, out=None):
     if rc != 0:
         raise ValueError("invalid oracle step arguments")
     return out_idx[:k.value], out_val[:k.value], k.value, th.value
+
+
+def cycle(t, worker, world):
+    """Algorithm 1's partition number of `worker` at iteration t."""
+    c = lib().micro_oracle_cycle(int(t), int(worker), int(world))
+    if c < 0:
+        raise ValueError("invalid cycle arguments")
+    return c
+
+
+def ef_step(grad, residual, t, worker, world, density, theta, rule=None, out=None):
+    """Algorithm 1 for one worker over the whole vector: every element
+    accumulates, only the partition of the worker's cycle is searched.
+    residual is updated in place.  Returns (idx, val, k, theta_next, cycle)."""
+    _f32(grad, "grad")
+    _f32(residual, "residual")
+    n_total = grad.size
+    if residual.size != n_total:
+        raise ValueError("grad and residual lengths differ")
+    _, length = partition(n_total, cycle(t, worker, world), world)
+    if out is None:
+        out = (np.empty(max(length, 1), np.int32), np.empty(max(length, 1), np.float32))
+    out_idx, out_val = out
+    if out_idx.size < length or out_val.size < length:
+        raise ValueError("output buffers smaller than the partition")
+    r = rule if rule is not None else default_rule()
+    th = ctypes.c_double(float(theta))
+    k = ctypes.c_int64()
+    c = ctypes.c_int32()
+    rc = lib().micro_oracle_ef_step(grad.ctypes.data, residual.ctypes.data, n_total,
+                                    int(t), worker, world, float(density), ctypes.byref(r),
+                                    ctypes.byref(th), out_idx.ctypes.data,
+                                    out_val.ctypes.data, ctypes.byref(k), ctypes.byref(c))
+    if rc != 0:
+        raise ValueError("invalid oracle EF step arguments")
+    return out_idx[:k.value], out_val[:k.value], k.value, th.value, c.value
+
+
+def _i32(a, name):
+    if not (isinstance(a, np.ndarray) and a.dtype == np.int32 and a.flags.c_contiguous):
+        raise TypeError(f"{name} must be a C-contiguous int32 numpy array")
+    return a
+
+
+def accumulate(grad, residual):
+    """Algorithm 1's accumulation: returns grad + residual (binary32)."""
+    _f32(grad, "grad")
+    _f32(residual, "residual")
+    if grad.size != residual.size:
+        raise ValueError("grad and residual lengths differ")
+    acc = np.empty(grad.size, np.float32)
+    lib().micro_oracle_accumulate(grad.ctypes.data, residual.ctypes.data, grad.size,
+                                  acc.ctypes.data)
+    return acc
+
+
+def _check_idx(idx, n):
+    _i32(idx, "idx")
+    if idx.size and (idx.min() < 0 or idx.max() >= n):
+        raise ValueError("index outside the vector")
+
+
+def gather(acc, idx):
+    """Algorithm 1's gathering: returns acc[idx]."""
+    _f32(acc, "acc")
+    _check_idx(idx, acc.size)
+    out = np.empty(max(idx.size, 1), np.float32)
+    lib().micro_oracle_gather(acc.ctypes.data, idx.ctypes.data, idx.size, out.ctypes.data)
+    return out[:idx.size].copy()
+
+
+def zero(acc, idx):
+    """Algorithm 1's reset: acc[idx] = +0 in place."""
+    _f32(acc, "acc")
+    _check_idx(idx, acc.size)
+    lib().micro_oracle_zero(acc.ctypes.data, idx.ctypes.data, idx.size)
+
+
+def update(x, idx, sums, world):
+    """Algorithm 1's model update: x[idx] -= sums / world in place (indices
+    distinct)."""
+    _f32(x, "x")
+    _f32(sums, "sums")
+    _check_idx(idx, x.size)
+    if sums.size != idx.size:
+        raise ValueError("sums and idx lengths differ")
+    if lib().micro_oracle_update(x.ctypes.data, idx.ctypes.data, sums.ctypes.data,
+                                 idx.size, int(world)) != 0:
+        raise ValueError("world must be >= 1")

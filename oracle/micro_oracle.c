@@ -113,3 +113,92 @@ int micro_oracle_step(const float *grad, float *residual, int64_t n_total,
     *k = selected;
     return 0;
 }
+
+/* Algorithm 1: the partition number advances by one for every worker at
+ * every iteration, so the n workers always hold n different partitions and
+ * each worker's search range covers the whole vector in n iterations. */
+int32_t micro_oracle_cycle(int64_t t, int32_t worker, int32_t world)
+{
+    if (t < 0 || world < 1 || worker < 0 || worker >= world)
+        return -1;
+    int64_t n = (int64_t)world;
+    return (int32_t)((t % n + (int64_t)worker) % n);
+}
+
+/* Algorithm 1 for one worker, element by element in index order: every
+ * element accumulates its new gradient into the local error; only elements of
+ * the worker's partition of this iteration are candidates for selection; a
+ * selected element's accumulated value is contributed and its local error
+ * restarts from zero, every other element carries its accumulated value. */
+int micro_oracle_ef_step(const float *grad, float *residual, int64_t n_total,
+                         int64_t t, int32_t worker, int32_t world,
+                         double density, const micro_oracle_rule *rule,
+                         double *theta, int32_t *out_idx, float *out_val,
+                         int64_t *k, int32_t *cycle)
+{
+    int64_t start = 0, len = 0;
+    if (grad == NULL || residual == NULL || rule == NULL || theta == NULL ||
+        k == NULL || cycle == NULL)
+        return -1;
+    int32_t part = micro_oracle_cycle(t, worker, world);
+    if (part < 0)
+        return -1;
+    if (micro_oracle_partition(n_total, part, world, &start, &len) != 0)
+        return -1;
+    if (!(density > 0.0 && density <= 1.0))
+        return -1;
+    if (!(*theta > 0.0) || isinf(*theta))
+        return -1;
+    if (len > 0 && (out_idx == NULL || out_val == NULL))
+        return -1;
+    int64_t selected = 0;
+    for (int64_t j = 0; j < n_total; ++j) {
+        float acc = grad[j] + residual[j];
+        int inside = j >= start && j < start + len;
+        if (inside && (double)fabsf(acc) >= *theta) {
+            out_idx[selected] = (int32_t)j;
+            out_val[selected] = acc;
+            selected = selected + 1;
+            residual[j] = 0.0f;
+        } else {
+            residual[j] = acc;
+        }
+    }
+    *theta = micro_oracle_estimate(rule, density, len, selected, *theta);
+    *k = selected;
+    *cycle = part;
+    return 0;
+}
+
+void micro_oracle_accumulate(const float *grad, const float *residual,
+                             int64_t n, float *acc)
+{
+    for (int64_t j = 0; j < n; ++j)
+        acc[j] = grad[j] + residual[j];
+}
+
+void micro_oracle_gather(const float *acc, const int32_t *idx, int64_t m,
+                         float *out)
+{
+    for (int64_t q = 0; q < m; ++q)
+        out[q] = acc[idx[q]];
+}
+
+void micro_oracle_zero(float *acc, const int32_t *idx, int64_t m)
+{
+    for (int64_t q = 0; q < m; ++q)
+        acc[idx[q]] = 0.0f;
+}
+
+int micro_oracle_update(float *x, const int32_t *idx, const float *sums,
+                        int64_t m, int32_t world)
+{
+    if (world < 1)
+        return -1;
+    float n = (float)world;
+    for (int64_t q = 0; q < m; ++q) {
+        float average = sums[q] / n;
+        x[idx[q]] = x[idx[q]] - average;
+    }
+    return 0;
+}

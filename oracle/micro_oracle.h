@@ -29,6 +29,22 @@
  *                           beta, lo, hi and alpha are "parity unpinned"
  *                           against the paper, which prints none.
  *   micro_oracle_step       one worker, one iteration: the three above.
+ *   micro_oracle_cycle      Algorithm 1 (cyclic assignment of partitions to
+ *                           workers) and Sec. 4.1 (the assignment rotates at
+ *                           the start of every iteration).
+ *   micro_oracle_ef_step    Algorithm 1 for one worker over the whole
+ *                           flattened vector: the error-feedback accumulation
+ *                           of every element, selection only in the partition
+ *                           of the worker's cycle, reset of the selected and
+ *                           carry of every other element, then Estimate.
+ *   micro_oracle_accumulate Algorithm 1, the accumulation of the new gradient
+ *                           into the local error, for every element.
+ *   micro_oracle_gather     Algorithm 1, the gathering of the accumulated
+ *                           values at the globally selected indices.
+ *   micro_oracle_zero       Algorithm 1, the reset of the accumulated values
+ *                           at the globally selected indices.
+ *   micro_oracle_update     Algorithm 1 and Sec. 4.4, the model update with the
+ *                           averaged (all-reduced sum divided by n) values.
  *
  * Precision: the accumulation is one binary32 addition (round to nearest even,
  * no fused multiply-add, subnormals kept); the threshold test compares the
@@ -88,6 +104,46 @@ int micro_oracle_step(const float *grad, float *residual, int64_t n_total,
                       int32_t rank, int32_t world, double density,
                       const micro_oracle_rule *rule, double *theta,
                       int32_t *out_idx, float *out_val, int64_t *k);
+
+/* Algorithm 1: the partition number that worker `worker` of `world` searches
+ * at iteration t, ((t mod n) + i) mod n.  Over any n consecutive iterations a
+ * worker visits every partition once, and at every iteration the workers'
+ * partitions are all different (Sec. 4.1).  Returns -1 for t < 0, world < 1 or
+ * worker outside [0, world). */
+int32_t micro_oracle_cycle(int64_t t, int32_t worker, int32_t world);
+
+/* Algorithm 1 for worker `worker` at iteration t, over the whole vector of
+ * n_total values: for every j, acc = grad[j] + residual[j] (one binary32
+ * addition); j inside the partition of the worker's cycle with |acc| >= theta
+ * is selected (pair appended, residual[j] = +0), every other j keeps
+ * residual[j] = acc.  Then theta = Estimate over the partition's length.
+ * *cycle receives the partition number.  out_idx and out_val must hold the
+ * partition's length.  Returns 0, or -1 on invalid arguments (nothing
+ * written). */
+int micro_oracle_ef_step(const float *grad, float *residual, int64_t n_total,
+                         int64_t t, int32_t worker, int32_t world,
+                         double density, const micro_oracle_rule *rule,
+                         double *theta, int32_t *out_idx, float *out_val,
+                         int64_t *k, int32_t *cycle);
+
+/* Algorithm 1: acc[j] = grad[j] + residual[j] for j in [0, n) (binary32). */
+void micro_oracle_accumulate(const float *grad, const float *residual,
+                             int64_t n, float *acc);
+
+/* Algorithm 1: out[q] = acc[idx[q]] for q in [0, m). */
+void micro_oracle_gather(const float *acc, const int32_t *idx, int64_t m,
+                         float *out);
+
+/* Algorithm 1: acc[idx[q]] = +0 for q in [0, m). */
+void micro_oracle_zero(float *acc, const int32_t *idx, int64_t m);
+
+/* Algorithm 1 and Sec. 4.4: x[idx[q]] = x[idx[q]] - sums[q] / n for q in
+ * [0, m): the all-reduced sum is averaged over the n workers (one binary32
+ * division by n) and subtracted (one binary32 subtraction); the learning rate
+ * is already inside the gradients.  The indices must be distinct.  Returns 0,
+ * or -1 for world < 1. */
+int micro_oracle_update(float *x, const int32_t *idx, const float *sums,
+                        int64_t m, int32_t world);
 
 #ifdef __cplusplus
 }
