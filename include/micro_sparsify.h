@@ -135,6 +135,76 @@ MICRO_API micro_status micro_sparsify_step(micro_ctx *ctx, const float *grad,
                                  double density, double *theta,
                                  int32_t *out_idx, float *out_val, int64_t *k);
 
+/* Algorithm 1 (cyclic assignment of partitions; Sec. 4.1): the partition
+ * number that worker `worker` of `world` searches at iteration t,
+ * ((t mod n) + worker) mod n (pure host arithmetic).  Returns MICRO_EINVAL
+ * for NULL output, t < 0, world < 1 or worker outside [0, world). */
+MICRO_API micro_status micro_cycle(int64_t t, int32_t worker, int32_t world, int32_t *cycle);
+
+/*
+ * Algorithm 1 for worker `worker` of `world` at iteration t over the whole
+ * vector (the error-feedback accumulation of every element, then selection in
+ * the worker's partition of this iteration only):
+ *   c = micro_cycle(t, worker, world), [s, e) = partition c (Sec. 4.1);
+ *   for every j in [0, n_total): acc = grad[j] + residual[j] (one binary32
+ *   addition); j in [s, e) with |acc| >= theta is selected (its pair goes to
+ *   the outputs, residual[j] = +0); every other j gets residual[j] = acc.
+ *   theta <- Estimate(density * (e - s), k, theta) (Sec. 4.3).
+ *   grad      device, n_total fp32, read only, all of it.
+ *   residual  device, n_total fp32, in/out, all of it.
+ *   out_idx, out_val, k, theta, density: as micro_sparsify_step, with
+ *             P = e - s of partition c.
+ *   cycle     host out (may be NULL): c.
+ * grad[0, n), residual[0, n), out_idx[0, P) and out_val[0, P) must not
+ * overlap.  Synchronous; errors as micro_sparsify_step.  A partition that is
+ * empty (n_total < world) still accumulates every element, with k = 0 and
+ * theta unchanged.
+ */
+MICRO_API micro_status micro_ef_step(micro_ctx *ctx, const float *grad, float *residual,
+                                     int64_t t, int32_t worker, int32_t world, double density,
+                                     double *theta, int32_t *out_idx, float *out_val,
+                                     int64_t *k, int32_t *cycle);
+
+/*
+ * Algorithm 1, after the all-gather of the selected indices: the worker's
+ * accumulated values at the union of all workers' selections (its part of
+ * the all-reduce) and their reset in its local error.
+ *   residual   device, n_total fp32, in/out: the local error as
+ *              micro_ef_step left it (acc at every unselected element).
+ *   union_idx  device int32[m]: the union, distinct indices in [0, n_total);
+ *              positions [own_first, own_first + own_count) hold this
+ *              worker's own selection of the same iteration, in the order
+ *              micro_ef_step wrote it (own_count = its k).
+ *   own_val    device fp32[own_count]: micro_ef_step's out_val.
+ *   out        device fp32[m], out: out[q] = acc at union_idx[q]
+ *              (own_val[q - own_first] inside the own run).
+ * Every union index outside the own run gets residual = +0 (those of the own
+ * run already are).  An index outside [0, n_total) touches nothing and gives
+ * out[q] = NaN.  Buffers must not overlap and must be 4-byte aligned.
+ * Enqueued on the context's stream: the call returns after the launch (with
+ * MICRO_FLAG_TIME_KERNEL it waits and records kernel_ms).  MICRO_EINVAL for
+ * m outside [0, n_total], an own run outside [0, m), NULL or overlapping
+ * buffers, before any device work.
+ */
+MICRO_API micro_status micro_union_gather(micro_ctx *ctx, float *residual, const int32_t *union_idx,
+                                          int64_t m, int64_t own_first, int64_t own_count,
+                                          const float *own_val, float *out);
+
+/*
+ * Algorithm 1 and Sec. 4.4, the model update with the averaged sums:
+ * x[union_idx[q]] = x[union_idx[q]] - sums[q] / world for q in [0, m) (one
+ * correctly rounded binary32 division by world, one binary32 subtraction;
+ * the learning rate is inside the gradients).
+ *   x          device, n_total fp32 model parameters, in/out.
+ *   union_idx  device int32[m], distinct; indices outside [0, n_total) are
+ *              skipped.
+ *   sums       device fp32[m]: the all-reduced (summed) values.
+ * Enqueued like micro_union_gather.  MICRO_EINVAL for m outside
+ * [0, n_total], world < 1, NULL or overlapping buffers.
+ */
+MICRO_API micro_status micro_sparse_update(micro_ctx *ctx, float *x, const int32_t *union_idx,
+                                           const float *sums, int64_t m, int32_t world);
+
 /* Sec. 4.1 partition bounds (pure host arithmetic, no device needed):
  * *start = floor(rank*n_total/world), *len = floor((rank+1)*n_total/world)
  * - *start.  Returns MICRO_EINVAL for world < 1, rank outside [0, world),

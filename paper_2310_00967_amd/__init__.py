@@ -2,6 +2,9 @@
 
     sp = Sparsifier(n_total)                       # on torch's current device/stream
     k, theta, idx, val = sp.step(grad, residual, rank, world, density, theta)
+    k, theta, cycle, idx, val = sp.ef_step(grad, residual, t, worker, world, density, theta)
+    g = sp.union_gather(residual, union_idx, own_first, val)   # around the exchange
+    sp.sparse_update(x, union_idx, summed, world)
 
 `grad` and `residual` are contiguous float32 device tensors of n_total values;
 `residual` is updated in place over the rank's partition only; `idx`/`val`
@@ -12,9 +15,9 @@ provides device memory and the stream.
 from . import _lib
 from ._lib import (MICRO_FLAG_TIME_KERNEL, MICRO_RULE_FIXED_STEP, MICRO_RULE_PROPORTIONAL,
                    MICRO_VARIANT_AUTO, MICRO_VARIANT_STAGED, MICRO_VARIANT_TICKET, MicroError, default_config,
-                   micro_estimate_threshold, micro_partition, micro_threshold_f32)
+                   micro_cycle, micro_estimate_threshold, micro_partition, micro_threshold_f32)
 
-__all__ = ["Sparsifier", "MicroError", "default_config", "micro_partition",
+__all__ = ["Sparsifier", "MicroError", "default_config", "micro_partition", "micro_cycle",
            "micro_estimate_threshold", "micro_threshold_f32", "MICRO_RULE_PROPORTIONAL",
            "MICRO_RULE_FIXED_STEP", "MICRO_VARIANT_AUTO", "MICRO_VARIANT_TICKET", "MICRO_VARIANT_STAGED",
            "MICRO_FLAG_TIME_KERNEL"]
@@ -95,6 +98,62 @@ class Sparsifier:
         k, th = _lib.micro_sparsify_step(self._ctx, grad.data_ptr(), residual.data_ptr(), rank, world,
                                          density, theta, out_idx.data_ptr(), out_val.data_ptr())
         return k, th, out_idx[:k], out_val[:k]
+
+    def ef_step(self, grad, residual, t, worker, world, density, theta, out_idx=None, out_val=None):
+        """Algorithm 1 for `worker` at iteration t over the whole vector: every
+        value accumulates, the partition of the worker's cycle is searched.
+        Returns (k, theta_next, cycle, idx[:k], val[:k])."""
+        import torch
+        if self._ctx is None:
+            raise RuntimeError("Sparsifier is closed")
+        self._check(grad, "grad", torch.float32)
+        self._check(residual, "residual", torch.float32)
+        if grad.numel() != self.n_total or residual.numel() != self.n_total:
+            raise ValueError(f"grad and residual must hold {self.n_total} values")
+        _, length = self.partition(_lib.micro_cycle(t, worker, world), world)
+        if out_idx is None or out_val is None:
+            out_idx, out_val = self.outputs(length)
+        self._check(out_idx, "out_idx", torch.int32)
+        self._check(out_val, "out_val", torch.float32)
+        if out_idx.numel() < length or out_val.numel() < length:
+            raise ValueError(f"output capacity below the partition length {length}")
+        k, th, c = _lib.micro_ef_step(self._ctx, grad.data_ptr(), residual.data_ptr(), t, worker, world,
+                                      density, theta, out_idx.data_ptr(), out_val.data_ptr())
+        return k, th, c, out_idx[:k], out_val[:k]
+
+    def union_gather(self, residual, union_idx, own_first, own_val, out=None):
+        """The accumulated values at the union of the workers' selections and
+        their reset in `residual`; own_val (this worker's k selected values)
+        sits at union positions [own_first, own_first + k).  Enqueued on the
+        context's stream.  Returns out (float32, len(union_idx))."""
+        import torch
+        self._check(residual, "residual", torch.float32)
+        self._check(union_idx, "union_idx", torch.int32)
+        self._check(own_val, "own_val", torch.float32)
+        if residual.numel() != self.n_total:
+            raise ValueError(f"residual must hold {self.n_total} values")
+        m = union_idx.numel()
+        if out is None:
+            out = torch.empty(max(1, m), dtype=torch.float32, device=self.device)[:m]
+        self._check(out, "out", torch.float32)
+        if out.numel() < m:
+            raise ValueError("out smaller than the union")
+        _lib.micro_union_gather(self._ctx, residual.data_ptr(), union_idx.data_ptr(), m, own_first,
+                                own_val.numel(), own_val.data_ptr(), out.data_ptr())
+        return out
+
+    def sparse_update(self, x, union_idx, sums, world):
+        """x[union_idx] -= sums / world (enqueued on the context's stream)."""
+        import torch
+        self._check(x, "x", torch.float32)
+        self._check(union_idx, "union_idx", torch.int32)
+        self._check(sums, "sums", torch.float32)
+        if x.numel() != self.n_total:
+            raise ValueError(f"x must hold {self.n_total} values")
+        if sums.numel() != union_idx.numel():
+            raise ValueError("sums and union_idx lengths differ")
+        _lib.micro_sparse_update(self._ctx, x.data_ptr(), union_idx.data_ptr(), sums.data_ptr(),
+                                 union_idx.numel(), world)
 
     def last_stats(self):
         """(kernel_ms, redone_tiles, variant) of the last step."""

@@ -42,6 +42,14 @@ SIGNATURES = {
                                            ctypes.c_int32, ctypes.c_int32, ctypes.c_double, _dblp,
                                            ctypes.c_void_p, ctypes.c_void_p, _i64p]),
     "micro_partition": (ctypes.c_int, [ctypes.c_int64, ctypes.c_int32, ctypes.c_int32, _i64p, _i64p]),
+    "micro_cycle": (ctypes.c_int, [ctypes.c_int64, ctypes.c_int32, ctypes.c_int32, ctypes.POINTER(ctypes.c_int32)]),
+    "micro_ef_step": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int64,
+                                     ctypes.c_int32, ctypes.c_int32, ctypes.c_double, _dblp,
+                                     ctypes.c_void_p, ctypes.c_void_p, _i64p, ctypes.POINTER(ctypes.c_int32)]),
+    "micro_union_gather": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int64,
+                                          ctypes.c_int64, ctypes.c_int64, ctypes.c_void_p, ctypes.c_void_p]),
+    "micro_sparse_update": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p,
+                                           ctypes.c_int64, ctypes.c_int32]),
     "micro_estimate_threshold": (ctypes.c_int, [_cfgp, ctypes.c_double, ctypes.c_int64,
                                                 ctypes.c_int64, _dblp]),
     "micro_threshold_f32": (ctypes.c_int, [ctypes.c_double, _fltp]),
@@ -134,6 +142,36 @@ def micro_sparsify_step(ctx, grad_ptr, residual_ptr, rank, world, density, theta
                                     ctypes.byref(k))
     check(st, ctx)
     return k.value, th.value
+
+
+def micro_cycle(t, worker, world):
+    c = ctypes.c_int32()
+    check(load().micro_cycle(int(t), int(worker), int(world), ctypes.byref(c)))
+    return c.value
+
+
+def micro_ef_step(ctx, grad_ptr, residual_ptr, t, worker, world, density, theta, out_idx_ptr, out_val_ptr):
+    """Raw call with device addresses; returns (k, theta_next, cycle)."""
+    th = ctypes.c_double(float(theta))
+    k = ctypes.c_int64()
+    c = ctypes.c_int32()
+    st = load().micro_ef_step(ctx, ctypes.c_void_p(grad_ptr), ctypes.c_void_p(residual_ptr), int(t),
+                              int(worker), int(world), float(density), ctypes.byref(th),
+                              ctypes.c_void_p(out_idx_ptr), ctypes.c_void_p(out_val_ptr), ctypes.byref(k),
+                              ctypes.byref(c))
+    check(st, ctx)
+    return k.value, th.value, c.value
+
+
+def micro_union_gather(ctx, residual_ptr, union_ptr, m, own_first, own_count, own_val_ptr, out_ptr):
+    check(load().micro_union_gather(ctx, ctypes.c_void_p(residual_ptr), ctypes.c_void_p(union_ptr), int(m),
+                                    int(own_first), int(own_count), ctypes.c_void_p(own_val_ptr),
+                                    ctypes.c_void_p(out_ptr)), ctx)
+
+
+def micro_sparse_update(ctx, x_ptr, union_ptr, sums_ptr, m, world):
+    check(load().micro_sparse_update(ctx, ctypes.c_void_p(x_ptr), ctypes.c_void_p(union_ptr),
+                                     ctypes.c_void_p(sums_ptr), int(m), int(world)), ctx)
 
 
 def micro_sparsify_last_stats(ctx):

@@ -3,8 +3,8 @@
 hipcc compiles the kernel (device + host stub) and the host library
 separately, then links one shared object whose exported symbols are exactly
 the C ABI of include/micro_sparsify.h.  Floating point: no contraction
-(-ffp-contract=off), no fast-math, subnormals kept, and the packed-fp32
-instructions disabled for device code.
+(-ffp-contract=off), no fast-math, subnormals kept, correctly rounded binary32
+division, and the packed-fp32 instructions disabled for device code.
 """
 import os
 import shutil
@@ -30,7 +30,8 @@ def hipcc():
 COMMON = ["-O3", "-std=c++17", "-fPIC", "-ffp-contract=off", "-fno-fast-math",
           "-Wall", "-Wextra", f"-I{INCLUDE}", f"-I{CSRC}"]
 DEVICE = [f"--offload-arch={ARCH}", "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
-          "-fvisibility=hidden"]
+          "-fhip-fp32-correctly-rounded-divide-sqrt", "-fvisibility=hidden"]
+KERNEL_SOURCES = ["sparsify_kernel.hip", "union_kernel.hip"]
 
 
 def _run(cmd, verbose):
@@ -43,14 +44,17 @@ def build_library(verbose=False, extra_device_flags=()):
     """Compiles every HIP source for gfx950 (every call) and returns the .so path."""
     os.makedirs(BUILD_DIR, exist_ok=True)
     cc = hipcc()
-    kobj = os.path.join(BUILD_DIR, "sparsify_kernel.o")
+    kobjs = []
+    for src in KERNEL_SOURCES:
+        obj = os.path.join(BUILD_DIR, os.path.splitext(src)[0] + ".o")
+        _run([cc, *COMMON, *DEVICE, *extra_device_flags, "-x", "hip", "-c",
+              os.path.join(CSRC, src), "-o", obj], verbose)
+        kobjs.append(obj)
     hobj = os.path.join(BUILD_DIR, "micro_sparsify.o")
-    _run([cc, *COMMON, *DEVICE, *extra_device_flags, "-x", "hip", "-c",
-          os.path.join(CSRC, "sparsify_kernel.hip"), "-o", kobj], verbose)
     _run([cc, *COMMON, "-fvisibility=hidden", "-c", os.path.join(CSRC, "micro_sparsify.cpp"),
           "-o", hobj], verbose)
     tmp = LIB + ".tmp"
-    _run([cc, f"--offload-arch={ARCH}", "-shared", "-fPIC", "-o", tmp, kobj, hobj], verbose)
+    _run([cc, f"--offload-arch={ARCH}", "-shared", "-fPIC", "-o", tmp, *kobjs, hobj], verbose)
     os.replace(tmp, LIB)
     return LIB
 

@@ -10,6 +10,7 @@
 #include <cstdarg>
 #include <cstdio>
 #include <cstring>
+#include <initializer_list>
 #include <limits>
 #include <new>
 #include <string>
@@ -143,6 +144,167 @@ void release(micro_ctx* ctx) {
         if (p) (void)hipFree(p);
     if (ctx->h_count) (void)hipHostFree(ctx->h_count);
     delete ctx;
+}
+
+
+bool misaligned4(std::initializer_list<const void*> ptrs) {
+    uintptr_t bits = 0;
+    for (const void* p : ptrs) bits |= reinterpret_cast<uintptr_t>(p);
+    return (bits & 3u) != 0;
+}
+
+// Validation, launch, count readback and threshold update of one sparsify
+// step over [start, start + len); with accumulate_outside the rest of the
+// vector is accumulated too (the full error-feedback pass).
+micro_status execute_step(micro_ctx* ctx, const float* grad, float* residual, int64_t start, int64_t len,
+                          bool accumulate_outside, double density, double* theta, int32_t* out_idx,
+                          float* out_val, int64_t* k) {
+    if (!grad || !residual || !theta || !out_idx || !out_val || !k) {
+        set_error(ctx, "NULL pointer argument");
+        return MICRO_EINVAL;
+    }
+    if (!density_valid(density)) {
+        set_error(ctx, "density %g outside (0, 1]", density);
+        return MICRO_EINVAL;
+    }
+    if (!theta_valid(*theta)) {
+        set_error(ctx, "threshold %g is not finite and positive", *theta);
+        return MICRO_EINVAL;
+    }
+    if (misaligned4({grad, residual, out_idx, out_val})) {
+        set_error(ctx, "buffers must be 4-byte aligned");
+        return MICRO_EINVAL;
+    }
+    // the ranges each buffer is accessed over
+    const int64_t span_start = accumulate_outside ? 0 : start;
+    const size_t span = static_cast<size_t>(accumulate_outside ? ctx->n_total : len) * sizeof(float);
+    const size_t pb = static_cast<size_t>(len) * sizeof(float);
+    const void* regions[4] = {grad + span_start, residual + span_start, out_idx, out_val};
+    const size_t sizes[4] = {span, span, pb, pb};
+    for (int i = 0; i < 4; ++i)
+        for (int j = i + 1; j < 4; ++j)
+            if (sizes[i] > 0 && sizes[j] > 0 && ranges_overlap(regions[i], sizes[i], regions[j], sizes[j])) {
+                set_error(ctx, "grad, residual and output ranges overlap");
+                return MICRO_EINVAL;
+            }
+    const int64_t n_outside = accumulate_outside ? ctx->n_total - len : 0;
+    if (len == 0 && n_outside == 0) {  // nothing to do: nothing selected, threshold unchanged
+        *k = 0;
+        return MICRO_OK;
+    }
+    if (ctx->needs_reset) {
+        micro_status s = reset_scratch(ctx);
+        if (s != MICRO_OK) return s;
+    }
+    if (ctx->epoch >= micro::kMaxEpoch) {  // epoch field would wrap: clear the status words
+        micro_status s = reset_scratch(ctx);
+        if (s != MICRO_OK) return s;
+    }
+    const bool vec4 = ((reinterpret_cast<uintptr_t>(grad) ^ reinterpret_cast<uintptr_t>(residual)) & 15u) == 0;
+    micro::AccumulateArgs acc{};
+    if (n_outside > 0) {
+        acc.grad = grad;
+        acc.residual = residual;
+        const int64_t lo[2] = {0, start + len}, hi[2] = {start, ctx->n_total};
+        for (int r = 0; r < 2; ++r) {
+            acc.start[r] = lo[r];
+            acc.end[r] = hi[r];
+            acc.base[r] = micro::tile_base_for(grad, lo[r], vec4);
+            acc.tiles[r] = hi[r] > lo[r] ? static_cast<uint32_t>((hi[r] - acc.base[r] + micro::kStreamTile - 1) /
+                                                                  micro::kStreamTile)
+                                         : 0u;
+        }
+    }
+    const int64_t tile_elems = ctx->staged ? micro::kStreamTile : micro::kTicketTile;
+    micro::LaunchArgs a{};
+    a.grad = grad;
+    a.residual = residual;
+    a.out_idx = out_idx;
+    a.out_val = out_val;
+    a.start = start;
+    a.end = start + len;
+    a.base = micro::tile_base_for(grad, start, vec4);
+    a.theta_f = threshold_as_f32(*theta);
+    a.epoch = ctx->epoch + 1;
+    const int64_t tiles = len > 0 ? (a.end - a.base + tile_elems - 1) / tile_elems : 0;
+    const int64_t chunks = (tiles + micro::kChunkTiles - 1) / micro::kChunkTiles;
+    if (tiles > ctx->tile_capacity || (ctx->staged && chunks > ctx->chunk_capacity)) {
+        set_error(ctx, "partition needs %lld tiles, scratch holds %lld", static_cast<long long>(tiles),
+                  static_cast<long long>(ctx->tile_capacity));
+        return MICRO_ECAPACITY;
+    }
+    a.num_tiles = static_cast<uint32_t>(tiles);
+    a.count_out = ctx->d_count;
+    a.host_count = ctx->h_count_dev;
+    a.tile_counts = ctx->d_tile_counts;
+    a.tile_excl = ctx->d_tile_excl;
+    a.flagged_list = ctx->d_flagged_list;
+    a.split_tile = ctx->d_split_tile;
+    {
+        // at most ceil((tiles + P) / kMoveSpan) move pieces, whatever k is
+        const int64_t pieces = (tiles + len + micro::kMoveSpan - 1) / micro::kMoveSpan;
+        a.move_blocks = static_cast<uint32_t>(pieces < micro::kMoveGrid ? pieces : micro::kMoveGrid);
+    }
+    a.stage = ctx->d_stage;
+    a.num_chunks = static_cast<uint32_t>(chunks);
+    a.chunk_status = ctx->d_chunk_status;
+    a.chunk_ticket = &ctx->d_tickets[1];
+    a.status = ctx->d_status;
+    a.ticket = &ctx->d_tickets[0];
+
+    hipError_t e;
+    const bool timed = (ctx->cfg.flags & MICRO_FLAG_TIME_KERNEL) != 0;
+    ctx->stats.kernel_ms = -1.0f;
+    ctx->stats.redone_tiles = 0;
+    if (timed && (e = hipEventRecord(ctx->ev[0], ctx->stream)) != hipSuccess)
+        return hip_fail(ctx, e, "hipEventRecord");
+    volatile int64_t* host_count = ctx->h_count;  // stored by the last kernel of the step
+    host_count[0] = len > 0 ? -1 : 0;
+    host_count[1] = len > 0 ? -1 : 0;
+    if (n_outside > 0 && (e = micro::launch_accumulate(acc, vec4, ctx->stream)) != hipSuccess)
+        return hip_fail(ctx, e, "accumulate kernel launch");
+    if (len > 0) {
+        ctx->epoch = a.epoch;
+        e = ctx->staged ? micro::launch_staged(a, vec4, ctx->stream) : micro::launch_ticket(a, vec4, ctx->stream);
+        if (e != hipSuccess) return hip_fail(ctx, e, "sparsify kernel launch");
+    }
+    if (timed && (e = hipEventRecord(ctx->ev[1], ctx->stream)) != hipSuccess)
+        return hip_fail(ctx, e, "hipEventRecord");
+    if ((e = hipStreamSynchronize(ctx->stream)) != hipSuccess) return hip_fail(ctx, e, "hipStreamSynchronize");
+    const int64_t selected = host_count[0];
+    if (selected < 0 || selected > len) {
+        set_error(ctx, "device reported %lld selected of %lld", static_cast<long long>(selected),
+                  static_cast<long long>(len));
+        ctx->needs_reset = true;
+        return MICRO_EHIP;
+    }
+    if (timed && (e = hipEventElapsedTime(&ctx->stats.kernel_ms, ctx->ev[0], ctx->ev[1])) != hipSuccess)
+        return hip_fail(ctx, e, "hipEventElapsedTime");
+    ctx->stats.redone_tiles = ctx->staged ? host_count[1] : 0;
+    *k = selected;
+    *theta = next_threshold(ctx->cfg, density, len, selected, *theta);
+    return MICRO_OK;
+}
+
+// Enqueues one union kernel on the context's stream.  With the timing flag
+// the call waits for it and records its duration; otherwise it returns after
+// the launch.
+template <class Launch>
+micro_status execute_union(micro_ctx* ctx, Launch launch) {
+    hipError_t e;
+    const bool timed = (ctx->cfg.flags & MICRO_FLAG_TIME_KERNEL) != 0;
+    ctx->stats.kernel_ms = -1.0f;
+    ctx->stats.redone_tiles = 0;
+    if (timed && (e = hipEventRecord(ctx->ev[0], ctx->stream)) != hipSuccess)
+        return hip_fail(ctx, e, "hipEventRecord");
+    if ((e = launch(ctx->stream)) != hipSuccess) return hip_fail(ctx, e, "union kernel launch");
+    if (timed) {
+        if ((e = hipEventRecord(ctx->ev[1], ctx->stream)) != hipSuccess) return hip_fail(ctx, e, "hipEventRecord");
+        if ((e = hipEventSynchronize(ctx->ev[1])) != hipSuccess) return hip_fail(ctx, e, "hipEventSynchronize");
+        if ((e = hipEventElapsedTime(&ctx->stats.kernel_ms, ctx->ev[0], ctx->ev[1])) != hipSuccess)
+            return hip_fail(ctx, e, "hipEventElapsedTime");
+    }
+    return MICRO_OK;
 }
 
 }  // namespace
@@ -287,115 +449,103 @@ micro_status micro_sparsify_step(micro_ctx* ctx, const float* grad, float* resid
         set_error(nullptr, "ctx is NULL");
         return MICRO_EINVAL;
     }
-    if (!grad || !residual || !theta || !out_idx || !out_val || !k) {
-        set_error(ctx, "NULL pointer argument");
-        return MICRO_EINVAL;
-    }
     int64_t start = 0, len = 0;
     if (micro_partition(ctx->n_total, rank, world, &start, &len) != MICRO_OK) {
         set_error(ctx, "invalid rank %d / world %d", rank, world);
         return MICRO_EINVAL;
     }
-    if (!density_valid(density)) {
-        set_error(ctx, "density %g outside (0, 1]", density);
+    return execute_step(ctx, grad, residual, start, len, false, density, theta, out_idx, out_val, k);
+}
+
+micro_status micro_cycle(int64_t t, int32_t worker, int32_t world, int32_t* cycle) {
+    if (!cycle || t < 0 || world < 1 || worker < 0 || worker >= world) return MICRO_EINVAL;
+    // Algorithm 1: the partition number advances by one every iteration.
+    const int64_t n = world;
+    *cycle = static_cast<int32_t>((t % n + worker) % n);
+    return MICRO_OK;
+}
+
+micro_status micro_ef_step(micro_ctx* ctx, const float* grad, float* residual, int64_t t, int32_t worker,
+                           int32_t world, double density, double* theta, int32_t* out_idx, float* out_val,
+                           int64_t* k, int32_t* cycle) {
+    if (!ctx) {
+        set_error(nullptr, "ctx is NULL");
         return MICRO_EINVAL;
     }
-    if (!theta_valid(*theta)) {
-        set_error(ctx, "threshold %g is not finite and positive", *theta);
+    int32_t part = 0;
+    if (micro_cycle(t, worker, world, &part) != MICRO_OK) {
+        set_error(ctx, "invalid iteration %lld / worker %d / world %d", static_cast<long long>(t), worker, world);
         return MICRO_EINVAL;
     }
-    const uintptr_t misaligned = (reinterpret_cast<uintptr_t>(grad) | reinterpret_cast<uintptr_t>(residual) |
-                                  reinterpret_cast<uintptr_t>(out_idx) | reinterpret_cast<uintptr_t>(out_val)) & 3u;
-    if (misaligned) {
+    int64_t start = 0, len = 0;
+    (void)micro_partition(ctx->n_total, part, world, &start, &len);
+    const micro_status st = execute_step(ctx, grad, residual, start, len, true, density, theta, out_idx, out_val, k);
+    if (st == MICRO_OK && cycle) *cycle = part;
+    return st;
+}
+
+micro_status micro_union_gather(micro_ctx* ctx, float* residual, const int32_t* union_idx, int64_t m,
+                                int64_t own_first, int64_t own_count, const float* own_val, float* out) {
+    if (!ctx) {
+        set_error(nullptr, "ctx is NULL");
+        return MICRO_EINVAL;
+    }
+    if (m < 0 || m > ctx->n_total || own_first < 0 || own_count < 0 || own_count > m - own_first) {
+        set_error(ctx, "invalid union length %lld or own run [%lld, +%lld)", static_cast<long long>(m),
+                  static_cast<long long>(own_first), static_cast<long long>(own_count));
+        return MICRO_EINVAL;
+    }
+    if (m == 0) return MICRO_OK;
+    if (!residual || !union_idx || !out || (own_count > 0 && !own_val)) {
+        set_error(ctx, "NULL pointer argument");
+        return MICRO_EINVAL;
+    }
+    if (misaligned4({residual, union_idx, own_val, out})) {
         set_error(ctx, "buffers must be 4-byte aligned");
         return MICRO_EINVAL;
     }
-    const size_t pb = static_cast<size_t>(len) * sizeof(float);
-    const void* regions[4] = {grad + start, residual + start, out_idx, out_val};
-    for (int i = 0; i < 4; ++i)
-        for (int j = i + 1; j < 4; ++j)
-            if (len > 0 && ranges_overlap(regions[i], pb, regions[j], pb)) {
-                set_error(ctx, "grad, residual and output ranges overlap");
-                return MICRO_EINVAL;
-            }
-    if (len == 0) {  // empty partition: nothing selected, threshold unchanged
-        *k = 0;
-        return MICRO_OK;
+    const size_t mb = static_cast<size_t>(m) * 4, nb = static_cast<size_t>(ctx->n_total) * 4,
+                 ob = static_cast<size_t>(own_count) * 4;
+    if (ranges_overlap(out, mb, residual, nb) || ranges_overlap(out, mb, union_idx, mb) ||
+        (own_count > 0 && (ranges_overlap(out, mb, own_val, ob) || ranges_overlap(residual, nb, own_val, ob))) ||
+        ranges_overlap(residual, nb, union_idx, mb)) {
+        set_error(ctx, "residual, union, own values and output overlap");
+        return MICRO_EINVAL;
     }
-    if (ctx->needs_reset) {
-        micro_status s = reset_scratch(ctx);
-        if (s != MICRO_OK) return s;
-    }
-    if (ctx->epoch >= micro::kMaxEpoch) {  // epoch field would wrap: clear the status words
-        micro_status s = reset_scratch(ctx);
-        if (s != MICRO_OK) return s;
-    }
-    const bool vec4 = ((reinterpret_cast<uintptr_t>(grad) ^ reinterpret_cast<uintptr_t>(residual)) & 15u) == 0;
-    const int64_t tile_elems = ctx->staged ? micro::kStreamTile : micro::kTicketTile;
-    micro::LaunchArgs a{};
-    a.grad = grad;
-    a.residual = residual;
-    a.out_idx = out_idx;
-    a.out_val = out_val;
-    a.start = start;
-    a.end = start + len;
-    a.base = micro::tile_base_for(grad, start, vec4);
-    a.theta_f = threshold_as_f32(*theta);
-    a.epoch = ctx->epoch + 1;
-    const int64_t tiles = (a.end - a.base + tile_elems - 1) / tile_elems;
-    const int64_t chunks = (tiles + micro::kChunkTiles - 1) / micro::kChunkTiles;
-    if (tiles > ctx->tile_capacity || (ctx->staged && chunks > ctx->chunk_capacity)) {
-        set_error(ctx, "partition needs %lld tiles, scratch holds %lld", static_cast<long long>(tiles),
-                  static_cast<long long>(ctx->tile_capacity));
-        return MICRO_ECAPACITY;
-    }
-    a.num_tiles = static_cast<uint32_t>(tiles);
-    a.count_out = ctx->d_count;
-    a.host_count = ctx->h_count_dev;
-    a.tile_counts = ctx->d_tile_counts;
-    a.tile_excl = ctx->d_tile_excl;
-    a.flagged_list = ctx->d_flagged_list;
-    a.split_tile = ctx->d_split_tile;
-    {
-        // at most ceil((tiles + P) / kMoveSpan) move pieces, whatever k is
-        const int64_t pieces = (tiles + len + micro::kMoveSpan - 1) / micro::kMoveSpan;
-        a.move_blocks = static_cast<uint32_t>(pieces < micro::kMoveGrid ? pieces : micro::kMoveGrid);
-    }
-    a.stage = ctx->d_stage;
-    a.num_chunks = static_cast<uint32_t>(chunks);
-    a.chunk_status = ctx->d_chunk_status;
-    a.chunk_ticket = &ctx->d_tickets[1];
-    a.status = ctx->d_status;
-    a.ticket = &ctx->d_tickets[0];
+    return execute_union(ctx, [&](hipStream_t s) {
+        return micro::launch_union_gather(residual, ctx->n_total, union_idx, m, own_first, own_count, own_val,
+                                          out, s);
+    });
+}
 
-    hipError_t e;
-    const bool timed = (ctx->cfg.flags & MICRO_FLAG_TIME_KERNEL) != 0;
-    ctx->stats.kernel_ms = -1.0f;
-    ctx->stats.redone_tiles = 0;
-    if (timed && (e = hipEventRecord(ctx->ev[0], ctx->stream)) != hipSuccess)
-        return hip_fail(ctx, e, "hipEventRecord");
-    ctx->epoch = a.epoch;
-    volatile int64_t* host_count = ctx->h_count;  // stored by the last kernel of the step
-    host_count[0] = -1;
-    host_count[1] = -1;
-    e = ctx->staged ? micro::launch_staged(a, vec4, ctx->stream) : micro::launch_ticket(a, vec4, ctx->stream);
-    if (e != hipSuccess) return hip_fail(ctx, e, "sparsify kernel launch");
-    if (timed && (e = hipEventRecord(ctx->ev[1], ctx->stream)) != hipSuccess)
-        return hip_fail(ctx, e, "hipEventRecord");
-    if ((e = hipStreamSynchronize(ctx->stream)) != hipSuccess) return hip_fail(ctx, e, "hipStreamSynchronize");
-    const int64_t selected = host_count[0];
-    if (selected < 0 || selected > len) {
-        set_error(ctx, "device reported %lld selected of %lld", static_cast<long long>(selected),
-                  static_cast<long long>(len));
-        ctx->needs_reset = true;
-        return MICRO_EHIP;
+micro_status micro_sparse_update(micro_ctx* ctx, float* x, const int32_t* union_idx, const float* sums,
+                                 int64_t m, int32_t world) {
+    if (!ctx) {
+        set_error(nullptr, "ctx is NULL");
+        return MICRO_EINVAL;
     }
-    if (timed && (e = hipEventElapsedTime(&ctx->stats.kernel_ms, ctx->ev[0], ctx->ev[1])) != hipSuccess)
-        return hip_fail(ctx, e, "hipEventElapsedTime");
-    ctx->stats.redone_tiles = ctx->staged ? host_count[1] : 0;
-    *k = selected;
-    *theta = next_threshold(ctx->cfg, density, len, selected, *theta);
-    return MICRO_OK;
+    if (m < 0 || m > ctx->n_total || world < 1) {
+        set_error(ctx, "invalid union length %lld or world %d", static_cast<long long>(m), world);
+        return MICRO_EINVAL;
+    }
+    if (m == 0) return MICRO_OK;
+    if (!x || !union_idx || !sums) {
+        set_error(ctx, "NULL pointer argument");
+        return MICRO_EINVAL;
+    }
+    if (misaligned4({x, union_idx, sums})) {
+        set_error(ctx, "buffers must be 4-byte aligned");
+        return MICRO_EINVAL;
+    }
+    const size_t mb = static_cast<size_t>(m) * 4, nb = static_cast<size_t>(ctx->n_total) * 4;
+    if (ranges_overlap(x, nb, union_idx, mb) || ranges_overlap(x, nb, sums, mb)) {
+        set_error(ctx, "model, union and sums overlap");
+        return MICRO_EINVAL;
+    }
+    const float n = static_cast<float>(world);
+    return execute_union(ctx, [&](hipStream_t s) {
+        return micro::launch_sparse_update(x, ctx->n_total, union_idx, sums, m, n, s);
+    });
 }
 
 micro_status micro_sparsify_last_stats(const micro_ctx* ctx, micro_step_stats* stats) {

@@ -62,6 +62,20 @@ struct LaunchArgs {
     unsigned long long* ticket;         // 0 at launch, rearmed by the kernel
 };
 
+// Error-feedback accumulation outside the searched partition (Algorithm 1,
+// every element accumulates its new gradient): residual = grad + residual
+// over ranges [start[r], end[r]), r = 0, 1, in tiles of kStreamTile values
+// whose first tile starts at base[r] (<= start[r]); workgroups
+// [0, tiles[0]) take range 0, the next tiles[1] range 1.
+struct AccumulateArgs {
+    const float* grad;
+    float* residual;
+    int64_t start[2];
+    int64_t end[2];
+    int64_t base[2];
+    uint32_t tiles[2];
+};
+
 // Global index of tile 0's first value: the start rounded down so that
 // grad + base is 16-byte aligned (vectorised kernels), or the start.
 int64_t tile_base_for(const float* grad, int64_t start, bool vec4);
@@ -70,5 +84,17 @@ int64_t tile_base_for(const float* grad, int64_t start, bool vec4);
 // the scalar-load kernels.  Each returns the launch status.
 hipError_t launch_staged(const LaunchArgs& args, bool vec4, hipStream_t stream);
 hipError_t launch_ticket(const LaunchArgs& args, bool vec4, hipStream_t stream);
+hipError_t launch_accumulate(const AccumulateArgs& args, bool vec4, hipStream_t stream);
+
+// Union kernels (union_kernel.hip).  Gather and reset at the union of the
+// workers' selections: out[q] = own_val[q - own_first] for q in
+// [own_first, own_first + own_count), else out[q] = residual[idx[q]] and
+// residual[idx[q]] = +0 (indices outside [0, n): no access, out[q] = NaN).
+hipError_t launch_union_gather(float* residual, int64_t n, const int32_t* idx, int64_t m, int64_t own_first,
+                               int64_t own_count, const float* own_val, float* out, hipStream_t stream);
+// Model update: x[idx[q]] = x[idx[q]] - sums[q] / world, q in [0, m)
+// (indices outside [0, n_x) skipped).
+hipError_t launch_sparse_update(float* x, int64_t n_x, const int32_t* idx, const float* sums, int64_t m,
+                                float world, hipStream_t stream);
 
 }  // namespace micro

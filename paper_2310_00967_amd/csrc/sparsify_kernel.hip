@@ -720,7 +720,48 @@ __global__ __launch_bounds__(kTicketBlock) void ticket_kernel(LaunchArgs a) {
     scatter_pairs(a, tid, t, sel, s_exclusive, row_base, lane_rank);
 }
 
+// ---------------------------------------------------------------------------
+// Error-feedback accumulation outside the searched partition
+// ---------------------------------------------------------------------------
+
+// residual = grad + residual (one binary32 addition per value) over the tiles
+// of two ranges, with the stream kernel's tile shape and non-temporal
+// accesses; every value is written back, nothing is selected.
+template <int VEC, int ROWS>
+__global__ __launch_bounds__(kStreamBlock) void accumulate_kernel(AccumulateArgs acc) {
+    static_assert(VEC * ROWS * kStreamBlock == kStreamTile, "tile size");
+    uint32_t tile = blockIdx.x;
+    int r = 0;
+    if (tile >= acc.tiles[0]) {
+        tile -= acc.tiles[0];
+        r = 1;
+    }
+    LaunchArgs a{};
+    a.grad = acc.grad;
+    a.residual = acc.residual;
+    a.start = acc.start[r];
+    a.end = acc.end[r];
+    const int tid = threadIdx.x;
+    Tile<VEC, ROWS, kStreamBlock> t;
+    load_tile<VEC, ROWS, kStreamBlock, true>(a, acc.base[r] + static_cast<int64_t>(tile) * kStreamTile, tid, t);
+#pragma unroll
+    for (int row = 0; row < ROWS; ++row)
+#pragma unroll
+        for (int c = 0; c < VEC; ++c) t.v[row][c] = t.v[row][c] + t.e[row][c];
+    store_residual<VEC, ROWS, kStreamBlock, true>(a, tid, t, 0u);
+}
+
 }  // namespace
+
+hipError_t launch_accumulate(const AccumulateArgs& args, bool vec4, hipStream_t stream) {
+    const uint32_t blocks = args.tiles[0] + args.tiles[1];
+    if (blocks == 0) return hipSuccess;
+    if (vec4)
+        hipLaunchKernelGGL((accumulate_kernel<4, 1>), dim3(blocks), dim3(kStreamBlock), 0, stream, args);
+    else
+        hipLaunchKernelGGL((accumulate_kernel<1, 4>), dim3(blocks), dim3(kStreamBlock), 0, stream, args);
+    return hipGetLastError();
+}
 
 int64_t tile_base_for(const float* grad, int64_t start, bool vec4) {
     if (!vec4) return start;

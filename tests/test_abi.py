@@ -146,6 +146,34 @@ def test_step_with_null_context_is_rejected():
     assert th.value == 1.0 and k.value == -7
 
 
+def test_cycle_matches_oracle():
+    for world in [1, 2, 3, 8, 16]:
+        for worker in range(world):
+            for t in [0, 1, 2, 7, 15, 16, 17, 2**33 + 5]:
+                assert _lib.micro_cycle(t, worker, world) == oracle.cycle(t, worker, world)
+
+
+def test_cycle_rejects_bad_arguments():
+    lib = _lib.load()
+    c = ctypes.c_int32(-9)
+    for args in [(-1, 0, 2), (0, 2, 2), (0, -1, 2), (0, 0, 0)]:
+        assert lib.micro_cycle(*args, ctypes.byref(c)) == _lib.MICRO_EINVAL
+        assert c.value == -9
+    assert lib.micro_cycle(0, 0, 1, None) == _lib.MICRO_EINVAL
+
+
+def test_ef_and_union_calls_with_null_context_are_rejected():
+    lib = _lib.load()
+    th = ctypes.c_double(1.0)
+    k = ctypes.c_int64(-7)
+    c = ctypes.c_int32(-9)
+    assert lib.micro_ef_step(None, None, None, 0, 0, 1, 0.1, ctypes.byref(th), None, None, ctypes.byref(k),
+                             ctypes.byref(c)) == _lib.MICRO_EINVAL
+    assert (th.value, k.value, c.value) == (1.0, -7, -9)
+    assert lib.micro_union_gather(None, None, None, 0, 0, 0, None, None) == _lib.MICRO_EINVAL
+    assert lib.micro_sparse_update(None, None, None, None, 0, 1) == _lib.MICRO_EINVAL
+
+
 def test_init_without_device_reports_hip_error():
     import torch
     if torch.cuda.is_available():
@@ -193,4 +221,60 @@ def test_step_validation_on_device():
     assert bool((oi == -1).all()) and bool((ov == -1.0).all())
     st, th, k = call()
     assert st == _lib.MICRO_OK and k >= 0
+    sp.close()
+
+
+@pytest.mark.gpu
+def test_ef_and_union_validation_on_device():
+    import torch
+    import paper_2310_00967_amd as micro
+    N = 1000
+    sp = micro.Sparsifier(N, device="cuda")
+    lib = _lib.load()
+    g = torch.randn(N, device="cuda")
+    r = torch.randn(N, device="cuda")
+    r0 = r.clone()
+    oi = torch.full((N,), -1, dtype=torch.int32, device="cuda")
+    ov = torch.full((N,), -1.0, device="cuda")
+
+    def ef(grad=g.data_ptr(), res=r.data_ptr(), t=0, worker=0, world=2, d=0.1, theta=1.0,
+           idx=oi.data_ptr(), val=ov.data_ptr()):
+        th = ctypes.c_double(theta)
+        k = ctypes.c_int64(-7)
+        c = ctypes.c_int32(-9)
+        st = lib.micro_ef_step(sp._ctx, ctypes.c_void_p(grad), ctypes.c_void_p(res), t, worker, world, d,
+                               ctypes.byref(th), ctypes.c_void_p(idx), ctypes.c_void_p(val), ctypes.byref(k),
+                               ctypes.byref(c))
+        return st, k.value, c.value
+
+    # the whole vectors are accessed: a residual overlapping any part of grad is refused
+    bad = [dict(grad=0), dict(res=0), dict(idx=0), dict(val=0), dict(t=-1), dict(worker=2), dict(worker=-1),
+           dict(world=0), dict(d=0.0), dict(theta=0.0), dict(theta=float("inf")),
+           dict(res=g.data_ptr() + 4 * 999), dict(idx=r.data_ptr() + 4 * 900), dict(grad=g.data_ptr() + 1)]
+    for kw in bad:
+        st, k, c = ef(**kw)
+        assert st == _lib.MICRO_EINVAL, kw
+        assert (k, c) == (-7, -9)
+    u = torch.arange(0, 100, dtype=torch.int32, device="cuda")
+    out = torch.full((100,), -1.0, device="cuda")
+    for args in [(r.data_ptr(), u.data_ptr(), -1, 0, 0, ov.data_ptr(), out.data_ptr()),
+                 (r.data_ptr(), u.data_ptr(), N + 1, 0, 0, ov.data_ptr(), out.data_ptr()),
+                 (r.data_ptr(), u.data_ptr(), 100, 90, 11, ov.data_ptr(), out.data_ptr()),
+                 (r.data_ptr(), u.data_ptr(), 100, -1, 1, ov.data_ptr(), out.data_ptr()),
+                 (r.data_ptr(), u.data_ptr(), 100, 0, 5, 0, out.data_ptr()),
+                 (0, u.data_ptr(), 100, 0, 0, ov.data_ptr(), out.data_ptr()),
+                 (r.data_ptr(), u.data_ptr(), 100, 0, 0, ov.data_ptr(), r.data_ptr() + 40)]:
+        assert lib.micro_union_gather(sp._ctx, *[ctypes.c_void_p(a) if i in (0, 1, 5, 6) else a
+                                                 for i, a in enumerate(args)]) == _lib.MICRO_EINVAL, args
+    for args in [(r.data_ptr(), u.data_ptr(), out.data_ptr(), 100, 0),
+                 (r.data_ptr(), u.data_ptr(), out.data_ptr(), -1, 2),
+                 (r.data_ptr(), u.data_ptr(), r.data_ptr() + 8, 100, 2),
+                 (0, u.data_ptr(), out.data_ptr(), 100, 2)]:
+        assert lib.micro_sparse_update(sp._ctx, *[ctypes.c_void_p(a) if i in (0, 1, 2) else a
+                                                  for i, a in enumerate(args)]) == _lib.MICRO_EINVAL, args
+    torch.cuda.synchronize()
+    assert torch.equal(r, r0)
+    assert bool((oi == -1).all()) and bool((ov == -1.0).all()) and bool((out == -1.0).all())
+    st, k, c = ef()
+    assert st == _lib.MICRO_OK and k >= 0 and c == 0
     sp.close()

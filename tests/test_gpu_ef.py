@@ -1,0 +1,260 @@
+"""Bit-exact parity of the full error-feedback pass (cyclic partitions) and of
+the union gather / reset / model update with the CPU oracle (GPU).
+
+Every call goes through the C ABI via the ctypes binding; indices, values,
+counts, thresholds, cycles, residuals and parameters must equal the oracle's
+bit for bit.
+"""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import paper_2310_00967_amd as micro
+from paper_2310_00967_amd import synth
+
+from gpu_harness import first_mismatch, note
+
+pytestmark = pytest.mark.gpu
+
+DEV = "cuda"
+
+
+def bits_equal(a, b):
+    return a.shape == b.shape and first_mismatch(np.ascontiguousarray(a), np.ascontiguousarray(b)) < 0
+
+
+class EFRun:
+    """One worker's full error-feedback passes on a workload, checked step by
+    step against the oracle's pass on a host mirror."""
+
+    def __init__(self, w, worker, density):
+        self.w, self.worker, self.d = w, worker, density
+        self.N = w.n_total
+        self.sp = micro.Sparsifier(self.N, device=DEV)
+        self.g_dev = torch.empty(self.N, dtype=torch.float32, device=DEV)
+        self.res_dev = torch.zeros(self.N, dtype=torch.float32, device=DEV)
+        self.g_host = torch.empty(self.N, dtype=torch.float32, pin_memory=True)
+        self.res_host = torch.empty(self.N, dtype=torch.float32, pin_memory=True)
+        self.mirror = np.zeros(self.N, np.float32)
+        cap = max(oracle.partition(self.N, c, w.world)[1] for c in range(w.world))
+        self.out = (np.empty(max(cap, 1), np.int32), np.empty(max(cap, 1), np.float32))
+        self.theta = None
+
+    def step(self, t):
+        synth.gradient(self.w, t, DEV, out=self.g_dev)
+        if self.theta is None:
+            c = oracle.cycle(t, self.worker, self.w.world)
+            s, ln = oracle.partition(self.N, c, self.w.world)
+            self.theta = synth.initial_theta(self.w, self.g_dev, s, s + ln, self.d)
+        self.g_host.copy_(self.g_dev)
+        k, th, c, idx, val = self.sp.ef_step(self.g_dev, self.res_dev, t, self.worker, self.w.world,
+                                             self.d, self.theta)
+        o_idx, o_val, k_or, th_or, c_or = oracle.ef_step(self.g_host.numpy(), self.mirror, t, self.worker,
+                                                        self.w.world, self.d, self.theta, out=self.out)
+        where = f"{self.w.name} worker {self.worker} step {t}"
+        assert (k, th, c) == (k_or, th_or, c_or), f"{where}: (k, theta, cycle)"
+        assert np.array_equal(idx.cpu().numpy(), o_idx), f"{where}: indices"
+        assert bits_equal(val.cpu().numpy(), o_val), f"{where}: values"
+        self.res_host.copy_(self.res_dev)
+        mm = first_mismatch(self.res_host.numpy(), self.mirror)
+        assert mm < 0, f"{where}: residual differs at {mm}"
+        self.theta = th_or
+        return k
+
+    def close(self):
+        self.sp.close()
+
+
+@pytest.mark.parametrize("name,worker,density,steps", [
+    ("toy", 1, 0.01, 12),
+    ("resnet18", 5, 0.01, 20),
+    ("resnet50", 0, 0.001, 20),
+    ("bert_large", 3, 0.01, 10),
+])
+def test_ef_workload_parity(name, worker, density, steps):
+    """The whole vector accumulates every step; the searched partition rotates
+    with the iteration (it covers every partition within n steps for toy and
+    ResNet-50 and visits 10 of BERT's 8-partition cycle positions)."""
+    w = synth.get(name)
+    note(f"ef parity {name} worker {worker} world {w.world} steps {steps}")
+    run = EFRun(w, worker, density)
+    try:
+        for t in range(steps):
+            run.step(t)
+    finally:
+        run.close()
+
+
+def ef_gpu_vs_oracle(g, res, t, worker, world, density, theta, phase_shift=0):
+    N = g.size
+    sp = micro.Sparsifier(N, device=DEV)
+    gbuf = torch.empty(N + 4, dtype=torch.float32, device=DEV)
+    g_dev = gbuf[phase_shift:phase_shift + N]
+    g_dev.copy_(torch.from_numpy(g))
+    r_dev = torch.from_numpy(res).to(DEV)
+    c = oracle.cycle(t, worker, world)
+    _, ln = oracle.partition(N, c, world)
+    out_idx = torch.full((max(1, ln) + 8,), -5, dtype=torch.int32, device=DEV)
+    out_val = torch.full((max(1, ln) + 8,), -5.0, dtype=torch.float32, device=DEV)
+    k, th, cy, idx, val = sp.ef_step(g_dev, r_dev, t, worker, world, density, theta, out_idx, out_val)
+    r_or = res.copy()
+    o_idx, o_val, k_or, th_or, c_or = oracle.ef_step(g, r_or, t, worker, world, density, theta)
+    assert (k, th, cy) == (k_or, th_or, c_or)
+    assert np.array_equal(idx.cpu().numpy(), o_idx)
+    assert bits_equal(val.cpu().numpy(), o_val)
+    assert bits_equal(r_dev.cpu().numpy(), r_or)
+    # nothing written past k
+    assert bool((out_idx[k:] == -5).all()) and bool((out_val[k:] == -5.0).all())
+    sp.close()
+    return k
+
+
+@pytest.mark.parametrize("phase_shift", [0, 1, 3])
+@pytest.mark.parametrize("N,world", [(1, 1), (3, 8), (1023, 2), (4099, 3), (70_001, 7), (1_100_003, 5)])
+def test_ef_ragged_sizes_and_phases(N, world, phase_shift):
+    """Ragged partitions and outside ranges at every 16-byte phase, empty
+    partitions (N < world), every worker and several iterations."""
+    rng = np.random.default_rng(N * 31 + world + phase_shift)
+    for t in [0, 1, world + 1]:
+        for worker in sorted({0, world - 1, world // 2}):
+            g = rng.standard_normal(N).astype(np.float32)
+            res = (rng.standard_normal(N) * 0.5).astype(np.float32)
+            ef_gpu_vs_oracle(g, res, t, worker, world, 0.05, 1.5, phase_shift)
+
+
+def test_ef_special_values():
+    """NaN, infinities and subnormals outside and inside the partition."""
+    N, world = 40_000, 4
+    rng = np.random.default_rng(4)
+    g = rng.standard_normal(N).astype(np.float32)
+    res = np.zeros(N, np.float32)
+    tiny = np.float32(2.0) ** -149
+    for pos in [0, 9_999, 10_000, 19_999, 20_000, 39_999, 12_345, 31_000]:
+        g[pos] = rng.choice([np.nan, np.inf, -np.inf, tiny, -tiny])
+        res[pos + 1 if pos + 1 < N else pos - 1] = np.float32(np.inf)
+    for t in range(world):
+        ef_gpu_vs_oracle(g, res, t, 2, world, 0.01, 2.0)
+
+
+# ---------------------------------------------------------------------------
+# union gather / reset and the model update
+# ---------------------------------------------------------------------------
+
+def simulate_workers(N, world, steps, seed, exact=False):
+    """Algorithm 1 for `world` workers on one device: every worker runs the
+    full pass, the union of their selections is assembled on the host (the
+    all-gather), each worker gathers and resets through the library, the sums
+    (in worker order) update the model through the library; the oracle does
+    the same on host mirrors.  Returns the device and oracle states."""
+    rng = np.random.default_rng(seed)
+    sp = micro.Sparsifier(N, device=DEV)
+    if exact:
+        x0 = (rng.integers(-64, 64, N) / 8).astype(np.float32)
+    else:
+        x0 = rng.standard_normal(N).astype(np.float32)
+    x_dev = torch.from_numpy(x0.copy()).to(DEV)
+    x_or = x0.copy()
+    res_dev = [torch.zeros(N, dtype=torch.float32, device=DEV) for _ in range(world)]
+    res_or = [np.zeros(N, np.float32) for _ in range(world)]
+    theta = [1.0] * world
+    total = np.zeros(N, np.float64)
+    for t in range(steps):
+        if exact:
+            grads = [(rng.integers(-16, 17, N) / 8).astype(np.float32) for _ in range(world)]
+        else:
+            grads = [(rng.standard_normal(N) * np.exp(rng.uniform(-2, 2, N))).astype(np.float32)
+                     for _ in range(world)]
+        for gi in grads:
+            total += gi
+        accs = [oracle.accumulate(grads[i], res_or[i]) for i in range(world)]
+        own = []
+        for i in range(world):
+            g_dev = torch.from_numpy(grads[i]).to(DEV)
+            oi = torch.empty(N, dtype=torch.int32, device=DEV)
+            ov = torch.empty(N, dtype=torch.float32, device=DEV)
+            k, th, c, idx, val = sp.ef_step(g_dev, res_dev[i], t, i, world, 0.05, theta[i], oi, ov)
+            o_idx, o_val, k_or, th_or, c_or = oracle.ef_step(grads[i], res_or[i], t, i, world, 0.05, theta[i])
+            assert (k, th, c) == (k_or, th_or, c_or)
+            assert np.array_equal(idx.cpu().numpy(), o_idx)
+            theta[i] = th
+            own.append((c, idx.clone(), val.clone()))
+        # all-gather: the union in partition order is sorted
+        order = sorted(range(world), key=lambda i: own[i][0])
+        union = torch.cat([own[i][1] for i in order]) if world else None
+        first = {}
+        pos = 0
+        for i in order:
+            first[i] = pos
+            pos += own[i][1].numel()
+        union_np = union.cpu().numpy()
+        assert np.all(np.diff(union_np) > 0)
+        summed_dev = torch.zeros(union.numel(), dtype=torch.float32, device=DEV)
+        summed_or = np.zeros(union.numel(), np.float32)
+        for i in range(world):
+            gathered = sp.union_gather(res_dev[i], union, first[i], own[i][2])
+            o = oracle.gather(accs[i], union_np)
+            assert bits_equal(gathered.cpu().numpy(), o), f"gathered values of worker {i} step {t}"
+            oracle.zero(accs[i], union_np)
+            res_or[i] = accs[i]
+            assert bits_equal(res_dev[i].cpu().numpy(), res_or[i]), f"reset residual of worker {i} step {t}"
+            summed_dev = summed_dev + gathered
+            summed_or = (summed_or + o).astype(np.float32)
+        assert bits_equal(summed_dev.cpu().numpy(), summed_or)
+        sp.sparse_update(x_dev, union, summed_dev, world)
+        oracle.update(x_or, union_np, summed_or, world)
+        assert bits_equal(x_dev.cpu().numpy(), x_or), f"model after step {t}"
+    torch.cuda.synchronize()
+    sp.close()
+    return x0, x_dev.cpu().numpy(), [r.cpu().numpy() for r in res_dev], total
+
+
+@pytest.mark.parametrize("N,world", [(10_007, 3), (262_144, 4), (1_000_003, 8)])
+def test_union_gather_reset_update_parity(N, world):
+    note(f"union parity N={N} world={world}")
+    simulate_workers(N, world, 4, seed=N + world)
+
+
+def test_union_path_loses_nothing():
+    """With binary32-exact values (multiples of 1/8, n a power of two) the
+    device path keeps Sec. 2's identity exactly: the workers' local errors
+    plus n times the model's descent equal the sum of every gradient."""
+    world = 4
+    x0, x, res, total = simulate_workers(50_000, world, 5, seed=3, exact=True)
+    lhs = sum(r.astype(np.float64) for r in res) + world * (x0.astype(np.float64) - x.astype(np.float64))
+    assert np.array_equal(lhs, total)
+
+
+def test_union_out_of_range_indices_touch_nothing():
+    N = 5_000
+    sp = micro.Sparsifier(N, device=DEV)
+    res = torch.arange(N, dtype=torch.float32, device=DEV)
+    union = torch.tensor([3, 10, N, N + 7, 4_999], dtype=torch.int32, device=DEV)
+    own_val = torch.empty(0, dtype=torch.float32, device=DEV)
+    out = sp.union_gather(res, union, 0, own_val)
+    o = out.cpu().numpy()
+    assert o[0] == 3 and o[1] == 10 and np.isnan(o[2]) and np.isnan(o[3]) and o[4] == 4_999
+    r = res.cpu().numpy()
+    assert r[3] == 0 and r[10] == 0 and r[4_999] == 0 and r[4] == 4 and r[4_998] == 4_998
+    x = torch.ones(N, dtype=torch.float32, device=DEV)
+    sp.sparse_update(x, union, torch.full((5,), 2.0, device=DEV), 2)
+    xv = x.cpu().numpy()
+    assert xv[3] == 0 and xv[10] == 0 and xv[4_999] == 0 and np.sum(xv == 0) == 3
+    sp.close()
+
+
+def test_union_empty_and_all_own():
+    """m = 0 is a no-op; a union that is only the worker's own run copies
+    own_val and leaves the residual untouched."""
+    N = 3_000
+    sp = micro.Sparsifier(N, device=DEV)
+    res = torch.randn(N, device=DEV)
+    r0 = res.clone()
+    empty = torch.empty(0, dtype=torch.int32, device=DEV)
+    out = sp.union_gather(res, empty, 0, torch.empty(0, device=DEV))
+    assert out.numel() == 0
+    union = torch.arange(0, N, 7, dtype=torch.int32, device=DEV)
+    own_val = torch.randn(union.numel(), device=DEV)
+    out = sp.union_gather(res, union, 0, own_val)
+    assert torch.equal(out, own_val) and torch.equal(res, r0)
+    sp.close()
