@@ -53,7 +53,14 @@ def parse_args():
                     help="kernel schedule (staged is the library default)")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only run a plain device copy of known size (HBM counter scaling)")
-    return ap.parse_args()
+    ap.add_argument("--path", default="step", choices=["step", "ef", "union"],
+                    help="step: the partition-only sparsify step (default); ef: the full error-feedback "
+                         "pass with cyclic partitions; union: the gather/reset and model update around "
+                         "the exchange")
+    args = ap.parse_args()
+    if args.path != "step" and args.workload == "gpt_1p3b" and "--workload" not in sys.argv:
+        args.workload = "bert_large"  # world 1 makes both paths degenerate
+    return args
 
 
 def kernel_sha256():
@@ -215,6 +222,197 @@ def cpu_baseline(w, density, pool, target_s):
     }
 
 
+def _partition_lengths(w):
+    import paper_2310_00967_amd as micro
+    return [micro.micro_partition(w.n_total, c, w.world)[1] for c in range(w.world)]
+
+
+def measure_ef(w, density, pool, sp, warmup, steps):
+    """Full error-feedback passes of worker w.ranks[0] at iterations 0, 1, ...
+    (its searched partition rotates): 12 B per value of the whole vector plus
+    8 B per selected value."""
+    import torch
+    import paper_2310_00967_amd as micro
+    from paper_2310_00967_amd import synth
+    worker = w.ranks[0]
+    N = w.n_total
+    res = torch.zeros(N, dtype=torch.float32, device="cuda")
+    out_idx, out_val = sp.outputs(max(_partition_lengths(w)))
+    s, ln = micro.micro_partition(N, micro.micro_cycle(0, worker, w.world), w.world)
+    theta = synth.initial_theta(w, pool[0], s, s + ln, density)
+    log = []
+    t0 = time.perf_counter()
+    for t in range(warmup + steps):
+        if t == warmup:
+            torch.cuda.synchronize()
+            t0 = time.perf_counter()
+        g = pool[t % len(pool)]
+        k, theta, _, _, _ = sp.ef_step(g, res, t, worker, w.world, density, theta, out_idx, out_val)
+        if t >= warmup:
+            log.append((N, k, sp.last_stats()[0]))
+    torch.cuda.synchronize()
+    elapsed = time.perf_counter() - t0
+    alg = sum(12 * n + 8 * k for n, k, _ in log)
+    kernel_s = sum(ms for _, _, ms in log) / 1e3
+    return {"g_elem_s": sum(n for n, _, _ in log) / elapsed / 1e9, "wall_gbs": alg / elapsed / 1e9,
+            "kernel_gbs": alg / kernel_s / 1e9, "kernel_ms_avg": kernel_s * 1e3 / len(log),
+            "alg_bytes_per_launch": alg / len(log), "ms_per_step": elapsed * 1e3 / steps,
+            "k_avg": sum(k for _, k, _ in log) / len(log), "worker": worker}
+
+
+def build_union(w, density, g, sp):
+    """The union of all n workers' selections on gradient g (each partition at
+    its calibrated threshold), in partition order, and worker w.ranks[0]'s own
+    run in it at its first cycle."""
+    import torch
+    import paper_2310_00967_amd as micro
+    from paper_2310_00967_amd import synth
+    parts, own_first = [], 0
+    worker = w.ranks[0]
+    mine = micro.micro_cycle(0, worker, w.world)
+    for c in range(w.world):
+        s, ln = micro.micro_partition(w.n_total, c, w.world)
+        th = synth.initial_theta(w, g, s, s + ln, density)
+        res = torch.zeros(w.n_total, dtype=torch.float32, device="cuda")
+        k, _, idx, val = sp.step(g, res, c, w.world, density, th)
+        if c == mine:
+            own_first = sum(p[0].numel() for p in parts)
+            own_val = val.clone()
+        parts.append((idx.clone(), val.clone()))
+        del res
+    union = torch.cat([p[0] for p in parts])
+    return union, own_first, own_val
+
+
+def measure_union(w, density, g, sp, warmup, steps):
+    """Gather/reset (micro_union_gather) and model update (micro_sparse_update)
+    over the union of all workers' selections.  Algorithmic bytes per union
+    entry: gather 16 B outside the worker's own run (index, residual read,
+    output, residual reset), 8 B inside it (own value, output); update 16 B
+    (index, sum, parameter read and write)."""
+    import torch
+    union, own_first, own_val = build_union(w, density, g, sp)
+    m, k_own = union.numel(), own_val.numel()
+    res = (g * 0.5).contiguous()           # any accumulated values
+    x = torch.ones(w.n_total, dtype=torch.float32, device="cuda")
+    out = torch.empty(m, dtype=torch.float32, device="cuda")
+    log = []
+    t0 = time.perf_counter()
+    for t in range(warmup + steps):
+        if t == warmup:
+            torch.cuda.synchronize()
+            t0 = time.perf_counter()
+        sp.union_gather(res, union, own_first, own_val, out)
+        ms_g = sp.last_stats()[0]
+        sp.sparse_update(x, union, out, w.world)
+        ms_u = sp.last_stats()[0]
+        if t >= warmup:
+            log.append((ms_g, ms_u))
+    torch.cuda.synchronize()
+    elapsed = time.perf_counter() - t0
+    alg_g = 16 * (m - k_own) + 8 * k_own
+    alg_u = 16 * m
+    kg = sum(a for a, _ in log) / 1e3
+    ku = sum(b for _, b in log) / 1e3
+    return {"g_entries_s": m * steps / elapsed / 1e9, "union_len": m, "own_len": k_own,
+            "wall_gbs": (alg_g + alg_u) * steps / elapsed / 1e9,
+            "kernel_gbs": (alg_g + alg_u) * steps / (kg + ku) / 1e9,
+            "gather_ms_avg": kg * 1e3 / steps, "update_ms_avg": ku * 1e3 / steps,
+            "gather_gbs": alg_g * steps / kg / 1e9, "update_gbs": alg_u * steps / ku / 1e9,
+            "alg_bytes_per_launch": (alg_g + alg_u), "ms_per_step": elapsed * 1e3 / steps,
+            "union": union, "own_first": own_first, "own_val": own_val}
+
+
+def cpu_baseline_ef(w, density, pool, target_s):
+    """The oracle's full pass on the host, as cpu_baseline does for the step."""
+    import numpy as np
+    import torch
+    import oracle
+    from paper_2310_00967_amd import synth
+    N = w.n_total
+    worker = w.ranks[0]
+    res = np.zeros(N, np.float32)
+    g_host = torch.empty(N, dtype=torch.float32, pin_memory=True)
+    cap = max(_partition_lengths(w))
+    out = (np.empty(max(1, cap), np.int32), np.empty(max(1, cap), np.float32))
+    res[:] = 0.0
+    out[0][:] = 0
+    out[1][:] = 0.0
+    s, ln = oracle.partition(N, oracle.cycle(0, worker, w.world), w.world)
+    theta = synth.initial_theta(w, pool[0], s, s + ln, density)
+    spent, elems, steps = 0.0, 0, 0
+    while spent < target_s and steps < 10000:
+        g_host.copy_(pool[steps % len(pool)])
+        gn = g_host.numpy()
+        t0 = time.perf_counter()
+        _, _, _, theta, _ = oracle.ef_step(gn, res, steps, worker, w.world, density, theta, out=out)
+        spent += time.perf_counter() - t0
+        elems += N
+        steps += 1
+    return {"value": elems / spent / 1e9, "unit": "G elem/s", "cores": 1, "kind": "oracle",
+            "sample": (f"{steps} full pass(es) of {w.name} worker {worker} at d={density} ({elems} values, "
+                       f"{spent:.1f} s of single-threaded oracle time); host {cpu_model()}, "
+                       f"nproc {os.cpu_count()}")}
+
+
+def cpu_baseline_union(w, g, union_res, target_s):
+    """The oracle's gather, reset and update over the same union on the host."""
+    import numpy as np
+    import oracle
+    union = union_res["union"].cpu().numpy()
+    acc = (g * 0.5).cpu().numpy()
+    x = np.ones(w.n_total, np.float32)
+    spent, entries, reps = 0.0, 0, 0
+    while spent < target_s and reps < 10000:
+        t0 = time.perf_counter()
+        vals = oracle.gather(acc, union)
+        oracle.zero(acc, union)
+        oracle.update(x, union, vals, w.world)
+        spent += time.perf_counter() - t0
+        entries += union.size
+        reps += 1
+    return {"value": entries / spent / 1e9, "unit": "G entries/s", "cores": 1, "kind": "oracle",
+            "sample": (f"{reps} gather+reset+update pass(es) over a {union.size}-entry union of {w.name} "
+                       f"({spent:.1f} s of single-threaded oracle time); host {cpu_model()}, "
+                       f"nproc {os.cpu_count()}")}
+
+
+def main_path(args, w, head, pool, n_pool, sp):
+    """The JSON line of --path ef / --path union."""
+    common = {"n_gpus": 1, "steps": args.steps, "warmup": args.warmup, "higher_is_better": True,
+              "scaling": "weak", "vs_baseline": None, "dtype": "f32", "data": "synthetic"}
+    cfg = {"workload": w.name, "n_total": w.n_total, "world": w.world, "worker": w.ranks[0],
+           "density": head, "distribution": w.dist, "gradient_pool": n_pool,
+           "parallelism": "one worker on one GPU", "path": args.path}
+    if args.path == "ef":
+        r = measure_ef(w, head, pool, sp, args.warmup, args.steps)
+        cpu = cpu_baseline_ef(w, head, pool, args.cpu_seconds) if args.cpu_seconds > 0 else None
+        line = {"metric": "full error-feedback pass throughput (G elem/s of the whole vector, HBM GB/s % of peak)",
+                "value": r["g_elem_s"], "unit": "G elem/s", "ms_per_step": r["ms_per_step"], **common,
+                "config": cfg, "k_avg": r["k_avg"],
+                "roofline": {"bound": "hbm", "achieved": r["kernel_gbs"], "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                             "frac": r["kernel_gbs"] / HBM_PEAK_GBS, "traffic": None,
+                             "kernel": "accumulate_kernel + stream_kernel + scan_kernel + move_kernel "
+                                       "(one pass, event-timed together)",
+                             "kernel_ms_avg": r["kernel_ms_avg"], "alg_bytes_per_launch": r["alg_bytes_per_launch"]},
+                "cpu_baseline": cpu}
+    else:
+        r = measure_union(w, head, pool[0], sp, args.warmup, args.steps)
+        cpu = cpu_baseline_union(w, pool[0], r, args.cpu_seconds) if args.cpu_seconds > 0 else None
+        cfg.update({"union_len": r["union_len"], "own_len": r["own_len"]})
+        line = {"metric": "union gather/reset + model update throughput (G union entries/s, HBM GB/s % of peak)",
+                "value": r["g_entries_s"], "unit": "G entries/s", "ms_per_step": r["ms_per_step"], **common,
+                "config": cfg,
+                "roofline": {"bound": "hbm", "achieved": r["kernel_gbs"], "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                             "frac": r["kernel_gbs"] / HBM_PEAK_GBS, "traffic": None,
+                             "kernel": "union_gather_kernel + sparse_update_kernel (event-timed each)",
+                             "gather_ms_avg": r["gather_ms_avg"], "update_ms_avg": r["update_ms_avg"],
+                             "gather_gbs": r["gather_gbs"], "update_gbs": r["update_gbs"],
+                             "alg_bytes_per_launch": r["alg_bytes_per_launch"]},
+                "cpu_baseline": cpu}
+    print(json.dumps(line), flush=True)
+
+
 def main():
     args = parse_args()
     if args.gpus != 1:
@@ -244,6 +442,10 @@ def main():
     torch.cuda.synchronize()
     variant = micro.MICRO_VARIANT_STAGED if args.variant == "staged" else micro.MICRO_VARIANT_TICKET
     sp = micro.Sparsifier(w.n_total, device="cuda", time_kernel=True, variant=variant)
+    if args.path != "step":
+        main_path(args, w, head, pool, n_pool, sp)
+        sp.close()
+        return
 
     main_res = measure(w, head, pool, sp, micro, args.warmup, args.steps)
     extra = {}
