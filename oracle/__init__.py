@@ -76,6 +76,13 @@ def lib():
                                           ctypes.c_void_p, ctypes.c_int64,
                                           ctypes.c_int32]
         L.micro_oracle_update.restype = ctypes.c_int
+        L.micro_oracle_sumsq.argtypes = [ctypes.c_void_p, ctypes.c_int64, ctypes.c_int64]
+        L.micro_oracle_sumsq.restype = ctypes.c_double
+        L.micro_oracle_sweep.argtypes = [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int64,
+                                         ctypes.c_int32, ctypes.c_double, ctypes.POINTER(Rule),
+                                         ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p,
+                                         ctypes.c_void_p, ctypes.c_void_p]
+        L.micro_oracle_sweep.restype = ctypes.c_int
         _lib = L
     return _lib
 
@@ -253,3 +260,41 @@ def update(x, idx, sums, world):
     if lib().micro_oracle_update(x.ctypes.data, idx.ctypes.data, sums.ctypes.data,
                                  idx.size, int(world)) != 0:
         raise ValueError("world must be >= 1")
+
+
+def sumsq(residual, start=0, length=None):
+    """Squared L2 norm of residual[start:start+length] (binary64, index order)."""
+    _f32(residual, "residual")
+    if length is None:
+        length = residual.size - start
+    if start < 0 or length < 0 or start + length > residual.size:
+        raise ValueError("range outside the array")
+    return lib().micro_oracle_sumsq(residual.ctypes.data, int(start), int(length))
+
+
+def sweep(grad, residual, world, density, thetas, rule=None):
+    """Every partition of the vector searched once with its own threshold.
+    residual is updated in place.  Returns (idx, val, k[world], thetas_next,
+    sumsq[world]); idx/val are the partitions' selections concatenated in
+    index order."""
+    _f32(grad, "grad")
+    _f32(residual, "residual")
+    n_total = grad.size
+    if residual.size != n_total:
+        raise ValueError("grad and residual lengths differ")
+    th = np.ascontiguousarray(np.asarray(thetas, dtype=np.float64).copy())
+    if th.size != world:
+        raise ValueError("one threshold per partition")
+    out_idx = np.empty(max(n_total, 1), np.int32)
+    out_val = np.empty(max(n_total, 1), np.float32)
+    k = np.zeros(max(world, 1), np.int64)
+    sq = np.zeros(max(world, 1), np.float64)
+    r = rule if rule is not None else default_rule()
+    rc = lib().micro_oracle_sweep(grad.ctypes.data, residual.ctypes.data, n_total, int(world),
+                                  float(density), ctypes.byref(r), th.ctypes.data,
+                                  out_idx.ctypes.data, out_val.ctypes.data, k.ctypes.data,
+                                  sq.ctypes.data)
+    if rc != 0:
+        raise ValueError("invalid oracle sweep arguments")
+    total = int(k[:world].sum())
+    return out_idx[:total], out_val[:total], k[:world].copy(), th, sq[:world].copy()

@@ -202,3 +202,47 @@ int micro_oracle_update(float *x, const int32_t *idx, const float *sums,
     }
     return 0;
 }
+
+/* Sec. 2: the local error is the vector of accumulated, not yet selected
+ * gradients; its L2 norm is the paper's per-worker error (Eq. 1 averages it
+ * over the workers).  This returns the squared norm over one range. */
+double micro_oracle_sumsq(const float *residual, int64_t start, int64_t len)
+{
+    double sum = 0.0;
+    for (int64_t j = start; j < start + len; ++j) {
+        double v = (double)residual[j];
+        sum = sum + v * v;
+    }
+    return sum;
+}
+
+int micro_oracle_sweep(const float *grad, float *residual, int64_t n_total,
+                       int32_t world, double density,
+                       const micro_oracle_rule *rule, double *theta,
+                       int32_t *out_idx, float *out_val, int64_t *k,
+                       double *sumsq)
+{
+    if (grad == NULL || residual == NULL || rule == NULL || theta == NULL ||
+        k == NULL || world < 1 || n_total < 0)
+        return -1;
+    if (!(density > 0.0 && density <= 1.0))
+        return -1;
+    for (int32_t r = 0; r < world; ++r)
+        if (!(theta[r] > 0.0) || isinf(theta[r]))
+            return -1;
+    if (n_total > 0 && (out_idx == NULL || out_val == NULL))
+        return -1;
+    int64_t written = 0;
+    for (int32_t r = 0; r < world; ++r) {
+        int64_t start = 0, len = 0;
+        micro_oracle_partition(n_total, r, world, &start, &len);
+        int64_t kr = micro_oracle_select(grad, residual, start, len, theta[r],
+                                         out_idx + written, out_val + written);
+        theta[r] = micro_oracle_estimate(rule, density, len, kr, theta[r]);
+        k[r] = kr;
+        written = written + kr;
+        if (sumsq != NULL)
+            sumsq[r] = micro_oracle_sumsq(residual, start, len);
+    }
+    return 0;
+}

@@ -45,6 +45,13 @@
  *                           at the globally selected indices.
  *   micro_oracle_update     Algorithm 1 and Sec. 4.4, the model update with the
  *                           averaged (all-reduced sum divided by n) values.
+ *   micro_oracle_sumsq      Sec. 2 and Eq. 1: the square of the L2 norm of
+ *                           (part of) the local error, the quantity the paper
+ *                           averages over workers as its error measure.
+ *   micro_oracle_sweep      every partition of one vector searched once, each
+ *                           with its own threshold (the selections of all n
+ *                           workers of Sec. 4.2 over one vector), with the
+ *                           squared norm of each partition's local error.
  *
  * Precision: the accumulation is one binary32 addition (round to nearest even,
  * no fused multiply-add, subnormals kept); the threshold test compares the
@@ -144,6 +151,24 @@ void micro_oracle_zero(float *acc, const int32_t *idx, int64_t m);
  * or -1 for world < 1. */
 int micro_oracle_update(float *x, const int32_t *idx, const float *sums,
                         int64_t m, int32_t world);
+
+/* Sec. 2 and Eq. 1: sum over j in [start, start+len) of residual[j]^2, each
+ * square formed in binary64 (exact for a binary32 value) and added in index
+ * order in binary64. */
+double micro_oracle_sumsq(const float *residual, int64_t start, int64_t len);
+
+/* Every partition r of `world` over one vector, in increasing r: the
+ * partition step with threshold theta[r] (updated in place), its pairs
+ * appended to out_idx/out_val after those of the partitions before it (so the
+ * outputs are the concatenation in index order), k[r] its count, and, when
+ * sumsq is not NULL, sumsq[r] = micro_oracle_sumsq over the partition after
+ * its step.  out_idx and out_val must hold n_total entries.  Returns 0, or -1
+ * on invalid arguments (nothing written). */
+int micro_oracle_sweep(const float *grad, float *residual, int64_t n_total,
+                       int32_t world, double density,
+                       const micro_oracle_rule *rule, double *theta,
+                       int32_t *out_idx, float *out_val, int64_t *k,
+                       double *sumsq);
 
 #ifdef __cplusplus
 }

@@ -261,3 +261,100 @@ def test_algorithm1_loses_nothing(world):
         oracle.update(x, union, summed, world)
     lhs = sum(r.astype(np.float64) for r in res) + world * (x0.astype(np.float64) - x.astype(np.float64))
     assert np.array_equal(lhs, total)
+
+
+# ---------------------------------------------------------------------------
+# local error norm (Sec. 2, Eq. 1) and the sweep of every partition
+# ---------------------------------------------------------------------------
+
+U = 2.0 ** -53  # unit roundoff of binary64
+
+
+def order_bound(n, exact):
+    """Error bound of any binary64 summation order for n nonnegative terms."""
+    g = (n - 1) * U
+    return g / (1 - g) * exact if n > 1 else 0.0
+
+
+def test_sumsq_within_the_summation_bound_of_the_exact_sum():
+    import math
+    rng = np.random.default_rng(31)
+    for n in [1, 2, 17, 1000, 100_003]:
+        r = (rng.standard_normal(n) * np.exp(rng.uniform(-20, 20, n))).astype(np.float32)
+        exact = math.fsum(float(v) * float(v) for v in r.astype(np.float64))  # squares exact in binary64
+        got = oracle.sumsq(r)
+        assert abs(got - exact) <= order_bound(n, exact)
+        s, ln = min(3, n), max(0, n - 7)
+        ex2 = math.fsum(float(v) ** 2 for v in r[s:s + ln].astype(np.float64))
+        assert abs(oracle.sumsq(r, s, ln) - ex2) <= order_bound(ln, ex2)
+
+
+def test_sumsq_special_cases():
+    assert oracle.sumsq(np.zeros(1000, np.float32)) == 0.0
+    assert oracle.sumsq(np.zeros(0, np.float32)) == 0.0
+    x = np.float32(3.0000002)
+    assert oracle.sumsq(np.array([x], np.float32)) == float(x) * float(x)  # exact square
+    tiny = np.float32(2.0) ** -149
+    assert oracle.sumsq(np.array([tiny, -tiny], np.float32)) == 2.0 * 2.0 ** -298
+    ints = np.arange(-500, 501, dtype=np.float32)
+    assert oracle.sumsq(ints) == 2 * sum(i * i for i in range(501))
+    assert np.isnan(oracle.sumsq(np.array([1.0, np.nan], np.float32)))
+    assert oracle.sumsq(np.array([1.0, -np.inf], np.float32)) == np.inf
+    # binary32 squares that overflow binary32 stay finite in binary64
+    big = np.float32(3e38)
+    assert oracle.sumsq(np.array([big], np.float32)) == float(big) ** 2
+
+
+@pytest.mark.parametrize("n,world", [(0, 3), (5, 8), (1000, 1), (65_537, 4), (200_003, 16)])
+def test_sweep_matches_numpy_per_partition_filter(n, world):
+    rng = np.random.default_rng(n + 7 * world)
+    g = (rng.standard_normal(n) * np.exp(rng.uniform(-2, 2, n))).astype(np.float32)
+    res0 = (rng.standard_normal(n) * 0.3).astype(np.float32)
+    thetas = np.exp(rng.uniform(-1, 1.5, world))
+    res = res0.copy()
+    idx, val, k, th, sq = oracle.sweep(g, res, world, 0.02, thetas)
+    acc = g + res0
+    want_idx, want_k = [], []
+    new_res = acc.copy()
+    for r in range(world):
+        s, ln = oracle.partition(n, r, world)
+        sel = np.flatnonzero(np.abs(acc[s:s + ln]).astype(np.float64) >= thetas[r]) + s
+        want_idx.append(sel)
+        want_k.append(sel.size)
+        new_res[sel] = 0.0
+        assert th[r] == oracle.estimate(0.02, ln, sel.size, thetas[r])
+        exact_sq = float(np.sum(new_res[s:s + ln].astype(np.float64) ** 2))
+        assert abs(sq[r] - exact_sq) <= 2 * order_bound(ln, exact_sq)
+    want_idx = np.concatenate(want_idx) if want_idx else np.zeros(0, np.int64)
+    assert np.array_equal(idx, want_idx) and np.array_equal(k, want_k)
+    assert np.array_equal(val.view(np.uint32), acc[want_idx].view(np.uint32))
+    assert np.array_equal(res.view(np.uint32), new_res.view(np.uint32))
+
+
+def test_sweep_does_not_depend_on_partition_order():
+    """Partitions are disjoint: taking the steps in reverse order gives the
+    same residual, pairs and thresholds."""
+    n, world = 77_777, 6
+    rng = np.random.default_rng(12)
+    g = rng.standard_normal(n).astype(np.float32)
+    res0 = (rng.standard_normal(n) * 0.5).astype(np.float32)
+    thetas = [1.0 + 0.2 * r for r in range(world)]
+    res = res0.copy()
+    idx, val, k, th, sq = oracle.sweep(g, res, world, 0.05, thetas)
+    res2 = res0.copy()
+    parts = {}
+    for r in reversed(range(world)):
+        parts[r] = oracle.step(g, res2, r, world, 0.05, thetas[r])
+    assert np.array_equal(res.view(np.uint32), res2.view(np.uint32))
+    assert np.array_equal(idx, np.concatenate([parts[r][0] for r in range(world)]))
+    assert [parts[r][2] for r in range(world)] == list(k)
+    assert [parts[r][3] for r in range(world)] == list(th)
+
+
+def test_sweep_rejects_bad_arguments():
+    g = np.ones(10, np.float32)
+    r = np.zeros(10, np.float32)
+    for world, d, th in [(0, 0.1, []), (2, 0.0, [1, 1]), (2, 0.1, [1, 0]), (2, 0.1, [1, np.inf])]:
+        with pytest.raises(ValueError):
+            oracle.sweep(g, r, world, d, th)
+    assert not np.any(r)
