@@ -135,6 +135,32 @@ MICRO_API micro_status micro_sparsify_step(micro_ctx *ctx, const float *grad,
                                  double density, double *theta,
                                  int32_t *out_idx, float *out_val, int64_t *k);
 
+/*
+ * Every partition r of `world` (1 <= world <= 64) searched once over one
+ * vector, each with its own threshold, in one launch of each kernel: the
+ * selections all n workers make at one iteration (Sec. 4.2), with the local
+ * error of Sec. 2 / Eq. 1 reduced on the way.
+ *   grad, residual  device, n_total fp32; residual in/out over all of it.
+ *   theta      host double[world], in/out: theta[r] for partition r, then its
+ *              next threshold (Sec. 4.3 over P_r).  Each finite and > 0.
+ *   out_idx, out_val  device, n_total entries each: the selected (index, acc)
+ *              pairs of all partitions, concatenated in index order, so
+ *              partition r's pairs start at k[0] + ... + k[r-1].
+ *   k          host int64[world], out: each partition's count.
+ *   sumsq      host double[world] out, or NULL: the squared L2 norm of each
+ *              partition's new residual, squares in binary64 added in a fixed
+ *              order (within (P_r - 1) * 2^-53 relative of the exact sum);
+ *              sqrt of their sum is the vector's local error norm.
+ * The pairs, counts, thresholds and residual equal those of world calls of
+ * micro_sparsify_step (rank 0 .. world-1) bit for bit.  Needs the staged
+ * schedule.  Synchronous; errors as micro_sparsify_step (MICRO_EINVAL also
+ * for world above 64 or the ticket variant).
+ */
+MICRO_API micro_status micro_sweep_step(micro_ctx *ctx, const float *grad, float *residual,
+                                        int32_t world, double density, double *theta,
+                                        int32_t *out_idx, float *out_val, int64_t *k,
+                                        double *sumsq);
+
 /* Algorithm 1 (cyclic assignment of partitions; Sec. 4.1): the partition
  * number that worker `worker` of `world` searches at iteration t,
  * ((t mod n) + worker) mod n (pure host arithmetic).  Returns MICRO_EINVAL

@@ -3,6 +3,7 @@
     sp = Sparsifier(n_total)                       # on torch's current device/stream
     k, theta, idx, val = sp.step(grad, residual, rank, world, density, theta)
     k, theta, cycle, idx, val = sp.ef_step(grad, residual, t, worker, world, density, theta)
+    ks, thetas, sumsq, idx, val = sp.sweep(grad, residual, world, density, thetas)
     g = sp.union_gather(residual, union_idx, own_first, val)   # around the exchange
     sp.sparse_update(x, union_idx, summed, world)
 
@@ -120,6 +121,31 @@ class Sparsifier:
         k, th, c = _lib.micro_ef_step(self._ctx, grad.data_ptr(), residual.data_ptr(), t, worker, world,
                                       density, theta, out_idx.data_ptr(), out_val.data_ptr())
         return k, th, c, out_idx[:k], out_val[:k]
+
+    def sweep(self, grad, residual, world, density, thetas, out_idx=None, out_val=None, want_sumsq=True):
+        """Every partition of `world` searched once, each with its own
+        threshold, in one launch of each kernel.  Returns (k list, thetas_next
+        list, sumsq list or None, idx[:sum k], val[:sum k]); partition r's
+        pairs start at sum(k[:r])."""
+        import torch
+        if self._ctx is None:
+            raise RuntimeError("Sparsifier is closed")
+        self._check(grad, "grad", torch.float32)
+        self._check(residual, "residual", torch.float32)
+        if grad.numel() != self.n_total or residual.numel() != self.n_total:
+            raise ValueError(f"grad and residual must hold {self.n_total} values")
+        if len(thetas) != world:
+            raise ValueError("one threshold per partition")
+        if out_idx is None or out_val is None:
+            out_idx, out_val = self.outputs(self.n_total)
+        self._check(out_idx, "out_idx", torch.int32)
+        self._check(out_val, "out_val", torch.float32)
+        if out_idx.numel() < self.n_total or out_val.numel() < self.n_total:
+            raise ValueError(f"output capacity below n_total {self.n_total}")
+        k, th, sq = _lib.micro_sweep_step(self._ctx, grad.data_ptr(), residual.data_ptr(), world, density,
+                                          thetas, out_idx.data_ptr(), out_val.data_ptr(), want_sumsq)
+        total = sum(k)
+        return k, th, sq, out_idx[:total], out_val[:total]
 
     def union_gather(self, residual, union_idx, own_first, own_val, out=None):
         """The accumulated values at the union of the workers' selections and

@@ -42,6 +42,9 @@ SIGNATURES = {
                                            ctypes.c_int32, ctypes.c_int32, ctypes.c_double, _dblp,
                                            ctypes.c_void_p, ctypes.c_void_p, _i64p]),
     "micro_partition": (ctypes.c_int, [ctypes.c_int64, ctypes.c_int32, ctypes.c_int32, _i64p, _i64p]),
+    "micro_sweep_step": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int32,
+                                        ctypes.c_double, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p,
+                                        ctypes.c_void_p, ctypes.c_void_p]),
     "micro_cycle": (ctypes.c_int, [ctypes.c_int64, ctypes.c_int32, ctypes.c_int32, ctypes.POINTER(ctypes.c_int32)]),
     "micro_ef_step": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int64,
                                      ctypes.c_int32, ctypes.c_int32, ctypes.c_double, _dblp,
@@ -142,6 +145,26 @@ def micro_sparsify_step(ctx, grad_ptr, residual_ptr, rank, world, density, theta
                                     ctypes.byref(k))
     check(st, ctx)
     return k.value, th.value
+
+
+MICRO_MAX_SWEEP = 64
+
+
+def micro_sweep_step(ctx, grad_ptr, residual_ptr, world, density, thetas, out_idx_ptr, out_val_ptr,
+                     want_sumsq=True):
+    """Raw call with device addresses; returns (k list, thetas_next list,
+    sumsq list or None)."""
+    world = int(world)
+    th = (ctypes.c_double * max(1, world))(*[float(x) for x in thetas])
+    k = (ctypes.c_int64 * max(1, world))()
+    sq = (ctypes.c_double * max(1, world))() if want_sumsq else None
+    st = load().micro_sweep_step(ctx, ctypes.c_void_p(grad_ptr), ctypes.c_void_p(residual_ptr), world,
+                                 float(density), ctypes.cast(th, ctypes.c_void_p),
+                                 ctypes.c_void_p(out_idx_ptr), ctypes.c_void_p(out_val_ptr),
+                                 ctypes.cast(k, ctypes.c_void_p),
+                                 ctypes.cast(sq, ctypes.c_void_p) if sq is not None else None)
+    check(st, ctx)
+    return list(k[:world]), list(th[:world]), (list(sq[:world]) if sq is not None else None)
 
 
 def micro_cycle(t, worker, world):

@@ -29,6 +29,8 @@ struct micro_ctx {
     uint32_t* d_tile_excl = nullptr;
     uint32_t* d_flagged_list = nullptr;
     uint32_t* d_split_tile = nullptr;
+    double* d_tile_sumsq = nullptr;          // sweep: per tile
+    double* d_chunk_sumsq = nullptr;         // sweep: per chunk
     int64_t split_capacity = 0;
     uint2* d_stage = nullptr;                // (index, value bits) pairs
     uint64_t* d_chunk_status = nullptr;
@@ -37,8 +39,11 @@ struct micro_ctx {
     uint64_t* d_status = nullptr;
     unsigned long long* d_tickets = nullptr; // [0] tile ticket, [1] chunk ticket
     int64_t* d_count = nullptr;              // [0] selected count, [1] flagged tiles
-    int64_t* h_count = nullptr;              // mapped pinned host copy of d_count, stored by the kernels
+    int64_t* h_count = nullptr;              // mapped pinned host memory stored by the kernels: [0] k,
+                                             // [1] redone tiles, [2 + r] a sweep's counts
     int64_t* h_count_dev = nullptr;          // the device's address of h_count
+    double* h_sumsq = nullptr;               // mapped pinned host memory: a sweep's squared norms
+    double* h_sumsq_dev = nullptr;
     uint32_t epoch = 0;                      // epoch of the last launch
     bool needs_reset = false;                // scratch state unknown after a failure
     hipEvent_t ev[2] = {nullptr, nullptr};
@@ -137,12 +142,13 @@ void release(micro_ctx* ctx) {
     if (ctx->device >= 0) (void)hipStreamSynchronize(ctx->stream);
     for (hipEvent_t ev : ctx->ev)
         if (ev) (void)hipEventDestroy(ev);
-    void* device_buffers[] = {ctx->d_tile_counts, ctx->d_tile_excl, ctx->d_flagged_list, ctx->d_split_tile, ctx->d_stage,
+    void* device_buffers[] = {ctx->d_tile_counts, ctx->d_tile_excl, ctx->d_flagged_list, ctx->d_split_tile, ctx->d_tile_sumsq, ctx->d_chunk_sumsq, ctx->d_stage,
                               ctx->d_chunk_status, ctx->d_status, ctx->d_tickets,
                               ctx->d_count};
     for (void* p : device_buffers)
         if (p) (void)hipFree(p);
     if (ctx->h_count) (void)hipHostFree(ctx->h_count);
+    if (ctx->h_sumsq) (void)hipHostFree(ctx->h_sumsq);
     delete ctx;
 }
 
@@ -286,6 +292,148 @@ micro_status execute_step(micro_ctx* ctx, const float* grad, float* residual, in
     return MICRO_OK;
 }
 
+// Every partition of `world` searched once in one launch of each staged
+// kernel; the pairs of all partitions form one compaction in index order.
+micro_status execute_sweep(micro_ctx* ctx, const float* grad, float* residual, int32_t world, double density,
+                           double* theta, int32_t* out_idx, float* out_val, int64_t* k, double* sumsq) {
+    if (!grad || !residual || !theta || !out_idx || !out_val || !k) {
+        set_error(ctx, "NULL pointer argument");
+        return MICRO_EINVAL;
+    }
+    if (world < 1 || world > micro::kMaxSweep) {
+        set_error(ctx, "sweep world %d outside [1, %d]", world, micro::kMaxSweep);
+        return MICRO_EINVAL;
+    }
+    if (!ctx->staged) {
+        set_error(ctx, "the sweep needs the staged schedule");
+        return MICRO_EINVAL;
+    }
+    if (!density_valid(density)) {
+        set_error(ctx, "density %g outside (0, 1]", density);
+        return MICRO_EINVAL;
+    }
+    for (int32_t r = 0; r < world; ++r)
+        if (!theta_valid(theta[r])) {
+            set_error(ctx, "threshold %g of partition %d is not finite and positive", theta[r], r);
+            return MICRO_EINVAL;
+        }
+    if (misaligned4({grad, residual, out_idx, out_val})) {
+        set_error(ctx, "buffers must be 4-byte aligned");
+        return MICRO_EINVAL;
+    }
+    const size_t nb = static_cast<size_t>(ctx->n_total) * sizeof(float);
+    const void* regions[4] = {grad, residual, out_idx, out_val};
+    for (int i = 0; i < 4; ++i)
+        for (int j = i + 1; j < 4; ++j)
+            if (nb > 0 && ranges_overlap(regions[i], nb, regions[j], nb)) {
+                set_error(ctx, "grad, residual and output ranges overlap");
+                return MICRO_EINVAL;
+            }
+    if (ctx->n_total == 0) {
+        for (int32_t r = 0; r < world; ++r) {
+            k[r] = 0;
+            if (sumsq) sumsq[r] = 0.0;
+        }
+        return MICRO_OK;
+    }
+    if (ctx->needs_reset || ctx->epoch >= micro::kMaxEpoch) {
+        micro_status st = reset_scratch(ctx);
+        if (st != MICRO_OK) return st;
+    }
+    const bool vec4 = ((reinterpret_cast<uintptr_t>(grad) ^ reinterpret_cast<uintptr_t>(residual)) & 15u) == 0;
+    micro::SweepTable table{};
+    table.count = static_cast<uint32_t>(world);
+    int64_t lens[micro::kMaxSweep];
+    int64_t tiles = 0, chunks = 0;
+    for (int32_t r = 0; r < world; ++r) {
+        int64_t start = 0, len = 0;
+        (void)micro_partition(ctx->n_total, r, world, &start, &len);
+        lens[r] = len;
+        micro::SweepSegment& sg = table.seg[r];
+        sg.start = start;
+        sg.end = start + len;
+        sg.base = micro::tile_base_for(grad, start, vec4);
+        sg.theta_f = threshold_as_f32(theta[r]);
+        sg.tile_first = static_cast<uint32_t>(tiles);
+        sg.chunk_first = static_cast<uint32_t>(chunks);
+        const int64_t seg_tiles = len > 0 ? (sg.end - sg.base + micro::kStreamTile - 1) / micro::kStreamTile : 0;
+        tiles += seg_tiles;
+        chunks += (seg_tiles + micro::kChunkTiles - 1) / micro::kChunkTiles;
+    }
+    table.seg[world].tile_first = static_cast<uint32_t>(tiles);
+    table.seg[world].chunk_first = static_cast<uint32_t>(chunks);
+    if (tiles > ctx->tile_capacity || chunks > ctx->chunk_capacity) {
+        set_error(ctx, "sweep needs %lld tiles, scratch holds %lld", static_cast<long long>(tiles),
+                  static_cast<long long>(ctx->tile_capacity));
+        return MICRO_ECAPACITY;
+    }
+    micro::LaunchArgs a{};
+    a.grad = grad;
+    a.residual = residual;
+    a.out_idx = out_idx;
+    a.out_val = out_val;
+    a.epoch = ctx->epoch + 1;
+    a.num_tiles = static_cast<uint32_t>(tiles);
+    a.count_out = ctx->d_count;
+    a.host_count = ctx->h_count_dev;
+    a.tile_counts = ctx->d_tile_counts;
+    a.tile_excl = ctx->d_tile_excl;
+    a.flagged_list = ctx->d_flagged_list;
+    a.split_tile = ctx->d_split_tile;
+    a.tile_sumsq = ctx->d_tile_sumsq;
+    a.chunk_sumsq = ctx->d_chunk_sumsq;
+    a.host_sumsq = ctx->h_sumsq_dev;
+    {
+        const int64_t pieces = (tiles + ctx->n_total + micro::kMoveSpan - 1) / micro::kMoveSpan;
+        int64_t blocks = pieces < micro::kMoveGrid ? pieces : micro::kMoveGrid;
+        if (blocks < world) blocks = world;  // workgroup r reduces segment r's squared norm
+        a.move_blocks = static_cast<uint32_t>(blocks);
+    }
+    a.stage = ctx->d_stage;
+    a.num_chunks = static_cast<uint32_t>(chunks);
+    a.chunk_status = ctx->d_chunk_status;
+    a.chunk_ticket = &ctx->d_tickets[1];
+
+    hipError_t e;
+    const bool timed = (ctx->cfg.flags & MICRO_FLAG_TIME_KERNEL) != 0;
+    ctx->stats.kernel_ms = -1.0f;
+    ctx->stats.redone_tiles = 0;
+    volatile int64_t* host_count = ctx->h_count;
+    volatile double* host_sumsq = ctx->h_sumsq;
+    for (int i = 0; i < 2 + world; ++i) host_count[i] = -1;
+    for (int32_t r = 0; r < world; ++r) host_sumsq[r] = -1.0;
+    if (timed && (e = hipEventRecord(ctx->ev[0], ctx->stream)) != hipSuccess)
+        return hip_fail(ctx, e, "hipEventRecord");
+    ctx->epoch = a.epoch;
+    if ((e = micro::launch_sweep(a, table, vec4, ctx->stream)) != hipSuccess)
+        return hip_fail(ctx, e, "sweep kernel launch");
+    if (timed && (e = hipEventRecord(ctx->ev[1], ctx->stream)) != hipSuccess)
+        return hip_fail(ctx, e, "hipEventRecord");
+    if ((e = hipStreamSynchronize(ctx->stream)) != hipSuccess) return hip_fail(ctx, e, "hipStreamSynchronize");
+    int64_t sum = 0;
+    bool ok = host_count[0] >= 0 && host_count[0] <= ctx->n_total;
+    for (int32_t r = 0; ok && r < world; ++r) {
+        const int64_t kr = host_count[2 + r];
+        ok = kr >= 0 && kr <= lens[r] && host_sumsq[r] != -1.0;  // a NaN residual gives a NaN norm
+        sum += kr;
+    }
+    if (!ok || sum != host_count[0]) {
+        set_error(ctx, "device reported inconsistent sweep counts (total %lld)",
+                  static_cast<long long>(host_count[0]));
+        ctx->needs_reset = true;
+        return MICRO_EHIP;
+    }
+    if (timed && (e = hipEventElapsedTime(&ctx->stats.kernel_ms, ctx->ev[0], ctx->ev[1])) != hipSuccess)
+        return hip_fail(ctx, e, "hipEventElapsedTime");
+    ctx->stats.redone_tiles = host_count[1];
+    for (int32_t r = 0; r < world; ++r) {
+        k[r] = host_count[2 + r];
+        theta[r] = next_threshold(ctx->cfg, density, lens[r], k[r], theta[r]);
+        if (sumsq) sumsq[r] = host_sumsq[r];
+    }
+    return MICRO_OK;
+}
+
 // Enqueues one union kernel on the context's stream.  With the timing flag
 // the call waits for it and records its duration; otherwise it returns after
 // the launch.
@@ -398,18 +546,24 @@ micro_status micro_sparsify_init(micro_ctx** out, int64_t n_total, void* hip_str
     ctx->staged = c.variant != MICRO_VARIANT_TICKET;
     bool ok = hipMalloc(&ctx->d_tickets, 2 * sizeof(unsigned long long)) == hipSuccess &&
               hipMalloc(&ctx->d_count, 2 * sizeof(int64_t)) == hipSuccess &&
-              hipHostMalloc(&ctx->h_count, 2 * sizeof(int64_t), hipHostMallocMapped | hipHostMallocCoherent) ==
-                  hipSuccess &&
-              hipHostGetDevicePointer(reinterpret_cast<void**>(&ctx->h_count_dev), ctx->h_count, 0) == hipSuccess;
+              hipHostMalloc(&ctx->h_count, (2 + micro::kMaxSweep) * sizeof(int64_t),
+                            hipHostMallocMapped | hipHostMallocCoherent) == hipSuccess &&
+              hipHostGetDevicePointer(reinterpret_cast<void**>(&ctx->h_count_dev), ctx->h_count, 0) == hipSuccess &&
+              hipHostMalloc(&ctx->h_sumsq, micro::kMaxSweep * sizeof(double),
+                            hipHostMallocMapped | hipHostMallocCoherent) == hipSuccess &&
+              hipHostGetDevicePointer(reinterpret_cast<void**>(&ctx->h_sumsq_dev), ctx->h_sumsq, 0) == hipSuccess;
     if (ok && ctx->staged) {
-        ctx->tile_capacity = n_total / micro::kStreamTile + 2;
-        ctx->chunk_capacity = ctx->tile_capacity / micro::kChunkTiles + 2;
+        // a sweep's segments each add at most one tile (alignment) and one chunk
+        ctx->tile_capacity = n_total / micro::kStreamTile + 2 + micro::kMaxSweep;
+        ctx->chunk_capacity = ctx->tile_capacity / micro::kChunkTiles + 2 + micro::kMaxSweep;
         ctx->split_capacity = (ctx->tile_capacity + n_total) / micro::kMoveSpan + 2;
         const size_t stage = static_cast<size_t>(ctx->tile_capacity) * micro::kStageCap;
         ok = hipMalloc(&ctx->d_tile_counts, sizeof(uint32_t) * ctx->tile_capacity) == hipSuccess &&
              hipMalloc(&ctx->d_tile_excl, sizeof(uint32_t) * ctx->tile_capacity) == hipSuccess &&
              hipMalloc(&ctx->d_flagged_list, sizeof(uint32_t) * ctx->tile_capacity) == hipSuccess &&
              hipMalloc(&ctx->d_split_tile, sizeof(uint32_t) * ctx->split_capacity) == hipSuccess &&
+             hipMalloc(&ctx->d_tile_sumsq, sizeof(double) * ctx->tile_capacity) == hipSuccess &&
+             hipMalloc(&ctx->d_chunk_sumsq, sizeof(double) * ctx->chunk_capacity) == hipSuccess &&
              hipMalloc(&ctx->d_stage, sizeof(uint2) * stage) == hipSuccess &&
              hipMalloc(&ctx->d_chunk_status, sizeof(uint64_t) * ctx->chunk_capacity) == hipSuccess;
     } else if (ok) {
@@ -455,6 +609,15 @@ micro_status micro_sparsify_step(micro_ctx* ctx, const float* grad, float* resid
         return MICRO_EINVAL;
     }
     return execute_step(ctx, grad, residual, start, len, false, density, theta, out_idx, out_val, k);
+}
+
+micro_status micro_sweep_step(micro_ctx* ctx, const float* grad, float* residual, int32_t world, double density,
+                              double* theta, int32_t* out_idx, float* out_val, int64_t* k, double* sumsq) {
+    if (!ctx) {
+        set_error(nullptr, "ctx is NULL");
+        return MICRO_EINVAL;
+    }
+    return execute_sweep(ctx, grad, residual, world, density, theta, out_idx, out_val, k, sumsq);
 }
 
 micro_status micro_cycle(int64_t t, int32_t worker, int32_t world, int32_t* cycle) {

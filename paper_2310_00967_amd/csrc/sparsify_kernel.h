@@ -34,6 +34,28 @@ constexpr int kTicketTile = 4096;
 constexpr int kEpochShift = 34;
 constexpr uint32_t kMaxEpoch = (1u << 30) - 1;
 
+// Sweep of every partition of one vector with one launch of each staged
+// kernel: the partitions are segments of the tile sequence (each with its own
+// threshold, range and tile grid), and scan chunks never straddle two of them.
+// The pairs of all segments form one compaction in index order.
+constexpr int kMaxSweep = 64;
+
+struct SweepSegment {
+    int64_t start;          // partition [start, end)
+    int64_t end;
+    int64_t base;           // global index of the segment's first tile's first value
+    float theta_f;          // the segment's binary32 threshold
+    uint32_t tile_first;    // first global tile of the segment
+    uint32_t chunk_first;   // first global scan chunk of the segment
+    uint32_t pad;
+};
+
+struct SweepTable {
+    uint32_t count;                       // segments
+    uint32_t pad;
+    SweepSegment seg[kMaxSweep + 1];      // seg[count]: tile_first / chunk_first = the totals
+};
+
 struct LaunchArgs {
     const float* grad;      // device, global indexing
     float* residual;        // device, global indexing
@@ -46,12 +68,16 @@ struct LaunchArgs {
     uint32_t epoch;         // 1 .. kMaxEpoch
     uint32_t num_tiles;     // tiles covering [base, end)
     int64_t* count_out;     // device: [0] selected count, [1] flagged tiles (redone by the move kernel)
-    int64_t* host_count;    // mapped pinned host memory: the final count_out, stored by the last kernel
+    int64_t* host_count;    // mapped pinned host memory: the final count_out, stored by the last kernel;
+                            // a sweep adds each segment's count from [2] on
     // staged schedule
     uint32_t* tile_counts;  // num_tiles counts (bit 31: tile left to the scan kernel)
     uint32_t* tile_excl;    // num_tiles output offsets (bit 31: flagged tile)
     uint32_t* flagged_list; // count_out[1] flagged tiles, in no particular order
     uint32_t* split_tile;   // >= ceil((num_tiles + P) / kMoveSpan) tiles holding each piece's first item
+    double* tile_sumsq;     // sweep: per tile, squared norm of its new residual (binary64)
+    double* chunk_sumsq;    // sweep: per chunk, the sum of its tiles' squared norms
+    double* host_sumsq;     // sweep: mapped host memory, one squared norm per segment
     uint32_t move_blocks;   // workgroups of the move kernel
     uint2* stage;           // num_tiles * kStageCap staged (index, value bits) pairs
     uint32_t num_chunks;    // ceil(num_tiles / kChunkTiles)
@@ -84,6 +110,8 @@ int64_t tile_base_for(const float* grad, int64_t start, bool vec4);
 // the scalar-load kernels.  Each returns the launch status.
 hipError_t launch_staged(const LaunchArgs& args, bool vec4, hipStream_t stream);
 hipError_t launch_ticket(const LaunchArgs& args, bool vec4, hipStream_t stream);
+// The sweep: num_tiles / num_chunks are the totals over the table's segments.
+hipError_t launch_sweep(const LaunchArgs& args, const SweepTable& table, bool vec4, hipStream_t stream);
 hipError_t launch_accumulate(const AccumulateArgs& args, bool vec4, hipStream_t stream);
 
 // Union kernels (union_kernel.hip).  Gather and reset at the union of the

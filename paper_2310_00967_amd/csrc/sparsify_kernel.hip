@@ -331,22 +331,95 @@ __device__ __forceinline__ uint32_t draw_ticket(unsigned long long* counter, uin
     return drawn;
 }
 
-template <int VEC, int ROWS>
-__global__ __launch_bounds__(kStreamBlock) void stream_kernel(LaunchArgs a) {
+// Segment of a sweep holding global tile `tile` (or scan chunk `chunk`): the
+// last segment whose first tile (chunk) is <= it, so empty segments are
+// skipped.  Uniform binary search over the table in the kernel arguments.
+__device__ __forceinline__ uint32_t segment_of_tile(const SweepTable* tbl, uint32_t tile) {
+    uint32_t lo = 0, hi = tbl->count;
+    while (hi - lo > 1) {
+        const uint32_t mid = (lo + hi) / 2;
+        if (tbl->seg[mid].tile_first <= tile)
+            lo = mid;
+        else
+            hi = mid;
+    }
+    return lo;
+}
+
+__device__ __forceinline__ uint32_t segment_of_chunk(const SweepTable* tbl, uint32_t chunk) {
+    uint32_t lo = 0, hi = tbl->count;
+    while (hi - lo > 1) {
+        const uint32_t mid = (lo + hi) / 2;
+        if (tbl->seg[mid].chunk_first <= chunk)
+            lo = mid;
+        else
+            hi = mid;
+    }
+    return lo;
+}
+
+// A sweep segment's range and threshold in the fields the tile helpers read;
+// returns the global index of the first value of the segment's tile `tile`.
+__device__ __forceinline__ int64_t enter_segment(LaunchArgs& a, const SweepTable* tbl, uint32_t tile) {
+    const SweepSegment& sg = tbl->seg[segment_of_tile(tbl, tile)];
+    a.start = sg.start;
+    a.end = sg.end;
+    a.theta_f = sg.theta_f;
+    return sg.base + static_cast<int64_t>(tile - sg.tile_first) * kStreamTile;
+}
+
+// Sum over the workgroup of one binary64 value per thread, in a fixed order
+// (a butterfly inside each wavefront, then the wavefronts in order); the
+// result is valid in thread 0.  Contains one barrier.
+template <int WAVES>
+__device__ __forceinline__ double block_sum(double v, int lane, int wave, double* s_part) {
+#pragma unroll
+    for (int off = 32; off > 0; off >>= 1) v += __shfl_xor(v, off, kWaveSize);
+    if (lane == 0) s_part[wave] = v;
+    __syncthreads();
+    double total = 0.0;
+    if (wave == 0 && lane == 0) {
+#pragma unroll
+        for (int w = 0; w < WAVES; ++w) total += s_part[w];
+    }
+    return total;
+}
+
+// Stream pass over one tile (see the file comment).  In a sweep the tile's
+// segment supplies range and threshold, and the tile also stores the squared
+// norm of its new residual (also for a tile left to the move kernel, whose
+// new residual is fixed by its selection bits all the same).
+template <int VEC, int ROWS, bool SWEEP>
+__device__ __forceinline__ void stream_tile(LaunchArgs a, const SweepTable* tbl) {
     constexpr int WAVES = kStreamBlock / kWaveSize;
     static_assert(VEC * ROWS * kStreamBlock == kStreamTile, "tile size");
     __shared__ uint32_t s_wave_total[ROWS * WAVES];
     __shared__ uint2 s_pair[kStageCap];  // (index, value bits)
+    __shared__ double s_sq[WAVES];
 
     const int tid = threadIdx.x;
     const int lane = tid & (kWaveSize - 1);
     const int wave = tid / kWaveSize;
     const uint32_t tile = blockIdx.x;
+    const int64_t tile_base = SWEEP ? enter_segment(a, tbl, tile) : a.base + static_cast<int64_t>(tile) * kStreamTile;
 
     Tile<VEC, ROWS, kStreamBlock> t;
     uint32_t lane_rank[ROWS], row_count[ROWS], row_base[ROWS];
-    load_tile<VEC, ROWS, kStreamBlock, true>(a, a.base + static_cast<int64_t>(tile) * kStreamTile, tid, t);
+    load_tile<VEC, ROWS, kStreamBlock, true>(a, tile_base, tid, t);
     const uint32_t sel = compute_tile(a, tid, t);
+    if constexpr (SWEEP) {
+        double sq = 0.0;
+#pragma unroll
+        for (int r = 0; r < ROWS; ++r)
+#pragma unroll
+            for (int c = 0; c < VEC; ++c) {
+                const int64_t i = elem_index(t, r, tid, c);
+                const double v = selected<VEC>(sel, r, c) ? 0.0 : static_cast<double>(t.v[r][c]);
+                if (i >= a.start && i < a.end) sq += v * v;
+            }
+        const double total = block_sum<WAVES>(sq, lane, wave, s_sq);
+        if (tid == 0) a.tile_sumsq[tile] = total;
+    }
     wave_ranks<VEC, ROWS>(sel, lane_rank, row_count);
     const uint32_t count = tile_ranks<ROWS, WAVES>(row_count, lane, wave, s_wave_total, row_base);
     if (tile == 0 && tid == 0) a.count_out[1] = 0;  // the scan kernel adds the flagged tiles
@@ -375,15 +448,25 @@ __global__ __launch_bounds__(kStreamBlock) void stream_kernel(LaunchArgs a) {
     if (tid == 0) a.tile_counts[tile] = count;
 }
 
+template <int VEC, int ROWS>
+__global__ __launch_bounds__(kStreamBlock) void stream_kernel(LaunchArgs a) {
+    stream_tile<VEC, ROWS, false>(a, nullptr);
+}
+
+template <int VEC, int ROWS>
+__global__ __launch_bounds__(kStreamBlock) void stream_sweep_kernel(LaunchArgs a, SweepTable tbl) {
+    stream_tile<VEC, ROWS, true>(a, &tbl);
+}
+
 // Full processing of one flagged tile by one wavefront with its pairs from
 // position out_base on: the tile's values in index order, 256 at a time (one
-// part in registers keeps the move kernel's register budget).
+// part in registers keeps the move kernel's register budget).  a carries the
+// tile's range and threshold; tile_base is its first value's global index.
 template <int VEC>
-__device__ void redo_tile(const LaunchArgs& a, uint32_t tile, int lane, uint32_t out_base) {
+__device__ void redo_tile(const LaunchArgs& a, int64_t tile_base, int lane, uint32_t out_base) {
     constexpr int ROWS = 4 / VEC;
     using T = Tile<VEC, ROWS, kWaveSize>;
     static_assert(kStreamTile % T::kElems == 0, "whole parts");
-    const int64_t tile_base = a.base + static_cast<int64_t>(tile) * kStreamTile;
     uint32_t run = out_base;
 #pragma unroll 1
     for (int part = 0; part < kStreamTile / T::kElems; ++part) {
@@ -410,13 +493,18 @@ __device__ void redo_tile(const LaunchArgs& a, uint32_t tile, int lane, uint32_t
 // (bit 31: flagged tile), records for every move piece the tile that holds
 // its first item, and appends the chunk's flagged tiles to the list that the
 // move kernel redoes.
-__global__ __launch_bounds__(kScanBlock) void scan_kernel(LaunchArgs a) {
+// In a sweep the chunk lies inside one segment (chunks never straddle two)
+// and also sums its tiles' squared norms; the look-back and the offsets are
+// global, since the segments' pairs form one compaction in index order.
+template <bool SWEEP>
+__device__ __forceinline__ void scan_chunk(const LaunchArgs& a, const SweepTable* tbl) {
     constexpr int WAVES = kScanBlock / kWaveSize;
     constexpr int PER_THREAD = kChunkTiles / kScanBlock;
     static_assert(PER_THREAD % 4 == 0, "whole uint4s of counts per thread");
     __shared__ uint32_t s_chunk, s_exclusive, s_num_flagged, s_list_base;
     __shared__ uint32_t s_wave_total[WAVES];
     __shared__ uint32_t s_flagged[kChunkTiles];
+    __shared__ double s_sq[WAVES];
 
     const int tid = threadIdx.x;
     const int lane = tid & (kWaveSize - 1);
@@ -428,10 +516,18 @@ __global__ __launch_bounds__(kScanBlock) void scan_kernel(LaunchArgs a) {
     __syncthreads();
     const uint32_t chunk = s_chunk;
     if (chunk >= a.num_chunks) return;  // only reachable if the counter was not rearmed
-    const uint32_t first_tile = chunk * kChunkTiles + tid * PER_THREAD;
+    uint32_t chunk_tile = chunk * kChunkTiles, end_tile = a.num_tiles;
+    if constexpr (SWEEP) {
+        const uint32_t r = segment_of_chunk(tbl, chunk);
+        chunk_tile = tbl->seg[r].tile_first + (chunk - tbl->seg[r].chunk_first) * kChunkTiles;
+        const uint32_t seg_end = tbl->seg[r + 1].tile_first;
+        end_tile = chunk_tile + kChunkTiles < seg_end ? chunk_tile + kChunkTiles : seg_end;
+    }
+    const uint32_t first_tile = chunk_tile + tid * PER_THREAD;
+    const bool whole = first_tile % 4 == 0 && first_tile + PER_THREAD <= end_tile;
 
     uint32_t raw[PER_THREAD];
-    if (first_tile + PER_THREAD <= a.num_tiles) {
+    if (whole) {
 #pragma unroll
         for (int i = 0; i < PER_THREAD; i += 4) {
             const uint4 v = *reinterpret_cast<const uint4*>(a.tile_counts + first_tile + i);
@@ -442,7 +538,15 @@ __global__ __launch_bounds__(kScanBlock) void scan_kernel(LaunchArgs a) {
         }
     } else {
 #pragma unroll
-        for (int i = 0; i < PER_THREAD; ++i) raw[i] = first_tile + i < a.num_tiles ? a.tile_counts[first_tile + i] : 0u;
+        for (int i = 0; i < PER_THREAD; ++i) raw[i] = first_tile + i < end_tile ? a.tile_counts[first_tile + i] : 0u;
+    }
+    if constexpr (SWEEP) {
+        double sq = 0.0;
+#pragma unroll
+        for (int i = 0; i < PER_THREAD; ++i)
+            if (first_tile + i < end_tile) sq += a.tile_sumsq[first_tile + i];
+        const double total = block_sum<WAVES>(sq, lane, wave, s_sq);
+        if (tid == 0) a.chunk_sumsq[chunk] = total;
     }
     uint32_t mine = 0;
 #pragma unroll
@@ -486,7 +590,7 @@ __global__ __launch_bounds__(kScanBlock) void scan_kernel(LaunchArgs a) {
         // The move piece whose first item falls among this tile's items: the
         // tile's own item sits at tile + pos in the merged sequence and its
         // count pairs follow it; count < kMoveSpan, so there is at most one.
-        if (first_tile + i < a.num_tiles) {
+        if (first_tile + i < end_tile) {
             const uint64_t item = static_cast<uint64_t>(first_tile + i) + pos;
             const uint64_t m = (item + kMoveSpan - 1) / kMoveSpan;
             if (m * kMoveSpan < item + 1 + count) a.split_tile[m] = first_tile + i;
@@ -494,7 +598,7 @@ __global__ __launch_bounds__(kScanBlock) void scan_kernel(LaunchArgs a) {
         if (raw[i] & kOverflow) s_flagged[atomicAdd(&s_num_flagged, 1u)] = first_tile + i;
         pos += count;
     }
-    if (first_tile + PER_THREAD <= a.num_tiles) {
+    if (whole) {
 #pragma unroll
         for (int i = 0; i < PER_THREAD; i += 4)
             *reinterpret_cast<uint4*>(a.tile_excl + first_tile + i) =
@@ -502,7 +606,7 @@ __global__ __launch_bounds__(kScanBlock) void scan_kernel(LaunchArgs a) {
     } else {
 #pragma unroll
         for (int i = 0; i < PER_THREAD; ++i)
-            if (first_tile + i < a.num_tiles) a.tile_excl[first_tile + i] = offs[i];
+            if (first_tile + i < end_tile) a.tile_excl[first_tile + i] = offs[i];
     }
     __syncthreads();
     const uint32_t flagged = s_num_flagged;
@@ -512,6 +616,12 @@ __global__ __launch_bounds__(kScanBlock) void scan_kernel(LaunchArgs a) {
                                                       static_cast<unsigned long long>(flagged)));
     __syncthreads();
     for (uint32_t f = tid; f < flagged; f += kScanBlock) a.flagged_list[s_list_base + f] = s_flagged[f];
+}
+
+__global__ __launch_bounds__(kScanBlock) void scan_kernel(LaunchArgs a) { scan_chunk<false>(a, nullptr); }
+
+__global__ __launch_bounds__(kScanBlock) void scan_sweep_kernel(LaunchArgs a, SweepTable tbl) {
+    scan_chunk<true>(a, &tbl);
 }
 
 // Number of output pairs before item x of the merged sequence, given the tile
@@ -568,8 +678,8 @@ __device__ __forceinline__ void block_max_scan(uint16_t* v, uint32_t n, int tid,
 // coalesced write.  Before its pieces, every workgroup redoes its share of the
 // flagged tiles, so a dense region of the partition costs the whole grid a
 // second pass over it rather than one workgroup a serial one.
-template <int VEC>
-__global__ __launch_bounds__(kMoveBlock) void move_kernel(LaunchArgs a) {
+template <int VEC, bool SWEEP>
+__device__ __forceinline__ void move_pieces(const LaunchArgs& a, const SweepTable* tbl) {
     constexpr uint32_t kWindow = kMoveSpan + 1;
     constexpr int WAVES = kMoveBlock / kWaveSize;
     static_assert(kWindow <= 65536, "window indices fit in 16 bits");
@@ -577,21 +687,48 @@ __global__ __launch_bounds__(kMoveBlock) void move_kernel(LaunchArgs a) {
     __shared__ uint32_t s_flag_bits[(kWindow + 31) / 32];
     __shared__ uint16_t s_owner[kMoveSpan];
     __shared__ uint32_t s_wave_max[WAVES];
+    __shared__ double s_sq[WAVES];
 
     const int tid = threadIdx.x;
+    const int lane = tid & (kWaveSize - 1);
     const int64_t k = a.count_out[0];
     if (blockIdx.x == 0 && tid == 0) {  // the scan kernel has finished both counts
         a.host_count[0] = k;
         a.host_count[1] = a.count_out[1];
     }
+    if constexpr (SWEEP) {
+        // Each segment's count: the difference of the global offsets of its
+        // first tile and of the next segment's first tile.
+        if (blockIdx.x == 0 && tid < static_cast<int>(tbl->count)) {
+            const uint32_t t0 = tbl->seg[tid].tile_first, t1 = tbl->seg[tid + 1].tile_first;
+            const int64_t e0 = t0 < a.num_tiles ? (a.tile_excl[t0] & ~kOverflow) : k;
+            const int64_t e1 = t1 < a.num_tiles ? (a.tile_excl[t1] & ~kOverflow) : k;
+            a.host_count[2 + tid] = t1 > t0 ? e1 - e0 : 0;
+        }
+        // Workgroup b < count: the squared norm of segment b, its chunks'
+        // sums added in a fixed order.
+        if (blockIdx.x < tbl->count) {
+            const uint32_t c0 = tbl->seg[blockIdx.x].chunk_first, c1 = tbl->seg[blockIdx.x + 1].chunk_first;
+            double sq = 0.0;
+            for (uint32_t c = c0 + tid; c < c1; c += kMoveBlock) sq += a.chunk_sumsq[c];
+            const double total = block_sum<WAVES>(sq, lane, tid / kWaveSize, s_sq);
+            if (tid == 0) a.host_sumsq[blockIdx.x] = total;
+        }
+    }
     if (k == 0) return;
     // Flagged tiles first, one wavefront each over the whole grid: the
     // wavefront recomputes the tile and writes its pairs and residual.
     const uint32_t flagged = static_cast<uint32_t>(a.count_out[1]);
-    const int lane = tid & (kWaveSize - 1);
     for (uint32_t f = blockIdx.x * WAVES + tid / kWaveSize; f < flagged; f += gridDim.x * WAVES) {
         const uint32_t tile = a.flagged_list[f];
-        redo_tile<VEC>(a, tile, lane, a.tile_excl[tile] & ~kOverflow);
+        const uint32_t out_base = a.tile_excl[tile] & ~kOverflow;
+        if constexpr (SWEEP) {
+            LaunchArgs seg_args = a;
+            const int64_t tile_base = enter_segment(seg_args, tbl, tile);
+            redo_tile<VEC>(seg_args, tile_base, lane, out_base);
+        } else {
+            redo_tile<VEC>(a, a.base + static_cast<int64_t>(tile) * kStreamTile, lane, out_base);
+        }
     }
     const uint64_t total = static_cast<uint64_t>(a.num_tiles) + static_cast<uint64_t>(k);
     const uint32_t pieces = static_cast<uint32_t>((total + kMoveSpan - 1) / kMoveSpan);
@@ -659,6 +796,16 @@ __global__ __launch_bounds__(kMoveBlock) void move_kernel(LaunchArgs a) {
         }
         __syncthreads();  // the window is reloaded for the next piece
     }
+}
+
+template <int VEC>
+__global__ __launch_bounds__(kMoveBlock) void move_kernel(LaunchArgs a) {
+    move_pieces<VEC, false>(a, nullptr);
+}
+
+template <int VEC>
+__global__ __launch_bounds__(kMoveBlock) void move_sweep_kernel(LaunchArgs a, SweepTable tbl) {
+    move_pieces<VEC, true>(a, &tbl);
 }
 
 // ---------------------------------------------------------------------------
@@ -779,6 +926,20 @@ hipError_t launch_staged(const LaunchArgs& args, bool vec4, hipStream_t stream) 
         hipLaunchKernelGGL((stream_kernel<1, 4>), grid_stream, dim3(kStreamBlock), 0, stream, args);
         hipLaunchKernelGGL(scan_kernel, grid_scan, dim3(kScanBlock), 0, stream, args);
         hipLaunchKernelGGL(move_kernel<1>, grid_move, dim3(kMoveBlock), 0, stream, args);
+    }
+    return hipGetLastError();
+}
+
+hipError_t launch_sweep(const LaunchArgs& args, const SweepTable& table, bool vec4, hipStream_t stream) {
+    const dim3 grid_stream(args.num_tiles), grid_scan(args.num_chunks), grid_move(args.move_blocks);
+    if (vec4) {
+        hipLaunchKernelGGL((stream_sweep_kernel<4, 1>), grid_stream, dim3(kStreamBlock), 0, stream, args, table);
+        hipLaunchKernelGGL(scan_sweep_kernel, grid_scan, dim3(kScanBlock), 0, stream, args, table);
+        hipLaunchKernelGGL(move_sweep_kernel<4>, grid_move, dim3(kMoveBlock), 0, stream, args, table);
+    } else {
+        hipLaunchKernelGGL((stream_sweep_kernel<1, 4>), grid_stream, dim3(kStreamBlock), 0, stream, args, table);
+        hipLaunchKernelGGL(scan_sweep_kernel, grid_scan, dim3(kScanBlock), 0, stream, args, table);
+        hipLaunchKernelGGL(move_sweep_kernel<1>, grid_move, dim3(kMoveBlock), 0, stream, args, table);
     }
     return hipGetLastError();
 }
