@@ -53,13 +53,15 @@ def parse_args():
                     help="kernel schedule (staged is the library default)")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only run a plain device copy of known size (HBM counter scaling)")
-    ap.add_argument("--path", default="step", choices=["step", "ef", "union"],
+    ap.add_argument("--path", default="step", choices=["step", "ef", "union", "sweep"],
                     help="step: the partition-only sparsify step (default); ef: the full error-feedback "
                          "pass with cyclic partitions; union: the gather/reset and model update around "
-                         "the exchange")
+                         "the exchange; sweep: every partition in one launch of each kernel, with the "
+                         "local-error norms")
     args = ap.parse_args()
     if args.path != "step" and args.workload == "gpt_1p3b" and "--workload" not in sys.argv:
-        args.workload = "bert_large"  # world 1 makes both paths degenerate
+        # world 1 makes these paths degenerate
+        args.workload = "resnet18" if args.path == "sweep" else "bert_large"
     return args
 
 
@@ -260,6 +262,39 @@ def measure_ef(w, density, pool, sp, warmup, steps):
             "k_avg": sum(k for _, k, _ in log) / len(log), "worker": worker}
 
 
+def measure_sweep(w, density, pool, sp, warmup, steps):
+    """Every partition of the workload per step in one micro_sweep_step call
+    (with the local-error norms): 12 B per value plus 8 B per selected value."""
+    import torch
+    from paper_2310_00967_amd import synth
+    N = w.n_total
+    res = torch.zeros(N, dtype=torch.float32, device="cuda")
+    out_idx, out_val = sp.outputs(N)
+    thetas = []
+    for r in range(w.world):
+        s, ln = sp.partition(r, w.world)
+        thetas.append(synth.initial_theta(w, pool[0], s, s + ln, density))
+    log, errs = [], []
+    t0 = time.perf_counter()
+    for t in range(warmup + steps):
+        if t == warmup:
+            torch.cuda.synchronize()
+            t0 = time.perf_counter()
+        g = pool[t % len(pool)]
+        k, thetas, sq, _, _ = sp.sweep(g, res, w.world, density, thetas, out_idx, out_val)
+        if t >= warmup:
+            log.append((N, sum(k), sp.last_stats()[0]))
+            errs.append(math.sqrt(sum(sq)))
+    torch.cuda.synchronize()
+    elapsed = time.perf_counter() - t0
+    alg = sum(12 * n + 8 * k for n, k, _ in log)
+    kernel_s = sum(ms for _, _, ms in log) / 1e3
+    return {"g_elem_s": sum(n for n, _, _ in log) / elapsed / 1e9, "wall_gbs": alg / elapsed / 1e9,
+            "kernel_gbs": alg / kernel_s / 1e9, "kernel_ms_avg": kernel_s * 1e3 / len(log),
+            "alg_bytes_per_launch": alg / len(log), "ms_per_step": elapsed * 1e3 / steps,
+            "k_avg": sum(k for _, k, _ in log) / len(log), "local_error_last": errs[-1]}
+
+
 def build_union(w, density, g, sp):
     """The union of all n workers' selections on gradient g (each partition at
     its calibrated threshold), in partition order, and worker w.ranks[0]'s own
@@ -355,6 +390,35 @@ def cpu_baseline_ef(w, density, pool, target_s):
                        f"nproc {os.cpu_count()}")}
 
 
+def cpu_baseline_sweep(w, density, pool, target_s):
+    """The oracle's sweep (every partition, with the squared norms) on the host."""
+    import numpy as np
+    import torch
+    import oracle
+    from paper_2310_00967_amd import synth
+    N = w.n_total
+    res = np.zeros(N, np.float32)
+    res[:] = 0.0
+    g_host = torch.empty(N, dtype=torch.float32, pin_memory=True)
+    thetas = []
+    for r in range(w.world):
+        s, ln = oracle.partition(N, r, w.world)
+        thetas.append(synth.initial_theta(w, pool[0], s, s + ln, density))
+    spent, elems, steps = 0.0, 0, 0
+    while spent < target_s and steps < 10000:
+        g_host.copy_(pool[steps % len(pool)])
+        gn = g_host.numpy()
+        t0 = time.perf_counter()
+        _, _, _, thetas, _ = oracle.sweep(gn, res, w.world, density, thetas)
+        spent += time.perf_counter() - t0
+        elems += N
+        steps += 1
+    return {"value": elems / spent / 1e9, "unit": "G elem/s", "cores": 1, "kind": "oracle",
+            "sample": (f"{steps} sweep(s) of {w.name} over {w.world} partitions at d={density} ({elems} values, "
+                       f"{spent:.1f} s of single-threaded oracle time); host {cpu_model()}, "
+                       f"nproc {os.cpu_count()}")}
+
+
 def cpu_baseline_union(w, g, union_res, target_s):
     """The oracle's gather, reset and update over the same union on the host."""
     import numpy as np
@@ -384,7 +448,21 @@ def main_path(args, w, head, pool, n_pool, sp):
     cfg = {"workload": w.name, "n_total": w.n_total, "world": w.world, "worker": w.ranks[0],
            "density": head, "distribution": w.dist, "gradient_pool": n_pool,
            "parallelism": "one worker on one GPU", "path": args.path}
-    if args.path == "ef":
+    if args.path == "sweep":
+        r = measure_sweep(w, head, pool, sp, args.warmup, args.steps)
+        cpu = cpu_baseline_sweep(w, head, pool, args.cpu_seconds) if args.cpu_seconds > 0 else None
+        cfg["parallelism"] = "every partition of one vector on one GPU"
+        cfg["ranks"] = list(range(w.world))
+        line = {"metric": "partition-sweep throughput (G elem/s of the whole vector, HBM GB/s % of peak)",
+                "value": r["g_elem_s"], "unit": "G elem/s", "ms_per_step": r["ms_per_step"], **common,
+                "config": cfg, "k_avg": r["k_avg"], "local_error_last": r["local_error_last"],
+                "roofline": {"bound": "hbm", "achieved": r["kernel_gbs"], "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                             "frac": r["kernel_gbs"] / HBM_PEAK_GBS, "traffic": None,
+                             "kernel": "stream_sweep_kernel + scan_sweep_kernel + move_sweep_kernel "
+                                       "(one sweep, event-timed together)",
+                             "kernel_ms_avg": r["kernel_ms_avg"], "alg_bytes_per_launch": r["alg_bytes_per_launch"]},
+                "cpu_baseline": cpu}
+    elif args.path == "ef":
         r = measure_ef(w, head, pool, sp, args.warmup, args.steps)
         cpu = cpu_baseline_ef(w, head, pool, args.cpu_seconds) if args.cpu_seconds > 0 else None
         line = {"metric": "full error-feedback pass throughput (G elem/s of the whole vector, HBM GB/s % of peak)",
