@@ -49,8 +49,9 @@ def parse_args():
                     help="target CPU time of the oracle baseline sample (0 disables)")
     ap.add_argument("--pool-gb", type=float, default=100.0,
                     help="HBM budget for the pre-generated gradient pool")
-    ap.add_argument("--variant", default="staged", choices=["staged", "ticket"],
-                    help="kernel schedule (staged is the library default)")
+    ap.add_argument("--variant", default="auto", choices=["auto", "staged", "ticket"],
+                    help="kernel schedule (auto, the library default, runs the ticket schedule up to "
+                         "2^20 values per partition and the staged one above)")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only run a plain device copy of known size (HBM counter scaling)")
     ap.add_argument("--path", default="step", choices=["step", "ef", "union", "sweep"],
@@ -129,7 +130,8 @@ class Run:
         cap = max(ln for _, ln in self.bounds.values())
         self.out_idx, self.out_val = sp.outputs(cap)
         self.t = 0
-        self.log = []   # (rank, P, k, kernel_ms, tiles redone by the gather pass)
+        self.log = []   # (rank, P, k, kernel_ms, tiles redone by the move kernel)
+        self.variant = None  # schedule of the last step
 
     def step(self, timed):
         g = self.pool[self.t % len(self.pool)]
@@ -138,8 +140,9 @@ class Run:
             k, th, _, _ = self.sp.step(g, self.res, r, self.w.world, self.d, self.theta[r],
                                        self.out_idx, self.out_val)
             self.theta[r] = th
-            kernel_ms, redone, _ = self.sp.last_stats()
+            kernel_ms, redone, variant = self.sp.last_stats()
             self.log.append((r, ln, k, kernel_ms if timed else None, redone))
+            self.variant = variant
         self.t += 1
 
 
@@ -176,6 +179,7 @@ def measure(w, density, pool, sp, micro, warmup, steps):
         "theta0": run.theta0,
         "theta_final": run.theta,
         "ms_per_step": elapsed * 1e3 / steps,
+        "variant": run.variant,
     }
 
 
@@ -518,7 +522,8 @@ def main():
     n_pool = max(1, min(args.warmup + args.steps, int(args.pool_gb * 1e9 // (4 * w.n_total))))
     pool = [synth.gradient(w, t, "cuda") for t in range(n_pool)]
     torch.cuda.synchronize()
-    variant = micro.MICRO_VARIANT_STAGED if args.variant == "staged" else micro.MICRO_VARIANT_TICKET
+    variant = {"auto": micro.MICRO_VARIANT_AUTO, "staged": micro.MICRO_VARIANT_STAGED,
+               "ticket": micro.MICRO_VARIANT_TICKET}[args.variant]
     sp = micro.Sparsifier(w.n_total, device="cuda", time_kernel=True, variant=variant)
     if args.path != "step":
         main_path(args, w, head, pool, n_pool, sp)
@@ -574,7 +579,7 @@ def main():
             "frac": main_res["kernel_gbs"] / HBM_PEAK_GBS,
             "traffic": traffic,
             "kernel": ("stream_kernel + scan_kernel + move_kernel (one step, event-timed together)"
-                       if args.variant == "staged" else "ticket_kernel"),
+                       if main_res["variant"] == micro.MICRO_VARIANT_STAGED else "ticket_kernel"),
             "kernel_ms_avg": main_res["kernel_ms_avg"],
             "alg_bytes_per_launch": main_res["alg_bytes_per_launch"],
             "redone_tiles_timed": main_res["redone_tiles"],

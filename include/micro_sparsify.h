@@ -55,14 +55,16 @@ typedef enum micro_status {
                                      theta * (1 - alpha) if k < k*, else theta   */
 
 /* Kernel schedules (both compute the same result). */
-#define MICRO_VARIANT_AUTO 0   /* the fastest measured schedule: STAGED          */
+#define MICRO_VARIANT_AUTO 0   /* per call, the faster measured schedule: TICKET
+                                  for partitions of up to 2^20 values (one
+                                  launch), STAGED above; both scratch sets     */
 #define MICRO_VARIANT_TICKET 1 /* one pass; tiles from a ticket counter, each
                                   tile's offset by decoupled look-back           */
 #define MICRO_VARIANT_STAGED 2 /* a streaming pass that stages each tile's pairs
-                                  (no inter-workgroup waits), then a gather pass
-                                  that places them (look-back per chunk of a
-                                  million values); scratch of about 2 bytes per
-                                  value of the vector                            */
+                                  (no inter-workgroup waits), a scan pass (look-
+                                  back per chunk of a million values) and a
+                                  balanced pass that places them; scratch of
+                                  about 2 bytes per value of the vector          */
 
 /* Flags. */
 #define MICRO_FLAG_TIME_KERNEL 1 /* record HIP events around each launch so
@@ -83,8 +85,9 @@ typedef struct micro_step_stats {
                                (MICRO_FLAG_TIME_KERNEL), else -1               */
     int64_t redone_tiles;   /* STAGED: 1024-value tiles with more selected
                                values than their staging slot holds (256),
-                               processed by the gather pass instead            */
-    int32_t variant;        /* MICRO_VARIANT_TICKET or MICRO_VARIANT_STAGED    */
+                               redone by the placing pass instead              */
+    int32_t variant;        /* the schedule the last step ran:
+                               MICRO_VARIANT_TICKET or MICRO_VARIANT_STAGED    */
 } micro_step_stats;
 
 /* Fills *cfg with the defaults listed above. */
@@ -96,7 +99,7 @@ MICRO_API void micro_config_default(micro_config *cfg);
  * NULL means the null stream).  cfg == NULL selects the defaults.
  * The context owns its device scratch (STAGED: a 256-pair staging slot and a
  * count per 1024 values of the vector plus look-back words, about 2 bytes per
- * value; TICKET: one look-back word per 4096 values) and a pinned host word
+ * value; TICKET: one look-back word per 4096 values; AUTO: both) and a pinned host word
  * for the selected count; it never owns the caller's buffers.
  * Returns MICRO_EINVAL (ctx NULL, n_total < 0, bad cfg), MICRO_ERANGE
  * (n_total > INT32_MAX: indices are int32), MICRO_EHIP (no usable device) or

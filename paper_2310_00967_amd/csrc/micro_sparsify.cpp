@@ -22,8 +22,10 @@ struct micro_ctx {
     int64_t n_total = 0;
     hipStream_t stream = nullptr;
     micro_config cfg{};
-    bool staged = true;                      // staged schedule, else ticket
-    int64_t tile_capacity = 0;               // tiles of the largest partition
+    bool has_staged = true;                  // scratch of the staged schedule allocated
+    bool has_ticket = false;                 // scratch of the ticket schedule allocated
+    int64_t tile_capacity = 0;               // staged tiles of the largest partition (or sweep)
+    int64_t ticket_capacity = 0;             // ticket tiles of the largest partition
     // staged schedule: tile counts, staged pairs, chunk look-back words
     uint32_t* d_tile_counts = nullptr;
     uint32_t* d_tile_excl = nullptr;
@@ -52,6 +54,12 @@ struct micro_ctx {
 };
 
 namespace {
+
+// Largest partition that an AUTO context runs on the ticket schedule.  On
+// MI355X the ticket schedule's single launch took 8.8 us of device time for
+// 262,144 values against 16.8 us for the staged schedule's three, and lost
+// from 3.2M values on (27 us against 23 us).
+constexpr int64_t kAutoTicketMax = int64_t(1) << 20;
 
 thread_local std::string g_init_error = "no error";
 
@@ -127,7 +135,7 @@ micro_status reset_scratch(micro_ctx* ctx) {
     hipError_t e = hipMemsetAsync(ctx->d_tickets, 0, 2 * sizeof(unsigned long long), ctx->stream);
     if (e == hipSuccess) e = hipMemsetAsync(ctx->d_count, 0, 2 * sizeof(int64_t), ctx->stream);
     if (e == hipSuccess && ctx->d_status)
-        e = hipMemsetAsync(ctx->d_status, 0, sizeof(uint64_t) * ctx->tile_capacity, ctx->stream);
+        e = hipMemsetAsync(ctx->d_status, 0, sizeof(uint64_t) * ctx->ticket_capacity, ctx->stream);
     if (e == hipSuccess && ctx->d_chunk_status)
         e = hipMemsetAsync(ctx->d_chunk_status, 0, sizeof(uint64_t) * ctx->chunk_capacity, ctx->stream);
     if (e == hipSuccess) e = hipStreamSynchronize(ctx->stream);
@@ -221,7 +229,12 @@ micro_status execute_step(micro_ctx* ctx, const float* grad, float* residual, in
                                          : 0u;
         }
     }
-    const int64_t tile_elems = ctx->staged ? micro::kStreamTile : micro::kTicketTile;
+    // AUTO contexts take the one-pass ticket schedule for partitions of up to
+    // kAutoTicketMax values, where one launch beats three, and the staged
+    // schedule above, where the ticket schedule's per-tile round trips cost
+    // bandwidth.
+    const bool staged = ctx->has_staged && !(ctx->has_ticket && len <= kAutoTicketMax);
+    const int64_t tile_elems = staged ? micro::kStreamTile : micro::kTicketTile;
     micro::LaunchArgs a{};
     a.grad = grad;
     a.residual = residual;
@@ -234,9 +247,10 @@ micro_status execute_step(micro_ctx* ctx, const float* grad, float* residual, in
     a.epoch = ctx->epoch + 1;
     const int64_t tiles = len > 0 ? (a.end - a.base + tile_elems - 1) / tile_elems : 0;
     const int64_t chunks = (tiles + micro::kChunkTiles - 1) / micro::kChunkTiles;
-    if (tiles > ctx->tile_capacity || (ctx->staged && chunks > ctx->chunk_capacity)) {
+    const int64_t capacity = staged ? ctx->tile_capacity : ctx->ticket_capacity;
+    if (tiles > capacity || (staged && chunks > ctx->chunk_capacity)) {
         set_error(ctx, "partition needs %lld tiles, scratch holds %lld", static_cast<long long>(tiles),
-                  static_cast<long long>(ctx->tile_capacity));
+                  static_cast<long long>(capacity));
         return MICRO_ECAPACITY;
     }
     a.num_tiles = static_cast<uint32_t>(tiles);
@@ -271,7 +285,7 @@ micro_status execute_step(micro_ctx* ctx, const float* grad, float* residual, in
         return hip_fail(ctx, e, "accumulate kernel launch");
     if (len > 0) {
         ctx->epoch = a.epoch;
-        e = ctx->staged ? micro::launch_staged(a, vec4, ctx->stream) : micro::launch_ticket(a, vec4, ctx->stream);
+        e = staged ? micro::launch_staged(a, vec4, ctx->stream) : micro::launch_ticket(a, vec4, ctx->stream);
         if (e != hipSuccess) return hip_fail(ctx, e, "sparsify kernel launch");
     }
     if (timed && (e = hipEventRecord(ctx->ev[1], ctx->stream)) != hipSuccess)
@@ -286,7 +300,8 @@ micro_status execute_step(micro_ctx* ctx, const float* grad, float* residual, in
     }
     if (timed && (e = hipEventElapsedTime(&ctx->stats.kernel_ms, ctx->ev[0], ctx->ev[1])) != hipSuccess)
         return hip_fail(ctx, e, "hipEventElapsedTime");
-    ctx->stats.redone_tiles = ctx->staged ? host_count[1] : 0;
+    ctx->stats.redone_tiles = staged ? host_count[1] : 0;
+    ctx->stats.variant = staged ? MICRO_VARIANT_STAGED : MICRO_VARIANT_TICKET;
     *k = selected;
     *theta = next_threshold(ctx->cfg, density, len, selected, *theta);
     return MICRO_OK;
@@ -304,7 +319,7 @@ micro_status execute_sweep(micro_ctx* ctx, const float* grad, float* residual, i
         set_error(ctx, "sweep world %d outside [1, %d]", world, micro::kMaxSweep);
         return MICRO_EINVAL;
     }
-    if (!ctx->staged) {
+    if (!ctx->has_staged) {
         set_error(ctx, "the sweep needs the staged schedule");
         return MICRO_EINVAL;
     }
@@ -543,7 +558,8 @@ micro_status micro_sparsify_init(micro_ctx** out, int64_t n_total, void* hip_str
     }
     // Scratch sized for the largest possible partition (the whole vector),
     // plus one tile for the alignment of the first tile.
-    ctx->staged = c.variant != MICRO_VARIANT_TICKET;
+    ctx->has_staged = c.variant != MICRO_VARIANT_TICKET;
+    ctx->has_ticket = c.variant != MICRO_VARIANT_STAGED;
     bool ok = hipMalloc(&ctx->d_tickets, 2 * sizeof(unsigned long long)) == hipSuccess &&
               hipMalloc(&ctx->d_count, 2 * sizeof(int64_t)) == hipSuccess &&
               hipHostMalloc(&ctx->h_count, (2 + micro::kMaxSweep) * sizeof(int64_t),
@@ -552,7 +568,7 @@ micro_status micro_sparsify_init(micro_ctx** out, int64_t n_total, void* hip_str
               hipHostMalloc(&ctx->h_sumsq, micro::kMaxSweep * sizeof(double),
                             hipHostMallocMapped | hipHostMallocCoherent) == hipSuccess &&
               hipHostGetDevicePointer(reinterpret_cast<void**>(&ctx->h_sumsq_dev), ctx->h_sumsq, 0) == hipSuccess;
-    if (ok && ctx->staged) {
+    if (ok && ctx->has_staged) {
         // a sweep's segments each add at most one tile (alignment) and one chunk
         ctx->tile_capacity = n_total / micro::kStreamTile + 2 + micro::kMaxSweep;
         ctx->chunk_capacity = ctx->tile_capacity / micro::kChunkTiles + 2 + micro::kMaxSweep;
@@ -566,9 +582,10 @@ micro_status micro_sparsify_init(micro_ctx** out, int64_t n_total, void* hip_str
              hipMalloc(&ctx->d_chunk_sumsq, sizeof(double) * ctx->chunk_capacity) == hipSuccess &&
              hipMalloc(&ctx->d_stage, sizeof(uint2) * stage) == hipSuccess &&
              hipMalloc(&ctx->d_chunk_status, sizeof(uint64_t) * ctx->chunk_capacity) == hipSuccess;
-    } else if (ok) {
-        ctx->tile_capacity = n_total / micro::kTicketTile + 2;
-        ok = hipMalloc(&ctx->d_status, sizeof(uint64_t) * ctx->tile_capacity) == hipSuccess;
+    }
+    if (ok && ctx->has_ticket) {
+        ctx->ticket_capacity = n_total / micro::kTicketTile + 2;
+        ok = hipMalloc(&ctx->d_status, sizeof(uint64_t) * ctx->ticket_capacity) == hipSuccess;
     }
     if (!ok) {
         set_error(nullptr, "device or pinned host allocation failed");
@@ -586,7 +603,7 @@ micro_status micro_sparsify_init(micro_ctx** out, int64_t n_total, void* hip_str
     }
     ctx->stats.kernel_ms = -1.0f;
     ctx->stats.redone_tiles = 0;
-    ctx->stats.variant = ctx->staged ? MICRO_VARIANT_STAGED : MICRO_VARIANT_TICKET;
+    ctx->stats.variant = ctx->has_staged ? MICRO_VARIANT_STAGED : MICRO_VARIANT_TICKET;
     if (reset_scratch(ctx) != MICRO_OK) {
         set_error(nullptr, "%s", ctx->last_error.c_str());
         release(ctx);

@@ -266,3 +266,25 @@ def test_fixed_step_rule_matches_oracle():
         run.run(6, verbose=False)
     finally:
         run.close()
+
+
+def test_auto_schedule_picks_by_partition_length():
+    """AUTO runs the one-pass ticket schedule up to 2^20 values and the staged
+    schedule above, with the same bits either way (lengths on both sides of
+    the boundary, compared with the oracle)."""
+    rng = np.random.default_rng(20)
+    for N, want in [(1 << 20, TICKET), ((1 << 20) + 1, STAGED), (262_144, TICKET), (3_000_000, STAGED)]:
+        g = rng.standard_normal(N).astype(np.float32)
+        res = (rng.standard_normal(N) * 0.5).astype(np.float32)
+        sp = micro.Sparsifier(N, device=DEV, time_kernel=True)
+        g_dev = torch.from_numpy(g).to(DEV)
+        r_dev = torch.from_numpy(res).to(DEV)
+        k, th, idx, val = sp.step(g_dev, r_dev, 0, 1, 0.01, 2.4)
+        assert sp.last_stats()[2] == want, N
+        r_or = res.copy()
+        o_idx, o_val, k_or, th_or = oracle.step(g, r_or, 0, 1, 0.01, 2.4)
+        assert (k, th) == (k_or, th_or)
+        assert np.array_equal(idx.cpu().numpy(), o_idx)
+        assert first_mismatch(val.cpu().numpy(), o_val) < 0
+        assert first_mismatch(r_dev.cpu().numpy(), r_or) < 0
+        sp.close()
