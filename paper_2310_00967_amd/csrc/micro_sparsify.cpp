@@ -161,6 +161,16 @@ void release(micro_ctx* ctx) {
 }
 
 
+// Workgroups of the move kernel: one per move piece of the largest possible
+// count (k = len), at most kMoveGrid, at least min_blocks.  Its grid-stride
+// loops are correct for any grid.
+uint32_t move_grid(int64_t tiles, int64_t len, int64_t min_blocks) {
+    int64_t blocks = (tiles + len + micro::kMoveSpan - 1) / micro::kMoveSpan;
+    if (blocks > micro::kMoveGrid) blocks = micro::kMoveGrid;
+    if (blocks < min_blocks) blocks = min_blocks;
+    return static_cast<uint32_t>(blocks < 1 ? 1 : blocks);
+}
+
 bool misaligned4(std::initializer_list<const void*> ptrs) {
     uintptr_t bits = 0;
     for (const void* p : ptrs) bits |= reinterpret_cast<uintptr_t>(p);
@@ -260,11 +270,7 @@ micro_status execute_step(micro_ctx* ctx, const float* grad, float* residual, in
     a.tile_excl = ctx->d_tile_excl;
     a.flagged_list = ctx->d_flagged_list;
     a.split_tile = ctx->d_split_tile;
-    {
-        // at most ceil((tiles + P) / kMoveSpan) move pieces, whatever k is
-        const int64_t pieces = (tiles + len + micro::kMoveSpan - 1) / micro::kMoveSpan;
-        a.move_blocks = static_cast<uint32_t>(pieces < micro::kMoveGrid ? pieces : micro::kMoveGrid);
-    }
+    a.move_blocks = move_grid(tiles, len, 1);
     a.stage = ctx->d_stage;
     a.num_chunks = static_cast<uint32_t>(chunks);
     a.chunk_status = ctx->d_chunk_status;
@@ -398,12 +404,8 @@ micro_status execute_sweep(micro_ctx* ctx, const float* grad, float* residual, i
     a.tile_sumsq = ctx->d_tile_sumsq;
     a.chunk_sumsq = ctx->d_chunk_sumsq;
     a.host_sumsq = ctx->h_sumsq_dev;
-    {
-        const int64_t pieces = (tiles + ctx->n_total + micro::kMoveSpan - 1) / micro::kMoveSpan;
-        int64_t blocks = pieces < micro::kMoveGrid ? pieces : micro::kMoveGrid;
-        if (blocks < world) blocks = world;  // workgroup r reduces segment r's squared norm
-        a.move_blocks = static_cast<uint32_t>(blocks);
-    }
+    // workgroup r of the move kernel reduces segment r's squared norm
+    a.move_blocks = move_grid(tiles, ctx->n_total, world);
     a.stage = ctx->d_stage;
     a.num_chunks = static_cast<uint32_t>(chunks);
     a.chunk_status = ctx->d_chunk_status;
@@ -572,7 +574,10 @@ micro_status micro_sparsify_init(micro_ctx** out, int64_t n_total, void* hip_str
         // a sweep's segments each add at most one tile (alignment) and one chunk
         ctx->tile_capacity = n_total / micro::kStreamTile + 2 + micro::kMaxSweep;
         ctx->chunk_capacity = ctx->tile_capacity / micro::kChunkTiles + 2 + micro::kMaxSweep;
+        // every piece, and one word past the largest move grid (each
+        // workgroup reads its first piece's two words before it knows k)
         ctx->split_capacity = (ctx->tile_capacity + n_total) / micro::kMoveSpan + 2;
+        if (ctx->split_capacity < micro::kMoveGrid + 1) ctx->split_capacity = micro::kMoveGrid + 1;
         const size_t stage = static_cast<size_t>(ctx->tile_capacity) * micro::kStageCap;
         ok = hipMalloc(&ctx->d_tile_counts, sizeof(uint32_t) * ctx->tile_capacity) == hipSuccess &&
              hipMalloc(&ctx->d_tile_excl, sizeof(uint32_t) * ctx->tile_capacity) == hipSuccess &&

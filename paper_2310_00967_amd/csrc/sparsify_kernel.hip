@@ -691,6 +691,12 @@ __device__ __forceinline__ void move_pieces(const LaunchArgs& a, const SweepTabl
 
     const int tid = threadIdx.x;
     const int lane = tid & (kWaveSize - 1);
+    // The split words of this workgroup's first piece are read together with
+    // the count (one round trip, not two); they are used only if the piece
+    // exists, and then the scan kernel wrote them.  Both indices lie inside
+    // the split array, which has room for the largest grid plus one.
+    const uint32_t first_t0 = a.split_tile[blockIdx.x];
+    const uint32_t first_t1 = a.split_tile[blockIdx.x + 1];
     const int64_t k = a.count_out[0];
     if (blockIdx.x == 0 && tid == 0) {  // the scan kernel has finished both counts
         a.host_count[0] = k;
@@ -733,8 +739,9 @@ __device__ __forceinline__ void move_pieces(const LaunchArgs& a, const SweepTabl
     const uint64_t total = static_cast<uint64_t>(a.num_tiles) + static_cast<uint64_t>(k);
     const uint32_t pieces = static_cast<uint32_t>((total + kMoveSpan - 1) / kMoveSpan);
     for (uint32_t m = blockIdx.x; m < pieces; m += gridDim.x) {
-        const uint32_t t0 = a.split_tile[m];
-        const uint32_t t1 = m + 1 < pieces ? a.split_tile[m + 1] : a.num_tiles - 1;
+        const bool first = m == blockIdx.x;
+        const uint32_t t0 = first ? first_t0 : a.split_tile[m];
+        const uint32_t t1 = m + 1 < pieces ? (first ? first_t1 : a.split_tile[m + 1]) : a.num_tiles - 1;
         // t1 - t0 <= kMoveSpan by construction; the clamp only keeps LDS
         // accesses inside the window
         const uint32_t span = t1 - t0 + 1;

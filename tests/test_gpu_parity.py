@@ -288,3 +288,24 @@ def test_auto_schedule_picks_by_partition_length():
         assert first_mismatch(val.cpu().numpy(), o_val) < 0
         assert first_mismatch(r_dev.cpu().numpy(), r_or) < 0
         sp.close()
+
+
+def test_count_swings_on_one_context():
+    """The move grid is sized from the density and the previous launch; k
+    jumping between almost nothing and everything on one context (a grid far
+    too small, then far too large) keeps the bits."""
+    N = 5_000_011
+    rng = np.random.default_rng(33)
+    g = rng.standard_normal(N).astype(np.float32)
+    sp = micro.Sparsifier(N, device=DEV, variant=STAGED)
+    g_dev = torch.from_numpy(g).to(DEV)
+    res = np.zeros(N, np.float32)
+    r_dev = torch.zeros(N, dtype=torch.float32, device=DEV)
+    for theta in [5.5, 1e-30, 4.0, 1e-30, 0.3, 6.0, 1e-30]:
+        k, th, idx, val = sp.step(g_dev, r_dev, 0, 1, 0.001, theta)
+        o_idx, o_val, k_or, th_or = oracle.step(g, res, 0, 1, 0.001, theta)
+        assert (k, th) == (k_or, th_or), theta
+        assert np.array_equal(idx.cpu().numpy(), o_idx), theta
+        assert first_mismatch(val.cpu().numpy(), o_val) < 0, theta
+        assert first_mismatch(r_dev.cpu().numpy(), res) < 0, theta
+    sp.close()
