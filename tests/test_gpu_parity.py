@@ -309,3 +309,34 @@ def test_count_swings_on_one_context():
         assert first_mismatch(val.cpu().numpy(), o_val) < 0, theta
         assert first_mismatch(r_dev.cpu().numpy(), res) < 0, theta
     sp.close()
+
+
+def test_largest_vector_the_index_type_allows():
+    """n_total = 2^31 - 1, the largest vector int32 indices address: one
+    partition-wide step (staged) and one full error-feedback pass of world 2,
+    bit for bit against the oracle.  About 40 GB of device memory."""
+    N = 2**31 - 1
+    note(f"largest vector N={N}")
+    gen = torch.Generator(device=DEV).manual_seed(2024)
+    g_dev = torch.randn(N, generator=gen, device=DEV, dtype=torch.float32)
+    r_dev = (torch.randn(N, generator=gen, device=DEV, dtype=torch.float32) * 0.5)
+    g = g_dev.cpu().numpy()
+    res = r_dev.cpu().numpy()
+    sp = micro.Sparsifier(N, device=DEV)
+    k, th, idx, val = sp.step(g_dev, r_dev, 0, 1, 0.001, 3.3)
+    assert sp.last_stats()[2] == STAGED
+    o_idx, o_val, k_or, th_or = oracle.step(g, res, 0, 1, 0.001, 3.3)
+    assert (k, th) == (k_or, th_or)
+    assert np.array_equal(idx.cpu().numpy(), o_idx)
+    assert int(o_idx[-1]) > 2**31 - 2**20  # indices near the top of the range were selected
+    assert first_mismatch(val.cpu().numpy(), o_val) < 0
+    assert first_mismatch(r_dev.cpu().numpy(), res) < 0
+    del idx, val, o_idx, o_val
+    note("largest vector: full pass, world 2")
+    k, th, c, idx, val = sp.ef_step(g_dev, r_dev, 1, 0, 2, 0.001, 3.3)
+    o_idx, o_val, k_or, th_or, c_or = oracle.ef_step(g, res, 1, 0, 2, 0.001, 3.3)
+    assert (k, th, c) == (k_or, th_or, c_or) and c == 1
+    assert np.array_equal(idx.cpu().numpy(), o_idx)
+    assert first_mismatch(val.cpu().numpy(), o_val) < 0
+    assert first_mismatch(r_dev.cpu().numpy(), res) < 0
+    sp.close()
