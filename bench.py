@@ -59,6 +59,8 @@ def parse_args():
                          "pass with cyclic partitions; union: the gather/reset and model update around "
                          "the exchange; sweep: every partition in one launch of each kernel, with the "
                          "local-error norms")
+    ap.add_argument("--local-error", action="store_true",
+                    help="with --path ef: also return the squared norm of the whole residual (Eq. 1)")
     args = ap.parse_args()
     if args.path != "step" and args.workload == "gpt_1p3b" and "--workload" not in sys.argv:
         # world 1 makes these paths degenerate
@@ -233,7 +235,7 @@ def _partition_lengths(w):
     return [micro.micro_partition(w.n_total, c, w.world)[1] for c in range(w.world)]
 
 
-def measure_ef(w, density, pool, sp, warmup, steps):
+def measure_ef(w, density, pool, sp, warmup, steps, local_error=False):
     """Full error-feedback passes of worker w.ranks[0] at iterations 0, 1, ...
     (its searched partition rotates): 12 B per value of the whole vector plus
     8 B per selected value."""
@@ -253,7 +255,8 @@ def measure_ef(w, density, pool, sp, warmup, steps):
             torch.cuda.synchronize()
             t0 = time.perf_counter()
         g = pool[t % len(pool)]
-        k, theta, _, _, _ = sp.ef_step(g, res, t, worker, w.world, density, theta, out_idx, out_val)
+        out = sp.ef_step(g, res, t, worker, w.world, density, theta, out_idx, out_val, local_error=local_error)
+        k, theta = out[0], out[1]
         if t >= warmup:
             log.append((N, k, sp.last_stats()[0]))
     torch.cuda.synchronize()
@@ -467,15 +470,19 @@ def main_path(args, w, head, pool, n_pool, sp):
                              "kernel_ms_avg": r["kernel_ms_avg"], "alg_bytes_per_launch": r["alg_bytes_per_launch"]},
                 "cpu_baseline": cpu}
     elif args.path == "ef":
-        r = measure_ef(w, head, pool, sp, args.warmup, args.steps)
+        r = measure_ef(w, head, pool, sp, args.warmup, args.steps, args.local_error)
+        cfg["local_error"] = args.local_error
         cpu = cpu_baseline_ef(w, head, pool, args.cpu_seconds) if args.cpu_seconds > 0 else None
         line = {"metric": "full error-feedback pass throughput (G elem/s of the whole vector, HBM GB/s % of peak)",
                 "value": r["g_elem_s"], "unit": "G elem/s", "ms_per_step": r["ms_per_step"], **common,
                 "config": cfg, "k_avg": r["k_avg"],
                 "roofline": {"bound": "hbm", "achieved": r["kernel_gbs"], "peak": HBM_PEAK_GBS, "unit": "GB/s",
                              "frac": r["kernel_gbs"] / HBM_PEAK_GBS, "traffic": None,
-                             "kernel": "accumulate_kernel + stream_kernel + scan_kernel + move_kernel "
-                                       "(one pass, event-timed together)",
+                             "kernel": ("stream_sweep_kernel + scan_sweep_kernel + move_sweep_kernel over three "
+                                        "segments (one pass with the local error, event-timed together)"
+                                        if args.local_error else
+                                        "accumulate_kernel + stream_kernel + scan_kernel + move_kernel "
+                                        "(one pass, event-timed together)"),
                              "kernel_ms_avg": r["kernel_ms_avg"], "alg_bytes_per_launch": r["alg_bytes_per_launch"]},
                 "cpu_baseline": cpu}
     else:

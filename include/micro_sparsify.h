@@ -184,6 +184,12 @@ MICRO_API micro_status micro_cycle(int64_t t, int32_t worker, int32_t world, int
  *   out_idx, out_val, k, theta, density: as micro_sparsify_step, with
  *             P = e - s of partition c.
  *   cycle     host out (may be NULL): c.
+ *   sumsq     host out (may be NULL): the squared L2 norm of the whole new
+ *             residual, the worker's local error of Sec. 2 squared (Eq. 1
+ *             averages its square root over the workers); squares in binary64
+ *             added in a fixed order, within (n_total - 1) * 2^-53 relative of
+ *             the exact sum.  Requesting it runs the pass through the sweep's
+ *             kernels (the staged schedule; MICRO_EINVAL on a TICKET context).
  * grad[0, n), residual[0, n), out_idx[0, P) and out_val[0, P) must not
  * overlap.  Synchronous; errors as micro_sparsify_step.  A partition that is
  * empty (n_total < world) still accumulates every element, with k = 0 and
@@ -192,7 +198,7 @@ MICRO_API micro_status micro_cycle(int64_t t, int32_t worker, int32_t world, int
 MICRO_API micro_status micro_ef_step(micro_ctx *ctx, const float *grad, float *residual,
                                      int64_t t, int32_t worker, int32_t world, double density,
                                      double *theta, int32_t *out_idx, float *out_val,
-                                     int64_t *k, int32_t *cycle);
+                                     int64_t *k, int32_t *cycle, double *sumsq);
 
 /*
  * Algorithm 1, after the all-gather of the selected indices: the worker's

@@ -100,10 +100,13 @@ class Sparsifier:
                                          density, theta, out_idx.data_ptr(), out_val.data_ptr())
         return k, th, out_idx[:k], out_val[:k]
 
-    def ef_step(self, grad, residual, t, worker, world, density, theta, out_idx=None, out_val=None):
+    def ef_step(self, grad, residual, t, worker, world, density, theta, out_idx=None, out_val=None,
+                local_error=False):
         """Algorithm 1 for `worker` at iteration t over the whole vector: every
         value accumulates, the partition of the worker's cycle is searched.
-        Returns (k, theta_next, cycle, idx[:k], val[:k])."""
+        Returns (k, theta_next, cycle, idx[:k], val[:k]); with local_error,
+        (k, theta_next, cycle, idx[:k], val[:k], sumsq) where sumsq is the
+        squared norm of the whole new residual."""
         import torch
         if self._ctx is None:
             raise RuntimeError("Sparsifier is closed")
@@ -118,8 +121,10 @@ class Sparsifier:
         self._check(out_val, "out_val", torch.float32)
         if out_idx.numel() < length or out_val.numel() < length:
             raise ValueError(f"output capacity below the partition length {length}")
-        k, th, c = _lib.micro_ef_step(self._ctx, grad.data_ptr(), residual.data_ptr(), t, worker, world,
-                                      density, theta, out_idx.data_ptr(), out_val.data_ptr())
+        k, th, c, sq = _lib.micro_ef_step(self._ctx, grad.data_ptr(), residual.data_ptr(), t, worker, world,
+                                          density, theta, out_idx.data_ptr(), out_val.data_ptr(), local_error)
+        if local_error:
+            return k, th, c, out_idx[:k], out_val[:k], sq
         return k, th, c, out_idx[:k], out_val[:k]
 
     def sweep(self, grad, residual, world, density, thetas, out_idx=None, out_val=None, want_sumsq=True):

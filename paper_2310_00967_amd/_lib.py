@@ -48,7 +48,8 @@ SIGNATURES = {
     "micro_cycle": (ctypes.c_int, [ctypes.c_int64, ctypes.c_int32, ctypes.c_int32, ctypes.POINTER(ctypes.c_int32)]),
     "micro_ef_step": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int64,
                                      ctypes.c_int32, ctypes.c_int32, ctypes.c_double, _dblp,
-                                     ctypes.c_void_p, ctypes.c_void_p, _i64p, ctypes.POINTER(ctypes.c_int32)]),
+                                     ctypes.c_void_p, ctypes.c_void_p, _i64p, ctypes.POINTER(ctypes.c_int32),
+                                     _dblp]),
     "micro_union_gather": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int64,
                                           ctypes.c_int64, ctypes.c_int64, ctypes.c_void_p, ctypes.c_void_p]),
     "micro_sparse_update": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p,
@@ -173,17 +174,20 @@ def micro_cycle(t, worker, world):
     return c.value
 
 
-def micro_ef_step(ctx, grad_ptr, residual_ptr, t, worker, world, density, theta, out_idx_ptr, out_val_ptr):
-    """Raw call with device addresses; returns (k, theta_next, cycle)."""
+def micro_ef_step(ctx, grad_ptr, residual_ptr, t, worker, world, density, theta, out_idx_ptr, out_val_ptr,
+                  want_sumsq=False):
+    """Raw call with device addresses; returns (k, theta_next, cycle, sumsq
+    or None)."""
     th = ctypes.c_double(float(theta))
     k = ctypes.c_int64()
     c = ctypes.c_int32()
+    sq = ctypes.c_double(-1.0)
     st = load().micro_ef_step(ctx, ctypes.c_void_p(grad_ptr), ctypes.c_void_p(residual_ptr), int(t),
                               int(worker), int(world), float(density), ctypes.byref(th),
                               ctypes.c_void_p(out_idx_ptr), ctypes.c_void_p(out_val_ptr), ctypes.byref(k),
-                              ctypes.byref(c))
+                              ctypes.byref(c), ctypes.byref(sq) if want_sumsq else None)
     check(st, ctx)
-    return k.value, th.value, c.value
+    return k.value, th.value, c.value, (sq.value if want_sumsq else None)
 
 
 def micro_union_gather(ctx, residual_ptr, union_ptr, m, own_first, own_count, own_val_ptr, out_ptr):

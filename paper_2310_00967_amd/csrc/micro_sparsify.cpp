@@ -177,12 +177,17 @@ bool misaligned4(std::initializer_list<const void*> ptrs) {
     return (bits & 3u) != 0;
 }
 
+micro_status run_segments(micro_ctx* ctx, const float* grad, float* residual, int32_t count, const int64_t* starts,
+                          const int64_t* lens, const float* threshold_f, int32_t* out_idx, float* out_val,
+                          int64_t* k, double* sumsq);
+
 // Validation, launch, count readback and threshold update of one sparsify
 // step over [start, start + len); with accumulate_outside the rest of the
-// vector is accumulated too (the full error-feedback pass).
+// vector is accumulated too (the full error-feedback pass), and with sumsq the
+// pass also returns the squared norm of the whole new residual.
 micro_status execute_step(micro_ctx* ctx, const float* grad, float* residual, int64_t start, int64_t len,
                           bool accumulate_outside, double density, double* theta, int32_t* out_idx,
-                          float* out_val, int64_t* k) {
+                          float* out_val, int64_t* k, double* sumsq) {
     if (!grad || !residual || !theta || !out_idx || !out_val || !k) {
         set_error(ctx, "NULL pointer argument");
         return MICRO_EINVAL;
@@ -214,6 +219,33 @@ micro_status execute_step(micro_ctx* ctx, const float* grad, float* residual, in
     const int64_t n_outside = accumulate_outside ? ctx->n_total - len : 0;
     if (len == 0 && n_outside == 0) {  // nothing to do: nothing selected, threshold unchanged
         *k = 0;
+        if (sumsq) *sumsq = 0.0;
+        return MICRO_OK;
+    }
+    if (sumsq) {
+        // The pass with its local error: the whole vector through the sweep
+        // kernels as three segments, the two outside the partition with a NaN
+        // threshold (nothing selected, everything accumulated).
+        if (!ctx->has_staged) {
+            set_error(ctx, "the local error needs the staged schedule");
+            return MICRO_EINVAL;
+        }
+        const float none = std::numeric_limits<float>::quiet_NaN();
+        const int64_t starts[3] = {0, start, start + len};
+        const int64_t lens[3] = {start, len, ctx->n_total - start - len};
+        const float thf[3] = {none, threshold_as_f32(*theta), none};
+        int64_t kk[3];
+        double sq[3];
+        const micro_status st = run_segments(ctx, grad, residual, 3, starts, lens, thf, out_idx, out_val, kk, sq);
+        if (st != MICRO_OK) return st;
+        if (kk[0] != 0 || kk[2] != 0) {
+            set_error(ctx, "device selected outside the partition");
+            ctx->needs_reset = true;
+            return MICRO_EHIP;
+        }
+        *k = kk[1];
+        *theta = next_threshold(ctx->cfg, density, len, kk[1], *theta);
+        *sumsq = sq[0] + sq[1] + sq[2];
         return MICRO_OK;
     }
     if (ctx->needs_reset) {
@@ -313,6 +345,114 @@ micro_status execute_step(micro_ctx* ctx, const float* grad, float* residual, in
     return MICRO_OK;
 }
 
+// One launch of each staged kernel over `count` segments of one vector: the
+// segment [starts[r], starts[r] + lens[r]) selects with threshold_f[r] (a NaN
+// threshold selects nothing: an ordered compare with NaN is false), all of
+// them accumulate; the pairs of all segments form one compaction in index
+// order.  k[r] and sumsq[r] (squared norm of the segment's new residual)
+// receive each segment's results.  Arguments are validated by the callers.
+micro_status run_segments(micro_ctx* ctx, const float* grad, float* residual, int32_t count, const int64_t* starts,
+                          const int64_t* lens, const float* threshold_f, int32_t* out_idx, float* out_val,
+                          int64_t* k, double* sumsq) {
+    if (ctx->needs_reset || ctx->epoch >= micro::kMaxEpoch) {
+        micro_status st = reset_scratch(ctx);
+        if (st != MICRO_OK) return st;
+    }
+    const bool vec4 = ((reinterpret_cast<uintptr_t>(grad) ^ reinterpret_cast<uintptr_t>(residual)) & 15u) == 0;
+    micro::SweepTable table{};
+    table.count = static_cast<uint32_t>(count);
+    int64_t tiles = 0, chunks = 0;
+    for (int32_t r = 0; r < count; ++r) {
+        micro::SweepSegment& sg = table.seg[r];
+        sg.start = starts[r];
+        sg.end = starts[r] + lens[r];
+        sg.base = micro::tile_base_for(grad, starts[r], vec4);
+        sg.theta_f = threshold_f[r];
+        sg.tile_first = static_cast<uint32_t>(tiles);
+        sg.chunk_first = static_cast<uint32_t>(chunks);
+        const int64_t seg_tiles = lens[r] > 0 ? (sg.end - sg.base + micro::kStreamTile - 1) / micro::kStreamTile : 0;
+        tiles += seg_tiles;
+        chunks += (seg_tiles + micro::kChunkTiles - 1) / micro::kChunkTiles;
+    }
+    table.seg[count].tile_first = static_cast<uint32_t>(tiles);
+    table.seg[count].chunk_first = static_cast<uint32_t>(chunks);
+    if (tiles > ctx->tile_capacity || chunks > ctx->chunk_capacity) {
+        set_error(ctx, "sweep needs %lld tiles, scratch holds %lld", static_cast<long long>(tiles),
+                  static_cast<long long>(ctx->tile_capacity));
+        return MICRO_ECAPACITY;
+    }
+    if (tiles == 0) {  // every segment empty
+        for (int32_t r = 0; r < count; ++r) {
+            k[r] = 0;
+            sumsq[r] = 0.0;
+        }
+        return MICRO_OK;
+    }
+    micro::LaunchArgs a{};
+    a.grad = grad;
+    a.residual = residual;
+    a.out_idx = out_idx;
+    a.out_val = out_val;
+    a.epoch = ctx->epoch + 1;
+    a.num_tiles = static_cast<uint32_t>(tiles);
+    a.count_out = ctx->d_count;
+    a.host_count = ctx->h_count_dev;
+    a.tile_counts = ctx->d_tile_counts;
+    a.tile_excl = ctx->d_tile_excl;
+    a.flagged_list = ctx->d_flagged_list;
+    a.split_tile = ctx->d_split_tile;
+    a.tile_sumsq = ctx->d_tile_sumsq;
+    a.chunk_sumsq = ctx->d_chunk_sumsq;
+    a.host_sumsq = ctx->h_sumsq_dev;
+    int64_t total_len = 0;
+    for (int32_t r = 0; r < count; ++r) total_len += lens[r];
+    // workgroup r of the move kernel reduces segment r's squared norm
+    a.move_blocks = move_grid(tiles, total_len, count);
+    a.stage = ctx->d_stage;
+    a.num_chunks = static_cast<uint32_t>(chunks);
+    a.chunk_status = ctx->d_chunk_status;
+    a.chunk_ticket = &ctx->d_tickets[1];
+
+    hipError_t e;
+    const bool timed = (ctx->cfg.flags & MICRO_FLAG_TIME_KERNEL) != 0;
+    ctx->stats.kernel_ms = -1.0f;
+    ctx->stats.redone_tiles = 0;
+    volatile int64_t* host_count = ctx->h_count;
+    volatile double* host_sumsq = ctx->h_sumsq;
+    for (int i = 0; i < 2 + count; ++i) host_count[i] = -1;
+    for (int32_t r = 0; r < count; ++r) host_sumsq[r] = -1.0;
+    if (timed && (e = hipEventRecord(ctx->ev[0], ctx->stream)) != hipSuccess)
+        return hip_fail(ctx, e, "hipEventRecord");
+    ctx->epoch = a.epoch;
+    if ((e = micro::launch_sweep(a, table, vec4, ctx->stream)) != hipSuccess)
+        return hip_fail(ctx, e, "sweep kernel launch");
+    if (timed && (e = hipEventRecord(ctx->ev[1], ctx->stream)) != hipSuccess)
+        return hip_fail(ctx, e, "hipEventRecord");
+    if ((e = hipStreamSynchronize(ctx->stream)) != hipSuccess) return hip_fail(ctx, e, "hipStreamSynchronize");
+    int64_t sum = 0;
+    bool ok = host_count[0] >= 0 && host_count[0] <= ctx->n_total;
+    for (int32_t r = 0; ok && r < count; ++r) {
+        const int64_t kr = host_count[2 + r];
+        ok = kr >= 0 && kr <= lens[r] && host_sumsq[r] != -1.0;  // a NaN residual gives a NaN norm
+        sum += kr;
+    }
+    if (!ok || sum != host_count[0]) {
+        set_error(ctx, "device reported inconsistent sweep counts (total %lld)",
+                  static_cast<long long>(host_count[0]));
+        ctx->needs_reset = true;
+        return MICRO_EHIP;
+    }
+    if (timed && (e = hipEventElapsedTime(&ctx->stats.kernel_ms, ctx->ev[0], ctx->ev[1])) != hipSuccess)
+        return hip_fail(ctx, e, "hipEventElapsedTime");
+    ctx->stats.redone_tiles = host_count[1];
+    ctx->stats.variant = MICRO_VARIANT_STAGED;
+    for (int32_t r = 0; r < count; ++r) {
+        k[r] = host_count[2 + r];
+        sumsq[r] = host_sumsq[r];
+    }
+    return MICRO_OK;
+}
+
 // Every partition of `world` searched once in one launch of each staged
 // kernel; the pairs of all partitions form one compaction in index order.
 micro_status execute_sweep(micro_ctx* ctx, const float* grad, float* residual, int32_t world, double density,
@@ -357,96 +497,18 @@ micro_status execute_sweep(micro_ctx* ctx, const float* grad, float* residual, i
         }
         return MICRO_OK;
     }
-    if (ctx->needs_reset || ctx->epoch >= micro::kMaxEpoch) {
-        micro_status st = reset_scratch(ctx);
-        if (st != MICRO_OK) return st;
-    }
-    const bool vec4 = ((reinterpret_cast<uintptr_t>(grad) ^ reinterpret_cast<uintptr_t>(residual)) & 15u) == 0;
-    micro::SweepTable table{};
-    table.count = static_cast<uint32_t>(world);
-    int64_t lens[micro::kMaxSweep];
-    int64_t tiles = 0, chunks = 0;
+    int64_t starts[micro::kMaxSweep], lens[micro::kMaxSweep];
+    float theta_f[micro::kMaxSweep];
     for (int32_t r = 0; r < world; ++r) {
-        int64_t start = 0, len = 0;
-        (void)micro_partition(ctx->n_total, r, world, &start, &len);
-        lens[r] = len;
-        micro::SweepSegment& sg = table.seg[r];
-        sg.start = start;
-        sg.end = start + len;
-        sg.base = micro::tile_base_for(grad, start, vec4);
-        sg.theta_f = threshold_as_f32(theta[r]);
-        sg.tile_first = static_cast<uint32_t>(tiles);
-        sg.chunk_first = static_cast<uint32_t>(chunks);
-        const int64_t seg_tiles = len > 0 ? (sg.end - sg.base + micro::kStreamTile - 1) / micro::kStreamTile : 0;
-        tiles += seg_tiles;
-        chunks += (seg_tiles + micro::kChunkTiles - 1) / micro::kChunkTiles;
+        (void)micro_partition(ctx->n_total, r, world, &starts[r], &lens[r]);
+        theta_f[r] = threshold_as_f32(theta[r]);
     }
-    table.seg[world].tile_first = static_cast<uint32_t>(tiles);
-    table.seg[world].chunk_first = static_cast<uint32_t>(chunks);
-    if (tiles > ctx->tile_capacity || chunks > ctx->chunk_capacity) {
-        set_error(ctx, "sweep needs %lld tiles, scratch holds %lld", static_cast<long long>(tiles),
-                  static_cast<long long>(ctx->tile_capacity));
-        return MICRO_ECAPACITY;
-    }
-    micro::LaunchArgs a{};
-    a.grad = grad;
-    a.residual = residual;
-    a.out_idx = out_idx;
-    a.out_val = out_val;
-    a.epoch = ctx->epoch + 1;
-    a.num_tiles = static_cast<uint32_t>(tiles);
-    a.count_out = ctx->d_count;
-    a.host_count = ctx->h_count_dev;
-    a.tile_counts = ctx->d_tile_counts;
-    a.tile_excl = ctx->d_tile_excl;
-    a.flagged_list = ctx->d_flagged_list;
-    a.split_tile = ctx->d_split_tile;
-    a.tile_sumsq = ctx->d_tile_sumsq;
-    a.chunk_sumsq = ctx->d_chunk_sumsq;
-    a.host_sumsq = ctx->h_sumsq_dev;
-    // workgroup r of the move kernel reduces segment r's squared norm
-    a.move_blocks = move_grid(tiles, ctx->n_total, world);
-    a.stage = ctx->d_stage;
-    a.num_chunks = static_cast<uint32_t>(chunks);
-    a.chunk_status = ctx->d_chunk_status;
-    a.chunk_ticket = &ctx->d_tickets[1];
-
-    hipError_t e;
-    const bool timed = (ctx->cfg.flags & MICRO_FLAG_TIME_KERNEL) != 0;
-    ctx->stats.kernel_ms = -1.0f;
-    ctx->stats.redone_tiles = 0;
-    volatile int64_t* host_count = ctx->h_count;
-    volatile double* host_sumsq = ctx->h_sumsq;
-    for (int i = 0; i < 2 + world; ++i) host_count[i] = -1;
-    for (int32_t r = 0; r < world; ++r) host_sumsq[r] = -1.0;
-    if (timed && (e = hipEventRecord(ctx->ev[0], ctx->stream)) != hipSuccess)
-        return hip_fail(ctx, e, "hipEventRecord");
-    ctx->epoch = a.epoch;
-    if ((e = micro::launch_sweep(a, table, vec4, ctx->stream)) != hipSuccess)
-        return hip_fail(ctx, e, "sweep kernel launch");
-    if (timed && (e = hipEventRecord(ctx->ev[1], ctx->stream)) != hipSuccess)
-        return hip_fail(ctx, e, "hipEventRecord");
-    if ((e = hipStreamSynchronize(ctx->stream)) != hipSuccess) return hip_fail(ctx, e, "hipStreamSynchronize");
-    int64_t sum = 0;
-    bool ok = host_count[0] >= 0 && host_count[0] <= ctx->n_total;
-    for (int32_t r = 0; ok && r < world; ++r) {
-        const int64_t kr = host_count[2 + r];
-        ok = kr >= 0 && kr <= lens[r] && host_sumsq[r] != -1.0;  // a NaN residual gives a NaN norm
-        sum += kr;
-    }
-    if (!ok || sum != host_count[0]) {
-        set_error(ctx, "device reported inconsistent sweep counts (total %lld)",
-                  static_cast<long long>(host_count[0]));
-        ctx->needs_reset = true;
-        return MICRO_EHIP;
-    }
-    if (timed && (e = hipEventElapsedTime(&ctx->stats.kernel_ms, ctx->ev[0], ctx->ev[1])) != hipSuccess)
-        return hip_fail(ctx, e, "hipEventElapsedTime");
-    ctx->stats.redone_tiles = host_count[1];
+    double sq[micro::kMaxSweep];
+    const micro_status st = run_segments(ctx, grad, residual, world, starts, lens, theta_f, out_idx, out_val, k, sq);
+    if (st != MICRO_OK) return st;
     for (int32_t r = 0; r < world; ++r) {
-        k[r] = host_count[2 + r];
         theta[r] = next_threshold(ctx->cfg, density, lens[r], k[r], theta[r]);
-        if (sumsq) sumsq[r] = host_sumsq[r];
+        if (sumsq) sumsq[r] = sq[r];
     }
     return MICRO_OK;
 }
@@ -630,7 +692,7 @@ micro_status micro_sparsify_step(micro_ctx* ctx, const float* grad, float* resid
         set_error(ctx, "invalid rank %d / world %d", rank, world);
         return MICRO_EINVAL;
     }
-    return execute_step(ctx, grad, residual, start, len, false, density, theta, out_idx, out_val, k);
+    return execute_step(ctx, grad, residual, start, len, false, density, theta, out_idx, out_val, k, nullptr);
 }
 
 micro_status micro_sweep_step(micro_ctx* ctx, const float* grad, float* residual, int32_t world, double density,
@@ -652,7 +714,7 @@ micro_status micro_cycle(int64_t t, int32_t worker, int32_t world, int32_t* cycl
 
 micro_status micro_ef_step(micro_ctx* ctx, const float* grad, float* residual, int64_t t, int32_t worker,
                            int32_t world, double density, double* theta, int32_t* out_idx, float* out_val,
-                           int64_t* k, int32_t* cycle) {
+                           int64_t* k, int32_t* cycle, double* sumsq) {
     if (!ctx) {
         set_error(nullptr, "ctx is NULL");
         return MICRO_EINVAL;
@@ -664,7 +726,8 @@ micro_status micro_ef_step(micro_ctx* ctx, const float* grad, float* residual, i
     }
     int64_t start = 0, len = 0;
     (void)micro_partition(ctx->n_total, part, world, &start, &len);
-    const micro_status st = execute_step(ctx, grad, residual, start, len, true, density, theta, out_idx, out_val, k);
+    const micro_status st =
+        execute_step(ctx, grad, residual, start, len, true, density, theta, out_idx, out_val, k, sumsq);
     if (st == MICRO_OK && cycle) *cycle = part;
     return st;
 }

@@ -168,7 +168,7 @@ def test_ef_and_union_calls_with_null_context_are_rejected():
     k = ctypes.c_int64(-7)
     c = ctypes.c_int32(-9)
     assert lib.micro_ef_step(None, None, None, 0, 0, 1, 0.1, ctypes.byref(th), None, None, ctypes.byref(k),
-                             ctypes.byref(c)) == _lib.MICRO_EINVAL
+                             ctypes.byref(c), None) == _lib.MICRO_EINVAL
     assert (th.value, k.value, c.value) == (1.0, -7, -9)
     assert lib.micro_union_gather(None, None, None, 0, 0, 0, None, None) == _lib.MICRO_EINVAL
     assert lib.micro_sparse_update(None, None, None, None, 0, 1) == _lib.MICRO_EINVAL
@@ -244,7 +244,7 @@ def test_ef_and_union_validation_on_device():
         c = ctypes.c_int32(-9)
         st = lib.micro_ef_step(sp._ctx, ctypes.c_void_p(grad), ctypes.c_void_p(res), t, worker, world, d,
                                ctypes.byref(th), ctypes.c_void_p(idx), ctypes.c_void_p(val), ctypes.byref(k),
-                               ctypes.byref(c))
+                               ctypes.byref(c), None)
         return st, k.value, c.value
 
     # the whole vectors are accessed: a residual overlapping any part of grad is refused

@@ -258,3 +258,120 @@ def test_union_empty_and_all_own():
     out = sp.union_gather(res, union, 0, own_val)
     assert torch.equal(out, own_val) and torch.equal(res, r0)
     sp.close()
+
+
+# ---------------------------------------------------------------------------
+# the full pass with its local error (Sec. 2, Eq. 1)
+# ---------------------------------------------------------------------------
+
+U = 2.0 ** -53
+
+
+def norm_tolerance(n, ref):
+    g = max(n - 1, 0) * U
+    return 2.0 * g / (1.0 - 2.0 * g) * abs(ref) * 1.01
+
+
+def ef_norm_vs_oracle(g, res, t, worker, world, density, theta, phase_shift=0):
+    """The pass with local_error against the oracle's pass and squared norm,
+    and against the pass without it (same bits)."""
+    N = g.size
+    sp = micro.Sparsifier(N, device=DEV)
+    gbuf = torch.empty(N + 4, dtype=torch.float32, device=DEV)
+    g_dev = gbuf[phase_shift:phase_shift + N]
+    g_dev.copy_(torch.from_numpy(g))
+    r_dev = torch.from_numpy(res).to(DEV)
+    r2_dev = r_dev.clone()
+    k, th, cy, idx, val, sq = sp.ef_step(g_dev, r_dev, t, worker, world, density, theta, local_error=True)
+    idx, val = idx.clone(), val.clone()
+    k2, th2, cy2, idx2, val2 = sp.ef_step(g_dev, r2_dev, t, worker, world, density, theta)
+    assert (k, th, cy) == (k2, th2, cy2)
+    assert torch.equal(idx, idx2) and torch.equal(val.view(torch.int32), val2.view(torch.int32))
+    assert torch.equal(r_dev.view(torch.int32), r2_dev.view(torch.int32))
+    r_or = res.copy()
+    o_idx, o_val, k_or, th_or, c_or = oracle.ef_step(g, r_or, t, worker, world, density, theta)
+    sq_or = oracle.sumsq(r_or)
+    assert (k, th, cy) == (k_or, th_or, c_or)
+    assert np.array_equal(idx.cpu().numpy(), o_idx)
+    assert bits_equal(val.cpu().numpy(), o_val)
+    assert bits_equal(r_dev.cpu().numpy(), r_or)
+    if np.isnan(sq_or):
+        assert np.isnan(sq)
+    elif np.isinf(sq_or):
+        assert sq == sq_or
+    else:
+        assert abs(sq - sq_or) <= norm_tolerance(N, sq_or), (sq, sq_or)
+    sp.close()
+    return sq
+
+
+@pytest.mark.parametrize("phase_shift", [0, 3])
+@pytest.mark.parametrize("N,world", [(1, 1), (3, 8), (4099, 3), (70_001, 7), (1_100_003, 5)])
+def test_ef_local_error_ragged(N, world, phase_shift):
+    rng = np.random.default_rng(N + 13 * world + phase_shift)
+    for t in [0, world + 1]:
+        for worker in sorted({0, world - 1}):
+            g = rng.standard_normal(N).astype(np.float32)
+            res = (rng.standard_normal(N) * 0.5).astype(np.float32)
+            ef_norm_vs_oracle(g, res, t, worker, world, 0.05, 1.5, phase_shift)
+
+
+def test_ef_local_error_special_values():
+    """Infinities outside the partition are accumulated, never selected; the
+    norm is then infinite; a NaN makes it NaN."""
+    N, world = 40_000, 4
+    rng = np.random.default_rng(14)
+    g = rng.standard_normal(N).astype(np.float32)
+    res = np.zeros(N, np.float32)
+    g[123] = np.inf
+    g[39_000] = -np.inf
+    for t in range(world):
+        sq = ef_norm_vs_oracle(g, res, t, 1, world, 0.01, 2.0)
+        assert sq == np.inf
+    g[20_000] = np.nan
+    assert np.isnan(ef_norm_vs_oracle(g, res, 0, 0, world, 0.01, 2.0))
+
+
+@pytest.mark.parametrize("name,worker,density,steps", [("resnet18", 5, 0.01, 6), ("bert_large", 3, 0.01, 3)])
+def test_ef_local_error_workload(name, worker, density, steps):
+    """Several passes with the local error on a workload, the residual
+    carried across passes, against the oracle's mirror."""
+    w = synth.get(name)
+    N = w.n_total
+    note(f"ef local error {name} worker {worker} steps {steps}")
+    sp = micro.Sparsifier(N, device=DEV)
+    g_dev = torch.empty(N, dtype=torch.float32, device=DEV)
+    r_dev = torch.zeros(N, dtype=torch.float32, device=DEV)
+    g_host = torch.empty(N, dtype=torch.float32, pin_memory=True)
+    mirror = np.zeros(N, np.float32)
+    theta = None
+    try:
+        for t in range(steps):
+            synth.gradient(w, t, DEV, out=g_dev)
+            if theta is None:
+                s, ln = oracle.partition(N, oracle.cycle(t, worker, w.world), w.world)
+                theta = synth.initial_theta(w, g_dev, s, s + ln, density)
+            g_host.copy_(g_dev)
+            k, th, c, idx, val, sq = sp.ef_step(g_dev, r_dev, t, worker, w.world, density, theta,
+                                                local_error=True)
+            o_idx, o_val, k_or, th_or, c_or = oracle.ef_step(g_host.numpy(), mirror, t, worker, w.world,
+                                                            density, theta)
+            assert (k, th, c) == (k_or, th_or, c_or)
+            assert np.array_equal(idx.cpu().numpy(), o_idx)
+            assert first_mismatch(r_dev.cpu().numpy(), mirror) < 0
+            sq_or = oracle.sumsq(mirror)
+            assert abs(sq - sq_or) <= norm_tolerance(N, sq_or), (t, sq, sq_or)
+            theta = th_or
+    finally:
+        sp.close()
+
+
+def test_ef_local_error_needs_the_staged_schedule():
+    N = 10_000
+    sp = micro.Sparsifier(N, device=DEV, variant=micro.MICRO_VARIANT_TICKET)
+    g = torch.randn(N, device=DEV)
+    r = torch.zeros(N, device=DEV)
+    with pytest.raises(micro.MicroError):
+        sp.ef_step(g, r, 0, 0, 2, 0.1, 1.0, local_error=True)
+    assert not bool(r.any())
+    sp.close()
