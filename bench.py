@@ -506,7 +506,7 @@ def main():
     args = parse_args()
     if args.gpus != 1:
         print(f"bench.py: --gpus {args.gpus} is not supported: the sparsify step has no collective "
-              "and this build measures one GPU (one worker's partition at its real size).",
+              "and this benchmark measures one GPU (one worker's partition at its real size).",
               file=sys.stderr)
         sys.exit(2)
     if args.copy_calibration:
