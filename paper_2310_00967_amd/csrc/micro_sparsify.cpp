@@ -55,6 +55,23 @@ struct micro_ctx {
 
 namespace {
 
+// Makes the context's device current for the scope of a call and restores the
+// caller's current device afterwards, so a context works whatever device the
+// calling thread has selected since init.
+struct DeviceScope {
+    int previous = -1;
+    bool switched = false;
+    explicit DeviceScope(int device) {
+        if (device >= 0 && hipGetDevice(&previous) == hipSuccess && previous != device)
+            switched = hipSetDevice(device) == hipSuccess;
+    }
+    ~DeviceScope() {
+        if (switched) (void)hipSetDevice(previous);
+    }
+    DeviceScope(const DeviceScope&) = delete;
+    DeviceScope& operator=(const DeviceScope&) = delete;
+};
+
 // Largest partition that an AUTO context runs on the ticket schedule.  On
 // MI355X the ticket schedule's single launch took 8.8 us of device time for
 // 262,144 values against 16.8 us for the staged schedule's three, and lost
@@ -147,6 +164,7 @@ micro_status reset_scratch(micro_ctx* ctx) {
 
 void release(micro_ctx* ctx) {
     if (!ctx) return;
+    DeviceScope scope(ctx->device);
     if (ctx->device >= 0) (void)hipStreamSynchronize(ctx->stream);
     for (hipEvent_t ev : ctx->ev)
         if (ev) (void)hipEventDestroy(ev);
@@ -188,6 +206,7 @@ micro_status run_segments(micro_ctx* ctx, const float* grad, float* residual, in
 micro_status execute_step(micro_ctx* ctx, const float* grad, float* residual, int64_t start, int64_t len,
                           bool accumulate_outside, double density, double* theta, int32_t* out_idx,
                           float* out_val, int64_t* k, double* sumsq) {
+    DeviceScope scope(ctx->device);
     if (!grad || !residual || !theta || !out_idx || !out_val || !k) {
         set_error(ctx, "NULL pointer argument");
         return MICRO_EINVAL;
@@ -457,6 +476,7 @@ micro_status run_segments(micro_ctx* ctx, const float* grad, float* residual, in
 // kernel; the pairs of all partitions form one compaction in index order.
 micro_status execute_sweep(micro_ctx* ctx, const float* grad, float* residual, int32_t world, double density,
                            double* theta, int32_t* out_idx, float* out_val, int64_t* k, double* sumsq) {
+    DeviceScope scope(ctx->device);
     if (!grad || !residual || !theta || !out_idx || !out_val || !k) {
         set_error(ctx, "NULL pointer argument");
         return MICRO_EINVAL;
@@ -518,6 +538,7 @@ micro_status execute_sweep(micro_ctx* ctx, const float* grad, float* residual, i
 // the launch.
 template <class Launch>
 micro_status execute_union(micro_ctx* ctx, Launch launch) {
+    DeviceScope scope(ctx->device);
     hipError_t e;
     const bool timed = (ctx->cfg.flags & MICRO_FLAG_TIME_KERNEL) != 0;
     ctx->stats.kernel_ms = -1.0f;

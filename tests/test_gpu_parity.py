@@ -340,3 +340,33 @@ def test_largest_vector_the_index_type_allows():
     assert first_mismatch(val.cpu().numpy(), o_val) < 0
     assert first_mismatch(r_dev.cpu().numpy(), res) < 0
     sp.close()
+
+
+def test_two_contexts_on_two_streams():
+    """Contexts own their scratch and stream: two contexts, each on its own
+    torch stream (default priority), stepping interleaved on different
+    workloads and schedules, each match the oracle."""
+    rng = np.random.default_rng(44)
+    cases = []
+    for N, variant, world, rank in [(2_500_003, STAGED, 3, 1), (300_001, TICKET, 2, 0)]:
+        s = torch.cuda.Stream()
+        with torch.cuda.stream(s):
+            sp = micro.Sparsifier(N, device=DEV, variant=variant, stream=s)
+            r_dev = torch.zeros(N, dtype=torch.float32, device=DEV)
+        cases.append(dict(N=N, sp=sp, stream=s, world=world, rank=rank, r_dev=r_dev,
+                          res=np.zeros(N, np.float32), theta=2.0, rng=rng))
+    for t in range(6):
+        for c in cases:
+            g = (c["rng"].standard_normal(c["N"])).astype(np.float32)
+            with torch.cuda.stream(c["stream"]):
+                g_dev = torch.from_numpy(g).to(DEV, non_blocking=False)
+                k, th, idx, val = c["sp"].step(g_dev, c["r_dev"], c["rank"], c["world"], 0.01, c["theta"])
+                idx_h, val_h, r_h = idx.cpu().numpy(), val.cpu().numpy(), c["r_dev"].cpu().numpy()
+            o_idx, o_val, k_or, th_or = oracle.step(g, c["res"], c["rank"], c["world"], 0.01, c["theta"])
+            assert (k, th) == (k_or, th_or)
+            assert np.array_equal(idx_h, o_idx)
+            assert first_mismatch(val_h, o_val) < 0
+            assert first_mismatch(r_h, c["res"]) < 0
+            c["theta"] = th
+    for c in cases:
+        c["sp"].close()
