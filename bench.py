@@ -68,9 +68,19 @@ def parse_args():
     return args
 
 
-def kernel_sha256():
-    with open(KERNEL_SRC, "rb") as f:
-        return hashlib.sha256(f.read()).hexdigest()
+def kernel_sha256(text=None):
+    """sha256 of the kernel source's code: // comments, trailing blanks and
+    blank lines removed, so the stored counters stay valid across comment
+    edits and go stale with any change to the code."""
+    if text is None:
+        with open(KERNEL_SRC, encoding="utf-8") as f:
+            text = f.read()
+    code = []
+    for line in text.splitlines():
+        line = line.split("//", 1)[0].rstrip()
+        if line:
+            code.append(line)
+    return hashlib.sha256("\n".join(code).encode()).hexdigest()
 
 
 def read_traffic():

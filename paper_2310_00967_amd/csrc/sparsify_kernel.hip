@@ -8,19 +8,20 @@
 // are written in index order (Algorithm 1, selection and gathering of the
 // accumulated values).
 //
-// Order-preserving compaction in the same pass:
+// Order-preserving compaction:
 //   * per wavefront row: one ballot per element slot and mbcnt give each
 //     lane's rank among the selected values before it in the row;
 //   * per workgroup: the wavefront row totals go through LDS, giving each
 //     row's offset inside the tile and the tile's count;
-//   * across workgroups: decoupled look-back over one 64-bit status word per
-//     tile (count | flag | epoch).  Wavefront 0 inspects 64 predecessors per
+//   * across workgroups: decoupled look-back over 64-bit status words
+//     (count | flag | epoch), one per tile (ticket schedule) or per chunk of
+//     tiles (staged schedule).  Wavefront 0 inspects 64 predecessors per
 //     round with agent-scope atomic loads, which read the memory level shared
 //     by all XCDs.  The count and its flag share one word, so relaxed atomics
 //     suffice: a reader sees either the whole published word or an older one.
 //
-// Staged schedule (default), three kernels; no workgroup of the first and the
-//   last ever waits for another:
+// Staged schedule, three kernels; no workgroup of the first and the last ever
+//   waits for another:
 //   stream_kernel: one 1024-value tile per 256-thread workgroup, one dwordx4
 //     per lane and stream, every HBM stream non-temporal.  It ranks the tile's
 //     selected values, writes the residual, packs the pairs in LDS and writes
@@ -36,13 +37,20 @@
 //   move_kernel: a fixed grid redoes the flagged tiles (one wavefront each)
 //     and moves the staged pairs to their final places in equal pieces of the
 //     merged sequence of tiles and pairs, whatever the clustering of the
-//     selection.
+//     selection; it also stores the counts into mapped host memory.
 //   HBM traffic beyond the 12 bytes per value of the stream: 16 bytes per
 //   selected value (staged write and read) and 8 bytes per 1024 values.
-// Ticket schedule (variant 1): a single pass; tiles are drawn from a ticket
+// Sweep: the same three kernels over a table of segments (every partition of
+//   a vector with its own threshold, or a full error-feedback pass split at
+//   its partition), each tile also reducing the squared norm of its new
+//   residual (the local error of Sec. 2) in a fixed order.
+// Ticket schedule: a single pass; 4096-value tiles are drawn from a ticket
 //   counter in increasing order, so a tile only waits for tiles claimed by
 //   running workgroups; the per-tile ticket and look-back round trips cost
-//   bandwidth.
+//   bandwidth, but one launch beats three for partitions of up to about a
+//   million values.
+// accumulate_kernel: the error-feedback addition alone, for the part of the
+//   vector a full pass does not search.
 #include "sparsify_kernel.h"
 
 namespace micro {
