@@ -397,7 +397,7 @@ __device__ __forceinline__ double block_sum(double v, int lane, int wave, double
 // segment supplies range and threshold, and the tile also stores the squared
 // norm of its new residual (also for a tile left to the move kernel, whose
 // new residual is fixed by its selection bits all the same).
-template <int VEC, int ROWS, bool SWEEP>
+template <int VEC, int ROWS, bool SWEEP, bool NT_RES>
 __device__ __forceinline__ void stream_tile(LaunchArgs a, const SweepTable* tbl) {
     constexpr int WAVES = kStreamBlock / kWaveSize;
     static_assert(VEC * ROWS * kStreamBlock == kStreamTile, "tile size");
@@ -413,7 +413,7 @@ __device__ __forceinline__ void stream_tile(LaunchArgs a, const SweepTable* tbl)
 
     Tile<VEC, ROWS, kStreamBlock> t;
     uint32_t lane_rank[ROWS], row_count[ROWS], row_base[ROWS];
-    load_tile<VEC, ROWS, kStreamBlock, true>(a, tile_base, tid, t);
+    load_tile<VEC, ROWS, kStreamBlock, NT_RES>(a, tile_base, tid, t);
     const uint32_t sel = compute_tile(a, tid, t);
     if constexpr (SWEEP) {
         double sq = 0.0;
@@ -435,7 +435,7 @@ __device__ __forceinline__ void stream_tile(LaunchArgs a, const SweepTable* tbl)
         if (tid == 0) a.tile_counts[tile] = count | kOverflow;
         return;
     }
-    store_residual<VEC, ROWS, kStreamBlock, true>(a, tid, t, sel);
+    store_residual<VEC, ROWS, kStreamBlock, NT_RES>(a, tid, t, sel);
 #pragma unroll
     for (int r = 0; r < ROWS; ++r) {
         uint32_t pos = row_base[r] + lane_rank[r];
@@ -456,14 +456,14 @@ __device__ __forceinline__ void stream_tile(LaunchArgs a, const SweepTable* tbl)
     if (tid == 0) a.tile_counts[tile] = count;
 }
 
-template <int VEC, int ROWS>
+template <int VEC, int ROWS, bool NT_RES>
 __global__ __launch_bounds__(kStreamBlock) void stream_kernel(LaunchArgs a) {
-    stream_tile<VEC, ROWS, false>(a, nullptr);
+    stream_tile<VEC, ROWS, false, NT_RES>(a, nullptr);
 }
 
-template <int VEC, int ROWS>
+template <int VEC, int ROWS, bool NT_RES>
 __global__ __launch_bounds__(kStreamBlock) void stream_sweep_kernel(LaunchArgs a, SweepTable tbl) {
-    stream_tile<VEC, ROWS, true>(a, &tbl);
+    stream_tile<VEC, ROWS, true, NT_RES>(a, &tbl);
 }
 
 // Full processing of one flagged tile by one wavefront with its pairs from
@@ -597,11 +597,13 @@ __device__ __forceinline__ void scan_chunk(const LaunchArgs& a, const SweepTable
         offs[i] = pos | (raw[i] & kOverflow);
         // The move piece whose first item falls among this tile's items: the
         // tile's own item sits at tile + pos in the merged sequence and its
-        // count pairs follow it; count < kMoveSpan, so there is at most one.
+        // count pairs follow it; count <= kStreamTile < piece size, so there
+        // is at most one.
         if (first_tile + i < end_tile) {
             const uint64_t item = static_cast<uint64_t>(first_tile + i) + pos;
-            const uint64_t m = (item + kMoveSpan - 1) / kMoveSpan;
-            if (m * kMoveSpan < item + 1 + count) a.split_tile[m] = first_tile + i;
+            const uint64_t span = a.move_span;
+            const uint64_t m = (item + span - 1) / span;
+            if (m * span < item + 1 + count) a.split_tile[m] = first_tile + i;
         }
         if (raw[i] & kOverflow) s_flagged[atomicAdd(&s_num_flagged, 1u)] = first_tile + i;
         pos += count;
@@ -674,11 +676,13 @@ __device__ __forceinline__ void block_max_scan(uint16_t* v, uint32_t n, int tid,
 }
 
 // Move kernel: a fixed grid walks the merged sequence of tiles and output
-// pairs in pieces of kMoveSpan items, so every piece costs about the same
-// whatever the clustering of the selection: many pairs from few tiles, or few
-// pairs scattered over many tiles.  Piece m's items lie in the tiles from
-// split_tile[m] to split_tile[m + 1] (recorded by the scan kernel), at most
-// kMoveSpan + 1 of them, and it holds the output positions [lo, hi).  The
+// pairs in pieces of move_span items (kMoveSpan, or kMoveSpanSmall for a
+// partition whose residual stays in the last-level cache: more, shorter
+// pieces), so every piece costs about the same whatever the clustering of the
+// selection: many pairs from few tiles, or few pairs scattered over many
+// tiles.  Piece m's items lie in the tiles from split_tile[m] to
+// split_tile[m + 1] (recorded by the scan kernel), at most move_span + 1 of
+// them, and it holds the output positions [lo, hi).  The
 // tiles' output offsets go to LDS; every tile that is the last of its offset
 // (so the one that owns the positions from that offset on) writes its window
 // index at its first position in the piece, and a running maximum fills in the
@@ -745,17 +749,18 @@ __device__ __forceinline__ void move_pieces(const LaunchArgs& a, const SweepTabl
         }
     }
     const uint64_t total = static_cast<uint64_t>(a.num_tiles) + static_cast<uint64_t>(k);
-    const uint32_t pieces = static_cast<uint32_t>((total + kMoveSpan - 1) / kMoveSpan);
+    const uint32_t span_items = a.move_span < kMoveSpan ? a.move_span : kMoveSpan;
+    const uint32_t pieces = static_cast<uint32_t>((total + span_items - 1) / span_items);
     for (uint32_t m = blockIdx.x; m < pieces; m += gridDim.x) {
         const bool first = m == blockIdx.x;
         const uint32_t t0 = first ? first_t0 : a.split_tile[m];
         const uint32_t t1 = m + 1 < pieces ? (first ? first_t1 : a.split_tile[m + 1]) : a.num_tiles - 1;
-        // t1 - t0 <= kMoveSpan by construction; the clamp only keeps LDS
+        // t1 - t0 <= span_items by construction; the clamp only keeps LDS
         // accesses inside the window
         const uint32_t span = t1 - t0 + 1;
         const uint32_t ntiles = span < kWindow ? span : kWindow;
         for (uint32_t i = tid; i < (ntiles + 31) / 32; i += kMoveBlock) s_flag_bits[i] = 0u;
-        for (uint32_t i = tid; i < kMoveSpan; i += kMoveBlock) s_owner[i] = 0;
+        for (uint32_t i = tid; i < span_items; i += kMoveBlock) s_owner[i] = 0;
         __syncthreads();
         for (uint32_t i = tid; i < ntiles; i += kMoveBlock) {
             const uint32_t v = a.tile_excl[t0 + i];
@@ -763,14 +768,14 @@ __device__ __forceinline__ void move_pieces(const LaunchArgs& a, const SweepTabl
             if (v & kOverflow) atomicOr(&s_flag_bits[i / 32], 1u << (i % 32));
         }
         __syncthreads();
-        const uint64_t x0 = static_cast<uint64_t>(m) * kMoveSpan;
-        const uint64_t x1 = x0 + kMoveSpan < total ? x0 + kMoveSpan : total;
+        const uint64_t x0 = static_cast<uint64_t>(m) * span_items;
+        const uint64_t x1 = x0 + span_items < total ? x0 + span_items : total;
         const uint32_t lo = pairs_before(x0, t0, s_off[0]);
         uint32_t hi = x1 == total ? static_cast<uint32_t>(k) : pairs_before(x1, t1, s_off[ntiles - 1]);
-        // lo <= hi <= lo + kMoveSpan and hi <= k hold by construction; the
+        // lo <= hi <= lo + span_items and hi <= k hold by construction; the
         // clamps only keep the accesses below inside their buffers
         hi = hi < lo ? lo : hi;
-        hi = hi - lo <= static_cast<uint32_t>(kMoveSpan) ? hi : lo + kMoveSpan;
+        hi = hi - lo <= span_items ? hi : lo + span_items;
         hi = static_cast<int64_t>(hi) <= k ? hi : static_cast<uint32_t>(k);
         hi = hi < lo ? lo : hi;
         // Tile q owns the positions from its offset up to the next tile's;
@@ -933,12 +938,19 @@ int64_t tile_base_for(const float* grad, int64_t start, bool vec4) {
 
 hipError_t launch_staged(const LaunchArgs& args, bool vec4, hipStream_t stream) {
     const dim3 grid_stream(args.num_tiles), grid_scan(args.num_chunks), grid_move(args.move_blocks);
+    const dim3 bs(kStreamBlock);
     if (vec4) {
-        hipLaunchKernelGGL((stream_kernel<4, 1>), grid_stream, dim3(kStreamBlock), 0, stream, args);
+        if (args.res_temporal)
+            hipLaunchKernelGGL((stream_kernel<4, 1, false>), grid_stream, bs, 0, stream, args);
+        else
+            hipLaunchKernelGGL((stream_kernel<4, 1, true>), grid_stream, bs, 0, stream, args);
         hipLaunchKernelGGL(scan_kernel, grid_scan, dim3(kScanBlock), 0, stream, args);
         hipLaunchKernelGGL(move_kernel<4>, grid_move, dim3(kMoveBlock), 0, stream, args);
     } else {
-        hipLaunchKernelGGL((stream_kernel<1, 4>), grid_stream, dim3(kStreamBlock), 0, stream, args);
+        if (args.res_temporal)
+            hipLaunchKernelGGL((stream_kernel<1, 4, false>), grid_stream, bs, 0, stream, args);
+        else
+            hipLaunchKernelGGL((stream_kernel<1, 4, true>), grid_stream, bs, 0, stream, args);
         hipLaunchKernelGGL(scan_kernel, grid_scan, dim3(kScanBlock), 0, stream, args);
         hipLaunchKernelGGL(move_kernel<1>, grid_move, dim3(kMoveBlock), 0, stream, args);
     }
@@ -947,12 +959,19 @@ hipError_t launch_staged(const LaunchArgs& args, bool vec4, hipStream_t stream) 
 
 hipError_t launch_sweep(const LaunchArgs& args, const SweepTable& table, bool vec4, hipStream_t stream) {
     const dim3 grid_stream(args.num_tiles), grid_scan(args.num_chunks), grid_move(args.move_blocks);
+    const dim3 bs(kStreamBlock);
     if (vec4) {
-        hipLaunchKernelGGL((stream_sweep_kernel<4, 1>), grid_stream, dim3(kStreamBlock), 0, stream, args, table);
+        if (args.res_temporal)
+            hipLaunchKernelGGL((stream_sweep_kernel<4, 1, false>), grid_stream, bs, 0, stream, args, table);
+        else
+            hipLaunchKernelGGL((stream_sweep_kernel<4, 1, true>), grid_stream, bs, 0, stream, args, table);
         hipLaunchKernelGGL(scan_sweep_kernel, grid_scan, dim3(kScanBlock), 0, stream, args, table);
         hipLaunchKernelGGL(move_sweep_kernel<4>, grid_move, dim3(kMoveBlock), 0, stream, args, table);
     } else {
-        hipLaunchKernelGGL((stream_sweep_kernel<1, 4>), grid_stream, dim3(kStreamBlock), 0, stream, args, table);
+        if (args.res_temporal)
+            hipLaunchKernelGGL((stream_sweep_kernel<1, 4, false>), grid_stream, bs, 0, stream, args, table);
+        else
+            hipLaunchKernelGGL((stream_sweep_kernel<1, 4, true>), grid_stream, bs, 0, stream, args, table);
         hipLaunchKernelGGL(scan_sweep_kernel, grid_scan, dim3(kScanBlock), 0, stream, args, table);
         hipLaunchKernelGGL(move_sweep_kernel<1>, grid_move, dim3(kMoveBlock), 0, stream, args, table);
     }
