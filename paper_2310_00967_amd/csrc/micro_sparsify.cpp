@@ -39,7 +39,7 @@ struct micro_ctx {
     int64_t chunk_capacity = 0;
     // ticket schedule: tile look-back words
     uint64_t* d_status = nullptr;
-    unsigned long long* d_tickets = nullptr; // [0] tile ticket, [1] chunk ticket
+    unsigned long long* d_tickets = nullptr; // [0] tile ticket of the one-pass schedule
     int64_t* d_count = nullptr;              // [0] selected count, [1] flagged tiles
     int64_t* h_count = nullptr;              // mapped pinned host memory stored by the kernels: [0] k,
                                              // [1] redone tiles, [2 + r] a sweep's counts
@@ -159,7 +159,7 @@ bool ranges_overlap(const void* a, size_t an, const void* b, size_t bn) {
 }
 
 micro_status reset_scratch(micro_ctx* ctx) {
-    hipError_t e = hipMemsetAsync(ctx->d_tickets, 0, 2 * sizeof(unsigned long long), ctx->stream);
+    hipError_t e = hipMemsetAsync(ctx->d_tickets, 0, sizeof(unsigned long long), ctx->stream);
     if (e == hipSuccess) e = hipMemsetAsync(ctx->d_count, 0, 2 * sizeof(int64_t), ctx->stream);
     if (e == hipSuccess && ctx->d_status)
         e = hipMemsetAsync(ctx->d_status, 0, sizeof(uint64_t) * ctx->ticket_capacity, ctx->stream);
@@ -339,7 +339,6 @@ micro_status execute_step(micro_ctx* ctx, const float* grad, float* residual, in
     a.stage = ctx->d_stage;
     a.num_chunks = static_cast<uint32_t>(chunks);
     a.chunk_status = ctx->d_chunk_status;
-    a.chunk_ticket = &ctx->d_tickets[1];
     a.status = ctx->d_status;
     a.ticket = &ctx->d_tickets[0];
 
@@ -447,7 +446,6 @@ micro_status run_segments(micro_ctx* ctx, const float* grad, float* residual, in
     a.stage = ctx->d_stage;
     a.num_chunks = static_cast<uint32_t>(chunks);
     a.chunk_status = ctx->d_chunk_status;
-    a.chunk_ticket = &ctx->d_tickets[1];
 
     hipError_t e;
     const bool timed = (ctx->cfg.flags & MICRO_FLAG_TIME_KERNEL) != 0;
@@ -662,7 +660,7 @@ micro_status micro_sparsify_init(micro_ctx** out, int64_t n_total, void* hip_str
     // plus one tile for the alignment of the first tile.
     ctx->has_staged = c.variant != MICRO_VARIANT_TICKET;
     ctx->has_ticket = c.variant != MICRO_VARIANT_STAGED;
-    bool ok = hipMalloc(&ctx->d_tickets, 2 * sizeof(unsigned long long)) == hipSuccess &&
+    bool ok = hipMalloc(&ctx->d_tickets, sizeof(unsigned long long)) == hipSuccess &&
               hipMalloc(&ctx->d_count, 2 * sizeof(int64_t)) == hipSuccess &&
               hipHostMalloc(&ctx->h_count, (2 + micro::kMaxSweep) * sizeof(int64_t),
                             hipHostMallocMapped | hipHostMallocCoherent) == hipSuccess &&

@@ -86,7 +86,6 @@ struct LaunchArgs {
     uint2* stage;           // num_tiles * kStageCap staged (index, value bits) pairs
     uint32_t num_chunks;    // ceil(num_tiles / kChunkTiles)
     uint64_t* chunk_status;             // >= num_chunks look-back words
-    unsigned long long* chunk_ticket;   // 0 at launch, rearmed by the kernel
     // ticket schedule
     uint64_t* status;                   // >= num_tiles look-back words
     unsigned long long* ticket;         // 0 at launch, rearmed by the kernel

@@ -23,17 +23,20 @@
 // Staged schedule, three kernels; no workgroup of the first and the last ever
 //   waits for another:
 //   stream_kernel: one 1024-value tile per 256-thread workgroup, one dwordx4
-//     per lane and stream, every HBM stream non-temporal.  It ranks the tile's
+//     per lane and stream, the gradient and the outputs non-temporal; the
+//     residual too unless the host asks for temporal accesses (a partition
+//     whose residual stays in the last-level cache).  It ranks the tile's
 //     selected values, writes the residual, packs the pairs in LDS and writes
 //     them with coalesced stores to the tile's staging slot (kStageCap
 //     8-byte (index, value) records), then stores the tile's count.  A tile
 //     with more than kStageCap selected values is left untouched and flagged.
-//   scan_kernel: one workgroup per chunk of kChunkTiles tiles, in ticket
-//     order: a scan of the chunk's tile counts and a decoupled look-back over
-//     chunk status words give every tile its output offset; it records the
-//     tile where each move piece starts and lists the flagged tiles.
-//     One ticket and one look-back per million values keep the cross-XCD
-//     round trips off the streaming pass.
+//   scan_kernel: one workgroup per chunk of kChunkTiles tiles: a scan of the
+//     chunk's tile counts and a decoupled look-back over chunk status words
+//     give every tile its output offset; it records the tile where each move
+//     piece starts and lists the flagged tiles.  One look-back per million
+//     values keeps the cross-XCD round trips off the streaming pass; a
+//     predecessor that has not published is recomputed from its tile counts,
+//     so chunks need no ticket.
 //   move_kernel: a fixed grid redoes the flagged tiles (one wavefront each)
 //     and moves the staged pairs to their final places in equal pieces of the
 //     merged sequence of tiles and pairs, whatever the clustering of the
@@ -495,9 +498,83 @@ __device__ void redo_tile(const LaunchArgs& a, int64_t tile_base, int lane, uint
     }
 }
 
-// Scan kernel: one workgroup per chunk of kChunkTiles tiles, in ticket order.
-// Scans the chunk's tile counts, finds the chunk's output offset by decoupled
-// look-back over chunk status words, publishes every tile's output offset
+// Tiles [first, end) of scan chunk `chunk`: kChunkTiles per chunk; in a
+// sweep each segment has chunks of its own, the last one possibly short.
+template <bool SWEEP>
+__device__ __forceinline__ void chunk_tiles(const LaunchArgs& a, const SweepTable* tbl, uint32_t chunk,
+                                            uint32_t& first, uint32_t& end) {
+    if constexpr (SWEEP) {
+        const uint32_t r = segment_of_chunk(tbl, chunk);
+        first = tbl->seg[r].tile_first + (chunk - tbl->seg[r].chunk_first) * kChunkTiles;
+        const uint32_t seg_end = tbl->seg[r + 1].tile_first;
+        end = first + kChunkTiles < seg_end ? first + kChunkTiles : seg_end;
+    } else {
+        first = chunk * kChunkTiles;
+        end = first + kChunkTiles < a.num_tiles ? first + kChunkTiles : a.num_tiles;
+    }
+}
+
+// Selected values of chunk `chunk`, summed from its tile counts by one
+// wavefront (uniform): the count the chunk's own workgroup publishes.
+template <bool SWEEP>
+__device__ uint32_t chunk_selected(const LaunchArgs& a, const SweepTable* tbl, uint32_t chunk, int lane) {
+    uint32_t first, end;
+    chunk_tiles<SWEEP>(a, tbl, chunk, first, end);
+    uint32_t v = 0;
+#pragma unroll
+    for (int i = 0; i < kChunkTiles / kWaveSize; ++i) {
+        const uint32_t t = first + i * kWaveSize + lane;
+        v += t < end ? (a.tile_counts[t] & ~kOverflow) : 0u;
+    }
+    return wave_sum(v);
+}
+
+constexpr int kLookbackPolls = 4;  // polls of a silent predecessor before its count is recomputed
+
+// Exclusive prefix of chunk `chunk`: a look-back by all 64 lanes of one
+// wavefront over the status words of the chunks before it, back to the
+// nearest inclusive prefix.  Chunks are not handed out in order (no ticket),
+// so a predecessor may not have run yet: a word still unpublished after a few
+// polls is replaced by the predecessor's count summed from its tile counts,
+// which are final before the scan kernel starts.  The look-back therefore
+// ends whatever order the workgroups run in.
+template <bool SWEEP>
+__device__ uint32_t chunk_lookback(const LaunchArgs& a, const SweepTable* tbl, uint32_t chunk, int lane) {
+    const uint64_t tag = static_cast<uint64_t>(a.epoch) << kEpochShift;
+    uint32_t exclusive = 0;
+    int64_t top = static_cast<int64_t>(chunk) - 1;
+    int polls = 0;
+    for (;;) {
+        const int64_t p = top - lane;
+        // positions before chunk 0 read as an inclusive prefix of zero
+        const uint64_t w = (p >= 0) ? load_status(&a.chunk_status[p]) : (tag | kFlagInclusive);
+        const bool valid = (w >> kEpochShift) == a.epoch && (w & kFlagMask) != 0;
+        const bool inclusive = valid && (w & kFlagMask) == kFlagInclusive;
+        const uint64_t inc_mask = __ballot(inclusive);
+        // lanes 0 .. first inclusive lane (all 64 when none is inclusive)
+        const uint64_t need = inc_mask ? (inc_mask ^ (inc_mask - 1)) : ~0ull;
+        uint64_t missing = __ballot(!valid) & need;
+        if (missing && ++polls < kLookbackPolls) {
+            __builtin_amdgcn_s_sleep(1);
+            continue;
+        }
+        polls = 0;
+        uint32_t v = ((need >> lane) & 1ull) && valid ? static_cast<uint32_t>(w & kCountMask) : 0u;
+        while (missing) {  // uniform
+            const int l = __builtin_ctzll(missing);
+            missing &= missing - 1;
+            const uint32_t c = chunk_selected<SWEEP>(a, tbl, static_cast<uint32_t>(top - l), lane);
+            if (lane == l) v = c;
+        }
+        exclusive += wave_sum(v);
+        if (inc_mask) return exclusive;
+        top -= kWaveSize;
+    }
+}
+
+// Scan kernel: one workgroup per chunk of kChunkTiles tiles (chunk =
+// workgroup index).  Scans the chunk's tile counts, finds the chunk's output
+// offset by decoupled look-back over chunk status words (chunk_lookback), publishes every tile's output offset
 // (bit 31: flagged tile), records for every move piece the tile that holds
 // its first item, and appends the chunk's flagged tiles to the list that the
 // move kernel redoes.
@@ -509,7 +586,7 @@ __device__ __forceinline__ void scan_chunk(const LaunchArgs& a, const SweepTable
     constexpr int WAVES = kScanBlock / kWaveSize;
     constexpr int PER_THREAD = kChunkTiles / kScanBlock;
     static_assert(PER_THREAD % 4 == 0, "whole uint4s of counts per thread");
-    __shared__ uint32_t s_chunk, s_exclusive, s_num_flagged, s_list_base;
+    __shared__ uint32_t s_exclusive, s_num_flagged, s_list_base;
     __shared__ uint32_t s_wave_total[WAVES];
     __shared__ uint32_t s_flagged[kChunkTiles];
     __shared__ double s_sq[WAVES];
@@ -517,20 +594,10 @@ __device__ __forceinline__ void scan_chunk(const LaunchArgs& a, const SweepTable
     const int tid = threadIdx.x;
     const int lane = tid & (kWaveSize - 1);
     const int wave = tid / kWaveSize;
-    if (tid == 0) {
-        s_chunk = draw_ticket(a.chunk_ticket, a.num_chunks - 1);
-        s_num_flagged = 0;
-    }
-    __syncthreads();
-    const uint32_t chunk = s_chunk;
-    if (chunk >= a.num_chunks) return;  // only reachable if the counter was not rearmed
-    uint32_t chunk_tile = chunk * kChunkTiles, end_tile = a.num_tiles;
-    if constexpr (SWEEP) {
-        const uint32_t r = segment_of_chunk(tbl, chunk);
-        chunk_tile = tbl->seg[r].tile_first + (chunk - tbl->seg[r].chunk_first) * kChunkTiles;
-        const uint32_t seg_end = tbl->seg[r + 1].tile_first;
-        end_tile = chunk_tile + kChunkTiles < seg_end ? chunk_tile + kChunkTiles : seg_end;
-    }
+    if (tid == 0) s_num_flagged = 0;
+    const uint32_t chunk = blockIdx.x;
+    uint32_t chunk_tile, end_tile;
+    chunk_tiles<SWEEP>(a, tbl, chunk, chunk_tile, end_tile);
     const uint32_t first_tile = chunk_tile + tid * PER_THREAD;
     const bool whole = first_tile % 4 == 0 && first_tile + PER_THREAD <= end_tile;
 
@@ -580,7 +647,7 @@ __device__ __forceinline__ void scan_chunk(const LaunchArgs& a, const SweepTable
             if (lane == 0) store_status(&a.chunk_status[0], tag | kFlagInclusive | total);
         } else {
             if (lane == 0) store_status(&a.chunk_status[chunk], tag | kFlagAggregate | total);
-            excl = lookback(a.chunk_status, chunk, a.epoch, lane);
+            excl = chunk_lookback<SWEEP>(a, tbl, chunk, lane);
             if (lane == 0) store_status(&a.chunk_status[chunk], tag | kFlagInclusive | (excl + total));
         }
         if (lane == 0) {
@@ -709,10 +776,13 @@ __device__ __forceinline__ void move_pieces(const LaunchArgs& a, const SweepTabl
     // the split array, which has room for the largest grid plus one.
     const uint32_t first_t0 = a.split_tile[blockIdx.x];
     const uint32_t first_t1 = a.split_tile[blockIdx.x + 1];
-    const int64_t k = a.count_out[0];
+    // both counts in one load: the flagged-tile count must not wait for k
+    const longlong2 counts = *reinterpret_cast<const longlong2*>(a.count_out);
+    const int64_t k = counts.x;
+    const uint32_t flagged = static_cast<uint32_t>(counts.y);
     if (blockIdx.x == 0 && tid == 0) {  // the scan kernel has finished both counts
         a.host_count[0] = k;
-        a.host_count[1] = a.count_out[1];
+        a.host_count[1] = counts.y;
     }
     if constexpr (SWEEP) {
         // Each segment's count: the difference of the global offsets of its
@@ -736,7 +806,6 @@ __device__ __forceinline__ void move_pieces(const LaunchArgs& a, const SweepTabl
     if (k == 0) return;
     // Flagged tiles first, one wavefront each over the whole grid: the
     // wavefront recomputes the tile and writes its pairs and residual.
-    const uint32_t flagged = static_cast<uint32_t>(a.count_out[1]);
     for (uint32_t f = blockIdx.x * WAVES + tid / kWaveSize; f < flagged; f += gridDim.x * WAVES) {
         const uint32_t tile = a.flagged_list[f];
         const uint32_t out_base = a.tile_excl[tile] & ~kOverflow;
