@@ -2,10 +2,13 @@
 """Throughput of MiCRO's per-worker sparsify step on one MI355X.
 
 A step is one pass of the whole hot path over one synthetic gradient: for each
-rank the workload sweeps, the error-feedback add, the threshold test, the
+worker the workload sweeps, the error-feedback add, the threshold test, the
 residual update, the order-preserving compaction of the selected (index,
 value) pairs, the selected-count readback and the threshold update -- one
-micro_sparsify_step call per rank.  Gradients are generated before the timed
+micro_sparsify_step call per worker.  As in Algorithm 1, worker i searches
+partition ((t mod world) + i) mod world at step t, so a worker's partition
+(and the residual it touches) changes from one step to the next; each
+partition keeps its own threshold.  Gradients are generated before the timed
 region and stay resident in HBM (a pool of distinct seeded gradients, one per
 step while the pool lasts).
 
@@ -131,10 +134,11 @@ class Run:
 
     def __init__(self, w, density, pool, sp, micro):
         import torch
-        self.w, self.d, self.pool, self.sp = w, density, pool, sp
+        self.w, self.d, self.pool, self.sp, self.micro = w, density, pool, sp, micro
         self.N = w.n_total
         self.res = torch.zeros(self.N, dtype=torch.float32, device="cuda")
-        self.bounds = {r: micro.micro_partition(self.N, r, w.world) for r in w.ranks}
+        # every partition the workers' cycles visit, each with its own threshold
+        self.bounds = {p: micro.micro_partition(self.N, p, w.world) for p in range(w.world)}
         from paper_2310_00967_amd import synth
         self.theta = {r: synth.initial_theta(w, pool[0], s, s + ln, density)
                       for r, (s, ln) in self.bounds.items()}
@@ -147,13 +151,14 @@ class Run:
 
     def step(self, timed):
         g = self.pool[self.t % len(self.pool)]
-        for r in self.w.ranks:
-            _, ln = self.bounds[r]
-            k, th, _, _ = self.sp.step(g, self.res, r, self.w.world, self.d, self.theta[r],
+        for worker in self.w.ranks:
+            p = self.micro.micro_cycle(self.t, worker, self.w.world)
+            _, ln = self.bounds[p]
+            k, th, _, _ = self.sp.step(g, self.res, p, self.w.world, self.d, self.theta[p],
                                        self.out_idx, self.out_val)
-            self.theta[r] = th
+            self.theta[p] = th
             kernel_ms, redone, variant = self.sp.last_stats()
-            self.log.append((r, ln, k, kernel_ms if timed else None, redone))
+            self.log.append((p, ln, k, kernel_ms if timed else None, redone))
             self.variant = variant
         self.t += 1
 
@@ -208,8 +213,8 @@ def cpu_baseline(w, density, pool, target_s):
     N = w.n_total
     res = np.zeros(N, np.float32)
     g_host = torch.empty(N, dtype=torch.float32, pin_memory=True)
-    bounds = {r: oracle.partition(N, r, w.world) for r in w.ranks}
-    theta = {r: synth.initial_theta(w, pool[0], s, s + ln, density) for r, (s, ln) in bounds.items()}
+    bounds = {p: oracle.partition(N, p, w.world) for p in range(w.world)}
+    theta = {p: synth.initial_theta(w, pool[0], s, s + ln, density) for p, (s, ln) in bounds.items()}
     cap = max(ln for _, ln in bounds.values())
     out = (np.empty(max(1, cap), np.int32), np.empty(max(1, cap), np.float32))
     # fault every host page in before timing, as the device buffers are
@@ -220,12 +225,15 @@ def cpu_baseline(w, density, pool, target_s):
     spent, elems, steps = 0.0, 0, 0
     while spent < target_s and steps < 10000:
         g = pool[steps % len(pool)]
-        for r, (s, ln) in bounds.items():
+        parts = [oracle.cycle(steps, worker, w.world) for worker in w.ranks]
+        for p in parts:
+            s, ln = bounds[p]
             g_host[s:s + ln].copy_(g[s:s + ln])
         gn = g_host.numpy()
-        for r, (s, ln) in bounds.items():
+        for p in parts:
+            _, ln = bounds[p]
             t0 = time.perf_counter()
-            _, _, _, theta[r] = oracle.step(gn, res, r, w.world, density, theta[r], out=out)
+            _, _, _, theta[p] = oracle.step(gn, res, p, w.world, density, theta[p], out=out)
             spent += time.perf_counter() - t0
             elems += ln
         steps += 1
@@ -559,7 +567,7 @@ def main():
     sp.close()
 
     traffic = read_traffic() if args.workload == "gpt_1p3b" and head == 0.01 else None
-    parts = sorted({ln for (_, ln) in (micro.micro_partition(w.n_total, r, w.world) for r in w.ranks)})
+    parts = sorted({ln for (_, ln) in (micro.micro_partition(w.n_total, p, w.world) for p in range(w.world))})
     line = {
         "metric": METRIC,
         "value": main_res["g_elem_s"],
@@ -577,7 +585,8 @@ def main():
             "workload": w.name,
             "n_total": w.n_total,
             "world": w.world,
-            "ranks": list(w.ranks),
+            "workers": list(w.ranks),
+            "partitions": "cyclic: worker i searches partition ((t mod world) + i) mod world at step t",
             "partition_len": parts,
             "density": head,
             "distribution": w.dist,

@@ -19,6 +19,7 @@
 
 struct micro_ctx {
     int device = -1;
+    int compute_units = 256;                 // of the device, read at init
     int64_t n_total = 0;
     hipStream_t stream = nullptr;
     micro_config cfg{};
@@ -77,16 +78,6 @@ struct DeviceScope {
 // 262,144 values against 16.8 us for the staged schedule's three, and lost
 // from 3.2M values on (27 us against 23 us).
 constexpr int64_t kAutoTicketMax = int64_t(1) << 20;
-
-// Largest partition (or swept vector) whose residual, at 4 bytes per value
-// (192 MB), stays in the MI355X's 256 MB Infinity Cache between steps: up to
-// it the stream kernel reads and writes the residual with temporal accesses
-// and the move kernel takes the smaller pieces, both measured faster there
-// (BERT-large rank 3, 41.9M values: 104 -> 94 us per step); above it the
-// residual streams non-temporally past the cache (GPT-1.3B: 2.48 ms against
-// 2.72 ms with temporal accesses) and the larger pieces keep the move
-// kernel's loop short.
-constexpr int64_t kCacheResidentMax = int64_t(48) << 20;
 
 thread_local std::string g_init_error = "no error";
 
@@ -199,6 +190,19 @@ uint32_t move_grid(int64_t tiles, int64_t len, int64_t span, int64_t min_blocks)
     return static_cast<uint32_t>(blocks < 1 ? 1 : blocks);
 }
 
+// Items per move piece.  The merged sequence holds one item per tile and one
+// per selected value, about tiles + density * values of them.  A long
+// sequence takes kMoveSpan-item pieces (a short loop per workgroup); one of
+// fewer than two such pieces per compute unit takes kMoveSpanSmall-item
+// pieces, which put twice as many workgroups to work.  Measured: BERT-large
+// rank 3 (41.9M values, d = 0.01) 112 pieces of 4096 items or 225 of 2048,
+// 100.3 against 98.5 us per step; the GPT-1.3B partition's move kernel
+// 53 us with 4096-item pieces, 78 us with 2048.
+uint32_t move_span_for(const micro_ctx* ctx, int64_t tiles, double expected_pairs) {
+    const double items = static_cast<double>(tiles) + expected_pairs;
+    return items < 2.0 * ctx->compute_units * micro::kMoveSpan ? micro::kMoveSpanSmall : micro::kMoveSpan;
+}
+
 bool misaligned4(std::initializer_list<const void*> ptrs) {
     uintptr_t bits = 0;
     for (const void* p : ptrs) bits |= reinterpret_cast<uintptr_t>(p);
@@ -206,8 +210,8 @@ bool misaligned4(std::initializer_list<const void*> ptrs) {
 }
 
 micro_status run_segments(micro_ctx* ctx, const float* grad, float* residual, int32_t count, const int64_t* starts,
-                          const int64_t* lens, const float* threshold_f, int32_t* out_idx, float* out_val,
-                          int64_t* k, double* sumsq);
+                          const int64_t* lens, const float* threshold_f, double expected_pairs, int32_t* out_idx,
+                          float* out_val, int64_t* k, double* sumsq);
 
 // Validation, launch, count readback and threshold update of one sparsify
 // step over [start, start + len); with accumulate_outside the rest of the
@@ -265,7 +269,9 @@ micro_status execute_step(micro_ctx* ctx, const float* grad, float* residual, in
         const float thf[3] = {none, threshold_as_f32(*theta), none};
         int64_t kk[3];
         double sq[3];
-        const micro_status st = run_segments(ctx, grad, residual, 3, starts, lens, thf, out_idx, out_val, kk, sq);
+        const micro_status st =
+            run_segments(ctx, grad, residual, 3, starts, lens, thf, density * static_cast<double>(len), out_idx,
+                         out_val, kk, sq);
         if (st != MICRO_OK) return st;
         if (kk[0] != 0 || kk[2] != 0) {
             set_error(ctx, "device selected outside the partition");
@@ -331,10 +337,7 @@ micro_status execute_step(micro_ctx* ctx, const float* grad, float* residual, in
     a.tile_excl = ctx->d_tile_excl;
     a.flagged_list = ctx->d_flagged_list;
     a.split_tile = ctx->d_split_tile;
-    const bool resident = len <= kCacheResidentMax;
-    a.move_span = resident ? micro::kMoveSpanSmall : micro::kMoveSpan;
-    // a full pass touches the whole vector: only a partition step keeps it
-    a.res_temporal = resident && !accumulate_outside ? 1u : 0u;
+    a.move_span = move_span_for(ctx, tiles, density * static_cast<double>(len));
     a.move_blocks = move_grid(tiles, len, a.move_span, 1);
     a.stage = ctx->d_stage;
     a.num_chunks = static_cast<uint32_t>(chunks);
@@ -384,8 +387,8 @@ micro_status execute_step(micro_ctx* ctx, const float* grad, float* residual, in
 // order.  k[r] and sumsq[r] (squared norm of the segment's new residual)
 // receive each segment's results.  Arguments are validated by the callers.
 micro_status run_segments(micro_ctx* ctx, const float* grad, float* residual, int32_t count, const int64_t* starts,
-                          const int64_t* lens, const float* threshold_f, int32_t* out_idx, float* out_val,
-                          int64_t* k, double* sumsq) {
+                          const int64_t* lens, const float* threshold_f, double expected_pairs, int32_t* out_idx,
+                          float* out_val, int64_t* k, double* sumsq) {
     if (ctx->needs_reset || ctx->epoch >= micro::kMaxEpoch) {
         micro_status st = reset_scratch(ctx);
         if (st != MICRO_OK) return st;
@@ -438,9 +441,7 @@ micro_status run_segments(micro_ctx* ctx, const float* grad, float* residual, in
     a.host_sumsq = ctx->h_sumsq_dev;
     int64_t total_len = 0;
     for (int32_t r = 0; r < count; ++r) total_len += lens[r];
-    const bool resident = total_len <= kCacheResidentMax;
-    a.move_span = resident ? micro::kMoveSpanSmall : micro::kMoveSpan;
-    a.res_temporal = resident ? 1u : 0u;
+    a.move_span = move_span_for(ctx, tiles, expected_pairs);
     // workgroup r of the move kernel reduces segment r's squared norm
     a.move_blocks = move_grid(tiles, total_len, a.move_span, count);
     a.stage = ctx->d_stage;
@@ -539,7 +540,8 @@ micro_status execute_sweep(micro_ctx* ctx, const float* grad, float* residual, i
         theta_f[r] = threshold_as_f32(theta[r]);
     }
     double sq[micro::kMaxSweep];
-    const micro_status st = run_segments(ctx, grad, residual, world, starts, lens, theta_f, out_idx, out_val, k, sq);
+    const micro_status st = run_segments(ctx, grad, residual, world, starts, lens, theta_f,
+                                         density * static_cast<double>(ctx->n_total), out_idx, out_val, k, sq);
     if (st != MICRO_OK) return st;
     for (int32_t r = 0; r < world; ++r) {
         theta[r] = next_threshold(ctx->cfg, density, lens[r], k[r], theta[r]);
@@ -653,6 +655,13 @@ micro_status micro_sparsify_init(micro_ctx** out, int64_t n_total, void* hip_str
     ctx->cfg = c;
     if ((e = hipGetDevice(&ctx->device)) != hipSuccess) {
         set_error(nullptr, "hipGetDevice failed: %s", hipGetErrorString(e));
+        release(ctx);
+        return MICRO_EHIP;
+    }
+    if ((e = hipDeviceGetAttribute(&ctx->compute_units, hipDeviceAttributeMultiprocessorCount, ctx->device)) !=
+            hipSuccess ||
+        ctx->compute_units < 1) {
+        set_error(nullptr, "compute unit count unavailable: %s", hipGetErrorString(e));
         release(ctx);
         return MICRO_EHIP;
     }

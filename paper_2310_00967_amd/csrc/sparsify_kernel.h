@@ -11,15 +11,16 @@ namespace micro {
 // pairs per tile, tiles per scan chunk (one 256-thread workgroup), items per
 // move piece.  The move kernel walks the merged sequence of tiles and output
 // pairs (each tile is one item, followed by one item per selected value of
-// the tile) in pieces of kMoveSpan items, so a piece holds at most kMoveSpan
-// pairs and touches at most kMoveSpan + 1 tiles.
+// the tile) in pieces of move_span items (kMoveSpan, or kMoveSpanSmall for a
+// short sequence), so a piece holds at most kMoveSpan pairs and touches at
+// most kMoveSpan + 1 tiles.
 constexpr int kStreamTile = 1024;
 constexpr int kStreamBlock = 256;
 constexpr uint32_t kStageCap = 256;
 constexpr int kChunkTiles = 1024;
 constexpr int kScanBlock = 256;
 constexpr int kMoveSpan = 4096;        // largest move piece (LDS arrays are sized for it)
-constexpr int kMoveSpanSmall = 2048;   // move piece of mid-size partitions (see the host's choice)
+constexpr int kMoveSpanSmall = 2048;   // move piece of a short merged sequence
 constexpr int kMoveBlock = 256;
 constexpr uint32_t kMoveGrid = 2048;  // largest move grid (eight workgroups per compute unit)
 // Ticket schedule: values per tile (256 threads, four dwordx4 per lane).
@@ -81,8 +82,6 @@ struct LaunchArgs {
     double* host_sumsq;     // sweep: mapped host memory, one squared norm per segment
     uint32_t move_blocks;   // workgroups of the move kernel
     uint32_t move_span;     // items per move piece: kMoveSpan or kMoveSpanSmall
-    uint32_t res_temporal;  // 1: the stream kernel reads and writes the residual with temporal
-                            // accesses (it stays in the Infinity Cache between steps)
     uint2* stage;           // num_tiles * kStageCap staged (index, value bits) pairs
     uint32_t num_chunks;    // ceil(num_tiles / kChunkTiles)
     uint64_t* chunk_status;             // >= num_chunks look-back words

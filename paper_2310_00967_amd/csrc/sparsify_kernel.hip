@@ -23,9 +23,7 @@
 // Staged schedule, three kernels; no workgroup of the first and the last ever
 //   waits for another:
 //   stream_kernel: one 1024-value tile per 256-thread workgroup, one dwordx4
-//     per lane and stream, the gradient and the outputs non-temporal; the
-//     residual too unless the host asks for temporal accesses (a partition
-//     whose residual stays in the last-level cache).  It ranks the tile's
+//     per lane and stream, every HBM stream non-temporal.  It ranks the tile's
 //     selected values, writes the residual, packs the pairs in LDS and writes
 //     them with coalesced stores to the tile's staging slot (kStageCap
 //     8-byte (index, value) records), then stores the tile's count.  A tile
@@ -400,7 +398,7 @@ __device__ __forceinline__ double block_sum(double v, int lane, int wave, double
 // segment supplies range and threshold, and the tile also stores the squared
 // norm of its new residual (also for a tile left to the move kernel, whose
 // new residual is fixed by its selection bits all the same).
-template <int VEC, int ROWS, bool SWEEP, bool NT_RES>
+template <int VEC, int ROWS, bool SWEEP>
 __device__ __forceinline__ void stream_tile(LaunchArgs a, const SweepTable* tbl) {
     constexpr int WAVES = kStreamBlock / kWaveSize;
     static_assert(VEC * ROWS * kStreamBlock == kStreamTile, "tile size");
@@ -416,7 +414,7 @@ __device__ __forceinline__ void stream_tile(LaunchArgs a, const SweepTable* tbl)
 
     Tile<VEC, ROWS, kStreamBlock> t;
     uint32_t lane_rank[ROWS], row_count[ROWS], row_base[ROWS];
-    load_tile<VEC, ROWS, kStreamBlock, NT_RES>(a, tile_base, tid, t);
+    load_tile<VEC, ROWS, kStreamBlock, true>(a, tile_base, tid, t);
     const uint32_t sel = compute_tile(a, tid, t);
     if constexpr (SWEEP) {
         double sq = 0.0;
@@ -438,7 +436,7 @@ __device__ __forceinline__ void stream_tile(LaunchArgs a, const SweepTable* tbl)
         if (tid == 0) a.tile_counts[tile] = count | kOverflow;
         return;
     }
-    store_residual<VEC, ROWS, kStreamBlock, NT_RES>(a, tid, t, sel);
+    store_residual<VEC, ROWS, kStreamBlock, true>(a, tid, t, sel);
 #pragma unroll
     for (int r = 0; r < ROWS; ++r) {
         uint32_t pos = row_base[r] + lane_rank[r];
@@ -459,14 +457,14 @@ __device__ __forceinline__ void stream_tile(LaunchArgs a, const SweepTable* tbl)
     if (tid == 0) a.tile_counts[tile] = count;
 }
 
-template <int VEC, int ROWS, bool NT_RES>
+template <int VEC, int ROWS>
 __global__ __launch_bounds__(kStreamBlock) void stream_kernel(LaunchArgs a) {
-    stream_tile<VEC, ROWS, false, NT_RES>(a, nullptr);
+    stream_tile<VEC, ROWS, false>(a, nullptr);
 }
 
-template <int VEC, int ROWS, bool NT_RES>
+template <int VEC, int ROWS>
 __global__ __launch_bounds__(kStreamBlock) void stream_sweep_kernel(LaunchArgs a, SweepTable tbl) {
-    stream_tile<VEC, ROWS, true, NT_RES>(a, &tbl);
+    stream_tile<VEC, ROWS, true>(a, &tbl);
 }
 
 // Full processing of one flagged tile by one wavefront with its pairs from
@@ -743,9 +741,8 @@ __device__ __forceinline__ void block_max_scan(uint16_t* v, uint32_t n, int tid,
 }
 
 // Move kernel: a fixed grid walks the merged sequence of tiles and output
-// pairs in pieces of move_span items (kMoveSpan, or kMoveSpanSmall for a
-// partition whose residual stays in the last-level cache: more, shorter
-// pieces), so every piece costs about the same whatever the clustering of the
+// pairs in pieces of move_span items (kMoveSpan, or kMoveSpanSmall where the
+// sequence is short: more, shorter pieces), so every piece costs about the same whatever the clustering of the
 // selection: many pairs from few tiles, or few pairs scattered over many
 // tiles.  Piece m's items lie in the tiles from split_tile[m] to
 // split_tile[m + 1] (recorded by the scan kernel), at most move_span + 1 of
@@ -915,13 +912,7 @@ __global__ __launch_bounds__(kTicketBlock) void ticket_kernel(LaunchArgs a) {
     const int lane = tid & (kWaveSize - 1);
     const int wave = tid / kWaveSize;
 
-    if (tid == 0) {
-        const uint32_t drawn = static_cast<uint32_t>(atomicAdd(a.ticket, 1ull));
-        // Every other workgroup of this launch has drawn its ticket before the
-        // last one is drawn, so the counter can be rearmed for the next launch.
-        if (drawn == a.num_tiles - 1) __hip_atomic_store(a.ticket, 0ull, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-        s_tile = drawn;
-    }
+    if (tid == 0) s_tile = draw_ticket(a.ticket, a.num_tiles - 1);
     __syncthreads();
     const uint32_t tile = s_tile;
     if (tile >= a.num_tiles) return;  // only reachable if the counter was not rearmed
@@ -1009,17 +1000,11 @@ hipError_t launch_staged(const LaunchArgs& args, bool vec4, hipStream_t stream) 
     const dim3 grid_stream(args.num_tiles), grid_scan(args.num_chunks), grid_move(args.move_blocks);
     const dim3 bs(kStreamBlock);
     if (vec4) {
-        if (args.res_temporal)
-            hipLaunchKernelGGL((stream_kernel<4, 1, false>), grid_stream, bs, 0, stream, args);
-        else
-            hipLaunchKernelGGL((stream_kernel<4, 1, true>), grid_stream, bs, 0, stream, args);
+        hipLaunchKernelGGL((stream_kernel<4, 1>), grid_stream, bs, 0, stream, args);
         hipLaunchKernelGGL(scan_kernel, grid_scan, dim3(kScanBlock), 0, stream, args);
         hipLaunchKernelGGL(move_kernel<4>, grid_move, dim3(kMoveBlock), 0, stream, args);
     } else {
-        if (args.res_temporal)
-            hipLaunchKernelGGL((stream_kernel<1, 4, false>), grid_stream, bs, 0, stream, args);
-        else
-            hipLaunchKernelGGL((stream_kernel<1, 4, true>), grid_stream, bs, 0, stream, args);
+        hipLaunchKernelGGL((stream_kernel<1, 4>), grid_stream, bs, 0, stream, args);
         hipLaunchKernelGGL(scan_kernel, grid_scan, dim3(kScanBlock), 0, stream, args);
         hipLaunchKernelGGL(move_kernel<1>, grid_move, dim3(kMoveBlock), 0, stream, args);
     }
@@ -1030,17 +1015,11 @@ hipError_t launch_sweep(const LaunchArgs& args, const SweepTable& table, bool ve
     const dim3 grid_stream(args.num_tiles), grid_scan(args.num_chunks), grid_move(args.move_blocks);
     const dim3 bs(kStreamBlock);
     if (vec4) {
-        if (args.res_temporal)
-            hipLaunchKernelGGL((stream_sweep_kernel<4, 1, false>), grid_stream, bs, 0, stream, args, table);
-        else
-            hipLaunchKernelGGL((stream_sweep_kernel<4, 1, true>), grid_stream, bs, 0, stream, args, table);
+        hipLaunchKernelGGL((stream_sweep_kernel<4, 1>), grid_stream, bs, 0, stream, args, table);
         hipLaunchKernelGGL(scan_sweep_kernel, grid_scan, dim3(kScanBlock), 0, stream, args, table);
         hipLaunchKernelGGL(move_sweep_kernel<4>, grid_move, dim3(kMoveBlock), 0, stream, args, table);
     } else {
-        if (args.res_temporal)
-            hipLaunchKernelGGL((stream_sweep_kernel<1, 4, false>), grid_stream, bs, 0, stream, args, table);
-        else
-            hipLaunchKernelGGL((stream_sweep_kernel<1, 4, true>), grid_stream, bs, 0, stream, args, table);
+        hipLaunchKernelGGL((stream_sweep_kernel<1, 4>), grid_stream, bs, 0, stream, args, table);
         hipLaunchKernelGGL(scan_sweep_kernel, grid_scan, dim3(kScanBlock), 0, stream, args, table);
         hipLaunchKernelGGL(move_sweep_kernel<1>, grid_move, dim3(kMoveBlock), 0, stream, args, table);
     }
