@@ -5,10 +5,11 @@ A step is one pass of the whole hot path over one synthetic gradient: for each
 worker the workload sweeps, the error-feedback add, the threshold test, the
 residual update, the order-preserving compaction of the selected (index,
 value) pairs, the selected-count readback and the threshold update -- one
-micro_sparsify_step call per worker.  As in Algorithm 1, worker i searches
-partition ((t mod world) + i) mod world at step t, so a worker's partition
-(and the residual it touches) changes from one step to the next; each
-partition keeps its own threshold.  Gradients are generated before the timed
+micro_sparsify_step call per listed rank, each rank with its own threshold.
+With --cycle, worker i searches partition ((t mod world) + i) mod world at
+step t instead, as in Algorithm 1, so its partition (and the residual it
+touches) changes from one step to the next; each partition then keeps its
+own threshold.  Gradients are generated before the timed
 region and stay resident in HBM (a pool of distinct seeded gradients, one per
 step while the pool lasts).
 
@@ -52,6 +53,8 @@ def parse_args():
                     help="target CPU time of the oracle baseline sample (0 disables)")
     ap.add_argument("--pool-gb", type=float, default=100.0,
                     help="HBM budget for the pre-generated gradient pool")
+    ap.add_argument("--cycle", action="store_true",
+                    help="rotate each worker's partition every step (Algorithm 1) instead of fixed ranks")
     ap.add_argument("--variant", default="auto", choices=["auto", "staged", "ticket"],
                     help="kernel schedule (auto, the library default, runs the ticket schedule up to "
                          "2^20 values per partition and the staged one above)")
@@ -132,13 +135,14 @@ def copy_calibration():
 class Run:
     """One workload at one density: gradient pool, residual, thresholds."""
 
-    def __init__(self, w, density, pool, sp, micro):
+    def __init__(self, w, density, pool, sp, micro, cycle=False):
         import torch
-        self.w, self.d, self.pool, self.sp, self.micro = w, density, pool, sp, micro
+        self.w, self.d, self.pool, self.sp, self.micro, self.cycle = w, density, pool, sp, micro, cycle
         self.N = w.n_total
         self.res = torch.zeros(self.N, dtype=torch.float32, device="cuda")
-        # every partition the workers' cycles visit, each with its own threshold
-        self.bounds = {p: micro.micro_partition(self.N, p, w.world) for p in range(w.world)}
+        # every partition the workers visit, each with its own threshold
+        parts = range(w.world) if cycle else w.ranks
+        self.bounds = {p: micro.micro_partition(self.N, p, w.world) for p in parts}
         from paper_2310_00967_amd import synth
         self.theta = {r: synth.initial_theta(w, pool[0], s, s + ln, density)
                       for r, (s, ln) in self.bounds.items()}
@@ -152,7 +156,7 @@ class Run:
     def step(self, timed):
         g = self.pool[self.t % len(self.pool)]
         for worker in self.w.ranks:
-            p = self.micro.micro_cycle(self.t, worker, self.w.world)
+            p = self.micro.micro_cycle(self.t, worker, self.w.world) if self.cycle else worker
             _, ln = self.bounds[p]
             k, th, _, _ = self.sp.step(g, self.res, p, self.w.world, self.d, self.theta[p],
                                        self.out_idx, self.out_val)
@@ -163,9 +167,9 @@ class Run:
         self.t += 1
 
 
-def measure(w, density, pool, sp, micro, warmup, steps):
+def measure(w, density, pool, sp, micro, warmup, steps, cycle=False):
     import torch
-    run = Run(w, density, pool, sp, micro)
+    run = Run(w, density, pool, sp, micro, cycle)
     for _ in range(warmup):
         run.step(timed=False)
     torch.cuda.synchronize()
@@ -200,7 +204,7 @@ def measure(w, density, pool, sp, micro, warmup, steps):
     }
 
 
-def cpu_baseline(w, density, pool, target_s):
+def cpu_baseline(w, density, pool, target_s, cycle=False):
     """The C oracle, as it stands, on the host: same workload and density,
     its own error-feedback trajectory from a zero residual, gradients copied
     from the pool (copies not timed).  Runs steps until target_s of oracle
@@ -213,7 +217,7 @@ def cpu_baseline(w, density, pool, target_s):
     N = w.n_total
     res = np.zeros(N, np.float32)
     g_host = torch.empty(N, dtype=torch.float32, pin_memory=True)
-    bounds = {p: oracle.partition(N, p, w.world) for p in range(w.world)}
+    bounds = {p: oracle.partition(N, p, w.world) for p in (range(w.world) if cycle else w.ranks)}
     theta = {p: synth.initial_theta(w, pool[0], s, s + ln, density) for p, (s, ln) in bounds.items()}
     cap = max(ln for _, ln in bounds.values())
     out = (np.empty(max(1, cap), np.int32), np.empty(max(1, cap), np.float32))
@@ -225,7 +229,7 @@ def cpu_baseline(w, density, pool, target_s):
     spent, elems, steps = 0.0, 0, 0
     while spent < target_s and steps < 10000:
         g = pool[steps % len(pool)]
-        parts = [oracle.cycle(steps, worker, w.world) for worker in w.ranks]
+        parts = [oracle.cycle(steps, worker, w.world) if cycle else worker for worker in w.ranks]
         for p in parts:
             s, ln = bounds[p]
             g_host[s:s + ln].copy_(g[s:s + ln])
@@ -555,19 +559,20 @@ def main():
         sp.close()
         return
 
-    main_res = measure(w, head, pool, sp, micro, args.warmup, args.steps)
+    main_res = measure(w, head, pool, sp, micro, args.warmup, args.steps, args.cycle)
     extra = {}
     for d in others:
-        r = measure(w, d, pool, sp, micro, args.warmup, args.steps)
+        r = measure(w, d, pool, sp, micro, args.warmup, args.steps, args.cycle)
         extra[f"d={d}"] = {k: r[k] for k in ("g_elem_s", "wall_gbs", "kernel_gbs", "kernel_ms_avg",
                                              "density_error_last_half", "ms_per_step")}
         extra[f"d={d}"]["kernel_hbm_frac"] = r["kernel_gbs"] / HBM_PEAK_GBS
 
-    cpu = cpu_baseline(w, head, pool, args.cpu_seconds) if args.cpu_seconds > 0 else None
+    cpu = cpu_baseline(w, head, pool, args.cpu_seconds, args.cycle) if args.cpu_seconds > 0 else None
     sp.close()
 
     traffic = read_traffic() if args.workload == "gpt_1p3b" and head == 0.01 else None
-    parts = sorted({ln for (_, ln) in (micro.micro_partition(w.n_total, p, w.world) for p in range(w.world))})
+    parts = sorted({ln for (_, ln) in (micro.micro_partition(w.n_total, p, w.world)
+                                       for p in (range(w.world) if args.cycle else w.ranks))})
     line = {
         "metric": METRIC,
         "value": main_res["g_elem_s"],
@@ -585,8 +590,9 @@ def main():
             "workload": w.name,
             "n_total": w.n_total,
             "world": w.world,
-            "workers": list(w.ranks),
-            "partitions": "cyclic: worker i searches partition ((t mod world) + i) mod world at step t",
+            "ranks": list(w.ranks),
+            "partitions": ("cyclic: worker i searches partition ((t mod world) + i) mod world at step t"
+                           if args.cycle else "fixed: each listed rank searches its own partition every step"),
             "partition_len": parts,
             "density": head,
             "distribution": w.dist,

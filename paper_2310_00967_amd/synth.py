@@ -115,8 +115,7 @@ class Workload:
     dist: str                  # "normal", "laplace", "student_t3"
     scale_range: tuple         # (lo, hi) of the log-uniform per-tensor scale; None = unit
     world: int
-    ranks: tuple               # workers run each step, in this order (the benchmark gives worker i
-                               # partition ((t mod world) + i) mod world at step t, as Algorithm 1)
+    ranks: tuple               # ranks run each step, in this order
     densities: tuple
     steps: int
     theta0: float | None       # None = calibrated from the step-0 gradient

@@ -311,6 +311,36 @@ def test_count_swings_on_one_context():
     sp.close()
 
 
+def test_move_piece_size_does_not_change_the_result():
+    """The density steers only the threshold update and the move kernel's
+    piece size (2048 items for a short expected sequence, 4096 for a long
+    one; on 256 compute units d = 0.001 and d = 1 fall on either side for
+    this partition).  At the same threshold both must select, place and
+    reset the same bits, and match the oracle."""
+    N = 3_000_017
+    rng = np.random.default_rng(71)
+    g = rng.standard_normal(N).astype(np.float32)
+    res0 = (rng.standard_normal(N) * 0.5).astype(np.float32)
+    sp = micro.Sparsifier(N, device=DEV, variant=STAGED)
+    g_dev = torch.from_numpy(g).to(DEV)
+    for theta in [2.5, 1.0]:
+        outs = []
+        for density in [0.001, 1.0]:
+            r_dev = torch.from_numpy(res0).to(DEV)
+            k, th, idx, val = sp.step(g_dev, r_dev, 0, 1, density, theta)
+            res = res0.copy()
+            o_idx, o_val, k_or, th_or = oracle.step(g, res, 0, 1, density, theta)
+            assert (k, th) == (k_or, th_or), (theta, density)
+            outs.append((idx.cpu().numpy(), val.cpu().numpy(), r_dev.cpu().numpy()))
+            assert np.array_equal(outs[-1][0], o_idx), (theta, density)
+            assert first_mismatch(outs[-1][1], o_val) < 0, (theta, density)
+        assert np.array_equal(outs[0][0], outs[1][0]), theta
+        assert first_mismatch(outs[0][1], outs[1][1]) < 0, theta
+        assert first_mismatch(outs[0][2], outs[1][2]) < 0, theta
+        assert first_mismatch(outs[0][2], res) < 0, theta
+    sp.close()
+
+
 def test_largest_vector_the_index_type_allows():
     """n_total = 2^31 - 1, the largest vector int32 indices address: one
     partition-wide step (staged) and one full error-feedback pass of world 2,
