@@ -74,8 +74,8 @@ struct DeviceScope {
 };
 
 // Largest partition that an AUTO context runs on the ticket schedule.  On
-// MI355X the ticket schedule's single launch took 8.8 us of device time for
-// 262,144 values against 16.8 us for the staged schedule's three, and lost
+// MI355X the ticket schedule's single launch took 8.7 us of device time for
+// 262,144 values against 15.6 us for the staged schedule's three, and lost
 // from 3.2M values on (27 us against 23 us).
 constexpr int64_t kAutoTicketMax = int64_t(1) << 20;
 
@@ -196,7 +196,7 @@ uint32_t move_grid(int64_t tiles, int64_t len, int64_t span, int64_t min_blocks)
 // fewer than two such pieces per compute unit takes kMoveSpanSmall-item
 // pieces, which put twice as many workgroups to work.  Measured: BERT-large
 // rank 3 (41.9M values, d = 0.01) 112 pieces of 4096 items or 225 of 2048,
-// 100.3 against 98.5 us per step; the GPT-1.3B partition's move kernel
+// 98.9 against 96.6 us per step; the GPT-1.3B partition's move kernel
 // 53 us with 4096-item pieces, 78 us with 2048.
 uint32_t move_span_for(const micro_ctx* ctx, int64_t tiles, double expected_pairs) {
     const double items = static_cast<double>(tiles) + expected_pairs;
