@@ -53,6 +53,8 @@ def parse_args():
                     help="target CPU time of the oracle baseline sample (0 disables)")
     ap.add_argument("--pool-gb", type=float, default=100.0,
                     help="HBM budget for the pre-generated gradient pool")
+    ap.add_argument("--steps-jsonl", default=None, metavar="PATH",
+                    help="also write one JSON record per step call (warm-up and timed) to PATH")
     ap.add_argument("--cycle", action="store_true",
                     help="rotate each worker's partition every step (Algorithm 1) instead of fixed ranks")
     ap.add_argument("--variant", default="auto", choices=["auto", "staged", "ticket"],
@@ -151,6 +153,7 @@ class Run:
         self.out_idx, self.out_val = sp.outputs(cap)
         self.t = 0
         self.log = []   # (rank, P, k, kernel_ms, tiles redone by the move kernel)
+        self.records = []  # one dict per call: the per-step record of --steps-jsonl
         self.variant = None  # schedule of the last step
 
     def step(self, timed):
@@ -158,16 +161,29 @@ class Run:
         for worker in self.w.ranks:
             p = self.micro.micro_cycle(self.t, worker, self.w.world) if self.cycle else worker
             _, ln = self.bounds[p]
-            k, th, _, _ = self.sp.step(g, self.res, p, self.w.world, self.d, self.theta[p],
+            theta_in = self.theta[p]
+            t0 = time.perf_counter()
+            k, th, _, _ = self.sp.step(g, self.res, p, self.w.world, self.d, theta_in,
                                        self.out_idx, self.out_val)
+            wall_s = time.perf_counter() - t0
             self.theta[p] = th
             kernel_ms, redone, variant = self.sp.last_stats()
             self.log.append((p, ln, k, kernel_ms if timed else None, redone))
+            alg = 12 * ln + 8 * k
+            self.records.append({
+                "workload": self.w.name, "t": self.t, "timed": timed, "rank": p, "P": ln, "k": k,
+                "density": self.d, "d_act": k / ln if ln else 0.0,
+                "density_error": abs(k / ln - self.d) / self.d if ln else 0.0,
+                "theta": theta_in, "theta_next": th, "device_us": kernel_ms * 1e3 if kernel_ms >= 0 else None,
+                "wall_us": wall_s * 1e6, "alg_bytes": alg,
+                "kernel_gbs": alg / (kernel_ms * 1e-3) / 1e9 if kernel_ms > 0 else None,
+                "hbm_frac": alg / (kernel_ms * 1e-3) / 1e9 / HBM_PEAK_GBS if kernel_ms > 0 else None,
+                "redone_tiles": redone})
             self.variant = variant
         self.t += 1
 
 
-def measure(w, density, pool, sp, micro, warmup, steps, cycle=False):
+def measure(w, density, pool, sp, micro, warmup, steps, cycle=False, jsonl=None):
     import torch
     run = Run(w, density, pool, sp, micro, cycle)
     for _ in range(warmup):
@@ -178,6 +194,10 @@ def measure(w, density, pool, sp, micro, warmup, steps, cycle=False):
         run.step(timed=True)
     torch.cuda.synchronize()
     elapsed = time.perf_counter() - t0
+    if jsonl:
+        with open(jsonl, "a") as f:
+            for rec in run.records:
+                f.write(json.dumps(rec) + "\n")
     timed = [x for x in run.log if x[3] is not None]
     elems = sum(x[1] for x in timed)
     alg_bytes = sum(12 * x[1] + 8 * x[2] for x in timed)
@@ -559,10 +579,10 @@ def main():
         sp.close()
         return
 
-    main_res = measure(w, head, pool, sp, micro, args.warmup, args.steps, args.cycle)
+    main_res = measure(w, head, pool, sp, micro, args.warmup, args.steps, args.cycle, args.steps_jsonl)
     extra = {}
     for d in others:
-        r = measure(w, d, pool, sp, micro, args.warmup, args.steps, args.cycle)
+        r = measure(w, d, pool, sp, micro, args.warmup, args.steps, args.cycle, args.steps_jsonl)
         extra[f"d={d}"] = {k: r[k] for k in ("g_elem_s", "wall_gbs", "kernel_gbs", "kernel_ms_avg",
                                              "density_error_last_half", "ms_per_step")}
         extra[f"d={d}"]["kernel_hbm_frac"] = r["kernel_gbs"] / HBM_PEAK_GBS
