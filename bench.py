@@ -137,7 +137,7 @@ def copy_calibration():
 class Run:
     """One workload at one density: gradient pool, residual, thresholds."""
 
-    def __init__(self, w, density, pool, sp, micro, cycle=False):
+    def __init__(self, w, density, pool, sp, micro, cycle=False, keep_records=False):
         import torch
         self.w, self.d, self.pool, self.sp, self.micro, self.cycle = w, density, pool, sp, micro, cycle
         self.N = w.n_total
@@ -153,7 +153,7 @@ class Run:
         self.out_idx, self.out_val = sp.outputs(cap)
         self.t = 0
         self.log = []   # (rank, P, k, kernel_ms, tiles redone by the move kernel)
-        self.records = []  # one dict per call: the per-step record of --steps-jsonl
+        self.records = [] if keep_records else None  # one dict per call for --steps-jsonl
         self.variant = None  # schedule of the last step
 
     def step(self, timed):
@@ -169,6 +169,9 @@ class Run:
             self.theta[p] = th
             kernel_ms, redone, variant = self.sp.last_stats()
             self.log.append((p, ln, k, kernel_ms if timed else None, redone))
+            self.variant = variant
+            if self.records is None:
+                continue
             alg = 12 * ln + 8 * k
             self.records.append({
                 "workload": self.w.name, "t": self.t, "timed": timed, "rank": p, "P": ln, "k": k,
@@ -179,13 +182,12 @@ class Run:
                 "kernel_gbs": alg / (kernel_ms * 1e-3) / 1e9 if kernel_ms > 0 else None,
                 "hbm_frac": alg / (kernel_ms * 1e-3) / 1e9 / HBM_PEAK_GBS if kernel_ms > 0 else None,
                 "redone_tiles": redone})
-            self.variant = variant
         self.t += 1
 
 
 def measure(w, density, pool, sp, micro, warmup, steps, cycle=False, jsonl=None):
     import torch
-    run = Run(w, density, pool, sp, micro, cycle)
+    run = Run(w, density, pool, sp, micro, cycle, keep_records=bool(jsonl))
     for _ in range(warmup):
         run.step(timed=False)
     torch.cuda.synchronize()

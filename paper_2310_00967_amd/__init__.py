@@ -50,6 +50,7 @@ class Sparsifier:
             self._ctx = _lib.micro_sparsify_init(self.n_total, self.stream.cuda_stream, cfg)
         self._out_idx = None
         self._out_val = None
+        self._lengths = {}  # (rank, world) -> partition length
 
     def close(self):
         if getattr(self, "_ctx", None) is not None:
@@ -76,9 +77,17 @@ class Sparsifier:
 
     def _check(self, t, name, dtype):
         import torch
-        if not isinstance(t, torch.Tensor) or t.device != self.device or t.dtype != dtype \
-                or not t.is_contiguous():
+        if not isinstance(t, torch.Tensor) or t.dtype != dtype or not t.is_cuda \
+                or t.get_device() != self.device.index or not t.is_contiguous():
             raise TypeError(f"{name} must be a contiguous {dtype} tensor on {self.device}")
+
+    def _length(self, rank, world):
+        key = (rank, world)
+        length = self._lengths.get(key)
+        if length is None:
+            length = self.partition(rank, world)[1]
+            self._lengths[key] = length
+        return length
 
     def step(self, grad, residual, rank, world, density, theta, out_idx=None, out_val=None):
         """One sparsify step; returns (k, theta_next, idx[:k], val[:k])."""
@@ -89,7 +98,7 @@ class Sparsifier:
         self._check(residual, "residual", torch.float32)
         if grad.numel() != self.n_total or residual.numel() != self.n_total:
             raise ValueError(f"grad and residual must hold {self.n_total} values")
-        _, length = self.partition(rank, world)
+        length = self._length(rank, world)
         if out_idx is None or out_val is None:
             out_idx, out_val = self.outputs(length)
         self._check(out_idx, "out_idx", torch.int32)
