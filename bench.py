@@ -36,6 +36,7 @@ METRIC = ("sparsify-step throughput (G elem/s, HBM GB/s % of peak); "
           "density error |d_act−d|/d")
 HBM_PEAK_GBS = 8000.0
 KERNEL_SRC = os.path.join(ROOT, "paper_2310_00967_amd", "csrc", "sparsify_kernel.hip")
+KERNEL_HDR = os.path.join(ROOT, "paper_2310_00967_amd", "csrc", "sparsify_kernel.h")
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "sparsify_kernel_gpt_1p3b_traffic.txt")
 
 
@@ -77,12 +78,16 @@ def parse_args():
 
 
 def kernel_sha256(text=None):
-    """sha256 of the kernel source's code: // comments, trailing blanks and
+    """sha256 of the kernels' code (the kernel source followed by its header,
+    whose constants shape the launches): // comments, trailing blanks and
     blank lines removed, so the stored counters stay valid across comment
     edits and go stale with any change to the code."""
     if text is None:
-        with open(KERNEL_SRC, encoding="utf-8") as f:
-            text = f.read()
+        parts = []
+        for path in (KERNEL_SRC, KERNEL_HDR):
+            with open(path, encoding="utf-8") as f:
+                parts.append(f.read())
+        text = "\n".join(parts)
     code = []
     for line in text.splitlines():
         line = line.split("//", 1)[0].rstrip()

@@ -22,10 +22,13 @@ def test_kernel_hash_ignores_comments_trailing_blanks_and_blank_lines():
     assert bench.kernel_sha256(code) != bench.kernel_sha256("int a = 1;\n  int b = a + 2;\n")
 
 
-def test_kernel_hash_of_the_source_file_matches_its_text():
-    with open(bench.KERNEL_SRC, encoding="utf-8") as f:
-        text = f.read()
-    assert bench.kernel_sha256() == bench.kernel_sha256(text)
+def test_kernel_hash_covers_the_kernel_source_and_its_header():
+    texts = []
+    for path in (bench.KERNEL_SRC, bench.KERNEL_HDR):
+        with open(path, encoding="utf-8") as f:
+            texts.append(f.read())
+    assert bench.kernel_sha256() == bench.kernel_sha256("\n".join(texts))
+    assert bench.kernel_sha256() != bench.kernel_sha256(texts[0])  # the header's constants count
 
 
 def _traffic_file(path, sha, hbm="123456789"):
@@ -38,8 +41,11 @@ def _traffic_file(path, sha, hbm="123456789"):
 def test_traffic_is_reported_only_for_the_kernel_it_was_measured_on(tmp_path, monkeypatch):
     src = tmp_path / "kernel.hip"
     src.write_text("__global__ void k() {}\n")
+    hdr = tmp_path / "kernel.h"
+    hdr.write_text("constexpr int kTile = 1024;\n")
     traffic = tmp_path / "traffic.txt"
     monkeypatch.setattr(bench, "KERNEL_SRC", str(src))
+    monkeypatch.setattr(bench, "KERNEL_HDR", str(hdr))
     monkeypatch.setattr(bench, "TRAFFIC_FILE", str(traffic))
     assert bench.read_traffic() is None  # no summary
     _traffic_file(traffic, bench.kernel_sha256())
@@ -48,6 +54,10 @@ def test_traffic_is_reported_only_for_the_kernel_it_was_measured_on(tmp_path, mo
     assert bench.read_traffic() == 123456789.0
     src.write_text("__global__ void k() { int x = 0; }\n")
     assert bench.read_traffic() is None  # the code changed: the counters are stale
+    src.write_text("__global__ void k() {}\n")
+    assert bench.read_traffic() == 123456789.0
+    hdr.write_text("constexpr int kTile = 2048;\n")
+    assert bench.read_traffic() is None  # a constant of the header changed
     _traffic_file(traffic, bench.kernel_sha256(), hbm="not a number")
     assert bench.read_traffic() is None
 
