@@ -22,6 +22,21 @@
  * documented as "device" are HIP device addresses on the device that was
  * current when the context was created; "host" pointers are ordinary host
  * memory.  The caller owns every buffer it passes.
+ *
+ * Typical use, one worker of `world` over a gradient of n values already in
+ * device memory (error handling shortened):
+ *
+ *   micro_ctx *ctx;
+ *   micro_sparsify_init(&ctx, n, stream, NULL);          // NULL: default rule
+ *   double theta = theta0;                               // e.g. a calibrated start
+ *   for (int64_t t = 0; t < steps; ++t) {
+ *       int32_t part; int64_t k;
+ *       micro_cycle(t, worker, world, &part);            // Algorithm 1's rotation
+ *       micro_sparsify_step(ctx, grad, residual, part, world, density, &theta,
+ *                           out_idx, out_val, &k);       // out_* hold k pairs
+ *       ... exchange out_idx[0, k) / out_val[0, k) with the other workers ...
+ *   }
+ *   micro_sparsify_free(ctx);
  */
 #ifndef MICRO_SPARSIFY_H
 #define MICRO_SPARSIFY_H
