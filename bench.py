@@ -44,7 +44,8 @@ def parse_args():
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=20)
-    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--warmup", type=int, default=10,
+                    help="untimed steps first: the threshold settles from its calibrated start (default 10)")
     ap.add_argument("--workload", default="gpt_1p3b",
                     choices=["toy", "resnet18", "resnet50", "bert_large", "gpt_1p3b"])
     ap.add_argument("--density", type=float, default=None,
