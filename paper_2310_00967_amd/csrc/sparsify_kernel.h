@@ -23,6 +23,8 @@ constexpr int kMoveSpan = 4096;        // largest move piece (LDS arrays are siz
 constexpr int kMoveSpanSmall = 2048;   // move piece of a short merged sequence
 constexpr int kMoveBlock = 256;
 constexpr uint32_t kMoveGrid = 2048;  // largest move grid (eight workgroups per compute unit)
+static_assert((kMoveSpan & (kMoveSpan - 1)) == 0 && (kMoveSpanSmall & (kMoveSpanSmall - 1)) == 0,
+              "piece sizes are powers of two: the kernels divide by them with shifts");
 // Ticket schedule: values per tile (256 threads, four dwordx4 per lane).
 constexpr int kTicketTile = 4096;
 
@@ -81,7 +83,7 @@ struct LaunchArgs {
     double* chunk_sumsq;    // sweep: per chunk, the sum of its tiles' squared norms
     double* host_sumsq;     // sweep: mapped host memory, one squared norm per segment
     uint32_t move_blocks;   // workgroups of the move kernel
-    uint32_t move_span;     // items per move piece: kMoveSpan or kMoveSpanSmall
+    uint32_t move_span;     // items per move piece: kMoveSpan or kMoveSpanSmall (a power of two)
     uint2* stage;           // num_tiles * kStageCap staged (index, value bits) pairs
     uint32_t num_chunks;    // ceil(num_tiles / kChunkTiles)
     uint64_t* chunk_status;             // >= num_chunks look-back words

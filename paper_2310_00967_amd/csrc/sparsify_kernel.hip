@@ -330,6 +330,10 @@ __device__ __forceinline__ void scatter_pairs(const LaunchArgs& a, int lane, con
 
 constexpr uint32_t kOverflow = 0x80000000u;
 constexpr int kMoveBatch = 8;      // independent copies in flight per thread
+constexpr int kWindowBatch = 8;    // window loads in flight per thread
+// s_waitcnt operand (gfx9 encoding): vector-memory count 0, export and
+// LDS/scalar-memory counts at their maxima (not waited for)
+constexpr int kWaitVmcnt0 = 0x0F70;
 
 // Draws the workgroup's ticket (thread 0) and rearms the counter when the
 // last ticket of the launch is drawn: every other workgroup of the launch has
@@ -450,9 +454,10 @@ __device__ __forceinline__ void stream_tile(LaunchArgs a, const SweepTable* tbl)
         }
     }
     __syncthreads();
-    const size_t slot = static_cast<size_t>(tile) * kStageCap;
+    uint64_t* slot = reinterpret_cast<uint64_t*>(a.stage) + static_cast<size_t>(tile) * kStageCap;
     for (uint32_t j = tid; j < count; j += kStreamBlock) {
-        a.stage[slot + j] = s_pair[j];
+        const uint2 p = s_pair[j];  // index in the low word, value bits in the high word
+        __builtin_nontemporal_store(static_cast<uint64_t>(p.x) | (static_cast<uint64_t>(p.y) << 32), slot + j);
     }
     if (tid == 0) a.tile_counts[tile] = count;
 }
@@ -655,6 +660,7 @@ __device__ __forceinline__ void scan_chunk(const LaunchArgs& a, const SweepTable
     }
     __syncthreads();
     uint32_t pos = s_exclusive + before + x - mine;  // output offset of my first tile
+    const uint32_t span_shift = 31 - __builtin_clz(a.move_span);  // a power of two
     uint32_t offs[PER_THREAD];
 #pragma unroll
     for (int i = 0; i < PER_THREAD; ++i) {
@@ -666,9 +672,8 @@ __device__ __forceinline__ void scan_chunk(const LaunchArgs& a, const SweepTable
         // is at most one.
         if (first_tile + i < end_tile) {
             const uint64_t item = static_cast<uint64_t>(first_tile + i) + pos;
-            const uint64_t span = a.move_span;
-            const uint64_t m = (item + span - 1) / span;
-            if (m * span < item + 1 + count) a.split_tile[m] = first_tile + i;
+            const uint64_t m = (item + a.move_span - 1) >> span_shift;
+            if ((m << span_shift) < item + 1 + count) a.split_tile[m] = first_tile + i;
         }
         if (raw[i] & kOverflow) s_flagged[atomicAdd(&s_num_flagged, 1u)] = first_tile + i;
         pos += count;
@@ -707,21 +712,25 @@ __device__ __forceinline__ uint32_t pairs_before(uint64_t x, uint32_t t, uint32_
     return off + (x > item ? static_cast<uint32_t>(x - item - 1) : 0u);
 }
 
-// Inclusive running maximum over v[0, n) (n <= kMoveSpan) by the whole
-// workgroup: each thread takes kMovePer consecutive entries.  Contains two
-// barriers; the caller synchronises before the entries are read.
-__device__ __forceinline__ void block_max_scan(uint16_t* v, uint32_t n, int tid, uint32_t* s_wave_max) {
-    constexpr int kMovePer = kMoveSpan / kMoveBlock;
+// Inclusive running maximum over v[0, kMoveSpan) by the whole workgroup: each
+// thread takes 16 consecutive entries, read and written as two 16-byte words
+// (v is 16-byte aligned).  Contains two barriers; the caller synchronises
+// before the entries are read.
+__device__ __forceinline__ void block_max_scan(uint16_t* v, int tid, uint32_t* s_wave_max) {
+    static_assert(kMoveSpan == 16 * kMoveBlock, "16 entries per thread");
     const int lane = tid & (kWaveSize - 1);
     const int wave = tid / kWaveSize;
-    const uint32_t first = static_cast<uint32_t>(tid) * kMovePer;
-    uint32_t run[kMovePer];
+    uint4* p = reinterpret_cast<uint4*>(v) + 2 * tid;
+    const uint4 w0 = p[0], w1 = p[1];
+    uint32_t w[8] = {w0.x, w0.y, w0.z, w0.w, w1.x, w1.y, w1.z, w1.w};
     uint32_t m = 0;
 #pragma unroll
-    for (int i = 0; i < kMovePer; ++i) {
-        const uint32_t x = first + i < n ? v[first + i] : 0u;
-        m = x > m ? x : m;
-        run[i] = m;
+    for (int i = 0; i < 8; ++i) {  // two entries per word, the lower one first
+        const uint32_t e0 = w[i] & 0xffffu, e1 = w[i] >> 16;
+        m = e0 > m ? e0 : m;
+        const uint32_t r0 = m;
+        m = e1 > m ? e1 : m;
+        w[i] = r0 | (m << 16);
     }
     uint32_t incl = m;  // inclusive maximum over the threads of the wavefront
 #pragma unroll
@@ -733,74 +742,34 @@ __device__ __forceinline__ void block_max_scan(uint16_t* v, uint32_t n, int tid,
     if (lane == 0) before = 0;
     if (lane == kWaveSize - 1) s_wave_max[wave] = incl;
     __syncthreads();
-    for (int w = 0; w < wave; ++w) before = s_wave_max[w] > before ? s_wave_max[w] : before;
+    for (int k = 0; k < wave; ++k) before = s_wave_max[k] > before ? s_wave_max[k] : before;
 #pragma unroll
-    for (int i = 0; i < kMovePer; ++i)
-        if (first + i < n) v[first + i] = static_cast<uint16_t>(run[i] > before ? run[i] : before);
+    for (int i = 0; i < 8; ++i) {
+        uint32_t e0 = w[i] & 0xffffu, e1 = w[i] >> 16;
+        e0 = e0 > before ? e0 : before;
+        e1 = e1 > before ? e1 : before;
+        w[i] = e0 | (e1 << 16);
+    }
+    p[0] = make_uint4(w[0], w[1], w[2], w[3]);
+    p[1] = make_uint4(w[4], w[5], w[6], w[7]);
     __syncthreads();
 }
 
-// Move kernel: a fixed grid walks the merged sequence of tiles and output
-// pairs in pieces of move_span items (kMoveSpan, or kMoveSpanSmall where the
-// sequence is short: more, shorter pieces), so every piece costs about the same whatever the clustering of the
-// selection: many pairs from few tiles, or few pairs scattered over many
-// tiles.  Piece m's items lie in the tiles from split_tile[m] to
-// split_tile[m + 1] (recorded by the scan kernel), at most move_span + 1 of
-// them, and it holds the output positions [lo, hi).  The
-// tiles' output offsets go to LDS; every tile that is the last of its offset
-// (so the one that owns the positions from that offset on) writes its window
-// index at its first position in the piece, and a running maximum fills in the
-// owner of every position.  Each position then copies its staged pair with a
-// coalesced write.  Before its pieces, every workgroup redoes its share of the
-// flagged tiles, so a dense region of the partition costs the whole grid a
-// second pass over it rather than one workgroup a serial one.
+// The move kernel's work once the count k > 0 is known: the flagged tiles,
+// then this workgroup's pieces (first_t0 / first_t1: the split words of its
+// first piece, loaded with the counts).
 template <int VEC, bool SWEEP>
-__device__ __forceinline__ void move_pieces(const LaunchArgs& a, const SweepTable* tbl) {
+__device__ __forceinline__ void move_work(const LaunchArgs& a, const SweepTable* tbl, int64_t k, uint32_t flagged,
+                                          uint32_t first_t0, uint32_t first_t1) {
     constexpr uint32_t kWindow = kMoveSpan + 1;
     constexpr int WAVES = kMoveBlock / kWaveSize;
     static_assert(kWindow <= 65536, "window indices fit in 16 bits");
     __shared__ uint32_t s_off[kWindow];
     __shared__ uint32_t s_flag_bits[(kWindow + 31) / 32];
-    __shared__ uint16_t s_owner[kMoveSpan];
+    __shared__ __align__(16) uint16_t s_owner[kMoveSpan];
     __shared__ uint32_t s_wave_max[WAVES];
-    __shared__ double s_sq[WAVES];
-
     const int tid = threadIdx.x;
     const int lane = tid & (kWaveSize - 1);
-    // The split words of this workgroup's first piece are read together with
-    // the count (one round trip, not two); they are used only if the piece
-    // exists, and then the scan kernel wrote them.  Both indices lie inside
-    // the split array, which has room for the largest grid plus one.
-    const uint32_t first_t0 = a.split_tile[blockIdx.x];
-    const uint32_t first_t1 = a.split_tile[blockIdx.x + 1];
-    // both counts in one load: the flagged-tile count must not wait for k
-    const longlong2 counts = *reinterpret_cast<const longlong2*>(a.count_out);
-    const int64_t k = counts.x;
-    const uint32_t flagged = static_cast<uint32_t>(counts.y);
-    if (blockIdx.x == 0 && tid == 0) {  // the scan kernel has finished both counts
-        a.host_count[0] = k;
-        a.host_count[1] = counts.y;
-    }
-    if constexpr (SWEEP) {
-        // Each segment's count: the difference of the global offsets of its
-        // first tile and of the next segment's first tile.
-        if (blockIdx.x == 0 && tid < static_cast<int>(tbl->count)) {
-            const uint32_t t0 = tbl->seg[tid].tile_first, t1 = tbl->seg[tid + 1].tile_first;
-            const int64_t e0 = t0 < a.num_tiles ? (a.tile_excl[t0] & ~kOverflow) : k;
-            const int64_t e1 = t1 < a.num_tiles ? (a.tile_excl[t1] & ~kOverflow) : k;
-            a.host_count[2 + tid] = t1 > t0 ? e1 - e0 : 0;
-        }
-        // Workgroup b < count: the squared norm of segment b, its chunks'
-        // sums added in a fixed order.
-        if (blockIdx.x < tbl->count) {
-            const uint32_t c0 = tbl->seg[blockIdx.x].chunk_first, c1 = tbl->seg[blockIdx.x + 1].chunk_first;
-            double sq = 0.0;
-            for (uint32_t c = c0 + tid; c < c1; c += kMoveBlock) sq += a.chunk_sumsq[c];
-            const double total = block_sum<WAVES>(sq, lane, tid / kWaveSize, s_sq);
-            if (tid == 0) a.host_sumsq[blockIdx.x] = total;
-        }
-    }
-    if (k == 0) return;
     // Flagged tiles first, one wavefront each over the whole grid: the
     // wavefront recomputes the tile and writes its pairs and residual.
     for (uint32_t f = blockIdx.x * WAVES + tid / kWaveSize; f < flagged; f += gridDim.x * WAVES) {
@@ -816,7 +785,8 @@ __device__ __forceinline__ void move_pieces(const LaunchArgs& a, const SweepTabl
     }
     const uint64_t total = static_cast<uint64_t>(a.num_tiles) + static_cast<uint64_t>(k);
     const uint32_t span_items = a.move_span < kMoveSpan ? a.move_span : kMoveSpan;
-    const uint32_t pieces = static_cast<uint32_t>((total + span_items - 1) / span_items);
+    const uint32_t span_shift = 31 - __builtin_clz(span_items);  // a power of two
+    const uint32_t pieces = static_cast<uint32_t>((total + span_items - 1) >> span_shift);
     for (uint32_t m = blockIdx.x; m < pieces; m += gridDim.x) {
         const bool first = m == blockIdx.x;
         const uint32_t t0 = first ? first_t0 : a.split_tile[m];
@@ -826,12 +796,26 @@ __device__ __forceinline__ void move_pieces(const LaunchArgs& a, const SweepTabl
         const uint32_t span = t1 - t0 + 1;
         const uint32_t ntiles = span < kWindow ? span : kWindow;
         for (uint32_t i = tid; i < (ntiles + 31) / 32; i += kMoveBlock) s_flag_bits[i] = 0u;
-        for (uint32_t i = tid; i < span_items; i += kMoveBlock) s_owner[i] = 0;
+        reinterpret_cast<uint4*>(s_owner)[2 * tid] = make_uint4(0u, 0u, 0u, 0u);
+        reinterpret_cast<uint4*>(s_owner)[2 * tid + 1] = make_uint4(0u, 0u, 0u, 0u);
         __syncthreads();
-        for (uint32_t i = tid; i < ntiles; i += kMoveBlock) {
-            const uint32_t v = a.tile_excl[t0 + i];
-            s_off[i] = v & ~kOverflow;
-            if (v & kOverflow) atomicOr(&s_flag_bits[i / 32], 1u << (i % 32));
+        // the window's loads in batches of kWindowBatch per thread, each batch
+        // in flight at once (one batch covers up to 2048 tiles)
+        for (uint32_t i0 = 0; i0 < ntiles; i0 += kMoveBlock * kWindowBatch) {  // uniform
+            uint32_t win[kWindowBatch];
+#pragma unroll
+            for (int u = 0; u < kWindowBatch; ++u) {
+                const uint32_t i = i0 + tid + u * kMoveBlock;
+                win[u] = i < ntiles ? a.tile_excl[t0 + i] : 0u;
+            }
+#pragma unroll
+            for (int u = 0; u < kWindowBatch; ++u) {
+                const uint32_t i = i0 + tid + u * kMoveBlock;
+                if (i < ntiles) {
+                    s_off[i] = win[u] & ~kOverflow;
+                    if (win[u] & kOverflow) atomicOr(&s_flag_bits[i / 32], 1u << (i % 32));
+                }
+            }
         }
         __syncthreads();
         const uint64_t x0 = static_cast<uint64_t>(m) * span_items;
@@ -852,7 +836,7 @@ __device__ __forceinline__ void move_pieces(const LaunchArgs& a, const SweepTabl
             if (owner && off < hi) s_owner[(off > lo ? off : lo) - lo] = static_cast<uint16_t>(q);
         }
         __syncthreads();
-        block_max_scan(s_owner, hi - lo, tid, s_wave_max);
+        block_max_scan(s_owner, tid, s_wave_max);
         for (uint32_t j0 = lo + tid; j0 < hi; j0 += kMoveBlock * kMoveBatch) {
             size_t src[kMoveBatch];
             bool live[kMoveBatch];
@@ -867,10 +851,15 @@ __device__ __forceinline__ void move_pieces(const LaunchArgs& a, const SweepTabl
                     src[u] = static_cast<size_t>(t0 + q) * kStageCap + (j - s_off[q]);
                 }
             }
+            // Loads outside any branch (a lane with nothing to copy reads
+            // stage[0], inside the buffer since k > 0), then one wait for all
+            // of them: the stores below, each under its own branch, would
+            // otherwise wait for the vector-memory counter to drain, stores
+            // included, before each other.
             uint2 pair[kMoveBatch];
 #pragma unroll
-            for (int u = 0; u < kMoveBatch; ++u)
-                if (live[u]) pair[u] = a.stage[src[u]];
+            for (int u = 0; u < kMoveBatch; ++u) pair[u] = a.stage[src[u]];
+            __builtin_amdgcn_s_waitcnt(kWaitVmcnt0);
 #pragma unroll
             for (int u = 0; u < kMoveBatch; ++u) {
                 if (live[u]) {
@@ -881,6 +870,72 @@ __device__ __forceinline__ void move_pieces(const LaunchArgs& a, const SweepTabl
             }
         }
         __syncthreads();  // the window is reloaded for the next piece
+    }
+}
+
+// Move kernel: a fixed grid walks the merged sequence of tiles and output
+// pairs in pieces of move_span items (kMoveSpan, or kMoveSpanSmall where the
+// sequence is short: more, shorter pieces), so every piece costs about the same whatever the clustering of the
+// selection: many pairs from few tiles, or few pairs scattered over many
+// tiles.  Piece m's items lie in the tiles from split_tile[m] to
+// split_tile[m + 1] (recorded by the scan kernel), at most move_span + 1 of
+// them, and it holds the output positions [lo, hi).  The
+// tiles' output offsets go to LDS; every tile that is the last of its offset
+// (so the one that owns the positions from that offset on) writes its window
+// index at its first position in the piece, and a running maximum fills in the
+// owner of every position.  Each position then copies its staged pair with a
+// coalesced write.  Before its pieces, every workgroup redoes its share of the
+// flagged tiles, so a dense region of the partition costs the whole grid a
+// second pass over it rather than one workgroup a serial one.
+template <int VEC, bool SWEEP>
+__device__ __forceinline__ void move_pieces(const LaunchArgs& a, const SweepTable* tbl) {
+    constexpr int WAVES = kMoveBlock / kWaveSize;
+    __shared__ double s_sq[WAVES];
+
+    const int tid = threadIdx.x;
+    const int lane = tid & (kWaveSize - 1);
+    // The split words of this workgroup's first piece are read together with
+    // the count (one round trip, not two); they are used only if the piece
+    // exists, and then the scan kernel wrote them.  Both indices lie inside
+    // the split array, which has room for the largest grid plus one.
+    const uint32_t first_t0 = a.split_tile[blockIdx.x];
+    const uint32_t first_t1 = a.split_tile[blockIdx.x + 1];
+    // both counts in one load: the flagged-tile count must not wait for k
+    const longlong2 counts = *reinterpret_cast<const longlong2*>(a.count_out);
+    const int64_t k = counts.x;
+    const uint32_t flagged = static_cast<uint32_t>(counts.y);
+    // What goes to the host (the counts; in a sweep also each segment's
+    // count and squared norm) is stored after this workgroup's pieces: a
+    // store to mapped host memory takes a bus round trip, and a wait for any
+    // later load would include it.
+    int64_t seg_k = 0;
+    double seg_sq = 0.0;
+    if constexpr (SWEEP) {
+        // Each segment's count: the difference of the global offsets of its
+        // first tile and of the next segment's first tile.
+        if (blockIdx.x == 0 && tid < static_cast<int>(tbl->count)) {
+            const uint32_t t0 = tbl->seg[tid].tile_first, t1 = tbl->seg[tid + 1].tile_first;
+            const int64_t e0 = t0 < a.num_tiles ? (a.tile_excl[t0] & ~kOverflow) : k;
+            const int64_t e1 = t1 < a.num_tiles ? (a.tile_excl[t1] & ~kOverflow) : k;
+            seg_k = t1 > t0 ? e1 - e0 : 0;
+        }
+        // Workgroup b < count: the squared norm of segment b, its chunks'
+        // sums added in a fixed order.
+        if (blockIdx.x < tbl->count) {
+            const uint32_t c0 = tbl->seg[blockIdx.x].chunk_first, c1 = tbl->seg[blockIdx.x + 1].chunk_first;
+            double sq = 0.0;
+            for (uint32_t c = c0 + tid; c < c1; c += kMoveBlock) sq += a.chunk_sumsq[c];
+            seg_sq = block_sum<WAVES>(sq, lane, tid / kWaveSize, s_sq);
+        }
+    }
+    if (k != 0) move_work<VEC, SWEEP>(a, tbl, k, flagged, first_t0, first_t1);
+    if (blockIdx.x == 0 && tid == 0) {  // the scan kernel has finished both counts
+        a.host_count[0] = k;
+        a.host_count[1] = counts.y;
+    }
+    if constexpr (SWEEP) {
+        if (blockIdx.x == 0 && tid < static_cast<int>(tbl->count)) a.host_count[2 + tid] = seg_k;
+        if (blockIdx.x < tbl->count && tid == 0) a.host_sumsq[blockIdx.x] = seg_sq;
     }
 }
 
