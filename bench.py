@@ -62,6 +62,10 @@ def parse_args():
     ap.add_argument("--variant", default="auto", choices=["auto", "staged", "ticket"],
                     help="kernel schedule (auto, the library default, runs the ticket schedule up to "
                          "2^20 values per partition and the staged one above)")
+    ap.add_argument("--separate-scan", action="store_true",
+                    help="staged schedule: launch the scan pass on its own instead of inside the "
+                         "streaming launch (the library default for partitions of up to a few hundred "
+                         "million values)")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only run a plain device copy of known size (HBM counter scaling)")
     ap.add_argument("--path", default="step", choices=["step", "ef", "union", "sweep"],
@@ -173,7 +177,7 @@ class Run:
                                        self.out_idx, self.out_val)
             wall_s = time.perf_counter() - t0
             self.theta[p] = th
-            kernel_ms, redone, variant = self.sp.last_stats()
+            kernel_ms, redone, variant, fused = self.sp.last_stats()
             self.log.append((p, ln, k, kernel_ms if timed else None, redone))
             self.variant = variant
             if self.records is None:
@@ -187,7 +191,7 @@ class Run:
                 "wall_us": wall_s * 1e6, "alg_bytes": alg,
                 "kernel_gbs": alg / (kernel_ms * 1e-3) / 1e9 if kernel_ms > 0 else None,
                 "hbm_frac": alg / (kernel_ms * 1e-3) / 1e9 / HBM_PEAK_GBS if kernel_ms > 0 else None,
-                "redone_tiles": redone})
+                "redone_tiles": redone, "fused": bool(fused)})
         self.t += 1
 
 
@@ -581,7 +585,8 @@ def main():
     torch.cuda.synchronize()
     variant = {"auto": micro.MICRO_VARIANT_AUTO, "staged": micro.MICRO_VARIANT_STAGED,
                "ticket": micro.MICRO_VARIANT_TICKET}[args.variant]
-    sp = micro.Sparsifier(w.n_total, device="cuda", time_kernel=True, variant=variant)
+    sp = micro.Sparsifier(w.n_total, device="cuda", time_kernel=True, variant=variant,
+                          separate_scan=args.separate_scan)
     if args.path != "step":
         main_path(args, w, head, pool, n_pool, sp)
         sp.close()

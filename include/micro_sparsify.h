@@ -84,6 +84,11 @@ typedef enum micro_status {
 /* Flags. */
 #define MICRO_FLAG_TIME_KERNEL 1 /* record HIP events around each launch so
                                     micro_sparsify_last_kernel_ms can report it */
+#define MICRO_FLAG_SEPARATE_SCAN 2 /* STAGED: always launch the scan pass on its
+                                      own; by default micro_sparsify_step runs
+                                      the streaming and scan passes as one
+                                      launch for partitions of up to a few
+                                      hundred million values (same result)    */
 
 typedef struct micro_config {
     int32_t rule;    /* MICRO_RULE_*                                  (default 0)    */
@@ -103,6 +108,8 @@ typedef struct micro_step_stats {
                                redone by the placing pass instead              */
     int32_t variant;        /* the schedule the last step ran:
                                MICRO_VARIANT_TICKET or MICRO_VARIANT_STAGED    */
+    int32_t fused;          /* 1 if its streaming and scan passes ran as one
+                               launch (micro_sparsify_step, STAGED), else 0    */
 } micro_step_stats;
 
 /* Fills *cfg with the defaults listed above. */

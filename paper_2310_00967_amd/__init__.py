@@ -14,21 +14,22 @@ runs in the HIP library behind include/micro_sparsify.h; PyTorch only
 provides device memory and the stream.
 """
 from . import _lib
-from ._lib import (MICRO_FLAG_TIME_KERNEL, MICRO_RULE_FIXED_STEP, MICRO_RULE_PROPORTIONAL,
+from ._lib import (MICRO_FLAG_SEPARATE_SCAN, MICRO_FLAG_TIME_KERNEL, MICRO_RULE_FIXED_STEP, MICRO_RULE_PROPORTIONAL,
                    MICRO_VARIANT_AUTO, MICRO_VARIANT_STAGED, MICRO_VARIANT_TICKET, MicroError, default_config,
                    micro_cycle, micro_estimate_threshold, micro_partition, micro_threshold_f32)
 
 __all__ = ["Sparsifier", "MicroError", "default_config", "micro_partition", "micro_cycle",
            "micro_estimate_threshold", "micro_threshold_f32", "MICRO_RULE_PROPORTIONAL",
            "MICRO_RULE_FIXED_STEP", "MICRO_VARIANT_AUTO", "MICRO_VARIANT_TICKET", "MICRO_VARIANT_STAGED",
-           "MICRO_FLAG_TIME_KERNEL"]
+           "MICRO_FLAG_TIME_KERNEL", "MICRO_FLAG_SEPARATE_SCAN"]
 
 
 class Sparsifier:
     """One context of the C library bound to a torch device and stream."""
 
     def __init__(self, n_total, device=None, stream=None, rule=MICRO_RULE_PROPORTIONAL, beta=None,
-                 lo=None, hi=None, alpha=None, variant=MICRO_VARIANT_AUTO, time_kernel=False):
+                 lo=None, hi=None, alpha=None, variant=MICRO_VARIANT_AUTO, time_kernel=False,
+                 separate_scan=False):
         import torch
         if not torch.cuda.is_available():
             raise RuntimeError("Sparsifier needs a HIP device")
@@ -43,7 +44,7 @@ class Sparsifier:
             if v is not None:
                 setattr(cfg, name, float(v))
         cfg.variant = variant
-        cfg.flags = MICRO_FLAG_TIME_KERNEL if time_kernel else 0
+        cfg.flags = (MICRO_FLAG_TIME_KERNEL if time_kernel else 0) | (MICRO_FLAG_SEPARATE_SCAN if separate_scan else 0)
         self.config = cfg
         with torch.cuda.device(self.device):
             self.stream = stream if stream is not None else torch.cuda.current_stream(self.device)
@@ -196,9 +197,9 @@ class Sparsifier:
                                  union_idx.numel(), world)
 
     def last_stats(self):
-        """(kernel_ms, redone_tiles, variant) of the last step."""
+        """(kernel_ms, redone_tiles, variant, fused) of the last step."""
         st = _lib.micro_sparsify_last_stats(self._ctx)
-        return st.kernel_ms, st.redone_tiles, st.variant
+        return st.kernel_ms, st.redone_tiles, st.variant, st.fused
 
     def last_kernel_ms(self):
         return self.last_stats()[0]

@@ -14,6 +14,7 @@ MICRO_OK, MICRO_EINVAL, MICRO_ECAPACITY, MICRO_ERANGE, MICRO_ENOMEM, MICRO_EHIP 
 MICRO_RULE_PROPORTIONAL, MICRO_RULE_FIXED_STEP = 0, 1
 MICRO_VARIANT_AUTO, MICRO_VARIANT_TICKET, MICRO_VARIANT_STAGED = 0, 1, 2
 MICRO_FLAG_TIME_KERNEL = 1
+MICRO_FLAG_SEPARATE_SCAN = 2
 
 # Every function the header declares, with (restype, argtypes).
 _i64p = ctypes.POINTER(ctypes.c_int64)
@@ -29,7 +30,7 @@ class micro_config(ctypes.Structure):
 
 class micro_step_stats(ctypes.Structure):
     _fields_ = [("kernel_ms", ctypes.c_float), ("redone_tiles", ctypes.c_int64),
-                ("variant", ctypes.c_int32)]
+                ("variant", ctypes.c_int32), ("fused", ctypes.c_int32)]
 
 
 _cfgp = ctypes.POINTER(micro_config)

@@ -38,10 +38,12 @@ struct micro_ctx {
     uint2* d_stage = nullptr;                // (index, value bits) pairs
     uint64_t* d_chunk_status = nullptr;
     int64_t chunk_capacity = 0;
+    uint64_t* d_tile_words = nullptr;        // fused schedule: epoch-tagged tile counts
+    int64_t fused_max_chunks = 0;            // largest chunk count the fused schedule takes (0: none)
     // ticket schedule: tile look-back words
     uint64_t* d_status = nullptr;
     unsigned long long* d_tickets = nullptr; // [0] tile ticket of the one-pass schedule
-    int64_t* d_count = nullptr;              // [0] selected count, [1] flagged tiles
+    int64_t* d_count = nullptr;              // [0] selected count, [1] (epoch << 32) | flagged tiles
     int64_t* h_count = nullptr;              // mapped pinned host memory stored by the kernels: [0] k,
                                              // [1] redone tiles, [2 + r] a sweep's counts
     int64_t* h_count_dev = nullptr;          // the device's address of h_count
@@ -107,7 +109,7 @@ bool config_valid(const micro_config& c) {
     if (c.variant != MICRO_VARIANT_AUTO && c.variant != MICRO_VARIANT_TICKET &&
         c.variant != MICRO_VARIANT_STAGED)
         return false;
-    if ((c.flags & ~MICRO_FLAG_TIME_KERNEL) != 0) return false;
+    if ((c.flags & ~(MICRO_FLAG_TIME_KERNEL | MICRO_FLAG_SEPARATE_SCAN)) != 0) return false;
     return true;
 }
 
@@ -156,6 +158,8 @@ micro_status reset_scratch(micro_ctx* ctx) {
         e = hipMemsetAsync(ctx->d_status, 0, sizeof(uint64_t) * ctx->ticket_capacity, ctx->stream);
     if (e == hipSuccess && ctx->d_chunk_status)
         e = hipMemsetAsync(ctx->d_chunk_status, 0, sizeof(uint64_t) * ctx->chunk_capacity, ctx->stream);
+    if (e == hipSuccess && ctx->d_tile_words)
+        e = hipMemsetAsync(ctx->d_tile_words, 0, sizeof(uint64_t) * ctx->tile_capacity, ctx->stream);
     if (e == hipSuccess) e = hipStreamSynchronize(ctx->stream);
     if (e != hipSuccess) return hip_fail(ctx, e, "scratch reset");
     ctx->epoch = 0;
@@ -170,7 +174,7 @@ void release(micro_ctx* ctx) {
     for (hipEvent_t ev : ctx->ev)
         if (ev) (void)hipEventDestroy(ev);
     void* device_buffers[] = {ctx->d_tile_counts, ctx->d_tile_excl, ctx->d_flagged_list, ctx->d_split_tile, ctx->d_tile_sumsq, ctx->d_chunk_sumsq, ctx->d_stage,
-                              ctx->d_chunk_status, ctx->d_status, ctx->d_tickets,
+                              ctx->d_chunk_status, ctx->d_tile_words, ctx->d_status, ctx->d_tickets,
                               ctx->d_count};
     for (void* p : device_buffers)
         if (p) (void)hipFree(p);
@@ -334,6 +338,7 @@ micro_status execute_step(micro_ctx* ctx, const float* grad, float* residual, in
     a.count_out = ctx->d_count;
     a.host_count = ctx->h_count_dev;
     a.tile_counts = ctx->d_tile_counts;
+    a.tile_words = ctx->d_tile_words;
     a.tile_excl = ctx->d_tile_excl;
     a.flagged_list = ctx->d_flagged_list;
     a.split_tile = ctx->d_split_tile;
@@ -356,9 +361,14 @@ micro_status execute_step(micro_ctx* ctx, const float* grad, float* residual, in
     host_count[1] = len > 0 ? -1 : 0;
     if (n_outside > 0 && (e = micro::launch_accumulate(acc, vec4, ctx->stream)) != hipSuccess)
         return hip_fail(ctx, e, "accumulate kernel launch");
+    // The staged schedule's stream and scan kernels run as one launch while
+    // the partition's chunk count allows it (see fused_max_chunks).
+    const bool fused = staged && (ctx->cfg.flags & MICRO_FLAG_SEPARATE_SCAN) == 0 && chunks <= ctx->fused_max_chunks;
     if (len > 0) {
         ctx->epoch = a.epoch;
-        e = staged ? micro::launch_staged(a, vec4, ctx->stream) : micro::launch_ticket(a, vec4, ctx->stream);
+        e = !staged ? micro::launch_ticket(a, vec4, ctx->stream)
+            : fused ? micro::launch_fused(a, vec4, ctx->stream)
+                    : micro::launch_staged(a, vec4, ctx->stream);
         if (e != hipSuccess) return hip_fail(ctx, e, "sparsify kernel launch");
     }
     if (timed && (e = hipEventRecord(ctx->ev[1], ctx->stream)) != hipSuccess)
@@ -375,6 +385,7 @@ micro_status execute_step(micro_ctx* ctx, const float* grad, float* residual, in
         return hip_fail(ctx, e, "hipEventElapsedTime");
     ctx->stats.redone_tiles = staged ? host_count[1] : 0;
     ctx->stats.variant = staged ? MICRO_VARIANT_STAGED : MICRO_VARIANT_TICKET;
+    ctx->stats.fused = len > 0 && fused ? 1 : 0;
     *k = selected;
     *theta = next_threshold(ctx->cfg, density, len, selected, *theta);
     return MICRO_OK;
@@ -481,6 +492,7 @@ micro_status run_segments(micro_ctx* ctx, const float* grad, float* residual, in
         return hip_fail(ctx, e, "hipEventElapsedTime");
     ctx->stats.redone_tiles = host_count[1];
     ctx->stats.variant = MICRO_VARIANT_STAGED;
+    ctx->stats.fused = 0;
     for (int32_t r = 0; r < count; ++r) {
         k[r] = host_count[2 + r];
         sumsq[r] = host_sumsq[r];
@@ -693,7 +705,18 @@ micro_status micro_sparsify_init(micro_ctx** out, int64_t n_total, void* hip_str
              hipMalloc(&ctx->d_tile_sumsq, sizeof(double) * ctx->tile_capacity) == hipSuccess &&
              hipMalloc(&ctx->d_chunk_sumsq, sizeof(double) * ctx->chunk_capacity) == hipSuccess &&
              hipMalloc(&ctx->d_stage, sizeof(uint2) * stage) == hipSuccess &&
-             hipMalloc(&ctx->d_chunk_status, sizeof(uint64_t) * ctx->chunk_capacity) == hipSuccess;
+             hipMalloc(&ctx->d_chunk_status, sizeof(uint64_t) * ctx->chunk_capacity) == hipSuccess &&
+             hipMalloc(&ctx->d_tile_words, sizeof(uint64_t) * ctx->tile_capacity) == hipSuccess;
+    }
+    if (ok && ctx->has_staged) {
+        // The fused schedule's chunk workgroups wait for stream workgroups of
+        // the same launch: it is taken only while they fill at most half of
+        // the workgroups the device holds at once (both load widths).
+        int b4 = 0, b1 = 0;
+        if (micro::fused_blocks_per_cu(true, &b4) == hipSuccess && micro::fused_blocks_per_cu(false, &b1) == hipSuccess)
+            ctx->fused_max_chunks = static_cast<int64_t>(b4 < b1 ? b4 : b1) * ctx->compute_units / 2;
+        else
+            (void)hipGetLastError();  // no fused schedule; the separate kernels remain
     }
     if (ok && ctx->has_ticket) {
         ctx->ticket_capacity = n_total / micro::kTicketTile + 2;
@@ -716,6 +739,7 @@ micro_status micro_sparsify_init(micro_ctx** out, int64_t n_total, void* hip_str
     ctx->stats.kernel_ms = -1.0f;
     ctx->stats.redone_tiles = 0;
     ctx->stats.variant = ctx->has_staged ? MICRO_VARIANT_STAGED : MICRO_VARIANT_TICKET;
+    ctx->stats.fused = 0;
     if (reset_scratch(ctx) != MICRO_OK) {
         set_error(nullptr, "%s", ctx->last_error.c_str());
         release(ctx);

@@ -71,11 +71,13 @@ struct LaunchArgs {
     float theta_f;          // smallest binary32 >= theta
     uint32_t epoch;         // 1 .. kMaxEpoch
     uint32_t num_tiles;     // tiles covering [base, end)
-    int64_t* count_out;     // device: [0] selected count, [1] flagged tiles (redone by the move kernel)
+    int64_t* count_out;     // device: [0] selected count, [1] (epoch << 32) | flagged tiles (redone by the
+                            // move kernel; a word of an older launch counts none)
     int64_t* host_count;    // mapped pinned host memory: the final count_out, stored by the last kernel;
                             // a sweep adds each segment's count from [2] on
     // staged schedule
     uint32_t* tile_counts;  // num_tiles counts (bit 31: tile left to the scan kernel)
+    uint64_t* tile_words;   // fused schedule: num_tiles epoch-tagged counts (status word layout)
     uint32_t* tile_excl;    // num_tiles output offsets (bit 31: flagged tile)
     uint32_t* flagged_list; // count_out[1] flagged tiles, in no particular order
     uint32_t* split_tile;   // >= ceil((num_tiles + P) / kMoveSpan) tiles holding each piece's first item
@@ -113,6 +115,12 @@ int64_t tile_base_for(const float* grad, int64_t start, bool vec4);
 // vec4: grad and residual share their 16-byte phase (dwordx4 kernels), else
 // the scalar-load kernels.  Each returns the launch status.
 hipError_t launch_staged(const LaunchArgs& args, bool vec4, hipStream_t stream);
+// The staged schedule with its stream and scan kernels fused into one launch
+// (num_tiles + num_chunks workgroups, the chunk workgroups last); the host
+// takes it only while num_chunks is at most half the workgroups of that
+// kernel the device holds at once (fused_blocks_per_cu per compute unit).
+hipError_t launch_fused(const LaunchArgs& args, bool vec4, hipStream_t stream);
+hipError_t fused_blocks_per_cu(bool vec4, int* blocks);
 hipError_t launch_ticket(const LaunchArgs& args, bool vec4, hipStream_t stream);
 // The sweep: num_tiles / num_chunks are the totals over the table's segments.
 hipError_t launch_sweep(const LaunchArgs& args, const SweepTable& table, bool vec4, hipStream_t stream);

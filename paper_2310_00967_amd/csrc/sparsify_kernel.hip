@@ -39,6 +39,11 @@
 //     and moves the staged pairs to their final places in equal pieces of the
 //     merged sequence of tiles and pairs, whatever the clustering of the
 //     selection; it also stores the counts into mapped host memory.
+//   stream_scan_kernel (fused staged schedule, the default of a single
+//     partition of up to a few hundred chunks): the stream and scan kernels'
+//     work in one launch, the chunk workgroups after the tile workgroups,
+//     polling epoch-tagged tile words; saves a launch and its drain between
+//     the streaming pass and the scan.
 //   HBM traffic beyond the 12 bytes per value of the stream: 16 bytes per
 //   selected value (staged write and read) and 8 bytes per 1024 values.
 // Sweep: the same three kernels over a table of segments (every partition of
@@ -398,11 +403,22 @@ __device__ __forceinline__ double block_sum(double v, int lane, int wave, double
     return total;
 }
 
+// A tile's count (bit 31: left to the move kernel): a plain word for the scan
+// kernel of the next launch or, in the fused schedule, an epoch-tagged status
+// word that the chunk workgroups of the same launch poll.
+template <bool FUSED>
+__device__ __forceinline__ void publish_tile(const LaunchArgs& a, uint32_t tile, uint32_t raw) {
+    if constexpr (FUSED)
+        store_status(&a.tile_words[tile], (static_cast<uint64_t>(a.epoch) << kEpochShift) | kFlagAggregate | raw);
+    else
+        a.tile_counts[tile] = raw;
+}
+
 // Stream pass over one tile (see the file comment).  In a sweep the tile's
 // segment supplies range and threshold, and the tile also stores the squared
 // norm of its new residual (also for a tile left to the move kernel, whose
 // new residual is fixed by its selection bits all the same).
-template <int VEC, int ROWS, bool SWEEP>
+template <int VEC, int ROWS, bool SWEEP, bool FUSED = false>
 __device__ __forceinline__ void stream_tile(LaunchArgs a, const SweepTable* tbl) {
     constexpr int WAVES = kStreamBlock / kWaveSize;
     static_assert(VEC * ROWS * kStreamBlock == kStreamTile, "tile size");
@@ -435,9 +451,8 @@ __device__ __forceinline__ void stream_tile(LaunchArgs a, const SweepTable* tbl)
     }
     wave_ranks<VEC, ROWS>(sel, lane_rank, row_count);
     const uint32_t count = tile_ranks<ROWS, WAVES>(row_count, lane, wave, s_wave_total, row_base);
-    if (tile == 0 && tid == 0) a.count_out[1] = 0;  // the scan kernel adds the flagged tiles
     if (count > kStageCap) {  // uniform: left to the move kernel, residual untouched
-        if (tid == 0) a.tile_counts[tile] = count | kOverflow;
+        if (tid == 0) publish_tile<FUSED>(a, tile, count | kOverflow);
         return;
     }
     store_residual<VEC, ROWS, kStreamBlock, true>(a, tid, t, sel);
@@ -459,7 +474,7 @@ __device__ __forceinline__ void stream_tile(LaunchArgs a, const SweepTable* tbl)
         const uint2 p = s_pair[j];  // index in the low word, value bits in the high word
         __builtin_nontemporal_store(static_cast<uint64_t>(p.x) | (static_cast<uint64_t>(p.y) << 32), slot + j);
     }
-    if (tid == 0) a.tile_counts[tile] = count;
+    if (tid == 0) publish_tile<FUSED>(a, tile, count);
 }
 
 template <int VEC, int ROWS>
@@ -501,6 +516,28 @@ __device__ void redo_tile(const LaunchArgs& a, int64_t tile_base, int lane, uint
     }
 }
 
+// The flagged-tile counter count_out[1] holds (epoch << 32) | count; a word
+// of an older launch reads as zero, so it is never cleared between launches.
+// reserve_flagged adds n for this launch and returns the first list position
+// of the n entries (one compare-and-swap loop per chunk that has flagged
+// tiles; those are rare).
+__device__ __forceinline__ uint32_t reserve_flagged(const LaunchArgs& a, uint32_t n) {
+    unsigned long long* p = reinterpret_cast<unsigned long long*>(&a.count_out[1]);
+    unsigned long long old = __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    for (;;) {
+        const uint32_t base = (old >> 32) == a.epoch ? static_cast<uint32_t>(old) : 0u;
+        const unsigned long long next = (static_cast<unsigned long long>(a.epoch) << 32) | (base + n);
+        const unsigned long long seen = atomicCAS(p, old, next);
+        if (seen == old) return base;
+        old = seen;
+    }
+}
+
+__device__ __forceinline__ uint32_t flagged_count(const LaunchArgs& a, int64_t word) {
+    const uint64_t w = static_cast<uint64_t>(word);
+    return (w >> 32) == a.epoch ? static_cast<uint32_t>(w) : 0u;
+}
+
 // Tiles [first, end) of scan chunk `chunk`: kChunkTiles per chunk; in a
 // sweep each segment has chunks of its own, the last one possibly short.
 template <bool SWEEP>
@@ -514,6 +551,34 @@ __device__ __forceinline__ void chunk_tiles(const LaunchArgs& a, const SweepTabl
     } else {
         first = chunk * kChunkTiles;
         end = first + kChunkTiles < a.num_tiles ? first + kChunkTiles : a.num_tiles;
+    }
+}
+
+// The counts of N tiles (bit 31: left to the move kernel) of the fused
+// schedule, t[i] < end only (others read 0): their epoch-tagged words are
+// loaded together and the ones not yet published polled again.  Only stream
+// workgroups publish tile words and they wait for nobody, so the loop ends.
+template <int N>
+__device__ __forceinline__ void poll_tiles(const LaunchArgs& a, const uint32_t (&t)[N], uint32_t end,
+                                           uint32_t (&raw)[N]) {
+    uint32_t pending = 0;
+#pragma unroll
+    for (int i = 0; i < N; ++i) {
+        raw[i] = 0;
+        if (t[i] < end) pending |= 1u << i;
+    }
+    while (pending) {
+        uint64_t w[N];
+#pragma unroll
+        for (int i = 0; i < N; ++i) w[i] = (pending >> i) & 1u ? load_status(&a.tile_words[t[i]]) : 0ull;
+#pragma unroll
+        for (int i = 0; i < N; ++i) {
+            if (((pending >> i) & 1u) && (w[i] >> kEpochShift) == a.epoch && (w[i] & kFlagMask) != 0) {
+                raw[i] = static_cast<uint32_t>(w[i] & kCountMask);
+                pending &= ~(1u << i);
+            }
+        }
+        if (pending) __builtin_amdgcn_s_sleep(2);
     }
 }
 
@@ -540,8 +605,13 @@ constexpr int kLookbackPolls = 4;  // polls of a silent predecessor before its c
 // so a predecessor may not have run yet: a word still unpublished after a few
 // polls is replaced by the predecessor's count summed from its tile counts,
 // which are final before the scan kernel starts.  The look-back therefore
-// ends whatever order the workgroups run in.
-template <bool SWEEP>
+// ends whatever order the workgroups run in.  In the fused schedule the chunk
+// workgroups start as the stream workgroups drain, far apart, and a recompute
+// would have to wait for tile words anyway: there the look-back polls until
+// each predecessor has published (a chunk workgroup publishes its aggregate
+// as soon as its tile words are in, before its own look-back, so the wait
+// depends on stream workgroups only).
+template <bool SWEEP, bool FUSED = false>
 __device__ uint32_t chunk_lookback(const LaunchArgs& a, const SweepTable* tbl, uint32_t chunk, int lane) {
     const uint64_t tag = static_cast<uint64_t>(a.epoch) << kEpochShift;
     uint32_t exclusive = 0;
@@ -557,7 +627,7 @@ __device__ uint32_t chunk_lookback(const LaunchArgs& a, const SweepTable* tbl, u
         // lanes 0 .. first inclusive lane (all 64 when none is inclusive)
         const uint64_t need = inc_mask ? (inc_mask ^ (inc_mask - 1)) : ~0ull;
         uint64_t missing = __ballot(!valid) & need;
-        if (missing && ++polls < kLookbackPolls) {
+        if (missing && (FUSED || ++polls < kLookbackPolls)) {
             __builtin_amdgcn_s_sleep(1);
             continue;
         }
@@ -584,7 +654,7 @@ __device__ uint32_t chunk_lookback(const LaunchArgs& a, const SweepTable* tbl, u
 // In a sweep the chunk lies inside one segment (chunks never straddle two)
 // and also sums its tiles' squared norms; the look-back and the offsets are
 // global, since the segments' pairs form one compaction in index order.
-template <bool SWEEP>
+template <bool SWEEP, bool FUSED = false>
 __device__ __forceinline__ void scan_chunk(const LaunchArgs& a, const SweepTable* tbl) {
     constexpr int WAVES = kScanBlock / kWaveSize;
     constexpr int PER_THREAD = kChunkTiles / kScanBlock;
@@ -598,14 +668,20 @@ __device__ __forceinline__ void scan_chunk(const LaunchArgs& a, const SweepTable
     const int lane = tid & (kWaveSize - 1);
     const int wave = tid / kWaveSize;
     if (tid == 0) s_num_flagged = 0;
-    const uint32_t chunk = blockIdx.x;
+    // fused schedule: the chunk workgroups follow the num_tiles stream ones
+    const uint32_t chunk = FUSED ? blockIdx.x - a.num_tiles : blockIdx.x;
     uint32_t chunk_tile, end_tile;
     chunk_tiles<SWEEP>(a, tbl, chunk, chunk_tile, end_tile);
     const uint32_t first_tile = chunk_tile + tid * PER_THREAD;
     const bool whole = first_tile % 4 == 0 && first_tile + PER_THREAD <= end_tile;
 
     uint32_t raw[PER_THREAD];
-    if (whole) {
+    if constexpr (FUSED) {
+        uint32_t t[PER_THREAD];
+#pragma unroll
+        for (int i = 0; i < PER_THREAD; ++i) t[i] = first_tile + i;
+        poll_tiles<PER_THREAD>(a, t, end_tile, raw);
+    } else if (whole) {
 #pragma unroll
         for (int i = 0; i < PER_THREAD; i += 4) {
             const uint4 v = *reinterpret_cast<const uint4*>(a.tile_counts + first_tile + i);
@@ -650,7 +726,7 @@ __device__ __forceinline__ void scan_chunk(const LaunchArgs& a, const SweepTable
             if (lane == 0) store_status(&a.chunk_status[0], tag | kFlagInclusive | total);
         } else {
             if (lane == 0) store_status(&a.chunk_status[chunk], tag | kFlagAggregate | total);
-            excl = chunk_lookback<SWEEP>(a, tbl, chunk, lane);
+            excl = chunk_lookback<SWEEP, FUSED>(a, tbl, chunk, lane);
             if (lane == 0) store_status(&a.chunk_status[chunk], tag | kFlagInclusive | (excl + total));
         }
         if (lane == 0) {
@@ -691,14 +767,31 @@ __device__ __forceinline__ void scan_chunk(const LaunchArgs& a, const SweepTable
     __syncthreads();
     const uint32_t flagged = s_num_flagged;
     if (flagged == 0) return;  // uniform
-    if (tid == 0)
-        s_list_base = static_cast<uint32_t>(atomicAdd(reinterpret_cast<unsigned long long*>(&a.count_out[1]),
-                                                      static_cast<unsigned long long>(flagged)));
+    if (tid == 0) s_list_base = reserve_flagged(a, flagged);
     __syncthreads();
     for (uint32_t f = tid; f < flagged; f += kScanBlock) a.flagged_list[s_list_base + f] = s_flagged[f];
 }
 
 __global__ __launch_bounds__(kScanBlock) void scan_kernel(LaunchArgs a) { scan_chunk<false>(a, nullptr); }
+
+// Fused schedule: workgroups [0, num_tiles) stream the tiles (stream_kernel's
+// work, publishing epoch-tagged tile words), workgroups [num_tiles,
+// num_tiles + num_chunks) scan the chunks (scan_kernel's work, polling the
+// tile words of their chunk).  A chunk workgroup waits for stream workgroups,
+// which wait for nobody, and in its look-back for the aggregates of lower
+// chunk workgroups, which each publish once their own tile words are in.  The
+// host takes this schedule only while the chunk workgroups fill at most half
+// of the workgroups the device holds at once, so the stream workgroups and
+// the lower chunk workgroups always find room, in whatever order the hardware
+// dispatches the grid.
+template <int VEC, int ROWS>
+__global__ __launch_bounds__(kStreamBlock) void stream_scan_kernel(LaunchArgs a) {
+    static_assert(kStreamBlock == kScanBlock, "one workgroup size for both parts");
+    if (blockIdx.x < a.num_tiles)
+        stream_tile<VEC, ROWS, false, true>(a, nullptr);
+    else
+        scan_chunk<false, true>(a, nullptr);
+}
 
 __global__ __launch_bounds__(kScanBlock) void scan_sweep_kernel(LaunchArgs a, SweepTable tbl) {
     scan_chunk<true>(a, &tbl);
@@ -903,7 +996,7 @@ __device__ __forceinline__ void move_pieces(const LaunchArgs& a, const SweepTabl
     // both counts in one load: the flagged-tile count must not wait for k
     const longlong2 counts = *reinterpret_cast<const longlong2*>(a.count_out);
     const int64_t k = counts.x;
-    const uint32_t flagged = static_cast<uint32_t>(counts.y);
+    const uint32_t flagged = flagged_count(a, counts.y);
     // What goes to the host (the counts; in a sweep also each segment's
     // count and squared norm) is stored after this workgroup's pieces: a
     // store to mapped host memory takes a bus round trip, and a wait for any
@@ -931,7 +1024,7 @@ __device__ __forceinline__ void move_pieces(const LaunchArgs& a, const SweepTabl
     if (k != 0) move_work<VEC, SWEEP>(a, tbl, k, flagged, first_t0, first_t1);
     if (blockIdx.x == 0 && tid == 0) {  // the scan kernel has finished both counts
         a.host_count[0] = k;
-        a.host_count[1] = counts.y;
+        a.host_count[1] = flagged;
     }
     if constexpr (SWEEP) {
         if (blockIdx.x == 0 && tid < static_cast<int>(tbl->count)) a.host_count[2 + tid] = seg_k;
@@ -1064,6 +1157,23 @@ hipError_t launch_staged(const LaunchArgs& args, bool vec4, hipStream_t stream) 
         hipLaunchKernelGGL(move_kernel<1>, grid_move, dim3(kMoveBlock), 0, stream, args);
     }
     return hipGetLastError();
+}
+
+hipError_t launch_fused(const LaunchArgs& args, bool vec4, hipStream_t stream) {
+    const dim3 grid_fused(args.num_tiles + args.num_chunks), grid_move(args.move_blocks);
+    if (vec4) {
+        hipLaunchKernelGGL((stream_scan_kernel<4, 1>), grid_fused, dim3(kStreamBlock), 0, stream, args);
+        hipLaunchKernelGGL(move_kernel<4>, grid_move, dim3(kMoveBlock), 0, stream, args);
+    } else {
+        hipLaunchKernelGGL((stream_scan_kernel<1, 4>), grid_fused, dim3(kStreamBlock), 0, stream, args);
+        hipLaunchKernelGGL(move_kernel<1>, grid_move, dim3(kMoveBlock), 0, stream, args);
+    }
+    return hipGetLastError();
+}
+
+hipError_t fused_blocks_per_cu(bool vec4, int* blocks) {
+    return vec4 ? hipOccupancyMaxActiveBlocksPerMultiprocessor(blocks, stream_scan_kernel<4, 1>, kStreamBlock, 0)
+                : hipOccupancyMaxActiveBlocksPerMultiprocessor(blocks, stream_scan_kernel<1, 4>, kStreamBlock, 0);
 }
 
 hipError_t launch_sweep(const LaunchArgs& args, const SweepTable& table, bool vec4, hipStream_t stream) {

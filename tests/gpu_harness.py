@@ -51,14 +51,15 @@ class ParityRun:
     of one workload and checks each step."""
 
     def __init__(self, w, density, device="cuda", rule_kind=oracle.PROPORTIONAL,
-                 variant=micro.MICRO_VARIANT_AUTO):
+                 variant=micro.MICRO_VARIANT_AUTO, separate_scan=False):
         self.w = w
         self.d = density
         self.N = w.n_total
         self.dev = torch.device(device)
         self.sp = micro.Sparsifier(self.N, device=self.dev,
                                    rule=micro.MICRO_RULE_PROPORTIONAL if rule_kind == oracle.PROPORTIONAL
-                                   else micro.MICRO_RULE_FIXED_STEP, variant=variant)
+                                   else micro.MICRO_RULE_FIXED_STEP, variant=variant,
+                                   separate_scan=separate_scan)
         self.rule = oracle.make_rule(rule_kind)
         self.res_dev = torch.zeros(self.N, dtype=torch.float32, device=self.dev)
         self.g_dev = torch.empty(self.N, dtype=torch.float32, device=self.dev)

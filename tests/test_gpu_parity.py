@@ -18,11 +18,16 @@ pytestmark = pytest.mark.gpu
 
 DEV = "cuda"
 STAGED, TICKET = micro.MICRO_VARIANT_STAGED, micro.MICRO_VARIANT_TICKET
-VARIANTS = pytest.mark.parametrize("variant", [STAGED, TICKET], ids=["staged", "ticket"])
+# the staged schedule with its scan pass launched on its own
+# (MICRO_FLAG_SEPARATE_SCAN); plain STAGED fuses it into the streaming launch
+SEPARATE = -STAGED
+VARIANTS = pytest.mark.parametrize("variant", [STAGED, SEPARATE, TICKET], ids=["staged", "separate", "ticket"])
 
 
-def make_sparsifier(n, variant):
-    return micro.Sparsifier(n, device=DEV, variant=variant)
+def make_sparsifier(n, variant, **kw):
+    if variant == SEPARATE:
+        return micro.Sparsifier(n, device=DEV, variant=STAGED, separate_scan=True, **kw)
+    return micro.Sparsifier(n, device=DEV, variant=variant, **kw)
 
 
 @pytest.mark.parametrize("name,density,steps,variant", [
@@ -30,12 +35,14 @@ def make_sparsifier(n, variant):
     ("toy", 0.01, 20, TICKET),
     ("resnet18", 0.01, 100, STAGED),
     ("resnet50", 0.001, 100, STAGED),
+    ("resnet50", 0.001, 30, SEPARATE),
     ("bert_large", 0.01, 50, STAGED),
+    ("bert_large", 0.01, 20, SEPARATE),
     ("bert_large", 0.01, 10, TICKET),
 ])
 def test_workload_parity(name, density, steps, variant):
     note(f"parity {name} d={density} steps={steps} variant={variant}")
-    run = ParityRun(synth.get(name), density, DEV, variant=variant)
+    run = ParityRun(synth.get(name), density, DEV, variant=abs(variant), separate_scan=variant == SEPARATE)
     try:
         run.run(steps)
     finally:
@@ -180,7 +187,7 @@ def test_dense_tiles_redone_by_move_kernel_mixed_with_staged_ones(phase_shift):
     g_dev = torch.from_numpy(g).to(DEV)
     r_dev = torch.zeros(N, dtype=torch.float32, device=DEV)
     sp.step(g_dev, r_dev, 0, 1, 0.01, 3.0)
-    _, redone, variant = sp.last_stats()
+    _, redone, variant, _ = sp.last_stats()
     assert variant == STAGED and redone > 300
     sp.close()
 
@@ -266,6 +273,47 @@ def test_fixed_step_rule_matches_oracle():
         run.run(6, verbose=False)
     finally:
         run.close()
+
+
+def test_fused_and_separate_scans_on_one_context():
+    """STAGED steps run the streaming and scan passes as one launch (stats
+    fused = 1) unless MICRO_FLAG_SEPARATE_SCAN asks for two (fused = 0); both
+    give the oracle's bits.  A multi-chunk partition with a dense region (its
+    tiles overflow their staging slots) is stepped many times on one context,
+    with sweeps (always separate launches) in between: the epoch-tagged
+    flagged-tile counter is never cleared between launches, so a stale count
+    would misplace pairs or redo the wrong tiles."""
+    N = 9_000_011  # about nine scan chunks
+    rng = np.random.default_rng(77)
+    for sep in (False, True):
+        note(f"fused/separate N={N} separate={sep}")
+        sp = make_sparsifier(N, SEPARATE if sep else STAGED)
+        r_dev = torch.zeros(N, dtype=torch.float32, device=DEV)
+        r_host = np.zeros(N, np.float32)
+        theta, thetas, redone = 2.0, [2.0, 2.0, 2.0], 0
+        for t in range(8):
+            g = rng.standard_normal(N).astype(np.float32)
+            if t % 3 != 2:
+                g[6_000_000:6_400_000] *= 40.0  # dense: every tile there overflows
+            g_dev = torch.from_numpy(g).to(DEV)
+            if t % 4 == 3:
+                k, th, _, idx, val = sp.sweep(g_dev, r_dev, 3, 0.01, thetas)
+                o_idx, o_val, k_or, th_or, _ = oracle.sweep(g, r_host, 3, 0.01, thetas)
+                assert (k, th) == (list(k_or), list(th_or)), t
+                thetas = th
+            else:
+                k, th, idx, val = sp.step(g_dev, r_dev, 1, 2, 0.01, theta)
+                o_idx, o_val, k_or, th_or = oracle.step(g, r_host, 1, 2, 0.01, theta)
+                assert (k, th) == (k_or, th_or), t
+                _, redo, variant, fused = sp.last_stats()
+                assert variant == STAGED and fused == (0 if sep else 1), t
+                redone += redo
+                theta = th
+            assert np.array_equal(idx.cpu().numpy(), o_idx), t
+            assert first_mismatch(val.cpu().numpy(), o_val) < 0, t
+            assert first_mismatch(r_dev.cpu().numpy(), r_host) < 0, t
+        assert redone > 0
+        sp.close()
 
 
 def test_auto_schedule_picks_by_partition_length():
