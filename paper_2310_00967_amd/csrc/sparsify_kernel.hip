@@ -76,10 +76,60 @@ __device__ __forceinline__ uint32_t lanes_below(uint64_t mask) {
                                      __builtin_amdgcn_mbcnt_lo(static_cast<uint32_t>(mask), 0u));
 }
 
+// Cross-lane steps on the data-parallel-primitive (DPP) paths of gfx9: row
+// shifts inside rows of 16 lanes, then broadcasts of lane 15 and lane 31 to
+// the following rows.  A lane whose source lies outside its row, or a row the
+// mask leaves out, receives 0, the identity of both operations used here.
+// Every lane of the wavefront must be active.
+constexpr int kDppRowShr1 = 0x111, kDppRowShr2 = 0x112, kDppRowShr4 = 0x114, kDppRowShr8 = 0x118;
+constexpr int kDppRowBcast15 = 0x142, kDppRowBcast31 = 0x143, kDppWaveShr1 = 0x138;
+
+__device__ __forceinline__ uint32_t dpp(uint32_t x, int ctrl) {
+    switch (ctrl) {  // the control must be a constant of the instruction
+        case kDppRowShr1: return __builtin_amdgcn_update_dpp(0u, x, kDppRowShr1, 0xf, 0xf, false);
+        case kDppRowShr2: return __builtin_amdgcn_update_dpp(0u, x, kDppRowShr2, 0xf, 0xf, false);
+        case kDppRowShr4: return __builtin_amdgcn_update_dpp(0u, x, kDppRowShr4, 0xf, 0xf, false);
+        case kDppRowShr8: return __builtin_amdgcn_update_dpp(0u, x, kDppRowShr8, 0xf, 0xf, false);
+        case kDppRowBcast15: return __builtin_amdgcn_update_dpp(0u, x, kDppRowBcast15, 0xa, 0xf, false);
+        case kDppRowBcast31: return __builtin_amdgcn_update_dpp(0u, x, kDppRowBcast31, 0xc, 0xf, false);
+        default: return __builtin_amdgcn_update_dpp(0u, x, kDppWaveShr1, 0xf, 0xf, false);
+    }
+}
+
+// Inclusive sum / maximum over lanes 0 .. lane of the wavefront.
+__device__ __forceinline__ uint32_t wave_inclusive_sum(uint32_t x) {
+    x += dpp(x, kDppRowShr1);
+    x += dpp(x, kDppRowShr2);
+    x += dpp(x, kDppRowShr4);
+    x += dpp(x, kDppRowShr8);
+    x += dpp(x, kDppRowBcast15);
+    x += dpp(x, kDppRowBcast31);
+    return x;
+}
+
+__device__ __forceinline__ uint32_t wave_inclusive_max(uint32_t x) {
+    uint32_t y;
+    y = dpp(x, kDppRowShr1);
+    x = y > x ? y : x;
+    y = dpp(x, kDppRowShr2);
+    x = y > x ? y : x;
+    y = dpp(x, kDppRowShr4);
+    x = y > x ? y : x;
+    y = dpp(x, kDppRowShr8);
+    x = y > x ? y : x;
+    y = dpp(x, kDppRowBcast15);
+    x = y > x ? y : x;
+    y = dpp(x, kDppRowBcast31);
+    x = y > x ? y : x;
+    return x;
+}
+
+// The value of the lane below (0 in lane 0).
+__device__ __forceinline__ uint32_t wave_shift_up1(uint32_t x) { return dpp(x, kDppWaveShr1); }
+
+// Sum over the wavefront, in every lane.
 __device__ __forceinline__ uint32_t wave_sum(uint32_t v) {
-#pragma unroll
-    for (int off = 32; off > 0; off >>= 1) v += __shfl_xor(v, off, kWaveSize);
-    return v;
+    return __builtin_amdgcn_readlane(wave_inclusive_sum(v), kWaveSize - 1);
 }
 
 __device__ __forceinline__ uint64_t load_status(const uint64_t* p) {
@@ -705,12 +755,7 @@ __device__ __forceinline__ void scan_chunk(const LaunchArgs& a, const SweepTable
     uint32_t mine = 0;
 #pragma unroll
     for (int i = 0; i < PER_THREAD; ++i) mine += raw[i] & ~kOverflow;
-    uint32_t x = mine;  // inclusive scan of thread totals inside the wavefront
-#pragma unroll
-    for (int off = 1; off < kWaveSize; off <<= 1) {
-        const uint32_t y = __shfl_up(x, off, kWaveSize);
-        if (lane >= off) x += y;
-    }
+    const uint32_t x = wave_inclusive_sum(mine);  // inclusive scan of thread totals inside the wavefront
     if (lane == kWaveSize - 1) s_wave_total[wave] = x;
     __syncthreads();
     uint32_t before = 0, total = 0;
@@ -825,14 +870,8 @@ __device__ __forceinline__ void block_max_scan(uint16_t* v, int tid, uint32_t* s
         m = e1 > m ? e1 : m;
         w[i] = r0 | (m << 16);
     }
-    uint32_t incl = m;  // inclusive maximum over the threads of the wavefront
-#pragma unroll
-    for (int off = 1; off < kWaveSize; off <<= 1) {
-        const uint32_t y = __shfl_up(incl, off, kWaveSize);
-        if (lane >= off) incl = y > incl ? y : incl;
-    }
-    uint32_t before = __shfl_up(incl, 1, kWaveSize);
-    if (lane == 0) before = 0;
+    const uint32_t incl = wave_inclusive_max(m);  // over the threads of the wavefront
+    uint32_t before = wave_shift_up1(incl);
     if (lane == kWaveSize - 1) s_wave_max[wave] = incl;
     __syncthreads();
     for (int k = 0; k < wave; ++k) before = s_wave_max[k] > before ? s_wave_max[k] : before;
