@@ -165,6 +165,7 @@ class Run:
         self.log = []   # (rank, P, k, kernel_ms, tiles redone by the move kernel)
         self.records = [] if keep_records else None  # one dict per call for --steps-jsonl
         self.variant = None  # schedule of the last step
+        self.fused = False   # whether its stream and scan passes ran as one launch
 
     def step(self, timed):
         g = self.pool[self.t % len(self.pool)]
@@ -180,6 +181,7 @@ class Run:
             kernel_ms, redone, variant, fused = self.sp.last_stats()
             self.log.append((p, ln, k, kernel_ms if timed else None, redone))
             self.variant = variant
+            self.fused = bool(fused)
             if self.records is None:
                 continue
             alg = 12 * ln + 8 * k
@@ -233,6 +235,7 @@ def measure(w, density, pool, sp, micro, warmup, steps, cycle=False, jsonl=None)
         "theta_final": run.theta,
         "ms_per_step": elapsed * 1e3 / steps,
         "variant": run.variant,
+        "fused": run.fused,
     }
 
 
@@ -643,8 +646,9 @@ def main():
             "unit": "GB/s",
             "frac": main_res["kernel_gbs"] / HBM_PEAK_GBS,
             "traffic": traffic,
-            "kernel": ("stream_kernel + scan_kernel + move_kernel (one step, event-timed together)"
-                       if main_res["variant"] == micro.MICRO_VARIANT_STAGED else "ticket_kernel"),
+            "kernel": ("ticket_kernel" if main_res["variant"] != micro.MICRO_VARIANT_STAGED else
+                       "stream_scan_kernel + move_kernel (one step, event-timed together)" if main_res["fused"] else
+                       "stream_kernel + scan_kernel + move_kernel (one step, event-timed together)"),
             "kernel_ms_avg": main_res["kernel_ms_avg"],
             "alg_bytes_per_launch": main_res["alg_bytes_per_launch"],
             "redone_tiles_timed": main_res["redone_tiles"],

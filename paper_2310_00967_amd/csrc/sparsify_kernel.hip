@@ -632,6 +632,40 @@ __device__ __forceinline__ void poll_tiles(const LaunchArgs& a, const uint32_t (
     }
 }
 
+// poll_tiles for wavefront 0 of a fused chunk workgroup, which also reloads
+// the look-back's first window of chunk status words (lane l: chunk - 1 - l;
+// before chunk 0 an inclusive zero) in every round, until no lane of the
+// wavefront waits for a tile.  Returns the lane's word of the last round: by
+// the time a chunk's last tile is in, the chunk before it has usually
+// published, so the look-back often needs no round trip of its own.
+template <int N>
+__device__ __forceinline__ uint64_t poll_tiles_and_window(const LaunchArgs& a, const uint32_t (&t)[N], uint32_t end,
+                                                          uint32_t (&raw)[N], uint32_t chunk, int lane) {
+    const int64_t p = static_cast<int64_t>(chunk) - 1 - lane;
+    const uint64_t before_first = (static_cast<uint64_t>(a.epoch) << kEpochShift) | kFlagInclusive;
+    uint32_t pending = 0;
+#pragma unroll
+    for (int i = 0; i < N; ++i) {
+        raw[i] = 0;
+        if (t[i] < end) pending |= 1u << i;
+    }
+    for (;;) {  // uniform across the wavefront
+        uint64_t w[N];
+#pragma unroll
+        for (int i = 0; i < N; ++i) w[i] = (pending >> i) & 1u ? load_status(&a.tile_words[t[i]]) : 0ull;
+        const uint64_t win = p >= 0 ? load_status(&a.chunk_status[p]) : before_first;
+#pragma unroll
+        for (int i = 0; i < N; ++i) {
+            if (((pending >> i) & 1u) && (w[i] >> kEpochShift) == a.epoch && (w[i] & kFlagMask) != 0) {
+                raw[i] = static_cast<uint32_t>(w[i] & kCountMask);
+                pending &= ~(1u << i);
+            }
+        }
+        if (__ballot(pending != 0) == 0) return win;
+        __builtin_amdgcn_s_sleep(2);
+    }
+}
+
 // Selected values of chunk `chunk`, summed from its tile counts by one
 // wavefront (uniform): the count the chunk's own workgroup publishes.
 template <bool SWEEP>
@@ -662,15 +696,21 @@ constexpr int kLookbackPolls = 4;  // polls of a silent predecessor before its c
 // as soon as its tile words are in, before its own look-back, so the wait
 // depends on stream workgroups only).
 template <bool SWEEP, bool FUSED = false>
-__device__ uint32_t chunk_lookback(const LaunchArgs& a, const SweepTable* tbl, uint32_t chunk, int lane) {
+// In the fused schedule `first` is the lane's word of the first window, read
+// while the chunk's tile words were polled (an older observation of the same
+// word, which the look-back treats like any other poll).
+__device__ uint32_t chunk_lookback(const LaunchArgs& a, const SweepTable* tbl, uint32_t chunk, int lane,
+                                   uint64_t first = 0) {
     const uint64_t tag = static_cast<uint64_t>(a.epoch) << kEpochShift;
     uint32_t exclusive = 0;
     int64_t top = static_cast<int64_t>(chunk) - 1;
     int polls = 0;
+    bool have_first = FUSED;
     for (;;) {
         const int64_t p = top - lane;
         // positions before chunk 0 read as an inclusive prefix of zero
-        const uint64_t w = (p >= 0) ? load_status(&a.chunk_status[p]) : (tag | kFlagInclusive);
+        const uint64_t w = have_first ? first : (p >= 0) ? load_status(&a.chunk_status[p]) : (tag | kFlagInclusive);
+        have_first = false;
         const bool valid = (w >> kEpochShift) == a.epoch && (w & kFlagMask) != 0;
         const bool inclusive = valid && (w & kFlagMask) == kFlagInclusive;
         const uint64_t inc_mask = __ballot(inclusive);
@@ -726,11 +766,15 @@ __device__ __forceinline__ void scan_chunk(const LaunchArgs& a, const SweepTable
     const bool whole = first_tile % 4 == 0 && first_tile + PER_THREAD <= end_tile;
 
     uint32_t raw[PER_THREAD];
+    uint64_t window = 0;  // fused schedule, wave 0: the look-back's first window of status words
     if constexpr (FUSED) {
         uint32_t t[PER_THREAD];
 #pragma unroll
         for (int i = 0; i < PER_THREAD; ++i) t[i] = first_tile + i;
-        poll_tiles<PER_THREAD>(a, t, end_tile, raw);
+        if (wave == 0)
+            window = poll_tiles_and_window<PER_THREAD>(a, t, end_tile, raw, chunk, lane);
+        else
+            poll_tiles<PER_THREAD>(a, t, end_tile, raw);
     } else if (whole) {
 #pragma unroll
         for (int i = 0; i < PER_THREAD; i += 4) {
@@ -771,7 +815,7 @@ __device__ __forceinline__ void scan_chunk(const LaunchArgs& a, const SweepTable
             if (lane == 0) store_status(&a.chunk_status[0], tag | kFlagInclusive | total);
         } else {
             if (lane == 0) store_status(&a.chunk_status[chunk], tag | kFlagAggregate | total);
-            excl = chunk_lookback<SWEEP, FUSED>(a, tbl, chunk, lane);
+            excl = chunk_lookback<SWEEP, FUSED>(a, tbl, chunk, lane, window);
             if (lane == 0) store_status(&a.chunk_status[chunk], tag | kFlagInclusive | (excl + total));
         }
         if (lane == 0) {
