@@ -38,6 +38,7 @@ HBM_PEAK_GBS = 8000.0
 KERNEL_SRC = os.path.join(ROOT, "paper_2310_00967_amd", "csrc", "sparsify_kernel.hip")
 KERNEL_HDR = os.path.join(ROOT, "paper_2310_00967_amd", "csrc", "sparsify_kernel.h")
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "sparsify_kernel_gpt_1p3b_traffic.txt")
+TRAFFIC_FILE_BERT = os.path.join(ROOT, "profiles", "sparsify_kernel_bert_large_rank3_traffic.txt")
 
 
 def parse_args():
@@ -101,13 +102,15 @@ def kernel_sha256(text=None):
     return hashlib.sha256("\n".join(code).encode()).hexdigest()
 
 
-def read_traffic():
-    """HBM bytes per launch from the committed rocprofv3 counter summary, or
-    None when absent or taken on a different kernel source."""
-    if not os.path.exists(TRAFFIC_FILE):
+def read_traffic(path=None):
+    """HBM bytes per launch from a committed rocprofv3 counter summary (the
+    GPT-1.3B one by default), or None when absent or taken on a different
+    kernel source."""
+    path = path or TRAFFIC_FILE
+    if not os.path.exists(path):
         return None
     fields = {}
-    for line in open(TRAFFIC_FILE):
+    for line in open(path):
         if ":" in line:
             key, val = line.split(":", 1)
             fields[key.strip()] = val.strip()
@@ -316,6 +319,7 @@ def measure_ef(w, density, pool, sp, warmup, steps, local_error=False):
         k, theta = out[0], out[1]
         if t >= warmup:
             log.append((N, k, sp.last_stats()[0]))
+    fused = bool(sp.last_stats()[3])
     torch.cuda.synchronize()
     elapsed = time.perf_counter() - t0
     alg = sum(12 * n + 8 * k for n, k, _ in log)
@@ -323,7 +327,7 @@ def measure_ef(w, density, pool, sp, warmup, steps, local_error=False):
     return {"g_elem_s": sum(n for n, _, _ in log) / elapsed / 1e9, "wall_gbs": alg / elapsed / 1e9,
             "kernel_gbs": alg / kernel_s / 1e9, "kernel_ms_avg": kernel_s * 1e3 / len(log),
             "alg_bytes_per_launch": alg / len(log), "ms_per_step": elapsed * 1e3 / steps,
-            "k_avg": sum(k for _, k, _ in log) / len(log), "worker": worker}
+            "k_avg": sum(k for _, k, _ in log) / len(log), "worker": worker, "fused": fused}
 
 
 def measure_sweep(w, density, pool, sp, warmup, steps):
@@ -538,6 +542,8 @@ def main_path(args, w, head, pool, n_pool, sp):
                              "kernel": ("stream_sweep_kernel + scan_sweep_kernel + move_sweep_kernel over three "
                                         "segments (one pass with the local error, event-timed together)"
                                         if args.local_error else
+                                        "accumulate_kernel + stream_scan_kernel + move_kernel "
+                                        "(one pass, event-timed together)" if r["fused"] else
                                         "accumulate_kernel + stream_kernel + scan_kernel + move_kernel "
                                         "(one pass, event-timed together)"),
                              "kernel_ms_avg": r["kernel_ms_avg"], "alg_bytes_per_launch": r["alg_bytes_per_launch"]},
@@ -606,7 +612,9 @@ def main():
     cpu = cpu_baseline(w, head, pool, args.cpu_seconds, args.cycle) if args.cpu_seconds > 0 else None
     sp.close()
 
-    traffic = read_traffic() if args.workload == "gpt_1p3b" and head == 0.01 else None
+    traffic_file = {"gpt_1p3b": TRAFFIC_FILE, "bert_large": TRAFFIC_FILE_BERT}.get(args.workload)
+    traffic = (read_traffic(traffic_file) if traffic_file and head == 0.01 and not args.cycle
+               and not args.separate_scan and args.variant == "auto" else None)
     parts = sorted({ln for (_, ln) in (micro.micro_partition(w.n_total, p, w.world)
                                        for p in (range(w.world) if args.cycle else w.ranks))})
     line = {

@@ -62,14 +62,15 @@ def test_traffic_is_reported_only_for_the_kernel_it_was_measured_on(tmp_path, mo
     assert bench.read_traffic() is None
 
 
-def test_committed_traffic_summary_names_a_hash_and_a_byte_count():
+@pytest.mark.parametrize("path,values", [("TRAFFIC_FILE", 1_315_723_264), ("TRAFFIC_FILE_BERT", 41_892_736)])
+def test_committed_traffic_summaries_name_a_hash_and_a_byte_count(path, values):
     fields = {}
-    for line in open(bench.TRAFFIC_FILE):
+    for line in open(getattr(bench, path)):
         if ":" in line and not line.startswith("#"):
             key, val = line.split(":", 1)
             fields[key.strip()] = val.strip()
     assert len(fields["kernel_source_sha256"]) == 64
-    assert float(fields["hbm_bytes_per_launch"]) > 12 * 1_315_723_264  # at least the algorithmic bytes
+    assert float(fields["hbm_bytes_per_launch"]) > 12 * values  # at least the algorithmic bytes
 
 
 @pytest.mark.parametrize("n", ["2", "8"])
