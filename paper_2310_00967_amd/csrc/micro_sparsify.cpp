@@ -196,15 +196,22 @@ uint32_t move_grid(int64_t tiles, int64_t len, int64_t span, int64_t min_blocks)
 
 // Items per move piece.  The merged sequence holds one item per tile and one
 // per selected value, about tiles + density * values of them.  A long
-// sequence takes kMoveSpan-item pieces (a short loop per workgroup); one of
-// fewer than two such pieces per compute unit takes kMoveSpanSmall-item
-// pieces, which put twice as many workgroups to work.  Measured: BERT-large
-// rank 3 (41.9M values, d = 0.01) 112 pieces of 4096 items or 225 of 2048,
-// 98.9 against 96.6 us per step; the GPT-1.3B partition's move kernel
-// 53 us with 4096-item pieces, 78 us with 2048.
+// sequence (at least two kMoveSpan-item pieces per compute unit) takes
+// kMoveSpan-item pieces, a short loop per workgroup; a shorter one, whose
+// step is bound by the move kernel's round trips rather than its bytes,
+// takes smaller pieces, which put more workgroups to work and give each
+// less to copy after its last load: kMoveSpanSmall down to one such piece
+// per compute unit, kMoveSpanTiny below.  Measured (five runs each, same
+// box): BERT-large rank 3 (41.9M values, d = 0.01, about 460,000 items)
+// 70.6%, 71.4% and 71.2% of 8 TB/s with 2048-, 1024- and 512-item pieces;
+// ResNet-50 rank 0 (3.2M values, d = 0.001, about 6,300 items) 26.5%, 27.0%
+// and 27.3%; the GPT-1.3B partition's move kernel took 53 us with 4096-item
+// pieces and 78 us with 2048 (an earlier build of the kernel).
 uint32_t move_span_for(const micro_ctx* ctx, int64_t tiles, double expected_pairs) {
     const double items = static_cast<double>(tiles) + expected_pairs;
-    return items < 2.0 * ctx->compute_units * micro::kMoveSpan ? micro::kMoveSpanSmall : micro::kMoveSpan;
+    if (items >= 2.0 * ctx->compute_units * micro::kMoveSpan) return micro::kMoveSpan;
+    if (items >= 1.0 * ctx->compute_units * micro::kMoveSpanSmall) return micro::kMoveSpanSmall;
+    return micro::kMoveSpanTiny;
 }
 
 bool misaligned4(std::initializer_list<const void*> ptrs) {
@@ -695,7 +702,7 @@ micro_status micro_sparsify_init(micro_ctx** out, int64_t n_total, void* hip_str
         ctx->chunk_capacity = ctx->tile_capacity / micro::kChunkTiles + 2 + micro::kMaxSweep;
         // every piece, and one word past the largest move grid (each
         // workgroup reads its first piece's two words before it knows k)
-        ctx->split_capacity = (ctx->tile_capacity + n_total) / micro::kMoveSpanSmall + 2;
+        ctx->split_capacity = (ctx->tile_capacity + n_total) / micro::kMoveSpanTiny + 2;
         if (ctx->split_capacity < micro::kMoveGrid + 1) ctx->split_capacity = micro::kMoveGrid + 1;
         const size_t stage = static_cast<size_t>(ctx->tile_capacity) * micro::kStageCap;
         ok = hipMalloc(&ctx->d_tile_counts, sizeof(uint32_t) * ctx->tile_capacity) == hipSuccess &&

@@ -11,7 +11,7 @@ namespace micro {
 // pairs per tile, tiles per scan chunk (one 256-thread workgroup), items per
 // move piece.  The move kernel walks the merged sequence of tiles and output
 // pairs (each tile is one item, followed by one item per selected value of
-// the tile) in pieces of move_span items (kMoveSpan, or kMoveSpanSmall for a
+// the tile) in pieces of move_span items (kMoveSpan, or kMoveSpanSmall / kMoveSpanTiny for a
 // short sequence), so a piece holds at most kMoveSpan pairs and touches at
 // most kMoveSpan + 1 tiles.
 constexpr int kStreamTile = 1024;
@@ -20,10 +20,12 @@ constexpr uint32_t kStageCap = 256;
 constexpr int kChunkTiles = 1024;
 constexpr int kScanBlock = 256;
 constexpr int kMoveSpan = 4096;        // largest move piece (LDS arrays are sized for it)
-constexpr int kMoveSpanSmall = 2048;   // move piece of a short merged sequence
+constexpr int kMoveSpanSmall = 1024;   // move piece of a short merged sequence
+constexpr int kMoveSpanTiny = 512;     // move piece of a very short one
 constexpr int kMoveBlock = 256;
 constexpr uint32_t kMoveGrid = 2048;  // largest move grid (eight workgroups per compute unit)
-static_assert((kMoveSpan & (kMoveSpan - 1)) == 0 && (kMoveSpanSmall & (kMoveSpanSmall - 1)) == 0,
+static_assert((kMoveSpan & (kMoveSpan - 1)) == 0 && (kMoveSpanSmall & (kMoveSpanSmall - 1)) == 0 &&
+                  (kMoveSpanTiny & (kMoveSpanTiny - 1)) == 0 && kMoveSpanTiny <= kMoveSpanSmall,
               "piece sizes are powers of two: the kernels divide by them with shifts");
 // Ticket schedule: values per tile (256 threads, four dwordx4 per lane).
 constexpr int kTicketTile = 4096;
@@ -85,7 +87,7 @@ struct LaunchArgs {
     double* chunk_sumsq;    // sweep: per chunk, the sum of its tiles' squared norms
     double* host_sumsq;     // sweep: mapped host memory, one squared norm per segment
     uint32_t move_blocks;   // workgroups of the move kernel
-    uint32_t move_span;     // items per move piece: kMoveSpan or kMoveSpanSmall (a power of two)
+    uint32_t move_span;     // items per move piece: kMoveSpan, kMoveSpanSmall or kMoveSpanTiny (a power of two)
     uint2* stage;           // num_tiles * kStageCap staged (index, value bits) pairs
     uint32_t num_chunks;    // ceil(num_tiles / kChunkTiles)
     uint64_t* chunk_status;             // >= num_chunks look-back words

@@ -831,14 +831,16 @@ __device__ __forceinline__ void scan_chunk(const LaunchArgs& a, const SweepTable
     for (int i = 0; i < PER_THREAD; ++i) {
         const uint32_t count = raw[i] & ~kOverflow;
         offs[i] = pos | (raw[i] & kOverflow);
-        // The move piece whose first item falls among this tile's items: the
+        // The move pieces whose first item falls among this tile's items: the
         // tile's own item sits at tile + pos in the merged sequence and its
-        // count pairs follow it; count <= kStreamTile < piece size, so there
-        // is at most one.
+        // count pairs follow it.  A tile spans up to kStreamTile + 1 items,
+        // so with pieces of kStreamTile items or fewer it can hold several
+        // pieces' first items (at most three with 512-item pieces).
         if (first_tile + i < end_tile) {
             const uint64_t item = static_cast<uint64_t>(first_tile + i) + pos;
-            const uint64_t m = (item + a.move_span - 1) >> span_shift;
-            if ((m << span_shift) < item + 1 + count) a.split_tile[m] = first_tile + i;
+            const uint64_t end_item = item + 1 + count;
+            for (uint64_t m = (item + a.move_span - 1) >> span_shift; (m << span_shift) < end_item; ++m)
+                a.split_tile[m] = first_tile + i;
         }
         if (raw[i] & kOverflow) s_flagged[atomicAdd(&s_num_flagged, 1u)] = first_tile + i;
         pos += count;
@@ -1050,7 +1052,7 @@ __device__ __forceinline__ void move_work(const LaunchArgs& a, const SweepTable*
 }
 
 // Move kernel: a fixed grid walks the merged sequence of tiles and output
-// pairs in pieces of move_span items (kMoveSpan, or kMoveSpanSmall where the
+// pairs in pieces of move_span items (kMoveSpan, or a smaller size where the
 // sequence is short: more, shorter pieces), so every piece costs about the same whatever the clustering of the
 // selection: many pairs from few tiles, or few pairs scattered over many
 // tiles.  Piece m's items lie in the tiles from split_tile[m] to

@@ -361,10 +361,10 @@ def test_count_swings_on_one_context():
 
 def test_move_piece_size_does_not_change_the_result():
     """The density steers only the threshold update and the move kernel's
-    piece size (2048 items for a short expected sequence, 4096 for a long
-    one; on 256 compute units d = 0.001 and d = 1 fall on either side for
-    this partition).  At the same threshold both must select, place and
-    reset the same bits, and match the oracle."""
+    piece size (512, 1024 or 4096 items by the expected sequence length; on
+    256 compute units d = 0.001, 0.1 and 1 give the three sizes for this
+    partition).  At the same threshold all must select, place and reset the
+    same bits, and match the oracle."""
     N = 3_000_017
     rng = np.random.default_rng(71)
     g = rng.standard_normal(N).astype(np.float32)
@@ -373,7 +373,7 @@ def test_move_piece_size_does_not_change_the_result():
     g_dev = torch.from_numpy(g).to(DEV)
     for theta in [2.5, 1.0]:
         outs = []
-        for density in [0.001, 1.0]:
+        for density in [0.001, 0.1, 1.0]:
             r_dev = torch.from_numpy(res0).to(DEV)
             k, th, idx, val = sp.step(g_dev, r_dev, 0, 1, density, theta)
             res = res0.copy()
@@ -382,9 +382,10 @@ def test_move_piece_size_does_not_change_the_result():
             outs.append((idx.cpu().numpy(), val.cpu().numpy(), r_dev.cpu().numpy()))
             assert np.array_equal(outs[-1][0], o_idx), (theta, density)
             assert first_mismatch(outs[-1][1], o_val) < 0, (theta, density)
-        assert np.array_equal(outs[0][0], outs[1][0]), theta
-        assert first_mismatch(outs[0][1], outs[1][1]) < 0, theta
-        assert first_mismatch(outs[0][2], outs[1][2]) < 0, theta
+        for other in outs[1:]:
+            assert np.array_equal(outs[0][0], other[0]), theta
+            assert first_mismatch(outs[0][1], other[1]) < 0, theta
+            assert first_mismatch(outs[0][2], other[2]) < 0, theta
         assert first_mismatch(outs[0][2], res) < 0, theta
     sp.close()
 
