@@ -68,6 +68,7 @@ constexpr uint64_t kCountMask = 0xffffffffull;
 constexpr uint64_t kFlagAggregate = 1ull << 32;
 constexpr uint64_t kFlagInclusive = 2ull << 32;
 constexpr uint64_t kFlagMask = 3ull << 32;
+constexpr int kLookbackDepth = 4;  // chunk status words per lane and chunk look-back round
 
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 
@@ -633,15 +634,16 @@ __device__ __forceinline__ void poll_tiles(const LaunchArgs& a, const uint32_t (
 }
 
 // poll_tiles for wavefront 0 of a fused chunk workgroup, which also reloads
-// the look-back's first window of chunk status words (lane l: chunk - 1 - l;
-// before chunk 0 an inclusive zero) in every round, until no lane of the
-// wavefront waits for a tile.  Returns the lane's word of the last round: by
-// the time a chunk's last tile is in, the chunk before it has usually
-// published, so the look-back often needs no round trip of its own.
+// the look-back's first window of chunk status words (lane l, slot j: chunk
+// - 1 - (l * kLookbackDepth + j); before chunk 0 an inclusive zero) in every
+// round, until no lane of the wavefront waits for a tile.  win receives the
+// lane's words of the last round: by the time a chunk's last tile is in, the
+// chunk before it has usually published, so the look-back often needs no
+// round trip of its own.
 template <int N>
-__device__ __forceinline__ uint64_t poll_tiles_and_window(const LaunchArgs& a, const uint32_t (&t)[N], uint32_t end,
-                                                          uint32_t (&raw)[N], uint32_t chunk, int lane) {
-    const int64_t p = static_cast<int64_t>(chunk) - 1 - lane;
+__device__ __forceinline__ void poll_tiles_and_window(const LaunchArgs& a, const uint32_t (&t)[N], uint32_t end,
+                                                      uint32_t (&raw)[N], uint32_t chunk, int lane,
+                                                      uint64_t (&win)[kLookbackDepth]) {
     const uint64_t before_first = (static_cast<uint64_t>(a.epoch) << kEpochShift) | kFlagInclusive;
     uint32_t pending = 0;
 #pragma unroll
@@ -653,7 +655,11 @@ __device__ __forceinline__ uint64_t poll_tiles_and_window(const LaunchArgs& a, c
         uint64_t w[N];
 #pragma unroll
         for (int i = 0; i < N; ++i) w[i] = (pending >> i) & 1u ? load_status(&a.tile_words[t[i]]) : 0ull;
-        const uint64_t win = p >= 0 ? load_status(&a.chunk_status[p]) : before_first;
+#pragma unroll
+        for (int j = 0; j < kLookbackDepth; ++j) {
+            const int64_t p = static_cast<int64_t>(chunk) - 1 - (lane * kLookbackDepth + j);
+            win[j] = p >= 0 ? load_status(&a.chunk_status[p]) : before_first;
+        }
 #pragma unroll
         for (int i = 0; i < N; ++i) {
             if (((pending >> i) & 1u) && (w[i] >> kEpochShift) == a.epoch && (w[i] & kFlagMask) != 0) {
@@ -661,7 +667,7 @@ __device__ __forceinline__ uint64_t poll_tiles_and_window(const LaunchArgs& a, c
                 pending &= ~(1u << i);
             }
         }
-        if (__ballot(pending != 0) == 0) return win;
+        if (__ballot(pending != 0) == 0) return;
         __builtin_amdgcn_s_sleep(2);
     }
 }
@@ -695,43 +701,71 @@ constexpr int kLookbackPolls = 4;  // polls of a silent predecessor before its c
 // each predecessor has published (a chunk workgroup publishes its aggregate
 // as soon as its tile words are in, before its own look-back, so the wait
 // depends on stream workgroups only).
+// Each round a lane reads kLookbackDepth words, so a round covers 256
+// predecessors (the GPT-1.3B partition's 1,285 chunks need at most six
+// rounds instead of twenty-one).  In the fused schedule `first` holds the
+// lane's words of the first window, read while the chunk's tile words were
+// polled (older observations of the same words, which the look-back treats
+// like any other poll).
 template <bool SWEEP, bool FUSED = false>
-// In the fused schedule `first` is the lane's word of the first window, read
-// while the chunk's tile words were polled (an older observation of the same
-// word, which the look-back treats like any other poll).
 __device__ uint32_t chunk_lookback(const LaunchArgs& a, const SweepTable* tbl, uint32_t chunk, int lane,
-                                   uint64_t first = 0) {
+                                   const uint64_t (&first)[kLookbackDepth]) {
+    constexpr int D = kLookbackDepth;
     const uint64_t tag = static_cast<uint64_t>(a.epoch) << kEpochShift;
     uint32_t exclusive = 0;
     int64_t top = static_cast<int64_t>(chunk) - 1;
     int polls = 0;
     bool have_first = FUSED;
     for (;;) {
-        const int64_t p = top - lane;
-        // positions before chunk 0 read as an inclusive prefix of zero
-        const uint64_t w = have_first ? first : (p >= 0) ? load_status(&a.chunk_status[p]) : (tag | kFlagInclusive);
+        // slot j of lane l holds predecessor top - (l * D + j): the window's
+        // nearest word is lane 0's slot 0; positions before chunk 0 read as
+        // an inclusive prefix of zero
+        uint64_t w[D];
+        uint32_t valid_bits = 0, incl_bits = 0;
+#pragma unroll
+        for (int j = 0; j < D; ++j) {
+            const int64_t p = top - (lane * D + j);
+            w[j] = have_first ? first[j] : (p >= 0) ? load_status(&a.chunk_status[p]) : (tag | kFlagInclusive);
+        }
         have_first = false;
-        const bool valid = (w >> kEpochShift) == a.epoch && (w & kFlagMask) != 0;
-        const bool inclusive = valid && (w & kFlagMask) == kFlagInclusive;
-        const uint64_t inc_mask = __ballot(inclusive);
-        // lanes 0 .. first inclusive lane (all 64 when none is inclusive)
-        const uint64_t need = inc_mask ? (inc_mask ^ (inc_mask - 1)) : ~0ull;
-        uint64_t missing = __ballot(!valid) & need;
+#pragma unroll
+        for (int j = 0; j < D; ++j) {
+            const bool valid = (w[j] >> kEpochShift) == a.epoch && (w[j] & kFlagMask) != 0;
+            valid_bits |= static_cast<uint32_t>(valid) << j;
+            incl_bits |= static_cast<uint32_t>(valid && (w[j] & kFlagMask) == kFlagInclusive) << j;
+        }
+        const uint64_t inc_lanes = __ballot(incl_bits != 0);
+        const int first_lane = inc_lanes ? __builtin_ctzll(inc_lanes) : kWaveSize;  // uniform
+        // the slots up to the nearest inclusive word (all of them when there is none)
+        const uint32_t need_bits = lane < first_lane    ? (1u << D) - 1u
+                                   : lane == first_lane ? (2u << __builtin_ctz(incl_bits)) - 1u
+                                                        : 0u;
+        const uint32_t miss_bits = need_bits & ~valid_bits;
+        const bool missing = __ballot(miss_bits != 0) != 0;  // uniform
         if (missing && (FUSED || ++polls < kLookbackPolls)) {
             __builtin_amdgcn_s_sleep(1);
             continue;
         }
         polls = 0;
-        uint32_t v = ((need >> lane) & 1ull) && valid ? static_cast<uint32_t>(w & kCountMask) : 0u;
-        while (missing) {  // uniform
-            const int l = __builtin_ctzll(missing);
-            missing &= missing - 1;
-            const uint32_t c = chunk_selected<SWEEP>(a, tbl, static_cast<uint32_t>(top - l), lane);
-            if (lane == l) v = c;
+        uint32_t v = 0;
+#pragma unroll
+        for (int j = 0; j < D; ++j)
+            if (((need_bits & valid_bits) >> j) & 1u) v += static_cast<uint32_t>(w[j] & kCountMask);
+        if (missing) {  // uniform: sum each missing predecessor from its tile counts
+#pragma unroll 1
+            for (int j = 0; j < D; ++j) {
+                uint64_t m = __ballot((miss_bits >> j) & 1u);
+                while (m) {
+                    const int l = __builtin_ctzll(m);
+                    m &= m - 1;
+                    const uint32_t c = chunk_selected<SWEEP>(a, tbl, static_cast<uint32_t>(top - (l * D + j)), lane);
+                    if (lane == l) v += c;
+                }
+            }
         }
         exclusive += wave_sum(v);
-        if (inc_mask) return exclusive;
-        top -= kWaveSize;
+        if (inc_lanes) return exclusive;
+        top -= kWaveSize * D;
     }
 }
 
@@ -766,13 +800,13 @@ __device__ __forceinline__ void scan_chunk(const LaunchArgs& a, const SweepTable
     const bool whole = first_tile % 4 == 0 && first_tile + PER_THREAD <= end_tile;
 
     uint32_t raw[PER_THREAD];
-    uint64_t window = 0;  // fused schedule, wave 0: the look-back's first window of status words
+    uint64_t window[kLookbackDepth] = {};  // fused schedule, wave 0: the look-back's first window
     if constexpr (FUSED) {
         uint32_t t[PER_THREAD];
 #pragma unroll
         for (int i = 0; i < PER_THREAD; ++i) t[i] = first_tile + i;
         if (wave == 0)
-            window = poll_tiles_and_window<PER_THREAD>(a, t, end_tile, raw, chunk, lane);
+            poll_tiles_and_window<PER_THREAD>(a, t, end_tile, raw, chunk, lane, window);
         else
             poll_tiles<PER_THREAD>(a, t, end_tile, raw);
     } else if (whole) {
