@@ -15,9 +15,9 @@
 //     row's offset inside the tile and the tile's count;
 //   * across workgroups: decoupled look-back over 64-bit status words
 //     (count | flag | epoch), one per tile (ticket schedule) or per chunk of
-//     tiles (staged schedule).  Wavefront 0 inspects 64 predecessors per
-//     round with agent-scope atomic loads, which read the memory level shared
-//     by all XCDs.  The count and its flag share one word, so relaxed atomics
+//     tiles (staged schedule).  Wavefront 0 inspects 64 predecessor tiles
+//     or 256 predecessor chunks per round with agent-scope atomic loads,
+//     which read the memory level shared by all XCDs.  The count and its flag share one word, so relaxed atomics
 //     suffice: a reader sees either the whole published word or an older one.
 //
 // Staged schedule, three kernels; no workgroup of the first and the last ever
@@ -40,10 +40,11 @@
 //     merged sequence of tiles and pairs, whatever the clustering of the
 //     selection; it also stores the counts into mapped host memory.
 //   stream_scan_kernel (fused staged schedule, the default of a single
-//     partition of up to a few hundred chunks): the stream and scan kernels'
-//     work in one launch, the chunk workgroups after the tile workgroups,
-//     polling epoch-tagged tile words; saves a launch and its drain between
-//     the streaming pass and the scan.
+//     partition of up to half as many chunks as the device holds resident
+//     workgroups, about a billion values on MI355X): the stream and scan
+//     kernels' work in one launch, the chunk workgroups after the tile
+//     workgroups, polling epoch-tagged tile words; saves a launch and its
+//     drain between the streaming pass and the scan.
 //   HBM traffic beyond the 12 bytes per value of the stream: 16 bytes per
 //   selected value (staged write and read) and 8 bytes per 1024 values.
 // Sweep: the same three kernels over a table of segments (every partition of
@@ -53,7 +54,7 @@
 // Ticket schedule: a single pass; 4096-value tiles are drawn from a ticket
 //   counter in increasing order, so a tile only waits for tiles claimed by
 //   running workgroups; the per-tile ticket and look-back round trips cost
-//   bandwidth, but one launch beats three for partitions of up to about a
+//   bandwidth, but one launch beats two for partitions of up to about a
 //   million values.
 // accumulate_kernel: the error-feedback addition alone, for the part of the
 //   vector a full pass does not search.
