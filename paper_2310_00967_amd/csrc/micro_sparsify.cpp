@@ -207,6 +207,14 @@ uint32_t move_grid(int64_t tiles, int64_t len, int64_t span, int64_t min_blocks)
 // ResNet-50 rank 0 (3.2M values, d = 0.001, about 6,300 items) 26.5%, 27.0%
 // and 27.3%; the GPT-1.3B partition's move kernel took 53 us with 4096-item
 // pieces and 78 us with 2048 (an earlier build of the kernel).
+// Largest partition, in scan chunks of a million values, that takes the fused
+// stream-and-scan launch.  Measured on MI355X (one GPT-shaped vector, d =
+// 0.01, fused against separate device time per step): 20 chunks -1.7 us, 40
+// -3.1, 79 -3.0, 157 -3.9, 314 +2.2, 628 +3.1 (and the GPT-1.3B partition,
+// 1,285 chunks, +18 us): past a few hundred chunk workgroups, their scan and
+// polling at the end of the launch cost more than the separate launch.
+constexpr int64_t kFusedMaxChunks = 256;
+
 uint32_t move_span_for(const micro_ctx* ctx, int64_t tiles, double expected_pairs) {
     const double items = static_cast<double>(tiles) + expected_pairs;
     if (items >= 2.0 * ctx->compute_units * micro::kMoveSpan) return micro::kMoveSpan;
@@ -718,12 +726,15 @@ micro_status micro_sparsify_init(micro_ctx** out, int64_t n_total, void* hip_str
     if (ok && ctx->has_staged) {
         // The fused schedule's chunk workgroups wait for stream workgroups of
         // the same launch: it is taken only while they fill at most half of
-        // the workgroups the device holds at once (both load widths).
+        // the workgroups the device holds at once (both load widths), and not
+        // beyond kFusedMaxChunks, where it stops paying.
         int b4 = 0, b1 = 0;
-        if (micro::fused_blocks_per_cu(true, &b4) == hipSuccess && micro::fused_blocks_per_cu(false, &b1) == hipSuccess)
-            ctx->fused_max_chunks = static_cast<int64_t>(b4 < b1 ? b4 : b1) * ctx->compute_units / 2;
-        else
+        if (micro::fused_blocks_per_cu(true, &b4) == hipSuccess && micro::fused_blocks_per_cu(false, &b1) == hipSuccess) {
+            const int64_t half = static_cast<int64_t>(b4 < b1 ? b4 : b1) * ctx->compute_units / 2;
+            ctx->fused_max_chunks = half < kFusedMaxChunks ? half : kFusedMaxChunks;
+        } else {
             (void)hipGetLastError();  // no fused schedule; the separate kernels remain
+        }
     }
     if (ok && ctx->has_ticket) {
         ctx->ticket_capacity = n_total / micro::kTicketTile + 2;

@@ -120,7 +120,8 @@ hipError_t launch_staged(const LaunchArgs& args, bool vec4, hipStream_t stream);
 // The staged schedule with its stream and scan kernels fused into one launch
 // (num_tiles + num_chunks workgroups, the chunk workgroups last); the host
 // takes it only while num_chunks is at most half the workgroups of that
-// kernel the device holds at once (fused_blocks_per_cu per compute unit).
+// kernel the device holds at once (fused_blocks_per_cu per compute unit), and
+// at most 256.
 hipError_t launch_fused(const LaunchArgs& args, bool vec4, hipStream_t stream);
 hipError_t fused_blocks_per_cu(bool vec4, int* blocks);
 hipError_t launch_ticket(const LaunchArgs& args, bool vec4, hipStream_t stream);

@@ -40,11 +40,11 @@
 //     merged sequence of tiles and pairs, whatever the clustering of the
 //     selection; it also stores the counts into mapped host memory.
 //   stream_scan_kernel (fused staged schedule, the default of a single
-//     partition of up to half as many chunks as the device holds resident
-//     workgroups, about a billion values on MI355X): the stream and scan
-//     kernels' work in one launch, the chunk workgroups after the tile
-//     workgroups, polling epoch-tagged tile words; saves a launch and its
-//     drain between the streaming pass and the scan.
+//     partition of up to 256 chunks, and never more than half as many as
+//     the device holds resident workgroups): the stream and scan kernels'
+//     work in one launch, the chunk workgroups after the tile workgroups,
+//     polling epoch-tagged tile words; saves a launch and its drain between
+//     the streaming pass and the scan.
 //   HBM traffic beyond the 12 bytes per value of the stream: 16 bytes per
 //   selected value (staged write and read) and 8 bytes per 1024 values.
 // Sweep: the same three kernels over a table of segments (every partition of
