@@ -78,8 +78,10 @@ typedef enum micro_status {
 #define MICRO_VARIANT_STAGED 2 /* a streaming pass that stages each tile's pairs
                                   (no inter-workgroup waits), a scan pass (look-
                                   back per chunk of a million values) and a
-                                  balanced pass that places them; scratch of
-                                  about 2 bytes per value of the vector          */
+                                  balanced pass that places them, the first two
+                                  in one launch for partitions of up to 256
+                                  chunks (see MICRO_FLAG_SEPARATE_SCAN); scratch
+                                  of about 2 bytes per value of the vector      */
 
 /* Flags. */
 #define MICRO_FLAG_TIME_KERNEL 1 /* record HIP events around each launch so
@@ -87,8 +89,8 @@ typedef enum micro_status {
 #define MICRO_FLAG_SEPARATE_SCAN 2 /* STAGED: always launch the scan pass on its
                                       own; by default micro_sparsify_step runs
                                       the streaming and scan passes as one
-                                      launch for partitions of up to a few
-                                      hundred million values (same result)    */
+                                      launch for partitions of up to 256
+                                      chunks, 2^28 values (same result)       */
 
 typedef struct micro_config {
     int32_t rule;    /* MICRO_RULE_*                                  (default 0)    */
