@@ -585,6 +585,7 @@ __device__ __forceinline__ uint32_t reserve_flagged(const LaunchArgs& a, uint32_
     }
 }
 
+// This launch's flagged-tile count from the counter word.
 __device__ __forceinline__ uint32_t flagged_count(const LaunchArgs& a, int64_t word) {
     const uint64_t w = static_cast<uint64_t>(word);
     return (w >> 32) == a.epoch ? static_cast<uint32_t>(w) : 0u;
@@ -779,6 +780,8 @@ __device__ uint32_t chunk_lookback(const LaunchArgs& a, const SweepTable* tbl, u
 // In a sweep the chunk lies inside one segment (chunks never straddle two)
 // and also sums its tiles' squared norms; the look-back and the offsets are
 // global, since the segments' pairs form one compaction in index order.
+// FUSED: the same work by the chunk workgroups of stream_scan_kernel, which
+// poll their chunk's epoch-tagged tile words instead of reading final counts.
 template <bool SWEEP, bool FUSED = false>
 __device__ __forceinline__ void scan_chunk(const LaunchArgs& a, const SweepTable* tbl) {
     constexpr int WAVES = kScanBlock / kWaveSize;
