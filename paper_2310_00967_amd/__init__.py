@@ -13,6 +13,8 @@ are views of the first k entries of preallocated output tensors.  Every step
 runs in the HIP library behind include/micro_sparsify.h; PyTorch only
 provides device memory and the stream.
 """
+import ctypes
+
 from . import _lib
 from ._lib import (MICRO_FLAG_SEPARATE_SCAN, MICRO_FLAG_TIME_KERNEL, MICRO_RULE_FIXED_STEP, MICRO_RULE_PROPORTIONAL,
                    MICRO_VARIANT_AUTO, MICRO_VARIANT_STAGED, MICRO_VARIANT_TICKET, MicroError, default_config,
@@ -52,6 +54,19 @@ class Sparsifier:
         self._out_idx = None
         self._out_val = None
         self._lengths = {}  # (rank, world) -> partition length
+        # per-call marshalling objects, made once (a context serves one
+        # caller at a time): the step's in/out scalars and the stats record
+        lib = _lib.load()
+        self._step_fn = lib.micro_sparsify_step
+        self._stats_fn = lib.micro_sparsify_last_stats
+        self._theta_c = ctypes.c_double()
+        self._k_c = ctypes.c_int64()
+        self._theta_p = ctypes.pointer(self._theta_c)
+        self._k_p = ctypes.pointer(self._k_c)
+        self._stats_c = _lib.micro_step_stats()
+        self._stats_p = ctypes.pointer(self._stats_c)
+        self._f32, self._i32 = torch.float32, torch.int32
+        self._tensor = torch.Tensor
 
     def close(self):
         if getattr(self, "_ctx", None) is not None:
@@ -90,25 +105,36 @@ class Sparsifier:
             self._lengths[key] = length
         return length
 
+    def _fits(self, t, dtype):
+        return (isinstance(t, self._tensor) and t.dtype is dtype and t.is_cuda
+                and t.get_device() == self.device.index and t.is_contiguous())
+
     def step(self, grad, residual, rank, world, density, theta, out_idx=None, out_val=None):
         """One sparsify step; returns (k, theta_next, idx[:k], val[:k])."""
-        import torch
         if self._ctx is None:
             raise RuntimeError("Sparsifier is closed")
-        self._check(grad, "grad", torch.float32)
-        self._check(residual, "residual", torch.float32)
-        if grad.numel() != self.n_total or residual.numel() != self.n_total:
-            raise ValueError(f"grad and residual must hold {self.n_total} values")
         length = self._length(rank, world)
         if out_idx is None or out_val is None:
             out_idx, out_val = self.outputs(length)
-        self._check(out_idx, "out_idx", torch.int32)
-        self._check(out_val, "out_val", torch.float32)
+        f32 = self._f32
+        if not (self._fits(grad, f32) and self._fits(residual, f32) and self._fits(out_idx, self._i32)
+                and self._fits(out_val, f32)):
+            # name the offending argument
+            self._check(grad, "grad", f32)
+            self._check(residual, "residual", f32)
+            self._check(out_idx, "out_idx", self._i32)
+            self._check(out_val, "out_val", f32)
+        if grad.numel() != self.n_total or residual.numel() != self.n_total:
+            raise ValueError(f"grad and residual must hold {self.n_total} values")
         if out_idx.numel() < length or out_val.numel() < length:
             raise ValueError(f"output capacity below the partition length {length}")
-        k, th = _lib.micro_sparsify_step(self._ctx, grad.data_ptr(), residual.data_ptr(), rank, world,
-                                         density, theta, out_idx.data_ptr(), out_val.data_ptr())
-        return k, th, out_idx[:k], out_val[:k]
+        self._theta_c.value = float(theta)
+        st = self._step_fn(self._ctx, grad.data_ptr(), residual.data_ptr(), int(rank), int(world), float(density),
+                           self._theta_p, out_idx.data_ptr(), out_val.data_ptr(), self._k_p)
+        if st:
+            _lib.check(st, self._ctx)
+        k = self._k_c.value
+        return k, self._theta_c.value, out_idx[:k], out_val[:k]
 
     def ef_step(self, grad, residual, t, worker, world, density, theta, out_idx=None, out_val=None,
                 local_error=False):
@@ -198,8 +224,13 @@ class Sparsifier:
 
     def last_stats(self):
         """(kernel_ms, redone_tiles, variant, fused) of the last step."""
-        st = _lib.micro_sparsify_last_stats(self._ctx)
-        return st.kernel_ms, st.redone_tiles, st.variant, st.fused
+        if self._ctx is None:
+            raise RuntimeError("Sparsifier is closed")
+        st = self._stats_fn(self._ctx, self._stats_p)
+        if st:
+            _lib.check(st, self._ctx)
+        s = self._stats_c
+        return s.kernel_ms, s.redone_tiles, s.variant, s.fused
 
     def last_kernel_ms(self):
         return self.last_stats()[0]
