@@ -6,6 +6,7 @@
 
 #include <hip/hip_runtime.h>
 
+#include <algorithm>
 #include <cmath>
 #include <cstdarg>
 #include <cstdio>
@@ -184,9 +185,9 @@ void release(micro_ctx* ctx) {
 }
 
 
-// Workgroups of the move kernel: one per move piece of the largest possible
-// count (k = len), at most kMoveGrid, at least min_blocks.  Its grid-stride
-// loops are correct for any grid.
+// Workgroups of the move kernel: one per move piece of a count of len, at
+// most kMoveGrid, at least min_blocks.  Its grid-stride loops are correct for
+// any grid: a larger count only gives each workgroup more pieces.
 uint32_t move_grid(int64_t tiles, int64_t len, int64_t span, int64_t min_blocks) {
     int64_t blocks = (tiles + len + span - 1) / span;
     if (blocks > micro::kMoveGrid) blocks = micro::kMoveGrid;
@@ -358,7 +359,14 @@ micro_status execute_step(micro_ctx* ctx, const float* grad, float* residual, in
     a.flagged_list = ctx->d_flagged_list;
     a.split_tile = ctx->d_split_tile;
     a.move_span = move_span_for(ctx, tiles, density * static_cast<double>(len));
-    a.move_blocks = move_grid(tiles, len, a.move_span, 1);
+    // Sized for twice the expected count (the count of the first steps under
+    // error feedback), and at least four workgroups per compute unit so that
+    // a count far above it still spreads over the device.  Against a grid for
+    // the largest count, BERT-large rank 3 (1024 instead of 2048 workgroups):
+    // 71.2% against 71.0% of 8 TB/s (medians of four runs each, one box).
+    const double expected_pairs = density * static_cast<double>(len);
+    a.move_blocks = move_grid(tiles, static_cast<int64_t>(std::min(static_cast<double>(len), 2.0 * expected_pairs)),
+                              a.move_span, std::min<int64_t>(4 * ctx->compute_units, micro::kMoveGrid));
     a.stage = ctx->d_stage;
     a.num_chunks = static_cast<uint32_t>(chunks);
     a.chunk_status = ctx->d_chunk_status;
