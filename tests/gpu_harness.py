@@ -51,7 +51,10 @@ class ParityRun:
     of one workload and checks each step."""
 
     def __init__(self, w, density, device="cuda", rule_kind=oracle.PROPORTIONAL,
-                 variant=micro.MICRO_VARIANT_AUTO, separate_scan=False):
+                 variant=micro.MICRO_VARIANT_AUTO, separate_scan=False, expect_schedule=None):
+        # expect_schedule: the schedule every call must report having run
+        # (MICRO_VARIANT_TICKET or MICRO_VARIANT_STAGED), or None
+        self.expect_schedule = expect_schedule
         self.w = w
         self.d = density
         self.N = w.n_total
@@ -96,6 +99,9 @@ class ParityRun:
         o_idx, o_val, k_or, th_or = oracle.step(g_np, self.res_mirror, r, w.world, self.d, th,
                                                 rule=self.rule, out=(self.o_idx, self.o_val))
         where = f"{w.name} d={self.d} step {t} rank {r}"
+        if self.expect_schedule is not None:
+            ran = self.sp.last_stats()[2]
+            assert ran == self.expect_schedule, f"{where}: schedule {ran}, expected {self.expect_schedule}"
         assert k_gpu == k_or, f"{where}: k gpu {k_gpu} oracle {k_or}"
         assert th_gpu == th_or, f"{where}: theta gpu {th_gpu!r} oracle {th_or!r}"
         assert np.array_equal(idx_gpu, o_idx), f"{where}: indices differ"

@@ -49,6 +49,22 @@ def test_workload_parity(name, density, steps, variant):
         run.close()
 
 
+@pytest.mark.parametrize("name,density,steps,schedule", [
+    ("resnet18", 0.01, 100, TICKET),     # 730,594-value partitions: one pass
+    ("resnet50", 0.001, 100, STAGED),    # 3,194,629 values: the staged schedule
+])
+def test_workload_parity_default_schedule(name, density, steps, schedule):
+    """The workload under the library's default (AUTO) schedule, the one the
+    benchmark and any caller with a default configuration run, every rank at
+    every step, with the schedule each call took checked."""
+    note(f"parity {name} d={density} steps={steps} AUTO (expects {schedule})")
+    run = ParityRun(synth.get(name), density, DEV, variant=micro.MICRO_VARIANT_AUTO, expect_schedule=schedule)
+    try:
+        run.run(steps)
+    finally:
+        run.close()
+
+
 @pytest.mark.parametrize("density", [0.001, 0.01])
 def test_gpt_parity(density):
     """The 1.3B-value GPT gradient as one partition (world 1), 20 steps."""
