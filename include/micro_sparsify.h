@@ -163,6 +163,36 @@ MICRO_API micro_status micro_sparsify_step(micro_ctx *ctx, const float *grad,
                                  int32_t *out_idx, float *out_val, int64_t *k);
 
 /*
+ * micro_sparsify_step for callers that cannot allocate memory (tight serving
+ * loops, harnesses that forbid hipMalloc, code that must not allocate after
+ * start-up): no context, and no device or host allocation in the call.
+ * It runs the one-pass schedule (MICRO_VARIANT_TICKET) with its scratch in
+ * one static device array per device (4 MiB + 256 bytes, held from the first
+ * call on a device until the process ends): a ticket counter, the count and
+ * one look-back word per 4096 values of the partition, enough for any
+ * partition of up to 2^31 - 1 values.
+ *   grad, residual, rank, world, density, theta, out_idx, out_val, k:
+ *              as micro_sparsify_step, over a vector of n_total values on
+ *              the current HIP device; same results bit for bit.
+ *   hip_stream a hipStream_t of the current device (NULL: the null stream);
+ *              the call enqueues its kernel and the count readback there
+ *              and waits for them.
+ *   cfg        NULL for the defaults; only its threshold rule (rule, beta,
+ *              lo, hi, alpha) is used.
+ * Calls on one device share its scratch; the library serialises them (a lock
+ * per device, held until the count is read back), so they never overlap on
+ * it.  Returns MICRO_ERANGE for n_total above 2^31 - 1 (the most the scratch
+ * covers), MICRO_EINVAL for the argument errors of micro_sparsify_step (and
+ * an invalid cfg), MICRO_EHIP on a HIP failure; messages through
+ * micro_last_error(NULL) on the calling thread.
+ */
+MICRO_API micro_status micro_sparsify_step_noalloc(const float *grad, float *residual, int64_t n_total,
+                                                   int32_t rank, int32_t world, double density,
+                                                   double *theta, int32_t *out_idx, float *out_val,
+                                                   int64_t *k, void *hip_stream,
+                                                   const micro_config *cfg);
+
+/*
  * Every partition r of `world` (1 <= world <= 64) searched once over one
  * vector, each with its own threshold, in one launch of each kernel: the
  * selections all n workers make at one iteration (Sec. 4.2), with the local

@@ -42,6 +42,10 @@ SIGNATURES = {
     "micro_sparsify_step": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p,
                                            ctypes.c_int32, ctypes.c_int32, ctypes.c_double, _dblp,
                                            ctypes.c_void_p, ctypes.c_void_p, _i64p]),
+    "micro_sparsify_step_noalloc": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int64,
+                                                   ctypes.c_int32, ctypes.c_int32, ctypes.c_double, _dblp,
+                                                   ctypes.c_void_p, ctypes.c_void_p, _i64p, ctypes.c_void_p,
+                                                   _cfgp]),
     "micro_partition": (ctypes.c_int, [ctypes.c_int64, ctypes.c_int32, ctypes.c_int32, _i64p, _i64p]),
     "micro_sweep_step": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int32,
                                         ctypes.c_double, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p,
@@ -146,6 +150,22 @@ def micro_sparsify_step(ctx, grad_ptr, residual_ptr, rank, world, density, theta
                                     ctypes.c_void_p(out_idx_ptr), ctypes.c_void_p(out_val_ptr),
                                     ctypes.byref(k))
     check(st, ctx)
+    return k.value, th.value
+
+
+def micro_sparsify_step_noalloc(grad_ptr, residual_ptr, n_total, rank, world, density, theta, out_idx_ptr,
+                                out_val_ptr, stream_handle=None, cfg=None):
+    """Raw call of the allocation-free step with device addresses on the
+    current device; returns (k, theta_next)."""
+    th = ctypes.c_double(float(theta))
+    k = ctypes.c_int64()
+    st = load().micro_sparsify_step_noalloc(ctypes.c_void_p(grad_ptr), ctypes.c_void_p(residual_ptr),
+                                            int(n_total), int(rank), int(world), float(density),
+                                            ctypes.byref(th), ctypes.c_void_p(out_idx_ptr),
+                                            ctypes.c_void_p(out_val_ptr), ctypes.byref(k),
+                                            ctypes.c_void_p(stream_handle or 0),
+                                            ctypes.byref(cfg) if cfg is not None else None)
+    check(st)
     return k.value, th.value
 
 

@@ -13,10 +13,12 @@
 #include <cstring>
 #include <initializer_list>
 #include <limits>
+#include <mutex>
 #include <new>
 #include <string>
 
 #include "sparsify_kernel.h"
+#include "static_scratch.h"
 
 struct micro_ctx {
     int device = -1;
@@ -233,14 +235,13 @@ micro_status run_segments(micro_ctx* ctx, const float* grad, float* residual, in
                           const int64_t* lens, const float* threshold_f, double expected_pairs, int32_t* out_idx,
                           float* out_val, int64_t* k, double* sumsq);
 
-// Validation, launch, count readback and threshold update of one sparsify
-// step over [start, start + len); with accumulate_outside the rest of the
-// vector is accumulated too (the full error-feedback pass), and with sumsq the
-// pass also returns the squared norm of the whole new residual.
-micro_status execute_step(micro_ctx* ctx, const float* grad, float* residual, int64_t start, int64_t len,
-                          bool accumulate_outside, double density, double* theta, int32_t* out_idx,
-                          float* out_val, int64_t* k, double* sumsq) {
-    DeviceScope scope(ctx->device);
+// Arguments of a step over [start, start + len) of a vector of n_total values
+// (whole_vector: grad and residual are accessed over all of it): NULL
+// pointers, density, threshold, alignment and overlapping ranges.  The message
+// goes to ctx, or to the calling thread's error when ctx is NULL.
+micro_status check_step_args(micro_ctx* ctx, const float* grad, const float* residual, int64_t n_total,
+                             int64_t start, int64_t len, bool whole_vector, double density, const double* theta,
+                             const int32_t* out_idx, const float* out_val, const int64_t* k) {
     if (!grad || !residual || !theta || !out_idx || !out_val || !k) {
         set_error(ctx, "NULL pointer argument");
         return MICRO_EINVAL;
@@ -258,8 +259,8 @@ micro_status execute_step(micro_ctx* ctx, const float* grad, float* residual, in
         return MICRO_EINVAL;
     }
     // the ranges each buffer is accessed over
-    const int64_t span_start = accumulate_outside ? 0 : start;
-    const size_t span = static_cast<size_t>(accumulate_outside ? ctx->n_total : len) * sizeof(float);
+    const int64_t span_start = whole_vector ? 0 : start;
+    const size_t span = static_cast<size_t>(whole_vector ? n_total : len) * sizeof(float);
     const size_t pb = static_cast<size_t>(len) * sizeof(float);
     const void* regions[4] = {grad + span_start, residual + span_start, out_idx, out_val};
     const size_t sizes[4] = {span, span, pb, pb};
@@ -269,6 +270,20 @@ micro_status execute_step(micro_ctx* ctx, const float* grad, float* residual, in
                 set_error(ctx, "grad, residual and output ranges overlap");
                 return MICRO_EINVAL;
             }
+    return MICRO_OK;
+}
+
+// Validation, launch, count readback and threshold update of one sparsify
+// step over [start, start + len); with accumulate_outside the rest of the
+// vector is accumulated too (the full error-feedback pass), and with sumsq the
+// pass also returns the squared norm of the whole new residual.
+micro_status execute_step(micro_ctx* ctx, const float* grad, float* residual, int64_t start, int64_t len,
+                          bool accumulate_outside, double density, double* theta, int32_t* out_idx,
+                          float* out_val, int64_t* k, double* sumsq) {
+    DeviceScope scope(ctx->device);
+    const micro_status checked = check_step_args(ctx, grad, residual, ctx->n_total, start, len, accumulate_outside,
+                                                 density, theta, out_idx, out_val, k);
+    if (checked != MICRO_OK) return checked;
     const int64_t n_outside = accumulate_outside ? ctx->n_total - len : 0;
     if (len == 0 && n_outside == 0) {  // nothing to do: nothing selected, threshold unchanged
         *k = 0;
@@ -607,9 +622,115 @@ micro_status execute_union(micro_ctx* ctx, Launch launch) {
     return MICRO_OK;
 }
 
+// The allocation-free step's state on one device: the address of the
+// device's static scratch, the epoch of its last launch (the look-back words
+// carry it, so they are cleared only when it would wrap), and whether the
+// scratch must be cleared before the next launch (after a failure).  Calls on
+// one device hold its mutex from validation of the scratch to the count
+// readback, so they never overlap on the scratch.
+struct NoallocDevice {
+    std::mutex mutex;
+    uint64_t* words = nullptr;
+    uint32_t epoch = 0;
+    bool needs_reset = false;
+};
+
+constexpr int kMaxNoallocDevices = 64;
+NoallocDevice g_noalloc[kMaxNoallocDevices];
+
+micro_status noalloc_fail(NoallocDevice& dv, hipError_t err, const char* what) {
+    dv.needs_reset = true;
+    return hip_fail(nullptr, err, what);
+}
+
 }  // namespace
 
 extern "C" {
+
+micro_status micro_sparsify_step_noalloc(const float* grad, float* residual, int64_t n_total, int32_t rank,
+                                         int32_t world, double density, double* theta, int32_t* out_idx,
+                                         float* out_val, int64_t* k, void* hip_stream, const micro_config* cfg) {
+    micro_config c;
+    micro_config_default(&c);
+    if (cfg) c = *cfg;
+    if (n_total < 0 || !config_valid(c)) {
+        set_error(nullptr, "invalid n_total or configuration");
+        return MICRO_EINVAL;
+    }
+    if (n_total > std::numeric_limits<int32_t>::max()) {
+        set_error(nullptr, "n_total %lld exceeds 2^31 - 1 values, the int32 index range the static scratch covers",
+                  static_cast<long long>(n_total));
+        return MICRO_ERANGE;
+    }
+    int64_t start = 0, len = 0;
+    if (micro_partition(n_total, rank, world, &start, &len) != MICRO_OK) {
+        set_error(nullptr, "invalid rank %d / world %d", rank, world);
+        return MICRO_EINVAL;
+    }
+    const micro_status checked =
+        check_step_args(nullptr, grad, residual, n_total, start, len, false, density, theta, out_idx, out_val, k);
+    if (checked != MICRO_OK) return checked;
+    if (len == 0) {
+        *k = 0;
+        return MICRO_OK;
+    }
+    const bool vec4 = ((reinterpret_cast<uintptr_t>(grad) ^ reinterpret_cast<uintptr_t>(residual)) & 15u) == 0;
+    micro::LaunchArgs a{};
+    a.grad = grad;
+    a.residual = residual;
+    a.out_idx = out_idx;
+    a.out_val = out_val;
+    a.start = start;
+    a.end = start + len;
+    a.base = micro::tile_base_for(grad, start, vec4);
+    a.theta_f = threshold_as_f32(*theta);
+    const int64_t tiles = (a.end - a.base + micro::kTicketTile - 1) / micro::kTicketTile;
+    if (tiles > micro::kStaticMaxTiles) {  // not reachable below 2^31 values; kept as the guard of the scratch
+        set_error(nullptr, "partition needs %lld tiles, the static scratch holds %lld", static_cast<long long>(tiles),
+                  static_cast<long long>(micro::kStaticMaxTiles));
+        return MICRO_ECAPACITY;
+    }
+    a.num_tiles = static_cast<uint32_t>(tiles);
+    int device = -1;
+    hipError_t e = hipGetDevice(&device);
+    if (e != hipSuccess) return hip_fail(nullptr, e, "hipGetDevice");
+    if (device < 0 || device >= kMaxNoallocDevices) {
+        set_error(nullptr, "device %d is beyond the %d devices the static scratch tracks", device,
+                  kMaxNoallocDevices);
+        return MICRO_EHIP;
+    }
+    NoallocDevice& dv = g_noalloc[device];
+    std::lock_guard<std::mutex> lock(dv.mutex);
+    if (!dv.words && (e = micro::static_scratch_current_device(&dv.words)) != hipSuccess)
+        return hip_fail(nullptr, e, "static scratch lookup (hipGetSymbolAddress)");
+    const hipStream_t stream = static_cast<hipStream_t>(hip_stream);
+    if (dv.needs_reset || dv.epoch >= micro::kMaxEpoch) {
+        if ((e = micro::launch_clear_words(dv.words, micro::kStaticScratchWords, stream)) != hipSuccess)
+            return noalloc_fail(dv, e, "static scratch clear");
+        dv.epoch = 0;
+    }
+    a.ticket = reinterpret_cast<unsigned long long*>(dv.words);
+    a.count_out = reinterpret_cast<int64_t*>(dv.words + 1);
+    a.host_count = reinterpret_cast<int64_t*>(dv.words + 3);
+    a.status = dv.words + micro::kStaticHeaderWords;
+    a.epoch = dv.epoch + 1;
+    if ((e = micro::launch_ticket(a, vec4, stream)) != hipSuccess) return noalloc_fail(dv, e, "sparsify kernel launch");
+    dv.epoch = a.epoch;
+    int64_t selected = -1;
+    if ((e = hipMemcpyAsync(&selected, dv.words + 1, sizeof selected, hipMemcpyDeviceToHost, stream)) != hipSuccess)
+        return noalloc_fail(dv, e, "count readback");
+    if ((e = hipStreamSynchronize(stream)) != hipSuccess) return noalloc_fail(dv, e, "hipStreamSynchronize");
+    if (selected < 0 || selected > len) {
+        set_error(nullptr, "device reported %lld selected of %lld", static_cast<long long>(selected),
+                  static_cast<long long>(len));
+        dv.needs_reset = true;
+        return MICRO_EHIP;
+    }
+    dv.needs_reset = false;
+    *k = selected;
+    *theta = next_threshold(c, density, len, selected, *theta);
+    return MICRO_OK;
+}
 
 void micro_config_default(micro_config* cfg) {
     if (!cfg) return;

@@ -174,6 +174,41 @@ def test_ef_and_union_calls_with_null_context_are_rejected():
     assert lib.micro_sparse_update(None, None, None, None, 0, 1) == _lib.MICRO_EINVAL
 
 
+def test_noalloc_step_argument_errors_without_device_work():
+    """The allocation-free step refuses bad arguments before any HIP call
+    (these run without a device), with nothing modified; an empty partition
+    returns k = 0 and the threshold unchanged."""
+    lib = _lib.load()
+    p = ctypes.c_void_p
+    a, b, c, d = p(1 << 20), p(2 << 20), p(3 << 20), p(4 << 20)  # never dereferenced
+    th = ctypes.c_double(1.5)
+    k = ctypes.c_int64(-3)
+
+    def call(n, rank, world, density=0.1, theta=th, grad=a, res=b, cfg=None):
+        return lib.micro_sparsify_step_noalloc(grad, res, n, rank, world, density, ctypes.byref(theta), c, d,
+                                               ctypes.byref(k), None, cfg)
+
+    assert call(2**31, 0, 1) == _lib.MICRO_ERANGE
+    assert "2^31" in _lib.last_error()
+    assert call(-1, 0, 1) == _lib.MICRO_EINVAL
+    assert call(100, 3, 3) == _lib.MICRO_EINVAL
+    assert call(100, 0, 0) == _lib.MICRO_EINVAL
+    assert call(100, 0, 1, density=0.0) == _lib.MICRO_EINVAL
+    assert call(100, 0, 1, density=float("nan")) == _lib.MICRO_EINVAL
+    assert call(100, 0, 1, grad=None) == _lib.MICRO_EINVAL
+    assert call(100, 0, 1, res=a) == _lib.MICRO_EINVAL          # grad and residual overlap
+    assert call(100, 0, 1, res=p((2 << 20) + 2)) == _lib.MICRO_EINVAL  # misaligned
+    bad = ctypes.c_double(float("inf"))
+    assert call(100, 0, 1, theta=bad) == _lib.MICRO_EINVAL
+    cfg = _lib.default_config()
+    cfg.beta = -1.0
+    assert call(100, 0, 1, cfg=ctypes.byref(cfg)) == _lib.MICRO_EINVAL
+    assert th.value == 1.5 and k.value == -3
+    # 3 values over 5 partitions: partition 0 is empty
+    assert call(3, 0, 5) == _lib.MICRO_OK
+    assert k.value == 0 and th.value == 1.5
+
+
 def test_init_without_device_reports_hip_error():
     import torch
     if torch.cuda.is_available():
