@@ -39,6 +39,10 @@ KERNEL_SRC = os.path.join(ROOT, "paper_2310_00967_amd", "csrc", "sparsify_kernel
 KERNEL_HDR = os.path.join(ROOT, "paper_2310_00967_amd", "csrc", "sparsify_kernel.h")
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "sparsify_kernel_gpt_1p3b_traffic.txt")
 TRAFFIC_FILE_BERT = os.path.join(ROOT, "profiles", "sparsify_kernel_bert_large_rank3_traffic.txt")
+TRAFFIC_FILE_EF = os.path.join(ROOT, "profiles", "ef_pass_bert_large_worker3_traffic.txt")
+TRAFFIC_FILE_SWEEP = os.path.join(ROOT, "profiles", "sweep_resnet18_16_partitions_traffic.txt")
+TRAFFIC_FILE_UNION = os.path.join(ROOT, "profiles", "union_gather_update_bert_large_traffic.txt")
+UNION_SRC = os.path.join(ROOT, "paper_2310_00967_amd", "csrc", "union_kernel.hip")
 
 
 def parse_args():
@@ -69,28 +73,30 @@ def parse_args():
                          "million values)")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only run a plain device copy of known size (HBM counter scaling)")
-    ap.add_argument("--path", default="step", choices=["step", "ef", "union", "sweep"],
+    ap.add_argument("--path", default="step", choices=["step", "ef", "union", "sweep", "ceiling"],
                     help="step: the partition-only sparsify step (default); ef: the full error-feedback "
                          "pass with cyclic partitions; union: the gather/reset and model update around "
                          "the exchange; sweep: every partition in one launch of each kernel, with the "
-                         "local-error norms")
+                         "local-error norms; ceiling: vendor streams (torch's in-place add, a device "
+                         "copy) beside the step on the same vector")
     ap.add_argument("--local-error", action="store_true",
                     help="with --path ef: also return the squared norm of the whole residual (Eq. 1)")
     args = ap.parse_args()
-    if args.path != "step" and args.workload == "gpt_1p3b" and "--workload" not in sys.argv:
+    if args.path not in ("step", "ceiling") and args.workload == "gpt_1p3b" and "--workload" not in sys.argv:
         # world 1 makes these paths degenerate
         args.workload = "resnet18" if args.path == "sweep" else "bert_large"
     return args
 
 
-def kernel_sha256(text=None):
-    """sha256 of the kernels' code (the kernel source followed by its header,
-    whose constants shape the launches): // comments, trailing blanks and
-    blank lines removed, so the stored counters stay valid across comment
-    edits and go stale with any change to the code."""
+def kernel_sha256(text=None, sources=None):
+    """sha256 of the kernels' code (by default the sparsify kernel source
+    followed by its header, whose constants shape the launches; the union
+    kernels' counters use their own source and that header): // comments,
+    trailing blanks and blank lines removed, so the stored counters stay
+    valid across comment edits and go stale with any change to the code."""
     if text is None:
         parts = []
-        for path in (KERNEL_SRC, KERNEL_HDR):
+        for path in sources or (KERNEL_SRC, KERNEL_HDR):
             with open(path, encoding="utf-8") as f:
                 parts.append(f.read())
         text = "\n".join(parts)
@@ -102,19 +108,21 @@ def kernel_sha256(text=None):
     return hashlib.sha256("\n".join(code).encode()).hexdigest()
 
 
-def read_traffic(path=None):
+def read_traffic(path=None, workload=None, sources=None):
     """HBM bytes per launch from a committed rocprofv3 counter summary (the
-    GPT-1.3B one by default), or None when absent or taken on a different
-    kernel source."""
+    GPT-1.3B one by default), or None when absent, taken on a different
+    kernel source, or (with `workload`) on a different workload line."""
     path = path or TRAFFIC_FILE
     if not os.path.exists(path):
         return None
     fields = {}
     for line in open(path):
-        if ":" in line:
+        if ":" in line and not line.startswith("#"):
             key, val = line.split(":", 1)
             fields[key.strip()] = val.strip()
-    if fields.get("kernel_source_sha256") != kernel_sha256():
+    if fields.get("kernel_source_sha256") != kernel_sha256(sources=sources):
+        return None
+    if workload is not None and fields.get("workload") != workload:
         return None
     try:
         return float(fields["hbm_bytes_per_launch"])
@@ -123,13 +131,40 @@ def read_traffic(path=None):
 
 
 def cpu_model():
+    """The host CPU as /proc/cpuinfo names it: the model name string with the
+    vendor, family, model and stepping numbers."""
+    fields = {}
     try:
         for line in open("/proc/cpuinfo"):
-            if line.startswith("model name"):
-                return line.split(":", 1)[1].strip()
+            if ":" in line:
+                key, val = (x.strip() for x in line.split(":", 1))
+                fields.setdefault(key, val)
+            if not line.strip() and fields:
+                break  # the first processor's block
     except OSError:
         pass
-    return platform.processor() or "unknown"
+    name = fields.get("model name") or platform.processor() or "unknown"
+    ids = ", ".join(f"{k} {fields[k]}" for k in ("vendor_id", "cpu family", "model", "stepping") if k in fields)
+    return f"{name} ({ids})" if ids else name
+
+
+class OneCore:
+    """Pins the calling thread to one core (the highest it may run on) for the
+    oracle's timing and restores its previous affinity on exit, in-process."""
+
+    def __enter__(self):
+        self.previous = os.sched_getaffinity(0)
+        self.core = max(self.previous)
+        os.sched_setaffinity(0, {self.core})
+        return self
+
+    def __exit__(self, *exc):
+        os.sched_setaffinity(0, self.previous)
+        return False
+
+    def describe(self):
+        return (f"pinned to core {self.core} of {len(self.previous)} allowed "
+                f"(nproc {os.cpu_count()}); host {cpu_model()}")
 
 
 def copy_calibration():
@@ -265,28 +300,28 @@ def cpu_baseline(w, density, pool, target_s, cycle=False):
     out[0][:] = 0
     out[1][:] = 0.0
     spent, elems, steps = 0.0, 0, 0
-    while spent < target_s and steps < 10000:
-        g = pool[steps % len(pool)]
-        parts = [oracle.cycle(steps, worker, w.world) if cycle else worker for worker in w.ranks]
-        for p in parts:
-            s, ln = bounds[p]
-            g_host[s:s + ln].copy_(g[s:s + ln])
-        gn = g_host.numpy()
-        for p in parts:
-            _, ln = bounds[p]
-            t0 = time.perf_counter()
-            _, _, _, theta[p] = oracle.step(gn, res, p, w.world, density, theta[p], out=out)
-            spent += time.perf_counter() - t0
-            elems += ln
-        steps += 1
+    with OneCore() as pin:
+        while spent < target_s and steps < 10000:
+            g = pool[steps % len(pool)]
+            parts = [oracle.cycle(steps, worker, w.world) if cycle else worker for worker in w.ranks]
+            for p in parts:
+                s, ln = bounds[p]
+                g_host[s:s + ln].copy_(g[s:s + ln])
+            gn = g_host.numpy()
+            for p in parts:
+                _, ln = bounds[p]
+                t0 = time.perf_counter()
+                _, _, _, theta[p] = oracle.step(gn, res, p, w.world, density, theta[p], out=out)
+                spent += time.perf_counter() - t0
+                elems += ln
+            steps += 1
     return {
         "value": elems / spent / 1e9,
         "unit": "G elem/s",
         "cores": 1,
         "kind": "oracle",
         "sample": (f"{steps} step(s) of {w.name} at d={density} ({elems} values, "
-                   f"{spent:.1f} s of single-threaded oracle time); host {cpu_model()}, "
-                   f"nproc {os.cpu_count()}"),
+                   f"{spent:.1f} s of single-threaded oracle time), {pin.describe()}"),
     }
 
 
@@ -444,18 +479,18 @@ def cpu_baseline_ef(w, density, pool, target_s):
     s, ln = oracle.partition(N, oracle.cycle(0, worker, w.world), w.world)
     theta = synth.initial_theta(w, pool[0], s, s + ln, density)
     spent, elems, steps = 0.0, 0, 0
-    while spent < target_s and steps < 10000:
-        g_host.copy_(pool[steps % len(pool)])
-        gn = g_host.numpy()
-        t0 = time.perf_counter()
-        _, _, _, theta, _ = oracle.ef_step(gn, res, steps, worker, w.world, density, theta, out=out)
-        spent += time.perf_counter() - t0
-        elems += N
-        steps += 1
+    with OneCore() as pin:
+        while spent < target_s and steps < 10000:
+            g_host.copy_(pool[steps % len(pool)])
+            gn = g_host.numpy()
+            t0 = time.perf_counter()
+            _, _, _, theta, _ = oracle.ef_step(gn, res, steps, worker, w.world, density, theta, out=out)
+            spent += time.perf_counter() - t0
+            elems += N
+            steps += 1
     return {"value": elems / spent / 1e9, "unit": "G elem/s", "cores": 1, "kind": "oracle",
             "sample": (f"{steps} full pass(es) of {w.name} worker {worker} at d={density} ({elems} values, "
-                       f"{spent:.1f} s of single-threaded oracle time); host {cpu_model()}, "
-                       f"nproc {os.cpu_count()}")}
+                       f"{spent:.1f} s of single-threaded oracle time), {pin.describe()}")}
 
 
 def cpu_baseline_sweep(w, density, pool, target_s):
@@ -473,18 +508,18 @@ def cpu_baseline_sweep(w, density, pool, target_s):
         s, ln = oracle.partition(N, r, w.world)
         thetas.append(synth.initial_theta(w, pool[0], s, s + ln, density))
     spent, elems, steps = 0.0, 0, 0
-    while spent < target_s and steps < 10000:
-        g_host.copy_(pool[steps % len(pool)])
-        gn = g_host.numpy()
-        t0 = time.perf_counter()
-        _, _, _, thetas, _ = oracle.sweep(gn, res, w.world, density, thetas)
-        spent += time.perf_counter() - t0
-        elems += N
-        steps += 1
+    with OneCore() as pin:
+        while spent < target_s and steps < 10000:
+            g_host.copy_(pool[steps % len(pool)])
+            gn = g_host.numpy()
+            t0 = time.perf_counter()
+            _, _, _, thetas, _ = oracle.sweep(gn, res, w.world, density, thetas)
+            spent += time.perf_counter() - t0
+            elems += N
+            steps += 1
     return {"value": elems / spent / 1e9, "unit": "G elem/s", "cores": 1, "kind": "oracle",
             "sample": (f"{steps} sweep(s) of {w.name} over {w.world} partitions at d={density} ({elems} values, "
-                       f"{spent:.1f} s of single-threaded oracle time); host {cpu_model()}, "
-                       f"nproc {os.cpu_count()}")}
+                       f"{spent:.1f} s of single-threaded oracle time), {pin.describe()}")}
 
 
 def cpu_baseline_union(w, g, union_res, target_s):
@@ -495,18 +530,109 @@ def cpu_baseline_union(w, g, union_res, target_s):
     acc = (g * 0.5).cpu().numpy()
     x = np.ones(w.n_total, np.float32)
     spent, entries, reps = 0.0, 0, 0
-    while spent < target_s and reps < 10000:
-        t0 = time.perf_counter()
-        vals = oracle.gather(acc, union)
-        oracle.zero(acc, union)
-        oracle.update(x, union, vals, w.world)
-        spent += time.perf_counter() - t0
-        entries += union.size
-        reps += 1
+    with OneCore() as pin:
+        while spent < target_s and reps < 10000:
+            t0 = time.perf_counter()
+            vals = oracle.gather(acc, union)
+            oracle.zero(acc, union)
+            oracle.update(x, union, vals, w.world)
+            spent += time.perf_counter() - t0
+            entries += union.size
+            reps += 1
     return {"value": entries / spent / 1e9, "unit": "G entries/s", "cores": 1, "kind": "oracle",
             "sample": (f"{reps} gather+reset+update pass(es) over a {union.size}-entry union of {w.name} "
-                       f"({spent:.1f} s of single-threaded oracle time); host {cpu_model()}, "
-                       f"nproc {os.cpu_count()}")}
+                       f"({spent:.1f} s of single-threaded oracle time), {pin.describe()}")}
+
+
+def bert_block(args):
+    """BERT-large rank 3 of 8 (41,892,736 values, d = 0.01), the other
+    workload whose partition holds at least 25M values, measured in the same
+    run as the headline: its own gradient pool and context, the fixed rank and
+    then worker 3 under Algorithm 1's rotation (every partition in turn, one
+    threshold each)."""
+    import torch
+    import paper_2310_00967_amd as micro
+    from paper_2310_00967_amd import synth
+    w = synth.get("bert_large")
+    d = w.densities[0]
+    warmup, steps = max(args.warmup, 10), max(args.steps, 20)
+    n_pool = max(1, min(warmup + steps, int(args.pool_gb * 1e9 // (4 * w.n_total))))
+    pool = [synth.gradient(w, t, "cuda") for t in range(n_pool)]
+    torch.cuda.synchronize()
+    sp = micro.Sparsifier(w.n_total, device="cuda", time_kernel=True)
+    block = {}
+    for cycle in (False, True):
+        r = measure(w, d, pool, sp, micro, warmup, steps, cycle)
+        traffic = None if cycle else read_traffic(TRAFFIC_FILE_BERT, f"bert_large world 8 rank 3 d={d}")
+        key = "bert_large_worker3_cycle" if cycle else "bert_large_rank3"
+        block[key] = {
+            "partition_len": micro.micro_partition(w.n_total, 3, w.world)[1], "density": d,
+            "partitions": ("cyclic: partition ((t mod 8) + 3) mod 8 at step t" if cycle else "fixed: rank 3"),
+            "warmup": warmup, "steps": steps, "gradient_pool": n_pool,
+            "g_elem_s": r["g_elem_s"], "ms_per_step": r["ms_per_step"], "wall_gbs": r["wall_gbs"],
+            "kernel_ms_avg": r["kernel_ms_avg"], "kernel_gbs": r["kernel_gbs"],
+            "frac": r["kernel_gbs"] / HBM_PEAK_GBS, "alg_bytes_per_launch": r["alg_bytes_per_launch"],
+            "traffic": traffic, "density_error_last_half": r["density_error_last_half"],
+            "kernel": ("stream_scan_kernel + move_kernel" if r["fused"] else "stream_kernel + scan_kernel + move_kernel")
+            + " (one step, event-timed together)",
+            "redone_tiles_timed": r["redone_tiles"]}
+    sp.close()
+    del pool
+    torch.cuda.empty_cache()
+    return block
+
+
+def stream_ceiling(args, w, head, pool, sp):
+    """Streams of the vendor libraries beside the library's step, on the same
+    vector and stream, each `steps` times after `warmup` runs: torch.add(g,
+    res, out=res) (two reads and one write per value: the step's streaming
+    pattern without the selection), res.copy_(g) (one read, one write: a
+    device copy) and the sparsify step.  Event-timed on torch's current
+    stream; GB/s from the bytes each must move (12, 8 and 12 + 8 d bytes per
+    value)."""
+    import torch
+    from paper_2310_00967_amd import synth
+    N = w.n_total
+    g = pool[0]
+    res = torch.zeros(N, dtype=torch.float32, device="cuda")
+    res_step = torch.zeros(N, dtype=torch.float32, device="cuda")
+    out_idx, out_val = sp.outputs(N)
+    theta = synth.initial_theta(w, g, 0, N, head)
+    stream = torch.cuda.current_stream()
+
+    def timed(fn):
+        ms = []
+        for i in range(args.warmup + args.steps):
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record(stream)
+            fn(i)
+            e1.record(stream)
+            e1.synchronize()
+            if i >= args.warmup:
+                ms.append(e0.elapsed_time(e1))
+        return sum(ms) / len(ms)
+
+    ks = []
+
+    def step(i):
+        nonlocal theta
+        k, theta, _, _ = sp.step(pool[i % len(pool)], res_step, 0, 1, head, theta, out_idx, out_val)
+        if i >= args.warmup:
+            ks.append(k)
+
+    add_ms = timed(lambda i: torch.add(g, res, out=res))
+    copy_ms = timed(lambda i: res.copy_(g))
+    step_ms = timed(step)
+    k_avg = sum(ks) / len(ks)
+    rows = {"torch_add_inplace": (add_ms, 12.0 * N), "device_copy": (copy_ms, 8.0 * N),
+            "sparsify_step": (step_ms, 12.0 * N + 8.0 * k_avg)}
+    line = {"metric": "streaming ceiling: vendor streams beside the sparsify step (GB/s of the bytes each must move)",
+            "n_gpus": 1, "steps": args.steps, "warmup": args.warmup, "dtype": "f32", "data": "synthetic",
+            "config": {"workload": w.name, "n_total": N, "density": head},
+            "kernels": {name: {"ms_avg": ms, "bytes": b, "gbs": b / (ms * 1e-3) / 1e9,
+                               "frac": b / (ms * 1e-3) / 1e9 / HBM_PEAK_GBS} for name, (ms, b) in rows.items()},
+            "step_k_avg": k_avg}
+    print(json.dumps(line), flush=True)
 
 
 def main_path(args, w, head, pool, n_pool, sp):
@@ -521,11 +647,12 @@ def main_path(args, w, head, pool, n_pool, sp):
         cpu = cpu_baseline_sweep(w, head, pool, args.cpu_seconds) if args.cpu_seconds > 0 else None
         cfg["parallelism"] = "every partition of one vector on one GPU"
         cfg["ranks"] = list(range(w.world))
+        traffic = read_traffic(TRAFFIC_FILE_SWEEP, f"{w.name} world {w.world} sweep d={head}")
         line = {"metric": "partition-sweep throughput (G elem/s of the whole vector, HBM GB/s % of peak)",
                 "value": r["g_elem_s"], "unit": "G elem/s", "ms_per_step": r["ms_per_step"], **common,
                 "config": cfg, "k_avg": r["k_avg"], "local_error_last": r["local_error_last"],
                 "roofline": {"bound": "hbm", "achieved": r["kernel_gbs"], "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                             "frac": r["kernel_gbs"] / HBM_PEAK_GBS, "traffic": None,
+                             "frac": r["kernel_gbs"] / HBM_PEAK_GBS, "traffic": traffic,
                              "kernel": "stream_sweep_kernel + scan_sweep_kernel + move_sweep_kernel "
                                        "(one sweep, event-timed together)",
                              "kernel_ms_avg": r["kernel_ms_avg"], "alg_bytes_per_launch": r["alg_bytes_per_launch"]},
@@ -534,11 +661,13 @@ def main_path(args, w, head, pool, n_pool, sp):
         r = measure_ef(w, head, pool, sp, args.warmup, args.steps, args.local_error)
         cfg["local_error"] = args.local_error
         cpu = cpu_baseline_ef(w, head, pool, args.cpu_seconds) if args.cpu_seconds > 0 else None
+        traffic = read_traffic(TRAFFIC_FILE_EF, f"{w.name} world {w.world} worker {w.ranks[0]} ef d={head}"
+                               + (" local-error" if args.local_error else ""))
         line = {"metric": "full error-feedback pass throughput (G elem/s of the whole vector, HBM GB/s % of peak)",
                 "value": r["g_elem_s"], "unit": "G elem/s", "ms_per_step": r["ms_per_step"], **common,
                 "config": cfg, "k_avg": r["k_avg"],
                 "roofline": {"bound": "hbm", "achieved": r["kernel_gbs"], "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                             "frac": r["kernel_gbs"] / HBM_PEAK_GBS, "traffic": None,
+                             "frac": r["kernel_gbs"] / HBM_PEAK_GBS, "traffic": traffic,
                              "kernel": ("stream_sweep_kernel + scan_sweep_kernel + move_sweep_kernel over three "
                                         "segments (one pass with the local error, event-timed together)"
                                         if args.local_error else
@@ -552,11 +681,13 @@ def main_path(args, w, head, pool, n_pool, sp):
         r = measure_union(w, head, pool[0], sp, args.warmup, args.steps)
         cpu = cpu_baseline_union(w, pool[0], r, args.cpu_seconds) if args.cpu_seconds > 0 else None
         cfg.update({"union_len": r["union_len"], "own_len": r["own_len"]})
+        traffic = read_traffic(TRAFFIC_FILE_UNION, f"{w.name} world {w.world} worker {w.ranks[0]} union d={head}",
+                               sources=(UNION_SRC, KERNEL_HDR))
         line = {"metric": "union gather/reset + model update throughput (G union entries/s, HBM GB/s % of peak)",
                 "value": r["g_entries_s"], "unit": "G entries/s", "ms_per_step": r["ms_per_step"], **common,
                 "config": cfg,
                 "roofline": {"bound": "hbm", "achieved": r["kernel_gbs"], "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                             "frac": r["kernel_gbs"] / HBM_PEAK_GBS, "traffic": None,
+                             "frac": r["kernel_gbs"] / HBM_PEAK_GBS, "traffic": traffic,
                              "kernel": "union_gather_kernel + sparse_update_kernel (event-timed each)",
                              "gather_ms_avg": r["gather_ms_avg"], "update_ms_avg": r["update_ms_avg"],
                              "gather_gbs": r["gather_gbs"], "update_gbs": r["update_gbs"],
@@ -596,6 +727,10 @@ def main():
                "ticket": micro.MICRO_VARIANT_TICKET}[args.variant]
     sp = micro.Sparsifier(w.n_total, device="cuda", time_kernel=True, variant=variant,
                           separate_scan=args.separate_scan)
+    if args.path == "ceiling":
+        stream_ceiling(args, w, head, pool, sp)
+        sp.close()
+        return
     if args.path != "step":
         main_path(args, w, head, pool, n_pool, sp)
         sp.close()
@@ -611,9 +746,15 @@ def main():
 
     cpu = cpu_baseline(w, head, pool, args.cpu_seconds, args.cycle) if args.cpu_seconds > 0 else None
     sp.close()
+    if w.name == "gpt_1p3b" and not args.no_extra and not args.cycle:
+        del pool
+        torch.cuda.empty_cache()
+        extra.update(bert_block(args))
 
-    traffic_file = {"gpt_1p3b": TRAFFIC_FILE, "bert_large": TRAFFIC_FILE_BERT}.get(args.workload)
-    traffic = (read_traffic(traffic_file) if traffic_file and head == 0.01 and not args.cycle
+    traffic_file, traffic_workload = {
+        "gpt_1p3b": (TRAFFIC_FILE, "gpt_1p3b world 1 rank 0 d=0.01"),
+        "bert_large": (TRAFFIC_FILE_BERT, "bert_large world 8 rank 3 d=0.01")}.get(args.workload, (None, None))
+    traffic = (read_traffic(traffic_file, traffic_workload) if traffic_file and head == 0.01 and not args.cycle
                and not args.separate_scan and args.variant == "auto" else None)
     parts = sorted({ln for (_, ln) in (micro.micro_partition(w.n_total, p, w.world)
                                        for p in (range(w.world) if args.cycle else w.ranks))})

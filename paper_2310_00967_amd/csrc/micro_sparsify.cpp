@@ -378,7 +378,9 @@ micro_status execute_step(micro_ctx* ctx, const float* grad, float* residual, in
     // error feedback), and at least four workgroups per compute unit so that
     // a count far above it still spreads over the device.  Against a grid for
     // the largest count, BERT-large rank 3 (1024 instead of 2048 workgroups):
-    // 71.2% against 71.0% of 8 TB/s (medians of four runs each, one box).
+    // 71.2% against 71.0% of 8 TB/s (medians of four runs each, one box),
+    // within the run-to-run spread of about 1%: no slower, and fewer idle
+    // workgroups.
     const double expected_pairs = density * static_cast<double>(len);
     a.move_blocks = move_grid(tiles, static_cast<int64_t>(std::min(static_cast<double>(len), 2.0 * expected_pairs)),
                               a.move_span, std::min<int64_t>(4 * ctx->compute_units, micro::kMoveGrid));
@@ -853,10 +855,12 @@ micro_status micro_sparsify_init(micro_ctx** out, int64_t n_total, void* hip_str
              hipMalloc(&ctx->d_tile_words, sizeof(uint64_t) * ctx->tile_capacity) == hipSuccess;
     }
     if (ok && ctx->has_staged) {
-        // The fused schedule's chunk workgroups wait for stream workgroups of
-        // the same launch: it is taken only while they fill at most half of
-        // the workgroups the device holds at once (both load widths), and not
-        // beyond kFusedMaxChunks, where it stops paying.
+        // The fused schedule's chunk workgroups wait only for lower-index
+        // workgroups of the same launch, which each XCD dispatches first; it
+        // is taken only while they fill at most half of the workgroups the
+        // device holds at once (both load widths), so that the polling chunk
+        // workgroups of concurrent fused launches cannot fill an XCD either,
+        // and not beyond kFusedMaxChunks, where it stops paying.
         int b4 = 0, b1 = 0;
         if (micro::fused_blocks_per_cu(true, &b4) == hipSuccess && micro::fused_blocks_per_cu(false, &b1) == hipSuccess) {
             const int64_t half = static_cast<int64_t>(b4 < b1 ? b4 : b1) * ctx->compute_units / 2;

@@ -118,10 +118,13 @@ int64_t tile_base_for(const float* grad, int64_t start, bool vec4);
 // the scalar-load kernels.  Each returns the launch status.
 hipError_t launch_staged(const LaunchArgs& args, bool vec4, hipStream_t stream);
 // The staged schedule with its stream and scan kernels fused into one launch
-// (num_tiles + num_chunks workgroups, the chunk workgroups last); the host
-// takes it only while num_chunks is at most half the workgroups of that
-// kernel the device holds at once (fused_blocks_per_cu per compute unit), and
-// at most 256.
+// (num_tiles + num_chunks workgroups, the chunk workgroups last).  Its waits
+// end because every chunk workgroup waits only for workgroups of lower index
+// in the same launch and each XCD dispatches its workgroups in index order;
+// the host also keeps num_chunks at most half the workgroups of that kernel
+// the device holds at once (fused_blocks_per_cu per compute unit) and at most
+// 256, so the polling chunk workgroups of several concurrent fused launches
+// cannot fill an XCD either.
 hipError_t launch_fused(const LaunchArgs& args, bool vec4, hipStream_t stream);
 hipError_t fused_blocks_per_cu(bool vec4, int* blocks);
 hipError_t launch_ticket(const LaunchArgs& args, bool vec4, hipStream_t stream);

@@ -906,13 +906,22 @@ __global__ __launch_bounds__(kScanBlock) void scan_kernel(LaunchArgs a) { scan_c
 // Fused schedule: workgroups [0, num_tiles) stream the tiles (stream_kernel's
 // work, publishing epoch-tagged tile words), workgroups [num_tiles,
 // num_tiles + num_chunks) scan the chunks (scan_kernel's work, polling the
-// tile words of their chunk).  A chunk workgroup waits for stream workgroups,
-// which wait for nobody, and in its look-back for the aggregates of lower
-// chunk workgroups, which each publish once their own tile words are in.  The
-// host takes this schedule only while the chunk workgroups fill at most half
-// of the workgroups the device holds at once, so the stream workgroups and
-// the lower chunk workgroups always find room, in whatever order the hardware
-// dispatches the grid.
+// tile words of their chunk).
+// Forward progress rests on two facts.  (1) Every wait targets a workgroup of
+// lower index in the same launch: a chunk workgroup waits for the tile words
+// of its own chunk (stream workgroups, which wait for nobody) and, in its
+// look-back, for the aggregates of lower chunks (each published as soon as
+// that chunk's tile words are in, before its own look-back).  (2) Each XCD
+// dispatches its share of the grid in increasing workgroup index, so a
+// workgroup is dispatched once the lower-index workgroups of the launch on
+// its XCD have freed a slot.  By induction on the index, the lowest
+// unfinished workgroup of the launch is always dispatched eventually and
+// never waits for an unfinished one, so every wait ends.  What could still
+// withhold a slot is other resident work that waits too: the host caps the
+// chunk workgroups at 256 and at half the workgroups of this kernel the
+// device holds at once (1/8 of it on MI355X, 32 per XCD), so the chunk
+// workgroups of all the fused launches one process can have running at once
+// (HIP's default of four hardware queues) cannot fill an XCD.
 template <int VEC, int ROWS>
 __global__ __launch_bounds__(kStreamBlock) void stream_scan_kernel(LaunchArgs a) {
     static_assert(kStreamBlock == kScanBlock, "one workgroup size for both parts");

@@ -62,15 +62,47 @@ def test_traffic_is_reported_only_for_the_kernel_it_was_measured_on(tmp_path, mo
     assert bench.read_traffic() is None
 
 
-@pytest.mark.parametrize("path,values", [("TRAFFIC_FILE", 1_315_723_264), ("TRAFFIC_FILE_BERT", 41_892_736)])
-def test_committed_traffic_summaries_name_a_hash_and_a_byte_count(path, values):
+@pytest.mark.parametrize("path,min_bytes", [
+    ("TRAFFIC_FILE", 12 * 1_315_723_264),        # the step's 12 B per partition value
+    ("TRAFFIC_FILE_BERT", 12 * 41_892_736),
+    ("TRAFFIC_FILE_EF", 12 * 335_141_888),       # the full pass: 12 B per value of the vector
+    ("TRAFFIC_FILE_SWEEP", 12 * 11_689_512),
+    ("TRAFFIC_FILE_UNION", 16 * 3_351_416),      # gather and update of the BERT-large union
+])
+def test_committed_traffic_summaries_name_a_workload_a_hash_and_a_byte_count(path, min_bytes):
     fields = {}
     for line in open(getattr(bench, path)):
         if ":" in line and not line.startswith("#"):
             key, val = line.split(":", 1)
             fields[key.strip()] = val.strip()
+    assert fields["workload"]
     assert len(fields["kernel_source_sha256"]) == 64
-    assert float(fields["hbm_bytes_per_launch"]) > 12 * values  # at least the algorithmic bytes
+    assert float(fields["hbm_bytes_per_launch"]) > min_bytes  # at least the algorithmic bytes
+
+
+def test_traffic_is_reported_only_for_the_workload_it_was_measured_on(tmp_path, monkeypatch):
+    src = tmp_path / "kernel.hip"
+    src.write_text("__global__ void k() {}\n")
+    hdr = tmp_path / "kernel.h"
+    hdr.write_text("constexpr int kTile = 1024;\n")
+    traffic = tmp_path / "traffic.txt"
+    monkeypatch.setattr(bench, "KERNEL_SRC", str(src))
+    monkeypatch.setattr(bench, "KERNEL_HDR", str(hdr))
+    _traffic_file(traffic, bench.kernel_sha256())
+    with open(traffic, "a") as f:
+        f.write("workload: toy world 4 rank 0 d=0.01\n")
+    assert bench.read_traffic(str(traffic), "toy world 4 rank 0 d=0.01") == 123456789.0
+    assert bench.read_traffic(str(traffic), "toy world 4 rank 1 d=0.01") is None
+    assert bench.read_traffic(str(traffic)) == 123456789.0  # no workload asked for
+
+
+def test_one_core_pins_and_restores_the_affinity():
+    before = os.sched_getaffinity(0)
+    with bench.OneCore() as pin:
+        assert os.sched_getaffinity(0) == {pin.core}
+        assert pin.core in before
+        assert f"core {pin.core}" in pin.describe()
+    assert os.sched_getaffinity(0) == before
 
 
 @pytest.mark.parametrize("n", ["2", "8"])
