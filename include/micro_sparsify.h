@@ -79,18 +79,17 @@ typedef enum micro_status {
                                   (no inter-workgroup waits), a scan pass (look-
                                   back per chunk of a million values) and a
                                   balanced pass that places them, the first two
-                                  in one launch for partitions of up to 256
-                                  chunks (see MICRO_FLAG_SEPARATE_SCAN); scratch
-                                  of about 2 bytes per value of the vector      */
+                                  in one launch (see MICRO_FLAG_SEPARATE_SCAN);
+                                  scratch of about 2 bytes per value of the
+                                  vector                                          */
 
 /* Flags. */
 #define MICRO_FLAG_TIME_KERNEL 1 /* record HIP events around each launch so
                                     micro_sparsify_last_kernel_ms can report it */
-#define MICRO_FLAG_SEPARATE_SCAN 2 /* STAGED: always launch the scan pass on its
-                                      own; by default micro_sparsify_step runs
-                                      the streaming and scan passes as one
-                                      launch for partitions of up to 256
-                                      chunks, 2^28 values (same result)       */
+#define MICRO_FLAG_SEPARATE_SCAN 2 /* STAGED: launch the scan pass on its own;
+                                      by default micro_sparsify_step runs the
+                                      streaming and scan passes as one launch
+                                      (same result)                            */
 
 typedef struct micro_config {
     int32_t rule;    /* MICRO_RULE_*                                  (default 0)    */

@@ -42,7 +42,6 @@ struct micro_ctx {
     uint64_t* d_chunk_status = nullptr;
     int64_t chunk_capacity = 0;
     uint64_t* d_tile_words = nullptr;        // fused schedule: epoch-tagged tile counts
-    int64_t fused_max_chunks = 0;            // largest chunk count the fused schedule takes (0: none)
     // ticket schedule: tile look-back words
     uint64_t* d_status = nullptr;
     unsigned long long* d_tickets = nullptr; // [0] tile ticket of the one-pass schedule
@@ -210,14 +209,6 @@ uint32_t move_grid(int64_t tiles, int64_t len, int64_t span, int64_t min_blocks)
 // ResNet-50 rank 0 (3.2M values, d = 0.001, about 6,300 items) 26.5%, 27.0%
 // and 27.3%; the GPT-1.3B partition's move kernel took 53 us with 4096-item
 // pieces and 78 us with 2048 (an earlier build of the kernel).
-// Largest partition, in scan chunks of a million values, that takes the fused
-// stream-and-scan launch.  Measured on MI355X (one GPT-shaped vector, d =
-// 0.01, fused against separate device time per step): 20 chunks -1.7 us, 40
-// -3.1, 79 -3.0, 157 -3.9, 314 +2.2, 628 +3.1 (and the GPT-1.3B partition,
-// 1,285 chunks, +18 us): past a few hundred chunk workgroups, their scan and
-// polling at the end of the launch cost more than the separate launch.
-constexpr int64_t kFusedMaxChunks = 256;
-
 uint32_t move_span_for(const micro_ctx* ctx, int64_t tiles, double expected_pairs) {
     const double items = static_cast<double>(tiles) + expected_pairs;
     if (items >= 2.0 * ctx->compute_units * micro::kMoveSpan) return micro::kMoveSpan;
@@ -401,9 +392,9 @@ micro_status execute_step(micro_ctx* ctx, const float* grad, float* residual, in
     host_count[1] = len > 0 ? -1 : 0;
     if (n_outside > 0 && (e = micro::launch_accumulate(acc, vec4, ctx->stream)) != hipSuccess)
         return hip_fail(ctx, e, "accumulate kernel launch");
-    // The staged schedule's stream and scan kernels run as one launch while
-    // the partition's chunk count allows it (see fused_max_chunks).
-    const bool fused = staged && (ctx->cfg.flags & MICRO_FLAG_SEPARATE_SCAN) == 0 && chunks <= ctx->fused_max_chunks;
+    // The staged schedule's stream and scan kernels run as one launch unless
+    // the caller asked for the scan on its own.
+    const bool fused = staged && (ctx->cfg.flags & MICRO_FLAG_SEPARATE_SCAN) == 0;
     if (len > 0) {
         ctx->epoch = a.epoch;
         e = !staged ? micro::launch_ticket(a, vec4, ctx->stream)
@@ -853,21 +844,6 @@ micro_status micro_sparsify_init(micro_ctx** out, int64_t n_total, void* hip_str
              hipMalloc(&ctx->d_stage, sizeof(uint2) * stage) == hipSuccess &&
              hipMalloc(&ctx->d_chunk_status, sizeof(uint64_t) * ctx->chunk_capacity) == hipSuccess &&
              hipMalloc(&ctx->d_tile_words, sizeof(uint64_t) * ctx->tile_capacity) == hipSuccess;
-    }
-    if (ok && ctx->has_staged) {
-        // The fused schedule's chunk workgroups wait only for lower-index
-        // workgroups of the same launch, which each XCD dispatches first; it
-        // is taken only while they fill at most half of the workgroups the
-        // device holds at once (both load widths), so that the polling chunk
-        // workgroups of concurrent fused launches cannot fill an XCD either,
-        // and not beyond kFusedMaxChunks, where it stops paying.
-        int b4 = 0, b1 = 0;
-        if (micro::fused_blocks_per_cu(true, &b4) == hipSuccess && micro::fused_blocks_per_cu(false, &b1) == hipSuccess) {
-            const int64_t half = static_cast<int64_t>(b4 < b1 ? b4 : b1) * ctx->compute_units / 2;
-            ctx->fused_max_chunks = half < kFusedMaxChunks ? half : kFusedMaxChunks;
-        } else {
-            (void)hipGetLastError();  // no fused schedule; the separate kernels remain
-        }
     }
     if (ok && ctx->has_ticket) {
         ctx->ticket_capacity = n_total / micro::kTicketTile + 2;

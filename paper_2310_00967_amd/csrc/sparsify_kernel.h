@@ -30,6 +30,37 @@ static_assert((kMoveSpan & (kMoveSpan - 1)) == 0 && (kMoveSpanSmall & (kMoveSpan
 // Ticket schedule: values per tile (256 threads, four dwordx4 per lane).
 constexpr int kTicketTile = 4096;
 
+// Fused stream-and-scan launch: num_tiles + num_chunks workgroups.  The scan
+// workgroup of chunk c follows the stream workgroup of the last tile of chunk
+// c + kChunkLag, so it is dispatched when its own chunk's tiles have had about
+// kChunkLag * kChunkTiles dispatches to finish and scans while the stream goes
+// on; the chunks that have no such tile (the last kChunkLag or so) follow all
+// tiles, in order.  Every scan workgroup therefore comes after its chunk's
+// tiles and after the scan workgroups of all lower chunks.
+constexpr uint32_t kChunkLag = 2;
+
+struct FusedRole {
+    bool scan;      // a scan workgroup (else a stream workgroup)
+    uint32_t item;  // its chunk, or its tile
+};
+
+// Role of workgroup b of the fused launch.  Chunk c (num_chunks of them)
+// sits at position min(num_tiles, (c + kChunkLag + 1) * kChunkTiles) + c.
+// Chunks c < c0 = max(0, floor(num_tiles / kChunkTiles) - kChunkLag) are the
+// interleaved ones, at (c + kChunkLag + 1) * (kChunkTiles + 1) - (kChunkLag + 1);
+// the others sit at num_tiles + c.
+__host__ __device__ inline FusedRole fused_role(uint32_t b, uint32_t num_tiles, uint32_t num_chunks) {
+    const uint32_t whole = num_tiles / kChunkTiles;
+    const uint32_t c0 = whole > kChunkLag ? whole - kChunkLag : 0u;
+    if (b >= num_tiles + c0) return {true, b - num_tiles};
+    const uint32_t q = b + kChunkLag + 1;
+    const uint32_t g = q / (kChunkTiles + 1);
+    if (q % (kChunkTiles + 1) == 0 && g >= kChunkLag + 1) return {true, g - kChunkLag - 1};
+    const uint32_t before = g > kChunkLag ? (g - kChunkLag < c0 ? g - kChunkLag : c0) : 0u;
+    (void)num_chunks;
+    return {false, b - before};
+}
+
 // Bits of a look-back status word (one 64-bit word per tile or chunk):
 //   [0, 32)  count: the item's own selected count (aggregate) or the
 //            inclusive prefix of selected counts through this item
@@ -118,15 +149,10 @@ int64_t tile_base_for(const float* grad, int64_t start, bool vec4);
 // the scalar-load kernels.  Each returns the launch status.
 hipError_t launch_staged(const LaunchArgs& args, bool vec4, hipStream_t stream);
 // The staged schedule with its stream and scan kernels fused into one launch
-// (num_tiles + num_chunks workgroups, the chunk workgroups last).  Its waits
-// end because every chunk workgroup waits only for workgroups of lower index
-// in the same launch and each XCD dispatches its workgroups in index order;
-// the host also keeps num_chunks at most half the workgroups of that kernel
-// the device holds at once (fused_blocks_per_cu per compute unit) and at most
-// 256, so the polling chunk workgroups of several concurrent fused launches
-// cannot fill an XCD either.
+// (num_tiles + num_chunks workgroups, roles from fused_role).  Its waits end
+// because every chunk workgroup waits only for workgroups of lower index in
+// the same launch and each XCD dispatches its workgroups in index order.
 hipError_t launch_fused(const LaunchArgs& args, bool vec4, hipStream_t stream);
-hipError_t fused_blocks_per_cu(bool vec4, int* blocks);
 hipError_t launch_ticket(const LaunchArgs& args, bool vec4, hipStream_t stream);
 // The sweep: num_tiles / num_chunks are the totals over the table's segments.
 hipError_t launch_sweep(const LaunchArgs& args, const SweepTable& table, bool vec4, hipStream_t stream);

@@ -40,11 +40,10 @@
 //     merged sequence of tiles and pairs, whatever the clustering of the
 //     selection; it also stores the counts into mapped host memory.
 //   stream_scan_kernel (fused staged schedule, the default of a single
-//     partition of up to 256 chunks, and never more than half as many as
-//     the device holds resident workgroups): the stream and scan kernels'
-//     work in one launch, the chunk workgroups after the tile workgroups,
-//     polling epoch-tagged tile words; saves a launch and its drain between
-//     the streaming pass and the scan.
+//     partition): the stream and scan kernels' work in one launch, each chunk
+//     workgroup placed two chunks of tiles after its own chunk's tiles (the
+//     last ones after all tiles), polling epoch-tagged tile words; the scans
+//     run while the stream goes on, and a launch and its drain are saved.
 //   HBM traffic beyond the 12 bytes per value of the stream: 16 bytes per
 //   selected value (staged write and read) and 8 bytes per 1024 values.
 // Sweep: the same three kernels over a table of segments (every partition of
@@ -471,7 +470,7 @@ __device__ __forceinline__ void publish_tile(const LaunchArgs& a, uint32_t tile,
 // norm of its new residual (also for a tile left to the move kernel, whose
 // new residual is fixed by its selection bits all the same).
 template <int VEC, int ROWS, bool SWEEP, bool FUSED = false>
-__device__ __forceinline__ void stream_tile(LaunchArgs a, const SweepTable* tbl) {
+__device__ __forceinline__ void stream_tile(LaunchArgs a, const SweepTable* tbl, uint32_t tile) {
     constexpr int WAVES = kStreamBlock / kWaveSize;
     static_assert(VEC * ROWS * kStreamBlock == kStreamTile, "tile size");
     __shared__ uint32_t s_wave_total[ROWS * WAVES];
@@ -481,7 +480,6 @@ __device__ __forceinline__ void stream_tile(LaunchArgs a, const SweepTable* tbl)
     const int tid = threadIdx.x;
     const int lane = tid & (kWaveSize - 1);
     const int wave = tid / kWaveSize;
-    const uint32_t tile = blockIdx.x;
     const int64_t tile_base = SWEEP ? enter_segment(a, tbl, tile) : a.base + static_cast<int64_t>(tile) * kStreamTile;
 
     Tile<VEC, ROWS, kStreamBlock> t;
@@ -531,12 +529,12 @@ __device__ __forceinline__ void stream_tile(LaunchArgs a, const SweepTable* tbl)
 
 template <int VEC, int ROWS>
 __global__ __launch_bounds__(kStreamBlock) void stream_kernel(LaunchArgs a) {
-    stream_tile<VEC, ROWS, false>(a, nullptr);
+    stream_tile<VEC, ROWS, false>(a, nullptr, blockIdx.x);
 }
 
 template <int VEC, int ROWS>
 __global__ __launch_bounds__(kStreamBlock) void stream_sweep_kernel(LaunchArgs a, SweepTable tbl) {
-    stream_tile<VEC, ROWS, true>(a, &tbl);
+    stream_tile<VEC, ROWS, true>(a, &tbl, blockIdx.x);
 }
 
 // Full processing of one flagged tile by one wavefront with its pairs from
@@ -697,12 +695,12 @@ constexpr int kLookbackPolls = 4;  // polls of a silent predecessor before its c
 // so a predecessor may not have run yet: a word still unpublished after a few
 // polls is replaced by the predecessor's count summed from its tile counts,
 // which are final before the scan kernel starts.  The look-back therefore
-// ends whatever order the workgroups run in.  In the fused schedule the chunk
-// workgroups start as the stream workgroups drain, far apart, and a recompute
-// would have to wait for tile words anyway: there the look-back polls until
-// each predecessor has published (a chunk workgroup publishes its aggregate
-// as soon as its tile words are in, before its own look-back, so the wait
-// depends on stream workgroups only).
+// ends whatever order the workgroups run in.  In the fused schedule a
+// predecessor's tile words may still be missing, so a recompute would have to
+// wait for them anyway: there the look-back polls until each predecessor has
+// published (a chunk workgroup publishes its aggregate as soon as its tile
+// words are in, before its own look-back, so the wait depends on stream
+// workgroups only, and its predecessors sit at lower indices of the launch).
 // Each round a lane reads kLookbackDepth words, so a round covers 256
 // predecessors (the GPT-1.3B partition's 1,285 chunks need at most six
 // rounds instead of twenty-one).  In the fused schedule `first` holds the
@@ -783,7 +781,7 @@ __device__ uint32_t chunk_lookback(const LaunchArgs& a, const SweepTable* tbl, u
 // FUSED: the same work by the chunk workgroups of stream_scan_kernel, which
 // poll their chunk's epoch-tagged tile words instead of reading final counts.
 template <bool SWEEP, bool FUSED = false>
-__device__ __forceinline__ void scan_chunk(const LaunchArgs& a, const SweepTable* tbl) {
+__device__ __forceinline__ void scan_chunk(const LaunchArgs& a, const SweepTable* tbl, uint32_t chunk) {
     constexpr int WAVES = kScanBlock / kWaveSize;
     constexpr int PER_THREAD = kChunkTiles / kScanBlock;
     static_assert(PER_THREAD % 4 == 0, "whole uint4s of counts per thread");
@@ -796,8 +794,6 @@ __device__ __forceinline__ void scan_chunk(const LaunchArgs& a, const SweepTable
     const int lane = tid & (kWaveSize - 1);
     const int wave = tid / kWaveSize;
     if (tid == 0) s_num_flagged = 0;
-    // fused schedule: the chunk workgroups follow the num_tiles stream ones
-    const uint32_t chunk = FUSED ? blockIdx.x - a.num_tiles : blockIdx.x;
     uint32_t chunk_tile, end_tile;
     chunk_tiles<SWEEP>(a, tbl, chunk, chunk_tile, end_tile);
     const uint32_t first_tile = chunk_tile + tid * PER_THREAD;
@@ -901,7 +897,7 @@ __device__ __forceinline__ void scan_chunk(const LaunchArgs& a, const SweepTable
     for (uint32_t f = tid; f < flagged; f += kScanBlock) a.flagged_list[s_list_base + f] = s_flagged[f];
 }
 
-__global__ __launch_bounds__(kScanBlock) void scan_kernel(LaunchArgs a) { scan_chunk<false>(a, nullptr); }
+__global__ __launch_bounds__(kScanBlock) void scan_kernel(LaunchArgs a) { scan_chunk<false>(a, nullptr, blockIdx.x); }
 
 // Fused schedule: workgroups [0, num_tiles) stream the tiles (stream_kernel's
 // work, publishing epoch-tagged tile words), workgroups [num_tiles,
@@ -916,23 +912,23 @@ __global__ __launch_bounds__(kScanBlock) void scan_kernel(LaunchArgs a) { scan_c
 // workgroup is dispatched once the lower-index workgroups of the launch on
 // its XCD have freed a slot.  By induction on the index, the lowest
 // unfinished workgroup of the launch is always dispatched eventually and
-// never waits for an unfinished one, so every wait ends.  What could still
-// withhold a slot is other resident work that waits too: the host caps the
-// chunk workgroups at 256 and at half the workgroups of this kernel the
-// device holds at once (1/8 of it on MI355X, 32 per XCD), so the chunk
-// workgroups of all the fused launches one process can have running at once
-// (HIP's default of four hardware queues) cannot fill an XCD.
+// never waits for an unfinished one, so every wait ends.  Since each chunk
+// workgroup follows its own chunk's tiles by two chunks of tiles (fused_role),
+// it mostly finds them published, and at any moment only the few whose tiles
+// are still finishing poll, so they hold a negligible share of the slots that
+// other resident work could need.
 template <int VEC, int ROWS>
 __global__ __launch_bounds__(kStreamBlock) void stream_scan_kernel(LaunchArgs a) {
     static_assert(kStreamBlock == kScanBlock, "one workgroup size for both parts");
-    if (blockIdx.x < a.num_tiles)
-        stream_tile<VEC, ROWS, false, true>(a, nullptr);
+    const FusedRole role = fused_role(blockIdx.x, a.num_tiles, a.num_chunks);
+    if (role.scan)
+        scan_chunk<false, true>(a, nullptr, role.item);
     else
-        scan_chunk<false, true>(a, nullptr);
+        stream_tile<VEC, ROWS, false, true>(a, nullptr, role.item);
 }
 
 __global__ __launch_bounds__(kScanBlock) void scan_sweep_kernel(LaunchArgs a, SweepTable tbl) {
-    scan_chunk<true>(a, &tbl);
+    scan_chunk<true>(a, &tbl, blockIdx.x);
 }
 
 // Number of output pairs before item x of the merged sequence, given the tile
@@ -1301,11 +1297,6 @@ hipError_t launch_fused(const LaunchArgs& args, bool vec4, hipStream_t stream) {
         hipLaunchKernelGGL(move_kernel<1>, grid_move, dim3(kMoveBlock), 0, stream, args);
     }
     return hipGetLastError();
-}
-
-hipError_t fused_blocks_per_cu(bool vec4, int* blocks) {
-    return vec4 ? hipOccupancyMaxActiveBlocksPerMultiprocessor(blocks, stream_scan_kernel<4, 1>, kStreamBlock, 0)
-                : hipOccupancyMaxActiveBlocksPerMultiprocessor(blocks, stream_scan_kernel<1, 4>, kStreamBlock, 0);
 }
 
 hipError_t launch_sweep(const LaunchArgs& args, const SweepTable& table, bool vec4, hipStream_t stream) {

@@ -332,28 +332,37 @@ def test_fused_and_separate_scans_on_one_context():
         sp.close()
 
 
-def test_fused_launch_up_to_256_chunks():
-    """The fused stream-and-scan launch takes partitions of up to 256 scan
-    chunks (2^28 values); one more tile and the scan runs as its own launch.
-    Both sides of the limit give the oracle's bits."""
-    rng = np.random.default_rng(256)
-    for N, want in [(256 << 20, 1), ((256 << 20) + 1, 0)]:
-        note(f"fused limit N={N}")
-        g = rng.standard_normal(N, dtype=np.float32)
-        res = np.zeros(N, np.float32)
-        sp = micro.Sparsifier(N, device=DEV, variant=STAGED)
-        g_dev = torch.from_numpy(g).to(DEV)
-        r_dev = torch.zeros(N, dtype=torch.float32, device=DEV)
-        k, th, idx, val = sp.step(g_dev, r_dev, 0, 1, 0.01, 2.6)
-        assert sp.last_stats()[3] == want, N
-        o_idx, o_val, k_or, th_or = oracle.step(g, res, 0, 1, 0.01, 2.6)
-        assert (k, th) == (k_or, th_or), N
-        assert np.array_equal(idx.cpu().numpy(), o_idx), N
-        assert first_mismatch(val.cpu().numpy(), o_val) < 0, N
-        assert first_mismatch(r_dev.cpu().numpy(), res) < 0, N
-        sp.close()
-        del g_dev, r_dev
-        torch.cuda.empty_cache()
+@pytest.mark.parametrize("N", [
+    2 << 20,                     # 2,048 tiles, 2 chunks: every scan workgroup after the tiles
+    3 << 20,                     # 3 chunks: chunk 0's scan workgroup among the tiles
+    (3 << 20) + 1,               # one more tile, a one-tile last chunk
+    (7 << 20) + 17 * 1024 + 5,   # ragged last tile, five interleaved chunks
+    (256 << 20) + 1,             # 257 chunks
+])
+def test_fused_launch_interleaves_scan_workgroups(N):
+    """The fused stream-and-scan launch places the scan workgroup of chunk c
+    after the tiles of chunk c + 2 and the last chunks' after all tiles; it
+    takes every partition (stats fused = 1).  Sizes around the boundaries of
+    that layout give the oracle's bits."""
+    note(f"fused layout N={N}")
+    rng = np.random.default_rng(N % 1000)
+    g = rng.standard_normal(N, dtype=np.float32)
+    g[N // 3:N // 3 + 300_000] *= 30.0  # a dense region: its tiles overflow their staging slots
+    res = np.zeros(N, np.float32)
+    sp = micro.Sparsifier(N, device=DEV, variant=STAGED)
+    g_dev = torch.from_numpy(g).to(DEV)
+    r_dev = torch.zeros(N, dtype=torch.float32, device=DEV)
+    k, th, idx, val = sp.step(g_dev, r_dev, 0, 1, 0.01, 2.6)
+    assert sp.last_stats()[3] == 1, N
+    assert sp.last_stats()[1] > 0, N  # tiles redone by the move kernel
+    o_idx, o_val, k_or, th_or = oracle.step(g, res, 0, 1, 0.01, 2.6)
+    assert (k, th) == (k_or, th_or), N
+    assert np.array_equal(idx.cpu().numpy(), o_idx), N
+    assert first_mismatch(val.cpu().numpy(), o_val) < 0, N
+    assert first_mismatch(r_dev.cpu().numpy(), res) < 0, N
+    sp.close()
+    del g_dev, r_dev
+    torch.cuda.empty_cache()
 
 
 def test_auto_schedule_picks_by_partition_length():
