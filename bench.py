@@ -203,7 +203,7 @@ class Run:
         self.log = []   # (rank, P, k, kernel_ms, tiles redone by the move kernel)
         self.records = [] if keep_records else None  # one dict per call for --steps-jsonl
         self.variant = None  # schedule of the last step
-        self.fused = False   # whether its stream and scan passes ran as one launch
+        self.fused = 0       # whether its stream and scan passes ran as one launch
 
     def step(self, timed):
         g = self.pool[self.t % len(self.pool)]
@@ -211,17 +211,17 @@ class Run:
             p = self.micro.micro_cycle(self.t, worker, self.w.world) if self.cycle else worker
             _, ln = self.bounds[p]
             theta_in = self.theta[p]
-            t0 = time.perf_counter()
+            t0 = time.perf_counter() if self.records is not None else 0.0
             k, th, _, _ = self.sp.step(g, self.res, p, self.w.world, self.d, theta_in,
                                        self.out_idx, self.out_val)
-            wall_s = time.perf_counter() - t0
             self.theta[p] = th
             kernel_ms, redone, variant, fused = self.sp.last_stats()
             self.log.append((p, ln, k, kernel_ms if timed else None, redone))
             self.variant = variant
-            self.fused = bool(fused)
+            self.fused = fused
             if self.records is None:
                 continue
+            wall_s = time.perf_counter() - t0
             alg = 12 * ln + 8 * k
             self.records.append({
                 "workload": self.w.name, "t": self.t, "timed": timed, "rank": p, "P": ln, "k": k,
@@ -452,13 +452,42 @@ def measure_union(w, density, g, sp, warmup, steps):
     alg_u = 16 * m
     kg = sum(a for a, _ in log) / 1e3
     ku = sum(b for _, b in log) / 1e3
-    return {"g_entries_s": m * steps / elapsed / 1e9, "union_len": m, "own_len": k_own,
+    vendor = vendor_union_ops(union, res, x, out, w.world, warmup, steps)
+    return {"g_entries_s": m * steps / elapsed / 1e9, "union_len": m, "own_len": k_own, "vendor": vendor,
             "wall_gbs": (alg_g + alg_u) * steps / elapsed / 1e9,
             "kernel_gbs": (alg_g + alg_u) * steps / (kg + ku) / 1e9,
             "gather_ms_avg": kg * 1e3 / steps, "update_ms_avg": ku * 1e3 / steps,
             "gather_gbs": alg_g * steps / kg / 1e9, "update_gbs": alg_u * steps / ku / 1e9,
             "alg_bytes_per_launch": (alg_g + alg_u), "ms_per_step": elapsed * 1e3 / steps,
             "union": union, "own_first": own_first, "own_val": own_val}
+
+
+def vendor_union_ops(union, res, x, out, world, warmup, steps):
+    """torch's own random-access kernels on the same union, event-timed on
+    torch's stream, for comparison with the union kernels: a gather
+    (index_select), a scatter of zeros (index_fill_) and a scatter-add
+    (index_add_) at the union's indices (torch takes int64 indices)."""
+    import torch
+    idx64 = union.long()
+    stream = torch.cuda.current_stream()
+    vals = out.clone()
+
+    def timed(fn):
+        ms = []
+        for i in range(warmup + steps):
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record(stream)
+            fn()
+            e1.record(stream)
+            e1.synchronize()
+            if i >= warmup:
+                ms.append(e0.elapsed_time(e1))
+        return sum(ms) / len(ms)
+
+    return {"index_select_ms": timed(lambda: torch.index_select(res, 0, idx64)),
+            "index_fill_ms": timed(lambda: res.index_fill_(0, idx64, 0.0)),
+            "index_add_ms": timed(lambda: x.index_add_(0, idx64, vals, alpha=-1.0 / world)),
+            "entries": union.numel()}
 
 
 def cpu_baseline_ef(w, density, pool, target_s):
@@ -692,6 +721,7 @@ def main_path(args, w, head, pool, n_pool, sp):
                              "gather_ms_avg": r["gather_ms_avg"], "update_ms_avg": r["update_ms_avg"],
                              "gather_gbs": r["gather_gbs"], "update_gbs": r["update_gbs"],
                              "alg_bytes_per_launch": r["alg_bytes_per_launch"]},
+                "vendor_random_access": r["vendor"],
                 "cpu_baseline": cpu}
     print(json.dumps(line), flush=True)
 

@@ -68,6 +68,9 @@ typedef enum micro_status {
 #define MICRO_RULE_PROPORTIONAL 0 /* theta * clamp(1 + beta*(k - k*)/k*, lo, hi) */
 #define MICRO_RULE_FIXED_STEP 1   /* theta * (1 + alpha) if k > k*,
                                      theta * (1 - alpha) if k < k*, else theta   */
+#define MICRO_RULE_HARD_THRESHOLD 2 /* theta never changes: the hard-threshold
+                                       sparsifier the paper compares with
+                                       (Sec. 1, Sec. 5.2), a fixed threshold  */
 
 /* Kernel schedules (both compute the same result). */
 #define MICRO_VARIANT_AUTO 0   /* per call, the faster measured schedule: TICKET

@@ -16,13 +16,15 @@ provides device memory and the stream.
 import ctypes
 
 from . import _lib
-from ._lib import (MICRO_FLAG_SEPARATE_SCAN, MICRO_FLAG_TIME_KERNEL, MICRO_RULE_FIXED_STEP, MICRO_RULE_PROPORTIONAL,
-                   MICRO_VARIANT_AUTO, MICRO_VARIANT_STAGED, MICRO_VARIANT_TICKET, MicroError, default_config,
-                   micro_cycle, micro_estimate_threshold, micro_partition, micro_threshold_f32)
+from ._lib import (MICRO_FLAG_SEPARATE_SCAN, MICRO_FLAG_TIME_KERNEL, MICRO_RULE_FIXED_STEP,
+                   MICRO_RULE_HARD_THRESHOLD, MICRO_RULE_PROPORTIONAL, MICRO_VARIANT_AUTO, MICRO_VARIANT_STAGED,
+                   MICRO_VARIANT_TICKET, MicroError, default_config, micro_cycle, micro_estimate_threshold,
+                   micro_partition, micro_threshold_f32)
 
 __all__ = ["Sparsifier", "MicroError", "default_config", "micro_partition", "micro_cycle",
            "micro_estimate_threshold", "micro_threshold_f32", "MICRO_RULE_PROPORTIONAL",
-           "MICRO_RULE_FIXED_STEP", "MICRO_VARIANT_AUTO", "MICRO_VARIANT_TICKET", "MICRO_VARIANT_STAGED",
+           "MICRO_RULE_FIXED_STEP", "MICRO_RULE_HARD_THRESHOLD", "MICRO_VARIANT_AUTO", "MICRO_VARIANT_TICKET",
+           "MICRO_VARIANT_STAGED",
            "MICRO_FLAG_TIME_KERNEL", "MICRO_FLAG_SEPARATE_SCAN"]
 
 
@@ -67,6 +69,14 @@ class Sparsifier:
         self._stats_p = ctypes.pointer(self._stats_c)
         self._f32, self._i32 = torch.float32, torch.int32
         self._tensor = torch.Tensor
+        # the sweep's and the full pass's marshalling objects
+        self._sweep_fn = lib.micro_sweep_step
+        self._ef_fn = lib.micro_ef_step
+        self._sweep_arrays = {}  # world -> (thetas, ks, sumsq ctypes arrays and their addresses)
+        self._cycle_c = ctypes.c_int32()
+        self._cycle_p = ctypes.pointer(self._cycle_c)
+        self._sumsq_c = ctypes.c_double()
+        self._sumsq_p = ctypes.pointer(self._sumsq_c)
 
     def close(self):
         if getattr(self, "_ctx", None) is not None:
@@ -116,16 +126,7 @@ class Sparsifier:
         length = self._length(rank, world)
         if out_idx is None or out_val is None:
             out_idx, out_val = self.outputs(length)
-        f32 = self._f32
-        if not (self._fits(grad, f32) and self._fits(residual, f32) and self._fits(out_idx, self._i32)
-                and self._fits(out_val, f32)):
-            # name the offending argument
-            self._check(grad, "grad", f32)
-            self._check(residual, "residual", f32)
-            self._check(out_idx, "out_idx", self._i32)
-            self._check(out_val, "out_val", f32)
-        if grad.numel() != self.n_total or residual.numel() != self.n_total:
-            raise ValueError(f"grad and residual must hold {self.n_total} values")
+        self._check_vectors(grad, residual, out_idx, out_val)
         if out_idx.numel() < length or out_val.numel() < length:
             raise ValueError(f"output capacity below the partition length {length}")
         self._theta_c.value = float(theta)
@@ -136,6 +137,18 @@ class Sparsifier:
         k = self._k_c.value
         return k, self._theta_c.value, out_idx[:k], out_val[:k]
 
+    def _check_vectors(self, grad, residual, out_idx, out_val):
+        f32 = self._f32
+        if not (self._fits(grad, f32) and self._fits(residual, f32) and self._fits(out_idx, self._i32)
+                and self._fits(out_val, f32)):
+            # name the offending argument
+            self._check(grad, "grad", f32)
+            self._check(residual, "residual", f32)
+            self._check(out_idx, "out_idx", self._i32)
+            self._check(out_val, "out_val", f32)
+        if grad.numel() != self.n_total or residual.numel() != self.n_total:
+            raise ValueError(f"grad and residual must hold {self.n_total} values")
+
     def ef_step(self, grad, residual, t, worker, world, density, theta, out_idx=None, out_val=None,
                 local_error=False):
         """Algorithm 1 for `worker` at iteration t over the whole vector: every
@@ -143,50 +156,55 @@ class Sparsifier:
         Returns (k, theta_next, cycle, idx[:k], val[:k]); with local_error,
         (k, theta_next, cycle, idx[:k], val[:k], sumsq) where sumsq is the
         squared norm of the whole new residual."""
-        import torch
         if self._ctx is None:
             raise RuntimeError("Sparsifier is closed")
-        self._check(grad, "grad", torch.float32)
-        self._check(residual, "residual", torch.float32)
-        if grad.numel() != self.n_total or residual.numel() != self.n_total:
-            raise ValueError(f"grad and residual must hold {self.n_total} values")
-        _, length = self.partition(_lib.micro_cycle(t, worker, world), world)
+        length = self._length(_lib.micro_cycle(t, worker, world), world)
         if out_idx is None or out_val is None:
             out_idx, out_val = self.outputs(length)
-        self._check(out_idx, "out_idx", torch.int32)
-        self._check(out_val, "out_val", torch.float32)
+        self._check_vectors(grad, residual, out_idx, out_val)
         if out_idx.numel() < length or out_val.numel() < length:
             raise ValueError(f"output capacity below the partition length {length}")
-        k, th, c, sq = _lib.micro_ef_step(self._ctx, grad.data_ptr(), residual.data_ptr(), t, worker, world,
-                                          density, theta, out_idx.data_ptr(), out_val.data_ptr(), local_error)
+        self._theta_c.value = float(theta)
+        st = self._ef_fn(self._ctx, grad.data_ptr(), residual.data_ptr(), int(t), int(worker), int(world),
+                         float(density), self._theta_p, out_idx.data_ptr(), out_val.data_ptr(), self._k_p,
+                         self._cycle_p, self._sumsq_p if local_error else None)
+        if st:
+            _lib.check(st, self._ctx)
+        k = self._k_c.value
         if local_error:
-            return k, th, c, out_idx[:k], out_val[:k], sq
-        return k, th, c, out_idx[:k], out_val[:k]
+            return k, self._theta_c.value, self._cycle_c.value, out_idx[:k], out_val[:k], self._sumsq_c.value
+        return k, self._theta_c.value, self._cycle_c.value, out_idx[:k], out_val[:k]
 
     def sweep(self, grad, residual, world, density, thetas, out_idx=None, out_val=None, want_sumsq=True):
         """Every partition of `world` searched once, each with its own
         threshold, in one launch of each kernel.  Returns (k list, thetas_next
         list, sumsq list or None, idx[:sum k], val[:sum k]); partition r's
         pairs start at sum(k[:r])."""
-        import torch
         if self._ctx is None:
             raise RuntimeError("Sparsifier is closed")
-        self._check(grad, "grad", torch.float32)
-        self._check(residual, "residual", torch.float32)
-        if grad.numel() != self.n_total or residual.numel() != self.n_total:
-            raise ValueError(f"grad and residual must hold {self.n_total} values")
+        world = int(world)
         if len(thetas) != world:
             raise ValueError("one threshold per partition")
         if out_idx is None or out_val is None:
             out_idx, out_val = self.outputs(self.n_total)
-        self._check(out_idx, "out_idx", torch.int32)
-        self._check(out_val, "out_val", torch.float32)
+        self._check_vectors(grad, residual, out_idx, out_val)
         if out_idx.numel() < self.n_total or out_val.numel() < self.n_total:
             raise ValueError(f"output capacity below n_total {self.n_total}")
-        k, th, sq = _lib.micro_sweep_step(self._ctx, grad.data_ptr(), residual.data_ptr(), world, density,
-                                          thetas, out_idx.data_ptr(), out_val.data_ptr(), want_sumsq)
+        arrays = self._sweep_arrays.get(world)
+        if arrays is None:
+            n = max(1, world)
+            th, kk, sq = (ctypes.c_double * n)(), (ctypes.c_int64 * n)(), (ctypes.c_double * n)()
+            arrays = (th, kk, sq, ctypes.addressof(th), ctypes.addressof(kk), ctypes.addressof(sq))
+            self._sweep_arrays[world] = arrays
+        th, kk, sq, th_a, kk_a, sq_a = arrays
+        th[:world] = [float(x) for x in thetas]
+        st = self._sweep_fn(self._ctx, grad.data_ptr(), residual.data_ptr(), world, float(density), th_a,
+                            out_idx.data_ptr(), out_val.data_ptr(), kk_a, sq_a if want_sumsq else None)
+        if st:
+            _lib.check(st, self._ctx)
+        k = kk[:world]
         total = sum(k)
-        return k, th, sq, out_idx[:total], out_val[:total]
+        return k, th[:world], (sq[:world] if want_sumsq else None), out_idx[:total], out_val[:total]
 
     def union_gather(self, residual, union_idx, own_first, own_val, out=None):
         """The accumulated values at the union of the workers' selections and

@@ -104,7 +104,8 @@ micro_status hip_fail(micro_ctx* ctx, hipError_t err, const char* what) {
 }
 
 bool config_valid(const micro_config& c) {
-    if (c.rule != MICRO_RULE_PROPORTIONAL && c.rule != MICRO_RULE_FIXED_STEP) return false;
+    if (c.rule != MICRO_RULE_PROPORTIONAL && c.rule != MICRO_RULE_FIXED_STEP && c.rule != MICRO_RULE_HARD_THRESHOLD)
+        return false;
     if (!std::isfinite(c.beta) || c.beta < 0.0) return false;
     if (!std::isfinite(c.lo) || !std::isfinite(c.hi) || !(c.lo > 0.0) || !(c.hi >= c.lo)) return false;
     if (!std::isfinite(c.alpha) || c.alpha < 0.0 || !(c.alpha < 1.0)) return false;
@@ -123,10 +124,11 @@ bool theta_valid(double t) { return std::isfinite(t) && t > 0.0; }
 // target count is d * P; the proportional rule multiplies the threshold by
 // 1 + beta * (k - target) / target clamped to [lo, hi]; the fixed-step rule
 // by 1 + alpha or 1 - alpha according to the sign of k - target.  Each
-// operation is one IEEE binary64 rounding, in this order.
+// operation is one IEEE binary64 rounding, in this order.  The
+// hard-threshold comparator keeps the threshold as it is.
 double next_threshold(const micro_config& c, double density, int64_t part_len, int64_t k,
                       double theta) {
-    if (part_len == 0) return theta;
+    if (part_len == 0 || c.rule == MICRO_RULE_HARD_THRESHOLD) return theta;
     const double target = density * static_cast<double>(part_len);
     const double got = static_cast<double>(k);
     if (c.rule == MICRO_RULE_FIXED_STEP) {

@@ -59,11 +59,14 @@ class ParityRun:
         self.d = density
         self.N = w.n_total
         self.dev = torch.device(device)
-        self.sp = micro.Sparsifier(self.N, device=self.dev,
-                                   rule=micro.MICRO_RULE_PROPORTIONAL if rule_kind == oracle.PROPORTIONAL
-                                   else micro.MICRO_RULE_FIXED_STEP, variant=variant,
+        # rule_kind: oracle.PROPORTIONAL, oracle.FIXED_STEP or "hard" (the
+        # library's hard-threshold rule against the oracle's zero fixed step)
+        lib_rule = {oracle.PROPORTIONAL: micro.MICRO_RULE_PROPORTIONAL, oracle.FIXED_STEP: micro.MICRO_RULE_FIXED_STEP,
+                    "hard": micro.MICRO_RULE_HARD_THRESHOLD}[rule_kind]
+        self.sp = micro.Sparsifier(self.N, device=self.dev, rule=lib_rule, variant=variant,
                                    separate_scan=separate_scan)
-        self.rule = oracle.make_rule(rule_kind)
+        self.rule = (oracle.make_rule(oracle.FIXED_STEP, alpha=0.0) if rule_kind == "hard"
+                     else oracle.make_rule(rule_kind))
         self.res_dev = torch.zeros(self.N, dtype=torch.float32, device=self.dev)
         self.g_dev = torch.empty(self.N, dtype=torch.float32, device=self.dev)
         pin = torch.cuda.is_available()
@@ -84,6 +87,7 @@ class ParityRun:
         self.thetas = {}
         for r, (s, ln) in self.bounds.items():
             self.thetas[r] = synth.initial_theta(self.w, self.g_dev, s, s + ln, self.d)
+        self.thetas0 = dict(self.thetas)
 
     def check_rank(self, t, r):
         s, ln = self.bounds[r]

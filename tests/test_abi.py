@@ -79,6 +79,24 @@ def test_threshold_update_matches_oracle(kind):
         assert _lib.micro_estimate_threshold(d, P, k, th, cfg) == oracle.estimate(d, P, k, th, rule)
 
 
+def test_hard_threshold_rule_keeps_the_threshold():
+    """MICRO_RULE_HARD_THRESHOLD (the paper's hard-threshold comparator) never
+    changes theta, and equals the oracle's fixed-step rule with a zero step,
+    whose binary64 theta * (1 +- 0) is theta exactly."""
+    rng = np.random.default_rng(7)
+    cfg = _lib.default_config()
+    cfg.rule = _lib.MICRO_RULE_HARD_THRESHOLD
+    rule = oracle.make_rule(oracle.FIXED_STEP, alpha=0.0)
+    for _ in range(5000):
+        P = int(rng.integers(1, 2**31))
+        k = int(rng.integers(0, P + 1))
+        d = float(rng.choice([1e-3, 1e-2, 0.5, float(rng.uniform(1e-6, 1))]))
+        th = float(np.exp(rng.uniform(-40, 20)))
+        got = _lib.micro_estimate_threshold(d, P, k, th, cfg)
+        assert got == th
+        assert got == oracle.estimate(d, P, k, th, rule)
+
+
 def test_threshold_update_rejects_bad_arguments():
     for args in [(0.0, 10, 1, 1.0), (1.5, 10, 1, 1.0), (float("nan"), 10, 1, 1.0),
                  (0.1, -1, 0, 1.0), (0.1, 10, 11, 1.0), (0.1, 10, -1, 1.0)]:
