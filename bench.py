@@ -76,7 +76,7 @@ def parse_args():
     ap.add_argument("--path", default="step", choices=["step", "ef", "union", "sweep", "ceiling"],
                     help="step: the partition-only sparsify step (default); ef: the full error-feedback "
                          "pass with cyclic partitions; union: the gather/reset and model update around "
-                         "the exchange; sweep: every partition in one launch of each kernel, with the "
+                         "the exchange; sweep: every partition in one set of launches, with the "
                          "local-error norms; ceiling: vendor streams (torch's in-place add, a device "
                          "copy) beside the step on the same vector")
     ap.add_argument("--local-error", action="store_true",
@@ -395,7 +395,8 @@ def measure_sweep(w, density, pool, sp, warmup, steps):
     return {"g_elem_s": sum(n for n, _, _ in log) / elapsed / 1e9, "wall_gbs": alg / elapsed / 1e9,
             "kernel_gbs": alg / kernel_s / 1e9, "kernel_ms_avg": kernel_s * 1e3 / len(log),
             "alg_bytes_per_launch": alg / len(log), "ms_per_step": elapsed * 1e3 / steps,
-            "k_avg": sum(k for _, k, _ in log) / len(log), "local_error_last": errs[-1]}
+            "k_avg": sum(k for _, k, _ in log) / len(log), "local_error_last": errs[-1],
+            "fused": bool(sp.last_stats()[3])}
 
 
 def build_union(w, density, g, sp):
@@ -682,8 +683,9 @@ def main_path(args, w, head, pool, n_pool, sp):
                 "config": cfg, "k_avg": r["k_avg"], "local_error_last": r["local_error_last"],
                 "roofline": {"bound": "hbm", "achieved": r["kernel_gbs"], "peak": HBM_PEAK_GBS, "unit": "GB/s",
                              "frac": r["kernel_gbs"] / HBM_PEAK_GBS, "traffic": traffic,
-                             "kernel": "stream_sweep_kernel + scan_sweep_kernel + move_sweep_kernel "
-                                       "(one sweep, event-timed together)",
+                             "kernel": ("stream_scan_sweep_kernel + move_sweep_kernel" if r["fused"] else
+                                        "stream_sweep_kernel + scan_sweep_kernel + move_sweep_kernel")
+                                       + " (one sweep, event-timed together)",
                              "kernel_ms_avg": r["kernel_ms_avg"], "alg_bytes_per_launch": r["alg_bytes_per_launch"]},
                 "cpu_baseline": cpu}
     elif args.path == "ef":
@@ -697,8 +699,9 @@ def main_path(args, w, head, pool, n_pool, sp):
                 "config": cfg, "k_avg": r["k_avg"],
                 "roofline": {"bound": "hbm", "achieved": r["kernel_gbs"], "peak": HBM_PEAK_GBS, "unit": "GB/s",
                              "frac": r["kernel_gbs"] / HBM_PEAK_GBS, "traffic": traffic,
-                             "kernel": ("stream_sweep_kernel + scan_sweep_kernel + move_sweep_kernel over three "
-                                        "segments (one pass with the local error, event-timed together)"
+                             "kernel": (("stream_scan_sweep_kernel + move_sweep_kernel" if r["fused"] else
+                                         "stream_sweep_kernel + scan_sweep_kernel + move_sweep_kernel")
+                                        + " over three segments (one pass with the local error, event-timed together)"
                                         if args.local_error else
                                         "accumulate_kernel + stream_scan_kernel + move_kernel "
                                         "(one pass, event-timed together)" if r["fused"] else

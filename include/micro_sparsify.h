@@ -196,9 +196,11 @@ MICRO_API micro_status micro_sparsify_step_noalloc(const float *grad, float *res
 
 /*
  * Every partition r of `world` (1 <= world <= 64) searched once over one
- * vector, each with its own threshold, in one launch of each kernel: the
- * selections all n workers make at one iteration (Sec. 4.2), with the local
- * error of Sec. 2 / Eq. 1 reduced on the way.
+ * vector, each with its own threshold, in one set of launches (the streaming
+ * and scan passes of all partitions as one launch for vectors of up to 64
+ * scan chunks of a million values, unless MICRO_FLAG_SEPARATE_SCAN, then one
+ * placing launch): the selections all n workers make at one iteration
+ * (Sec. 4.2), with the local error of Sec. 2 / Eq. 1 reduced on the way.
  *   grad, residual  device, n_total fp32; residual in/out over all of it.
  *   theta      host double[world], in/out: theta[r] for partition r, then its
  *              next threshold (Sec. 4.3 over P_r).  Each finite and > 0.

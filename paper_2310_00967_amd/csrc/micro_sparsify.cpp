@@ -36,7 +36,6 @@ struct micro_ctx {
     uint32_t* d_flagged_list = nullptr;
     uint32_t* d_split_tile = nullptr;
     double* d_tile_sumsq = nullptr;          // sweep: per tile
-    double* d_chunk_sumsq = nullptr;         // sweep: per chunk
     int64_t split_capacity = 0;
     uint2* d_stage = nullptr;                // (index, value bits) pairs
     uint64_t* d_chunk_status = nullptr;
@@ -49,7 +48,7 @@ struct micro_ctx {
     int64_t* h_count = nullptr;              // mapped pinned host memory stored by the kernels: [0] k,
                                              // [1] redone tiles, [2 + r] a sweep's counts
     int64_t* h_count_dev = nullptr;          // the device's address of h_count
-    double* h_sumsq = nullptr;               // mapped pinned host memory: a sweep's squared norms
+    double* h_sumsq = nullptr;               // mapped pinned host memory: a sweep's squared norms, per chunk
     double* h_sumsq_dev = nullptr;
     uint32_t epoch = 0;                      // epoch of the last launch
     bool needs_reset = false;                // scratch state unknown after a failure
@@ -177,7 +176,7 @@ void release(micro_ctx* ctx) {
     if (ctx->device >= 0) (void)hipStreamSynchronize(ctx->stream);
     for (hipEvent_t ev : ctx->ev)
         if (ev) (void)hipEventDestroy(ev);
-    void* device_buffers[] = {ctx->d_tile_counts, ctx->d_tile_excl, ctx->d_flagged_list, ctx->d_split_tile, ctx->d_tile_sumsq, ctx->d_chunk_sumsq, ctx->d_stage,
+    void* device_buffers[] = {ctx->d_tile_counts, ctx->d_tile_excl, ctx->d_flagged_list, ctx->d_split_tile, ctx->d_tile_sumsq, ctx->d_stage,
                               ctx->d_chunk_status, ctx->d_tile_words, ctx->d_status, ctx->d_tickets,
                               ctx->d_count};
     for (void* p : device_buffers)
@@ -211,6 +210,13 @@ uint32_t move_grid(int64_t tiles, int64_t len, int64_t span, int64_t min_blocks)
 // ResNet-50 rank 0 (3.2M values, d = 0.001, about 6,300 items) 26.5%, 27.0%
 // and 27.3%; the GPT-1.3B partition's move kernel took 53 us with 4096-item
 // pieces and 78 us with 2048 (an earlier build of the kernel).
+// Largest sweep, in scan chunks of a million values, whose stream and scan
+// passes run as one launch.  Measured on MI355X (device time per sweep, fused
+// against separate, same box): ResNet-18's 16 partitions (16 chunks) 43.6
+// against 46.9 us, ResNet-50's 8 (32 chunks) 72.4-73.2 against 72.2 us,
+// BERT-large's 8 (320 chunks) 665-667 against 655-657 us.
+constexpr int64_t kFusedSweepMaxChunks = 64;
+
 uint32_t move_span_for(const micro_ctx* ctx, int64_t tiles, double expected_pairs) {
     const double items = static_cast<double>(tiles) + expected_pairs;
     if (items >= 2.0 * ctx->compute_units * micro::kMoveSpan) return micro::kMoveSpan;
@@ -449,12 +455,14 @@ micro_status run_segments(micro_ctx* ctx, const float* grad, float* residual, in
         sg.theta_f = threshold_f[r];
         sg.tile_first = static_cast<uint32_t>(tiles);
         sg.chunk_first = static_cast<uint32_t>(chunks);
+        sg.wg_first = static_cast<uint32_t>(tiles + chunks);  // the fused launch: segment after segment
         const int64_t seg_tiles = lens[r] > 0 ? (sg.end - sg.base + micro::kStreamTile - 1) / micro::kStreamTile : 0;
         tiles += seg_tiles;
         chunks += (seg_tiles + micro::kChunkTiles - 1) / micro::kChunkTiles;
     }
     table.seg[count].tile_first = static_cast<uint32_t>(tiles);
     table.seg[count].chunk_first = static_cast<uint32_t>(chunks);
+    table.seg[count].wg_first = static_cast<uint32_t>(tiles + chunks);
     if (tiles > ctx->tile_capacity || chunks > ctx->chunk_capacity) {
         set_error(ctx, "sweep needs %lld tiles, scratch holds %lld", static_cast<long long>(tiles),
                   static_cast<long long>(ctx->tile_capacity));
@@ -477,11 +485,11 @@ micro_status run_segments(micro_ctx* ctx, const float* grad, float* residual, in
     a.count_out = ctx->d_count;
     a.host_count = ctx->h_count_dev;
     a.tile_counts = ctx->d_tile_counts;
+    a.tile_words = ctx->d_tile_words;
     a.tile_excl = ctx->d_tile_excl;
     a.flagged_list = ctx->d_flagged_list;
     a.split_tile = ctx->d_split_tile;
     a.tile_sumsq = ctx->d_tile_sumsq;
-    a.chunk_sumsq = ctx->d_chunk_sumsq;
     a.host_sumsq = ctx->h_sumsq_dev;
     int64_t total_len = 0;
     for (int32_t r = 0; r < count; ++r) total_len += lens[r];
@@ -499,11 +507,15 @@ micro_status run_segments(micro_ctx* ctx, const float* grad, float* residual, in
     volatile int64_t* host_count = ctx->h_count;
     volatile double* host_sumsq = ctx->h_sumsq;
     for (int i = 0; i < 2 + count; ++i) host_count[i] = -1;
-    for (int32_t r = 0; r < count; ++r) host_sumsq[r] = -1.0;
+    for (int64_t c = 0; c < chunks; ++c) host_sumsq[c] = -1.0;
+    // The stream and scan passes run as one launch for sweeps of up to
+    // kFusedSweepMaxChunks scan chunks, unless the caller asked for the scan
+    // on its own.
+    const bool fused = (ctx->cfg.flags & MICRO_FLAG_SEPARATE_SCAN) == 0 && chunks <= kFusedSweepMaxChunks;
     if (timed && (e = hipEventRecord(ctx->ev[0], ctx->stream)) != hipSuccess)
         return hip_fail(ctx, e, "hipEventRecord");
     ctx->epoch = a.epoch;
-    if ((e = micro::launch_sweep(a, table, vec4, ctx->stream)) != hipSuccess)
+    if ((e = micro::launch_sweep(a, table, vec4, fused, ctx->stream)) != hipSuccess)
         return hip_fail(ctx, e, "sweep kernel launch");
     if (timed && (e = hipEventRecord(ctx->ev[1], ctx->stream)) != hipSuccess)
         return hip_fail(ctx, e, "hipEventRecord");
@@ -512,9 +524,10 @@ micro_status run_segments(micro_ctx* ctx, const float* grad, float* residual, in
     bool ok = host_count[0] >= 0 && host_count[0] <= ctx->n_total;
     for (int32_t r = 0; ok && r < count; ++r) {
         const int64_t kr = host_count[2 + r];
-        ok = kr >= 0 && kr <= lens[r] && host_sumsq[r] != -1.0;  // a NaN residual gives a NaN norm
+        ok = kr >= 0 && kr <= lens[r];
         sum += kr;
     }
+    for (int64_t c = 0; ok && c < chunks; ++c) ok = host_sumsq[c] != -1.0;  // a NaN residual gives a NaN norm
     if (!ok || sum != host_count[0]) {
         set_error(ctx, "device reported inconsistent sweep counts (total %lld)",
                   static_cast<long long>(host_count[0]));
@@ -525,10 +538,13 @@ micro_status run_segments(micro_ctx* ctx, const float* grad, float* residual, in
         return hip_fail(ctx, e, "hipEventElapsedTime");
     ctx->stats.redone_tiles = host_count[1];
     ctx->stats.variant = MICRO_VARIANT_STAGED;
-    ctx->stats.fused = 0;
+    ctx->stats.fused = fused ? 1 : 0;
     for (int32_t r = 0; r < count; ++r) {
         k[r] = host_count[2 + r];
-        sumsq[r] = host_sumsq[r];
+        // the segment's chunks in increasing order
+        double sq = 0.0;
+        for (uint32_t c = table.seg[r].chunk_first; c < table.seg[r + 1].chunk_first; ++c) sq += host_sumsq[c];
+        sumsq[r] = sq;
     }
     return MICRO_OK;
 }
@@ -824,10 +840,7 @@ micro_status micro_sparsify_init(micro_ctx** out, int64_t n_total, void* hip_str
               hipMalloc(&ctx->d_count, 2 * sizeof(int64_t)) == hipSuccess &&
               hipHostMalloc(&ctx->h_count, (2 + micro::kMaxSweep) * sizeof(int64_t),
                             hipHostMallocMapped | hipHostMallocCoherent) == hipSuccess &&
-              hipHostGetDevicePointer(reinterpret_cast<void**>(&ctx->h_count_dev), ctx->h_count, 0) == hipSuccess &&
-              hipHostMalloc(&ctx->h_sumsq, micro::kMaxSweep * sizeof(double),
-                            hipHostMallocMapped | hipHostMallocCoherent) == hipSuccess &&
-              hipHostGetDevicePointer(reinterpret_cast<void**>(&ctx->h_sumsq_dev), ctx->h_sumsq, 0) == hipSuccess;
+              hipHostGetDevicePointer(reinterpret_cast<void**>(&ctx->h_count_dev), ctx->h_count, 0) == hipSuccess;
     if (ok && ctx->has_staged) {
         // a sweep's segments each add at most one tile (alignment) and one chunk
         ctx->tile_capacity = n_total / micro::kStreamTile + 2 + micro::kMaxSweep;
@@ -842,7 +855,9 @@ micro_status micro_sparsify_init(micro_ctx** out, int64_t n_total, void* hip_str
              hipMalloc(&ctx->d_flagged_list, sizeof(uint32_t) * ctx->tile_capacity) == hipSuccess &&
              hipMalloc(&ctx->d_split_tile, sizeof(uint32_t) * ctx->split_capacity) == hipSuccess &&
              hipMalloc(&ctx->d_tile_sumsq, sizeof(double) * ctx->tile_capacity) == hipSuccess &&
-             hipMalloc(&ctx->d_chunk_sumsq, sizeof(double) * ctx->chunk_capacity) == hipSuccess &&
+             hipHostMalloc(&ctx->h_sumsq, sizeof(double) * ctx->chunk_capacity,
+                           hipHostMallocMapped | hipHostMallocCoherent) == hipSuccess &&
+             hipHostGetDevicePointer(reinterpret_cast<void**>(&ctx->h_sumsq_dev), ctx->h_sumsq, 0) == hipSuccess &&
              hipMalloc(&ctx->d_stage, sizeof(uint2) * stage) == hipSuccess &&
              hipMalloc(&ctx->d_chunk_status, sizeof(uint64_t) * ctx->chunk_capacity) == hipSuccess &&
              hipMalloc(&ctx->d_tile_words, sizeof(uint64_t) * ctx->tile_capacity) == hipSuccess;

@@ -84,7 +84,8 @@ struct SweepSegment {
     float theta_f;          // the segment's binary32 threshold
     uint32_t tile_first;    // first global tile of the segment
     uint32_t chunk_first;   // first global scan chunk of the segment
-    uint32_t pad;
+    uint32_t wg_first;      // fused sweep: first workgroup of the segment (its tiles and chunks, laid
+                            // out by fused_role); seg[count].wg_first = the launch's workgroups
 };
 
 struct SweepTable {
@@ -115,8 +116,8 @@ struct LaunchArgs {
     uint32_t* flagged_list; // count_out[1] flagged tiles, in no particular order
     uint32_t* split_tile;   // >= ceil((num_tiles + P) / kMoveSpan) tiles holding each piece's first item
     double* tile_sumsq;     // sweep: per tile, squared norm of its new residual (binary64)
-    double* chunk_sumsq;    // sweep: per chunk, the sum of its tiles' squared norms
-    double* host_sumsq;     // sweep: mapped host memory, one squared norm per segment
+    double* host_sumsq;     // sweep: mapped host memory, per scan chunk the sum of its tiles'
+                            // squared norms (the host adds each segment's chunks in order)
     uint32_t move_blocks;   // workgroups of the move kernel
     uint32_t move_span;     // items per move piece: kMoveSpan, kMoveSpanSmall or kMoveSpanTiny (a power of two)
     uint2* stage;           // num_tiles * kStageCap staged (index, value bits) pairs
@@ -155,7 +156,10 @@ hipError_t launch_staged(const LaunchArgs& args, bool vec4, hipStream_t stream);
 hipError_t launch_fused(const LaunchArgs& args, bool vec4, hipStream_t stream);
 hipError_t launch_ticket(const LaunchArgs& args, bool vec4, hipStream_t stream);
 // The sweep: num_tiles / num_chunks are the totals over the table's segments.
-hipError_t launch_sweep(const LaunchArgs& args, const SweepTable& table, bool vec4, hipStream_t stream);
+// fused: the stream and scan passes in one launch of num_tiles + num_chunks
+// workgroups, each segment's workgroups from its wg_first on as fused_role
+// lays out a single partition's.
+hipError_t launch_sweep(const LaunchArgs& args, const SweepTable& table, bool vec4, bool fused, hipStream_t stream);
 hipError_t launch_accumulate(const AccumulateArgs& args, bool vec4, hipStream_t stream);
 
 // Union kernels (union_kernel.hip).  Gather and reset at the union of the

@@ -788,7 +788,6 @@ __device__ __forceinline__ void scan_chunk(const LaunchArgs& a, const SweepTable
     __shared__ uint32_t s_exclusive, s_num_flagged, s_list_base;
     __shared__ uint32_t s_wave_total[WAVES];
     __shared__ uint32_t s_flagged[kChunkTiles];
-    __shared__ double s_sq[WAVES];
 
     const int tid = threadIdx.x;
     const int lane = tid & (kWaveSize - 1);
@@ -821,14 +820,6 @@ __device__ __forceinline__ void scan_chunk(const LaunchArgs& a, const SweepTable
     } else {
 #pragma unroll
         for (int i = 0; i < PER_THREAD; ++i) raw[i] = first_tile + i < end_tile ? a.tile_counts[first_tile + i] : 0u;
-    }
-    if constexpr (SWEEP) {
-        double sq = 0.0;
-#pragma unroll
-        for (int i = 0; i < PER_THREAD; ++i)
-            if (first_tile + i < end_tile) sq += a.tile_sumsq[first_tile + i];
-        const double total = block_sum<WAVES>(sq, lane, wave, s_sq);
-        if (tid == 0) a.chunk_sumsq[chunk] = total;
     }
     uint32_t mine = 0;
 #pragma unroll
@@ -929,6 +920,40 @@ __global__ __launch_bounds__(kStreamBlock) void stream_scan_kernel(LaunchArgs a)
 
 __global__ __launch_bounds__(kScanBlock) void scan_sweep_kernel(LaunchArgs a, SweepTable tbl) {
     scan_chunk<true>(a, &tbl, blockIdx.x);
+}
+
+// Segment of a fused sweep holding workgroup b: the last segment whose first
+// workgroup is <= b, so empty segments are skipped.  Uniform binary search
+// over the table in the kernel arguments.
+__device__ __forceinline__ uint32_t segment_of_workgroup(const SweepTable* tbl, uint32_t b) {
+    uint32_t lo = 0, hi = tbl->count;
+    while (hi - lo > 1) {
+        const uint32_t mid = (lo + hi) / 2;
+        if (tbl->seg[mid].wg_first <= b)
+            lo = mid;
+        else
+            hi = mid;
+    }
+    return lo;
+}
+
+// Fused sweep: the stream and scan passes of every segment in one launch.
+// Each segment's workgroups follow the previous segment's and are laid out
+// like a single partition's fused launch, so every scan workgroup still comes
+// after its chunk's tiles and after the scan workgroups of all lower chunks,
+// which is all the look-back waits for.
+template <int VEC, int ROWS>
+__global__ __launch_bounds__(kStreamBlock) void stream_scan_sweep_kernel(LaunchArgs a, SweepTable tbl) {
+    static_assert(kStreamBlock == kScanBlock, "one workgroup size for both parts");
+    const uint32_t r = segment_of_workgroup(&tbl, blockIdx.x);
+    const SweepSegment& sg = tbl.seg[r];
+    const SweepSegment& next = tbl.seg[r + 1];
+    const FusedRole role = fused_role(blockIdx.x - sg.wg_first, next.tile_first - sg.tile_first,
+                                      next.chunk_first - sg.chunk_first);
+    if (role.scan)
+        scan_chunk<true, true>(a, &tbl, sg.chunk_first + role.item);
+    else
+        stream_tile<VEC, ROWS, true, true>(a, &tbl, sg.tile_first + role.item);
 }
 
 // Number of output pairs before item x of the merged sequence, given the tile
@@ -1126,11 +1151,10 @@ __device__ __forceinline__ void move_pieces(const LaunchArgs& a, const SweepTabl
     const int64_t k = counts.x;
     const uint32_t flagged = flagged_count(a, counts.y);
     // What goes to the host (the counts; in a sweep also each segment's
-    // count and squared norm) is stored after this workgroup's pieces: a
-    // store to mapped host memory takes a bus round trip, and a wait for any
-    // later load would include it.
+    // count and each chunk's squared norm) is stored after this workgroup's
+    // pieces: a store to mapped host memory takes a bus round trip, and a wait
+    // for any later load would include it.
     int64_t seg_k = 0;
-    double seg_sq = 0.0;
     if constexpr (SWEEP) {
         // Each segment's count: the difference of the global offsets of its
         // first tile and of the next segment's first tile.
@@ -1140,14 +1164,6 @@ __device__ __forceinline__ void move_pieces(const LaunchArgs& a, const SweepTabl
             const int64_t e1 = t1 < a.num_tiles ? (a.tile_excl[t1] & ~kOverflow) : k;
             seg_k = t1 > t0 ? e1 - e0 : 0;
         }
-        // Workgroup b < count: the squared norm of segment b, its chunks'
-        // sums added in a fixed order.
-        if (blockIdx.x < tbl->count) {
-            const uint32_t c0 = tbl->seg[blockIdx.x].chunk_first, c1 = tbl->seg[blockIdx.x + 1].chunk_first;
-            double sq = 0.0;
-            for (uint32_t c = c0 + tid; c < c1; c += kMoveBlock) sq += a.chunk_sumsq[c];
-            seg_sq = block_sum<WAVES>(sq, lane, tid / kWaveSize, s_sq);
-        }
     }
     if (k != 0) move_work<VEC, SWEEP>(a, tbl, k, flagged, first_t0, first_t1);
     if (blockIdx.x == 0 && tid == 0) {  // the scan kernel has finished both counts
@@ -1156,7 +1172,20 @@ __device__ __forceinline__ void move_pieces(const LaunchArgs& a, const SweepTabl
     }
     if constexpr (SWEEP) {
         if (blockIdx.x == 0 && tid < static_cast<int>(tbl->count)) a.host_count[2 + tid] = seg_k;
-        if (blockIdx.x < tbl->count && tid == 0) a.host_sumsq[blockIdx.x] = seg_sq;
+        // Each chunk's squared norm, its tiles' norms added in a fixed order
+        // (each thread its tiles in increasing order, then the workgroup sum);
+        // the host adds a segment's chunks in increasing order.  The stream
+        // workgroups stored the tile norms in an earlier launch, so they are
+        // read here, not by the scan workgroups of a fused launch.
+        for (uint32_t c = blockIdx.x; c < a.num_chunks; c += gridDim.x) {  // uniform
+            uint32_t first, end;
+            chunk_tiles<true>(a, tbl, c, first, end);
+            double sq = 0.0;
+            for (uint32_t t = first + tid; t < end; t += kMoveBlock) sq += a.tile_sumsq[t];
+            const double total = block_sum<WAVES>(sq, lane, tid / kWaveSize, s_sq);
+            if (tid == 0) a.host_sumsq[c] = total;
+            __syncthreads();  // s_sq is written again for the next chunk
+        }
     }
 }
 
@@ -1254,6 +1283,18 @@ __global__ __launch_bounds__(kStreamBlock) void accumulate_kernel(AccumulateArgs
     store_residual<VEC, ROWS, kStreamBlock, true>(a, tid, t, 0u);
 }
 
+// Refuses a launch whose kernels would dereference a null scratch or output
+// pointer: every address a schedule's kernels use must be set by the host.
+template <class... P>
+bool all_set(const P*... p) {
+    return ((p != nullptr) && ...);
+}
+
+bool staged_args_set(const LaunchArgs& a) {
+    return all_set(a.grad, a.residual, a.out_idx, a.out_val, a.count_out, a.host_count, a.tile_excl, a.flagged_list,
+                   a.split_tile, a.stage, a.chunk_status);
+}
+
 }  // namespace
 
 hipError_t launch_accumulate(const AccumulateArgs& args, bool vec4, hipStream_t stream) {
@@ -1273,6 +1314,7 @@ int64_t tile_base_for(const float* grad, int64_t start, bool vec4) {
 }
 
 hipError_t launch_staged(const LaunchArgs& args, bool vec4, hipStream_t stream) {
+    if (!staged_args_set(args) || !args.tile_counts) return hipErrorInvalidValue;
     const dim3 grid_stream(args.num_tiles), grid_scan(args.num_chunks), grid_move(args.move_blocks);
     const dim3 bs(kStreamBlock);
     if (vec4) {
@@ -1288,6 +1330,7 @@ hipError_t launch_staged(const LaunchArgs& args, bool vec4, hipStream_t stream) 
 }
 
 hipError_t launch_fused(const LaunchArgs& args, bool vec4, hipStream_t stream) {
+    if (!staged_args_set(args) || !args.tile_words) return hipErrorInvalidValue;
     const dim3 grid_fused(args.num_tiles + args.num_chunks), grid_move(args.move_blocks);
     if (vec4) {
         hipLaunchKernelGGL((stream_scan_kernel<4, 1>), grid_fused, dim3(kStreamBlock), 0, stream, args);
@@ -1299,9 +1342,23 @@ hipError_t launch_fused(const LaunchArgs& args, bool vec4, hipStream_t stream) {
     return hipGetLastError();
 }
 
-hipError_t launch_sweep(const LaunchArgs& args, const SweepTable& table, bool vec4, hipStream_t stream) {
+hipError_t launch_sweep(const LaunchArgs& args, const SweepTable& table, bool vec4, bool fused, hipStream_t stream) {
+    if (!staged_args_set(args) || !all_set(args.tile_sumsq, args.host_sumsq) ||
+        !(fused ? args.tile_words != nullptr : args.tile_counts != nullptr))
+        return hipErrorInvalidValue;
     const dim3 grid_stream(args.num_tiles), grid_scan(args.num_chunks), grid_move(args.move_blocks);
     const dim3 bs(kStreamBlock);
+    if (fused) {
+        const dim3 grid_fused(args.num_tiles + args.num_chunks);
+        if (vec4) {
+            hipLaunchKernelGGL((stream_scan_sweep_kernel<4, 1>), grid_fused, bs, 0, stream, args, table);
+            hipLaunchKernelGGL(move_sweep_kernel<4>, grid_move, dim3(kMoveBlock), 0, stream, args, table);
+        } else {
+            hipLaunchKernelGGL((stream_scan_sweep_kernel<1, 4>), grid_fused, bs, 0, stream, args, table);
+            hipLaunchKernelGGL(move_sweep_kernel<1>, grid_move, dim3(kMoveBlock), 0, stream, args, table);
+        }
+        return hipGetLastError();
+    }
     if (vec4) {
         hipLaunchKernelGGL((stream_sweep_kernel<4, 1>), grid_stream, bs, 0, stream, args, table);
         hipLaunchKernelGGL(scan_sweep_kernel, grid_scan, dim3(kScanBlock), 0, stream, args, table);
@@ -1315,6 +1372,9 @@ hipError_t launch_sweep(const LaunchArgs& args, const SweepTable& table, bool ve
 }
 
 hipError_t launch_ticket(const LaunchArgs& args, bool vec4, hipStream_t stream) {
+    if (!all_set(args.grad, args.residual, args.out_idx, args.out_val, args.count_out, args.host_count, args.status,
+                 args.ticket))
+        return hipErrorInvalidValue;
     const dim3 grid(args.num_tiles), block(kTicketBlock);
     if (vec4)
         hipLaunchKernelGGL((ticket_kernel<4, 4>), grid, block, 0, stream, args);

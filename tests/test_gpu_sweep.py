@@ -1,4 +1,4 @@
-"""The sweep of every partition in one launch of each kernel (GPU): bit-exact
+"""The sweep of every partition in one set of launches (GPU): bit-exact
 pairs, counts, thresholds and residual against the oracle's sweep, and the
 partitions' local-error squared norms within the bound that any binary64
 summation order of nonnegative terms satisfies."""
@@ -126,6 +126,30 @@ def test_sweep_dense_partitions_and_specials():
     g[2_300_000] = np.inf
     thetas = [1e-3, 3.0, 1e-30, 2.0, 0.5]
     check_sweep(g, res, world, 0.01, thetas, where="dense")
+
+
+@pytest.mark.parametrize("N,world,fused_default", [(1_100_003, 16, 1), (40_000_019, 3, 1), (23_000_001, 9, 1),
+                                                   (70_000_003, 5, 0)])
+def test_sweep_fused_and_separate_launches_agree(N, world, fused_default):
+    """A sweep of up to 64 scan chunks runs its stream and scan passes as one
+    launch by default (each segment laid out like a single partition's fused
+    launch, stats fused = 1), a larger one apart, and MICRO_FLAG_SEPARATE_SCAN
+    always apart.  Both give the oracle's pairs, counts, thresholds and
+    residual, and its norms within the bound; the sizes give segments of one
+    to fourteen chunks, so scan workgroups are interleaved among a segment's
+    tiles, and a dense region overflows tiles."""
+    rng = np.random.default_rng(N % 997 + world)
+    g = (rng.standard_normal(N) * np.exp(rng.uniform(-1.0, 1.0, N))).astype(np.float32)
+    g[N // 2:N // 2 + 200_000] *= 40.0
+    res = (rng.standard_normal(N) * 0.3).astype(np.float32)
+    thetas = list(np.exp(rng.uniform(0.5, 1.2, world)))
+    for separate in (False, True):
+        note(f"sweep fused/separate N={N} world={world} separate={separate}")
+        sp = micro.Sparsifier(N, device=DEV, separate_scan=separate)
+        check_sweep(g, res, world, 0.01, thetas, sp=sp, where=f"N={N} world={world} separate={separate}")
+        _, redone, variant, fused = sp.last_stats()
+        assert fused == (0 if separate else fused_default) and redone > 0
+        sp.close()
 
 
 def test_sweep_equals_separate_steps():
