@@ -617,9 +617,9 @@ def stream_ceiling(args, w, head, pool, sp):
     vector and stream, each `steps` times after `warmup` runs: torch.add(g,
     res, out=res) (two reads and one write per value: the step's streaming
     pattern without the selection), res.copy_(g) (one read, one write: a
-    device copy) and the sparsify step.  Event-timed on torch's current
-    stream; GB/s from the bytes each must move (12, 8 and 12 + 8 d bytes per
-    value)."""
+    device copy), torch.sum(g) (reads only) and res.fill_ (writes only), and
+    the sparsify step.  Event-timed on torch's current stream; GB/s from the
+    bytes each must move (12, 8, 4, 4 and 12 + 8 d bytes per value)."""
     import torch
     from paper_2310_00967_amd import synth
     N = w.n_total
@@ -652,9 +652,12 @@ def stream_ceiling(args, w, head, pool, sp):
 
     add_ms = timed(lambda i: torch.add(g, res, out=res))
     copy_ms = timed(lambda i: res.copy_(g))
+    sum_ms = timed(lambda i: torch.sum(g))
+    fill_ms = timed(lambda i: res.fill_(1.0))
     step_ms = timed(step)
     k_avg = sum(ks) / len(ks)
     rows = {"torch_add_inplace": (add_ms, 12.0 * N), "device_copy": (copy_ms, 8.0 * N),
+            "torch_sum_read_only": (sum_ms, 4.0 * N), "torch_fill_write_only": (fill_ms, 4.0 * N),
             "sparsify_step": (step_ms, 12.0 * N + 8.0 * k_avg)}
     line = {"metric": "streaming ceiling: vendor streams beside the sparsify step (GB/s of the bytes each must move)",
             "n_gpus": 1, "steps": args.steps, "warmup": args.warmup, "dtype": "f32", "data": "synthetic",
