@@ -606,28 +606,68 @@ def bert_block(args):
             "kernel": ("stream_scan_kernel + move_kernel" if r["fused"] else "stream_kernel + scan_kernel + move_kernel")
             + " (one step, event-timed together)",
             "redone_tiles_timed": r["redone_tiles"]}
+    block["bert_large_rank3"]["vendor_add_rotating_out"] = vendor_add_rotating(w, pool, 3, warmup, steps)
     sp.close()
     del pool
     torch.cuda.empty_cache()
     return block
 
 
-def stream_ceiling(args, w, head, pool, sp):
-    """Streams of the vendor libraries beside the library's step, on the same
-    vector and stream, each `steps` times after `warmup` runs: torch.add(g,
-    res, out=res) (two reads and one write per value: the step's streaming
-    pattern without the selection), res.copy_(g) (one read, one write: a
-    device copy), torch.sum(g) (reads only) and res.fill_ (writes only), and
-    the sparsify step.  Event-timed on torch's current stream; GB/s from the
-    bytes each must move (12, 8, 4, 4 and 12 + 8 d bytes per value)."""
+def vendor_add_rotating(w, pool, rank, warmup, steps):
+    """torch.add(g, e, out=e) on one partition, the step's two-read, one-write
+    stream without the selection, with the gradient rotating over the pool and
+    e over three buffers (so no call re-reads an operand that the previous call
+    left in the Infinity Cache); HIP events around each call."""
     import torch
+    import paper_2310_00967_amd as micro
+    start, n = micro.micro_partition(w.n_total, rank, w.world)
+    gs = [g[start:start + n] for g in pool]
+    outs = [torch.zeros(n, dtype=torch.float32, device="cuda") for _ in range(3)]
+    stream = torch.cuda.current_stream()
+    ms = []
+    for i in range(warmup + steps):
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        torch.add(gs[i % len(gs)], outs[i % 3], out=outs[i % 3])
+        e1.record(stream)
+        e1.synchronize()
+        if i >= warmup:
+            ms.append(e0.elapsed_time(e1))
+    avg = sum(ms) / len(ms)
+    gbs = 12.0 * n / (avg * 1e-3) / 1e9
+    return {"ms_avg": avg, "bytes": 12.0 * n, "gbs": gbs, "frac": gbs / HBM_PEAK_GBS}
+
+
+MALL_BYTES = 256 * 1024 * 1024  # MI355X Infinity Cache
+
+
+def stream_ceiling(args, w, head, pool, sp):
+    """Streams of the vendor libraries beside the library's step, on the
+    worker's partition (the whole vector at world 1), each `steps` times after
+    `warmup` runs on torch's current stream: torch.add(g, res, out=res) (two
+    reads and one write per value: the step's streaming pattern without the
+    selection), res.copy_(g) (one read, one write: a device copy), torch.sum(g)
+    (reads only) and res.fill_ (writes only), and the sparsify step.  The
+    gradient rotates over the pool.  Where an operand fits the 256 MB Infinity
+    Cache, back-to-back calls on one output re-read it from that cache, which a
+    training step (forward and backward passes between two selections) does
+    not leave in place: the in-place add and the step are then also timed with
+    the output (the residual) rotating over three buffers.  Event-timed; GB/s
+    from the bytes each must move (12, 8, 4, 4 and 12 + 8 d bytes per value)."""
+    import torch
+    import paper_2310_00967_amd as micro
     from paper_2310_00967_amd import synth
-    N = w.n_total
-    g = pool[0]
+    rank = w.ranks[0]
+    start, N = micro.micro_partition(w.n_total, rank, w.world)
+    gs = [g[start:start + N] for g in pool]
     res = torch.zeros(N, dtype=torch.float32, device="cuda")
-    res_step = torch.zeros(N, dtype=torch.float32, device="cuda")
+    res_step = torch.zeros(w.n_total, dtype=torch.float32, device="cuda")
+    cache_sized = 4 * N <= MALL_BYTES
+    rot = [torch.zeros(N, dtype=torch.float32, device="cuda") for _ in range(3)] if cache_sized else []
+    rot_step = ([torch.zeros(w.n_total, dtype=torch.float32, device="cuda") for _ in range(2)] + [res_step]
+                if cache_sized else [])
     out_idx, out_val = sp.outputs(N)
-    theta = synth.initial_theta(w, g, 0, N, head)
+    theta0 = synth.initial_theta(w, pool[0], start, start + N, head)
     stream = torch.cuda.current_stream()
 
     def timed(fn):
@@ -642,29 +682,47 @@ def stream_ceiling(args, w, head, pool, sp):
                 ms.append(e0.elapsed_time(e1))
         return sum(ms) / len(ms)
 
-    ks = []
+    def stepper(residuals):
+        state = {"theta": theta0, "ks": [], "lib_ms": []}
 
-    def step(i):
-        nonlocal theta
-        k, theta, _, _ = sp.step(pool[i % len(pool)], res_step, 0, 1, head, theta, out_idx, out_val)
-        if i >= args.warmup:
-            ks.append(k)
+        def step(i):
+            k, state["theta"], _, _ = sp.step(pool[i % len(pool)], residuals[i % len(residuals)], rank, w.world,
+                                              head, state["theta"], out_idx, out_val)
+            if i >= args.warmup:
+                state["ks"].append(k)
+                state["lib_ms"].append(sp.last_stats()[0])
+        return step, state
 
-    add_ms = timed(lambda i: torch.add(g, res, out=res))
-    copy_ms = timed(lambda i: res.copy_(g))
-    sum_ms = timed(lambda i: torch.sum(g))
-    fill_ms = timed(lambda i: res.fill_(1.0))
+    rows = {}
+    rows["torch_add_inplace"] = (timed(lambda i: torch.add(gs[i % len(gs)], res, out=res)), 12.0 * N)
+    if rot:
+        rows["torch_add_inplace_rotating_out"] = (
+            timed(lambda i: torch.add(gs[i % len(gs)], rot[i % 3], out=rot[i % 3])), 12.0 * N)
+    rows["device_copy"] = (timed(lambda i: res.copy_(gs[i % len(gs)])), 8.0 * N)
+    rows["torch_sum_read_only"] = (timed(lambda i: torch.sum(gs[i % len(gs)])), 4.0 * N)
+    rows["torch_fill_write_only"] = (timed(lambda i: res.fill_(1.0)), 4.0 * N)
+    step, st = stepper([res_step])
     step_ms = timed(step)
-    k_avg = sum(ks) / len(ks)
-    rows = {"torch_add_inplace": (add_ms, 12.0 * N), "device_copy": (copy_ms, 8.0 * N),
-            "torch_sum_read_only": (sum_ms, 4.0 * N), "torch_fill_write_only": (fill_ms, 4.0 * N),
-            "sparsify_step": (step_ms, 12.0 * N + 8.0 * k_avg)}
+    k_avg = sum(st["ks"]) / len(st["ks"])
+    rows["sparsify_step"] = (step_ms, 12.0 * N + 8.0 * k_avg)
+    lib = {"sparsify_step": sum(st["lib_ms"]) / len(st["lib_ms"])}
+    if rot_step:
+        step, st = stepper(rot_step)
+        step_ms = timed(step)
+        k_rot = sum(st["ks"]) / len(st["ks"])
+        rows["sparsify_step_rotating_residual"] = (step_ms, 12.0 * N + 8.0 * k_rot)
+        lib["sparsify_step_rotating_residual"] = sum(st["lib_ms"]) / len(st["lib_ms"])
+    kernels = {name: {"ms_avg": ms, "bytes": b, "gbs": b / (ms * 1e-3) / 1e9,
+                      "frac": b / (ms * 1e-3) / 1e9 / HBM_PEAK_GBS} for name, (ms, b) in rows.items()}
+    for name, ms in lib.items():  # the library's own events around its two launches
+        b = rows[name][1]
+        kernels[name].update({"lib_ms_avg": ms, "lib_gbs": b / (ms * 1e-3) / 1e9,
+                              "lib_frac": b / (ms * 1e-3) / 1e9 / HBM_PEAK_GBS})
     line = {"metric": "streaming ceiling: vendor streams beside the sparsify step (GB/s of the bytes each must move)",
             "n_gpus": 1, "steps": args.steps, "warmup": args.warmup, "dtype": "f32", "data": "synthetic",
-            "config": {"workload": w.name, "n_total": N, "density": head},
-            "kernels": {name: {"ms_avg": ms, "bytes": b, "gbs": b / (ms * 1e-3) / 1e9,
-                               "frac": b / (ms * 1e-3) / 1e9 / HBM_PEAK_GBS} for name, (ms, b) in rows.items()},
-            "step_k_avg": k_avg}
+            "config": {"workload": w.name, "n_total": w.n_total, "world": w.world, "rank": rank,
+                       "partition_len": N, "density": head},
+            "kernels": kernels, "step_k_avg": k_avg}
     print(json.dumps(line), flush=True)
 
 
