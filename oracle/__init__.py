@@ -83,6 +83,12 @@ def lib():
                                          ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p,
                                          ctypes.c_void_p, ctypes.c_void_p]
         L.micro_oracle_sweep.restype = ctypes.c_int
+        L.micro_oracle_topk_count.argtypes = [ctypes.c_double, ctypes.c_int64]
+        L.micro_oracle_topk_count.restype = ctypes.c_int64
+        L.micro_oracle_topk_select.argtypes = [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int64,
+                                               ctypes.c_int64, ctypes.c_double, ctypes.c_void_p,
+                                               ctypes.c_void_p, i64p, ctypes.POINTER(ctypes.c_double)]
+        L.micro_oracle_topk_select.restype = ctypes.c_int
         _lib = L
     return _lib
 
@@ -298,3 +304,63 @@ def sweep(grad, residual, world, density, thetas, rule=None):
         raise ValueError("invalid oracle sweep arguments")
     total = int(k[:world].sum())
     return out_idx[:total], out_val[:total], k[:world].copy(), th, sq[:world].copy()
+
+
+def topk_count(density, length):
+    """k of the exact top-k comparator over `length` values:
+    max(1, floor(density * length)), at most length (0 for length 0)."""
+    return lib().micro_oracle_topk_count(float(density), int(length))
+
+
+def topk_select(grad, residual, start, length, density, kth=float("nan")):
+    """The exact top-k comparator over [start, start+length): the k largest
+    accumulated magnitudes (equal magnitudes by lower index, NaN never), in
+    index order.  residual is updated in place.  Returns (idx, val, k, kth):
+    kth is the smallest selected magnitude, or the given kth when nothing is
+    selected."""
+    _f32(grad, "grad")
+    _f32(residual, "residual")
+    if start < 0 or length < 0 or start + length > min(grad.size, residual.size):
+        raise ValueError("range outside the arrays")
+    out_idx = np.empty(max(length, 1), dtype=np.int32)
+    out_val = np.empty(max(length, 1), dtype=np.float32)
+    k = ctypes.c_int64()
+    th = ctypes.c_double(float(kth))
+    rc = lib().micro_oracle_topk_select(grad.ctypes.data, residual.ctypes.data, int(start), int(length),
+                                        float(density), out_idx.ctypes.data, out_val.ctypes.data,
+                                        ctypes.byref(k), ctypes.byref(th))
+    if rc != 0:
+        raise ValueError("invalid oracle top-k arguments")
+    return out_idx[:k.value].copy(), out_val[:k.value].copy(), k.value, th.value
+
+
+def topk_step(grad, residual, rank, world, density, theta):
+    """The top-k comparator as one worker's step over its partition: returns
+    (idx, val, k, theta_next), theta_next the smallest selected magnitude (theta
+    unchanged when nothing is selected)."""
+    _f32(grad, "grad")
+    _f32(residual, "residual")
+    if residual.size != grad.size:
+        raise ValueError("grad and residual lengths differ")
+    start, length = partition(grad.size, rank, world)
+    return topk_select(grad, residual, start, length, density, kth=theta)
+
+
+def topk_ef_step(grad, residual, t, worker, world, density, theta):
+    """Algorithm 1's pass with the top-k comparator in place of the threshold
+    rule: every element outside the worker's partition of iteration t
+    accumulates (residual = grad + residual), the partition goes through
+    topk_select.  Returns (idx, val, k, theta_next, cycle)."""
+    _f32(grad, "grad")
+    _f32(residual, "residual")
+    n_total = grad.size
+    if residual.size != n_total:
+        raise ValueError("grad and residual lengths differ")
+    c = cycle(t, worker, world)
+    start, length = partition(n_total, c, world)
+    for lo, hi in ((0, start), (start + length, n_total)):
+        if hi > lo:
+            lib().micro_oracle_accumulate(grad.ctypes.data + 4 * lo, residual.ctypes.data + 4 * lo,
+                                          hi - lo, residual.ctypes.data + 4 * lo)
+    idx, val, k, th = topk_select(grad, residual, start, length, density, kth=theta)
+    return idx, val, k, th, c

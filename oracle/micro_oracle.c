@@ -9,6 +9,7 @@
 
 #include <math.h>
 #include <stddef.h>
+#include <stdlib.h>
 
 void micro_oracle_default_rule(micro_oracle_rule *rule)
 {
@@ -244,5 +245,102 @@ int micro_oracle_sweep(const float *grad, float *residual, int64_t n_total,
         if (sumsq != NULL)
             sumsq[r] = micro_oracle_sumsq(residual, start, len);
     }
+    return 0;
+}
+
+/* Sec. 1 and its density footnote: a sorting-based sparsifier orders all
+ * values and keeps the k largest; the values here are the error-feedback
+ * accumulations of Sec. 2, ordered by magnitude.  Readings where the paper
+ * says nothing: equal magnitudes are ordered by index (the lower index ranks
+ * higher), and a NaN is never selected, as under the threshold rule, whose
+ * compare is false for NaN.  Written as the definition: accumulate, sort,
+ * take the first k, then emit in index order. */
+typedef struct oracle_ranked {
+    float mag;
+    int64_t idx;
+} oracle_ranked;
+
+static int larger_magnitude_first(const void *pa, const void *pb)
+{
+    const oracle_ranked *a = (const oracle_ranked *)pa;
+    const oracle_ranked *b = (const oracle_ranked *)pb;
+    if (a->mag > b->mag)
+        return -1;
+    if (a->mag < b->mag)
+        return 1;
+    if (a->idx < b->idx)
+        return -1;
+    if (a->idx > b->idx)
+        return 1;
+    return 0;
+}
+
+int64_t micro_oracle_topk_count(double density, int64_t len)
+{
+    if (len <= 0)
+        return 0;
+    double f = floor(density * (double)len);
+    int64_t k = (int64_t)f;
+    if (k < 1)
+        k = 1;
+    if (k > len)
+        k = len;
+    return k;
+}
+
+int micro_oracle_topk_select(const float *grad, float *residual, int64_t start,
+                             int64_t len, double density, int32_t *out_idx,
+                             float *out_val, int64_t *k_out, double *kth)
+{
+    if (grad == NULL || residual == NULL || k_out == NULL || kth == NULL ||
+        start < 0 || len < 0)
+        return -1;
+    if (!(density > 0.0 && density <= 1.0))
+        return -1;
+    if (len > 0 && (out_idx == NULL || out_val == NULL))
+        return -1;
+    size_t n = (size_t)len;
+    float *acc = (float *)malloc((n > 0 ? n : 1) * sizeof(float));
+    oracle_ranked *ranked =
+        (oracle_ranked *)malloc((n > 0 ? n : 1) * sizeof(oracle_ranked));
+    unsigned char *chosen = (unsigned char *)calloc(n > 0 ? n : 1, 1);
+    if (acc == NULL || ranked == NULL || chosen == NULL) {
+        free(acc);
+        free(ranked);
+        free(chosen);
+        return -1;
+    }
+    size_t valid = 0;
+    for (size_t i = 0; i < n; ++i) {
+        acc[i] = grad[start + (int64_t)i] + residual[start + (int64_t)i];
+        if (!isnan(acc[i])) {
+            ranked[valid].mag = fabsf(acc[i]);
+            ranked[valid].idx = start + (int64_t)i;
+            valid = valid + 1;
+        }
+    }
+    qsort(ranked, valid, sizeof(oracle_ranked), larger_magnitude_first);
+    int64_t want = micro_oracle_topk_count(density, len);
+    int64_t take = want < (int64_t)valid ? want : (int64_t)valid;
+    for (int64_t r = 0; r < take; ++r)
+        chosen[ranked[r].idx - start] = 1;
+    if (take > 0)
+        *kth = (double)ranked[take - 1].mag;
+    int64_t k = 0;
+    for (size_t i = 0; i < n; ++i) {
+        int64_t j = start + (int64_t)i;
+        if (chosen[i]) {
+            out_idx[k] = (int32_t)j;
+            out_val[k] = acc[i];
+            k = k + 1;
+            residual[j] = 0.0f;
+        } else {
+            residual[j] = acc[i];
+        }
+    }
+    *k_out = k;
+    free(acc);
+    free(ranked);
+    free(chosen);
     return 0;
 }

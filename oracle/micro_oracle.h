@@ -170,6 +170,27 @@ int micro_oracle_sweep(const float *grad, float *residual, int64_t n_total,
                        int32_t *out_idx, float *out_val, int64_t *k,
                        double *sumsq);
 
+/* The exact top-k comparator (Sec. 1: sorting-based sparsifiers select the
+ * k largest gradients; the density footnote: d = k / n_g) under the error
+ * feedback of Sec. 2.  micro_oracle_topk_count returns the k of a range of len
+ * values: floor(density * len) in binary64, at least 1, at most len; 0 when
+ * len is 0. */
+int64_t micro_oracle_topk_count(double density, int64_t len);
+
+/* For j in [start, start+len): acc[j] = grad[j] + residual[j] (binary32).
+ * The values ranked are the accumulated values that are not NaN, by |acc|
+ * descending, equal magnitudes by increasing j; the first
+ * min(k, number ranked) of them, k = micro_oracle_topk_count(density, len),
+ * are selected.  Then, for j in increasing order: a selected j appends
+ * (j, acc[j]) to the output lists and sets residual[j] = +0; every other j
+ * sets residual[j] = acc[j].  *k_out receives the selected count and, when it
+ * is positive, *kth the smallest selected magnitude (widened to binary64;
+ * unchanged otherwise).  out_idx and out_val must hold len entries.  Returns
+ * 0, or -1 on invalid arguments or a failed allocation (nothing written). */
+int micro_oracle_topk_select(const float *grad, float *residual, int64_t start,
+                             int64_t len, double density, int32_t *out_idx,
+                             float *out_val, int64_t *k_out, double *kth);
+
 #ifdef __cplusplus
 }
 #endif
