@@ -71,6 +71,26 @@ typedef enum micro_status {
 #define MICRO_RULE_HARD_THRESHOLD 2 /* theta never changes: the hard-threshold
                                        sparsifier the paper compares with
                                        (Sec. 1, Sec. 5.2), a fixed threshold  */
+#define MICRO_RULE_TOPK 3 /* the exact top-k sparsifier the paper compares
+                             with (Sec. 1: the k largest gradients; its density
+                             footnote: d = k / n_g).  Not a threshold rule: the
+                             step selects the k = max(1, floor(d * P)) values
+                             of [s, e) whose accumulated magnitude is largest,
+                             equal magnitudes by lower index, NaN never (so
+                             fewer than k when fewer than k are not NaN).  The
+                             incoming theta is neither checked nor used;
+                             theta receives the smallest selected magnitude
+                             (0 or +inf possible; unchanged when nothing is
+                             selected).  Through
+                             micro_sparsify_step and micro_ef_step only
+                             (MICRO_EINVAL in micro_sweep_step,
+                             micro_sparsify_step_noalloc and
+                             micro_estimate_threshold).  The k-th magnitude is
+                             found by a radix select (three histogram passes
+                             over the partition and a wait for their result)
+                             before the step's own launches at that magnitude;
+                             when several values share it, a final pass drops
+                             the surplus from the output list.             */
 
 /* Kernel schedules (both compute the same result). */
 #define MICRO_VARIANT_AUTO 0   /* per call, the faster measured schedule: TICKET
@@ -129,7 +149,9 @@ MICRO_API void micro_config_default(micro_config *cfg);
  * for the selected count; it never owns the caller's buffers.
  * Returns MICRO_EINVAL (ctx NULL, n_total < 0, bad cfg), MICRO_ERANGE
  * (n_total > INT32_MAX: indices are int32), MICRO_EHIP (no usable device) or
- * MICRO_ENOMEM.  On failure *ctx is set to NULL.
+ * MICRO_ENOMEM.  On failure *ctx is set to NULL.  Every context also holds
+ * the top-k comparator's 8 KB of radix-select counters and 64 bytes of mapped
+ * host memory.
  */
 MICRO_API micro_status micro_sparsify_init(micro_ctx **ctx, int64_t n_total,
                                  void *hip_stream, const micro_config *cfg);
@@ -143,7 +165,9 @@ MICRO_API micro_status micro_sparsify_init(micro_ctx **ctx, int64_t n_total,
  *   rank, world  0 <= rank < world, world >= 1.
  *   density   the user-set density d, 0 < d <= 1; the target count is d*P.
  *   theta     host, in/out: the threshold of this step in, the threshold of
- *             the next step out.  Must be finite and > 0.
+ *             the next step out.  Must be finite and > 0.  (MICRO_RULE_TOPK:
+ *             the selection is the top k instead and theta is only written,
+ *             see there.)
  *   out_idx   device int32, capacity >= P = e - s: the first k entries
  *             receive the selected global indices, strictly increasing.
  *   out_val   device fp32, capacity >= P: the first k entries receive acc
@@ -246,7 +270,8 @@ MICRO_API micro_status micro_cycle(int64_t t, int32_t worker, int32_t world, int
  *             residual, the worker's local error of Sec. 2 squared (Eq. 1
  *             averages its square root over the workers); squares in binary64
  *             added in a fixed order, within (n_total - 1) * 2^-53 relative of
- *             the exact sum.  Requesting it runs the pass through the sweep's
+ *             the exact sum (MICRO_RULE_TOPK with t values of the k-th
+ *             magnitude left out of the selection: (n_total + t) * 2^-53).  Requesting it runs the pass through the sweep's
  *             kernels (the staged schedule; MICRO_EINVAL on a TICKET context).
  * grad[0, n), residual[0, n), out_idx[0, P) and out_val[0, P) must not
  * overlap.  Synchronous; errors as micro_sparsify_step.  A partition that is

@@ -17,13 +17,15 @@ import ctypes
 
 from . import _lib
 from ._lib import (MICRO_FLAG_SEPARATE_SCAN, MICRO_FLAG_TIME_KERNEL, MICRO_RULE_FIXED_STEP,
-                   MICRO_RULE_HARD_THRESHOLD, MICRO_RULE_PROPORTIONAL, MICRO_VARIANT_AUTO, MICRO_VARIANT_STAGED,
+                   MICRO_RULE_HARD_THRESHOLD, MICRO_RULE_PROPORTIONAL, MICRO_RULE_TOPK, MICRO_VARIANT_AUTO,
+                   MICRO_VARIANT_STAGED,
                    MICRO_VARIANT_TICKET, MicroError, default_config, micro_cycle, micro_estimate_threshold,
                    micro_partition, micro_threshold_f32)
 
 __all__ = ["Sparsifier", "MicroError", "default_config", "micro_partition", "micro_cycle",
            "micro_estimate_threshold", "micro_threshold_f32", "MICRO_RULE_PROPORTIONAL",
-           "MICRO_RULE_FIXED_STEP", "MICRO_RULE_HARD_THRESHOLD", "MICRO_VARIANT_AUTO", "MICRO_VARIANT_TICKET",
+           "MICRO_RULE_FIXED_STEP", "MICRO_RULE_HARD_THRESHOLD", "MICRO_RULE_TOPK", "MICRO_VARIANT_AUTO",
+           "MICRO_VARIANT_TICKET",
            "MICRO_VARIANT_STAGED",
            "MICRO_FLAG_TIME_KERNEL", "MICRO_FLAG_SEPARATE_SCAN"]
 

@@ -11,7 +11,7 @@ import os
 LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libmicro_sparsify.so")
 
 MICRO_OK, MICRO_EINVAL, MICRO_ECAPACITY, MICRO_ERANGE, MICRO_ENOMEM, MICRO_EHIP = range(6)
-MICRO_RULE_PROPORTIONAL, MICRO_RULE_FIXED_STEP, MICRO_RULE_HARD_THRESHOLD = 0, 1, 2
+MICRO_RULE_PROPORTIONAL, MICRO_RULE_FIXED_STEP, MICRO_RULE_HARD_THRESHOLD, MICRO_RULE_TOPK = 0, 1, 2, 3
 MICRO_VARIANT_AUTO, MICRO_VARIANT_TICKET, MICRO_VARIANT_STAGED = 0, 1, 2
 MICRO_FLAG_TIME_KERNEL = 1
 MICRO_FLAG_SEPARATE_SCAN = 2

@@ -31,7 +31,7 @@ COMMON = ["-O3", "-std=c++17", "-fPIC", "-ffp-contract=off", "-fno-fast-math",
           "-Wall", "-Wextra", f"-I{INCLUDE}", f"-I{CSRC}"]
 DEVICE = [f"--offload-arch={ARCH}", "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
           "-fhip-fp32-correctly-rounded-divide-sqrt", "-fvisibility=hidden"]
-KERNEL_SOURCES = ["sparsify_kernel.hip", "union_kernel.hip", "static_scratch.hip"]
+KERNEL_SOURCES = ["sparsify_kernel.hip", "union_kernel.hip", "static_scratch.hip", "topk_kernel.hip"]
 
 
 def _run(cmd, verbose):

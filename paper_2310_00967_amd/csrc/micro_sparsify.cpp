@@ -19,6 +19,7 @@
 
 #include "sparsify_kernel.h"
 #include "static_scratch.h"
+#include "topk_kernel.h"
 
 struct micro_ctx {
     int device = -1;
@@ -50,6 +51,10 @@ struct micro_ctx {
     int64_t* h_count_dev = nullptr;          // the device's address of h_count
     double* h_sumsq = nullptr;               // mapped pinned host memory: a sweep's squared norms, per chunk
     double* h_sumsq_dev = nullptr;
+    // top-k comparator: radix-select counters and state, and its result for the host
+    uint32_t* d_topk = nullptr;              // kTopkBins counters (zero between passes), kTopkStateWords
+    int64_t* h_topk = nullptr;               // mapped pinned host memory, kTopkHostWords
+    int64_t* h_topk_dev = nullptr;
     uint32_t epoch = 0;                      // epoch of the last launch
     bool needs_reset = false;                // scratch state unknown after a failure
     hipEvent_t ev[2] = {nullptr, nullptr};
@@ -103,7 +108,8 @@ micro_status hip_fail(micro_ctx* ctx, hipError_t err, const char* what) {
 }
 
 bool config_valid(const micro_config& c) {
-    if (c.rule != MICRO_RULE_PROPORTIONAL && c.rule != MICRO_RULE_FIXED_STEP && c.rule != MICRO_RULE_HARD_THRESHOLD)
+    if (c.rule != MICRO_RULE_PROPORTIONAL && c.rule != MICRO_RULE_FIXED_STEP && c.rule != MICRO_RULE_HARD_THRESHOLD &&
+        c.rule != MICRO_RULE_TOPK)
         return false;
     if (!std::isfinite(c.beta) || c.beta < 0.0) return false;
     if (!std::isfinite(c.lo) || !std::isfinite(c.hi) || !(c.lo > 0.0) || !(c.hi >= c.lo)) return false;
@@ -124,10 +130,11 @@ bool theta_valid(double t) { return std::isfinite(t) && t > 0.0; }
 // 1 + beta * (k - target) / target clamped to [lo, hi]; the fixed-step rule
 // by 1 + alpha or 1 - alpha according to the sign of k - target.  Each
 // operation is one IEEE binary64 rounding, in this order.  The
-// hard-threshold comparator keeps the threshold as it is.
+// hard-threshold comparator keeps the threshold as it is.  (The top-k
+// comparator's threshold comes from the values: execute_step sets it.)
 double next_threshold(const micro_config& c, double density, int64_t part_len, int64_t k,
                       double theta) {
-    if (part_len == 0 || c.rule == MICRO_RULE_HARD_THRESHOLD) return theta;
+    if (part_len == 0 || c.rule == MICRO_RULE_HARD_THRESHOLD || c.rule == MICRO_RULE_TOPK) return theta;
     const double target = density * static_cast<double>(part_len);
     const double got = static_cast<double>(k);
     if (c.rule == MICRO_RULE_FIXED_STEP) {
@@ -163,6 +170,9 @@ micro_status reset_scratch(micro_ctx* ctx) {
         e = hipMemsetAsync(ctx->d_chunk_status, 0, sizeof(uint64_t) * ctx->chunk_capacity, ctx->stream);
     if (e == hipSuccess && ctx->d_tile_words)
         e = hipMemsetAsync(ctx->d_tile_words, 0, sizeof(uint64_t) * ctx->tile_capacity, ctx->stream);
+    if (e == hipSuccess && ctx->d_topk)
+        e = hipMemsetAsync(ctx->d_topk, 0, sizeof(uint32_t) * (micro::kTopkBins + micro::kTopkStateWords),
+                           ctx->stream);
     if (e == hipSuccess) e = hipStreamSynchronize(ctx->stream);
     if (e != hipSuccess) return hip_fail(ctx, e, "scratch reset");
     ctx->epoch = 0;
@@ -178,11 +188,12 @@ void release(micro_ctx* ctx) {
         if (ev) (void)hipEventDestroy(ev);
     void* device_buffers[] = {ctx->d_tile_counts, ctx->d_tile_excl, ctx->d_flagged_list, ctx->d_split_tile, ctx->d_tile_sumsq, ctx->d_stage,
                               ctx->d_chunk_status, ctx->d_tile_words, ctx->d_status, ctx->d_tickets,
-                              ctx->d_count};
+                              ctx->d_count, ctx->d_topk};
     for (void* p : device_buffers)
         if (p) (void)hipFree(p);
     if (ctx->h_count) (void)hipHostFree(ctx->h_count);
     if (ctx->h_sumsq) (void)hipHostFree(ctx->h_sumsq);
+    if (ctx->h_topk) (void)hipHostFree(ctx->h_topk);
     delete ctx;
 }
 
@@ -236,11 +247,13 @@ micro_status run_segments(micro_ctx* ctx, const float* grad, float* residual, in
 
 // Arguments of a step over [start, start + len) of a vector of n_total values
 // (whole_vector: grad and residual are accessed over all of it): NULL
-// pointers, density, threshold, alignment and overlapping ranges.  The message
-// goes to ctx, or to the calling thread's error when ctx is NULL.
+// pointers, density, threshold (unless the rule does not use it), alignment
+// and overlapping ranges.  The message goes to ctx, or to the calling
+// thread's error when ctx is NULL.
 micro_status check_step_args(micro_ctx* ctx, const float* grad, const float* residual, int64_t n_total,
                              int64_t start, int64_t len, bool whole_vector, double density, const double* theta,
-                             const int32_t* out_idx, const float* out_val, const int64_t* k) {
+                             const int32_t* out_idx, const float* out_val, const int64_t* k,
+                             bool threshold_used = true) {
     if (!grad || !residual || !theta || !out_idx || !out_val || !k) {
         set_error(ctx, "NULL pointer argument");
         return MICRO_EINVAL;
@@ -249,7 +262,7 @@ micro_status check_step_args(micro_ctx* ctx, const float* grad, const float* res
         set_error(ctx, "density %g outside (0, 1]", density);
         return MICRO_EINVAL;
     }
-    if (!theta_valid(*theta)) {
+    if (threshold_used && !theta_valid(*theta)) {
         set_error(ctx, "threshold %g is not finite and positive", *theta);
         return MICRO_EINVAL;
     }
@@ -272,6 +285,85 @@ micro_status check_step_args(micro_ctx* ctx, const float* grad, const float* res
     return MICRO_OK;
 }
 
+// The top-k comparator's k over a partition of len values: Sec. 1's
+// density footnote, d = k / n_g, read for a partition: floor(d * len) in
+// binary64, at least 1, at most len.
+int64_t topk_count(double density, int64_t len) {
+    if (len <= 0) return 0;
+    int64_t k = static_cast<int64_t>(std::floor(density * static_cast<double>(len)));
+    if (k < 1) k = 1;
+    if (k > len) k = len;
+    return k;
+}
+
+float float_from_bits(uint32_t b) {
+    float f;
+    std::memcpy(&f, &b, sizeof f);
+    return f;
+}
+
+// The exact k-th largest magnitude of a partition's accumulated values and
+// how the threshold step at that magnitude has to be trimmed: it selects the
+// `greater` larger magnitudes and all `equal` values of that magnitude, of
+// which the `keep` lowest indices belong to the top k.
+struct TopkPlan {
+    bool found = false;  // false: every value is NaN, nothing is selected
+    uint32_t key = 0;    // the k-th largest magnitude's binary32 bits
+    int64_t greater = 0;
+    int64_t equal = 0;
+    int64_t keep = 0;
+};
+
+// Radix select on the device (three histogram passes and selects over
+// acc = grad + residual of [start, start + len)), waited for.
+micro_status topk_plan(micro_ctx* ctx, const float* grad, const float* residual, int64_t start, int64_t len,
+                       double density, bool vec4, TopkPlan* plan) {
+    micro::TopkArgs t{};
+    t.grad = grad;
+    t.residual = residual;
+    t.start = start;
+    t.end = start + len;
+    t.vec4 = vec4;
+    if (vec4) {  // the 16-byte groups of both vectors (they share the phase)
+        const uintptr_t addr = reinterpret_cast<uintptr_t>(grad + start);
+        int64_t head = static_cast<int64_t>(((16u - (addr & 15u)) & 15u) / sizeof(float));
+        if (head > len) head = len;
+        t.body_first = start + head;
+        t.body_end = t.body_first + ((t.end - t.body_first) / 4) * 4;
+    }
+    const int64_t k = topk_count(density, len);
+    t.k = static_cast<uint32_t>(k);
+    t.words = ctx->d_topk;
+    t.host = ctx->h_topk_dev;
+    const int64_t per_block = static_cast<int64_t>(micro::kTopkHistBlock) * 8;  // two 16-byte groups a thread
+    const int64_t blocks = std::min<int64_t>((len + per_block - 1) / per_block, 4 * ctx->compute_units);
+    t.blocks = static_cast<uint32_t>(std::max<int64_t>(blocks, 1));
+    volatile int64_t* h = ctx->h_topk;
+    h[5] = 0;
+    hipError_t e = micro::launch_topk_select(t, ctx->stream);
+    if (e != hipSuccess) return hip_fail(ctx, e, "top-k select launch");
+    if ((e = hipStreamSynchronize(ctx->stream)) != hipSuccess) return hip_fail(ctx, e, "hipStreamSynchronize");
+    const int64_t status = h[5];
+    *plan = TopkPlan{};
+    if (status == 2) return MICRO_OK;
+    const int64_t key = h[0], greater = h[1], equal = h[2], keep = h[3], valid = h[4];
+    const int64_t want = std::min(k, valid);
+    if (status != 1 || key < 0 || key > micro::kTopkKeyMax || equal < 1 || keep < 1 || keep > equal ||
+        greater < 0 || greater + keep != want || greater + equal > len) {
+        set_error(ctx, "top-k select reported status %lld, key %lld, %lld above, %lld equal, %lld kept of %lld",
+                  static_cast<long long>(status), static_cast<long long>(key), static_cast<long long>(greater),
+                  static_cast<long long>(equal), static_cast<long long>(keep), static_cast<long long>(want));
+        ctx->needs_reset = true;
+        return MICRO_EHIP;
+    }
+    plan->found = true;
+    plan->key = static_cast<uint32_t>(key);
+    plan->greater = greater;
+    plan->equal = equal;
+    plan->keep = keep;
+    return MICRO_OK;
+}
+
 // Validation, launch, count readback and threshold update of one sparsify
 // step over [start, start + len); with accumulate_outside the rest of the
 // vector is accumulated too (the full error-feedback pass), and with sumsq the
@@ -281,9 +373,11 @@ micro_status execute_step(micro_ctx* ctx, const float* grad, float* residual, in
                           float* out_val, int64_t* k, double* sumsq) {
     DeviceScope scope(ctx->device);
     const micro_status checked = check_step_args(ctx, grad, residual, ctx->n_total, start, len, accumulate_outside,
-                                                 density, theta, out_idx, out_val, k);
+                                                 density, theta, out_idx, out_val, k,
+                                                 ctx->cfg.rule != MICRO_RULE_TOPK);
     if (checked != MICRO_OK) return checked;
     const int64_t n_outside = accumulate_outside ? ctx->n_total - len : 0;
+    const bool topk = ctx->cfg.rule == MICRO_RULE_TOPK;
     if (len == 0 && n_outside == 0) {  // nothing to do: nothing selected, threshold unchanged
         *k = 0;
         if (sumsq) *sumsq = 0.0;
@@ -300,7 +394,18 @@ micro_status execute_step(micro_ctx* ctx, const float* grad, float* residual, in
         const float none = std::numeric_limits<float>::quiet_NaN();
         const int64_t starts[3] = {0, start, start + len};
         const int64_t lens[3] = {start, len, ctx->n_total - start - len};
-        const float thf[3] = {none, threshold_as_f32(*theta), none};
+        float thf[3] = {none, threshold_as_f32(*theta), none};
+        TopkPlan plan;
+        if (topk && len > 0) {
+            if (ctx->needs_reset) {
+                micro_status s = reset_scratch(ctx);
+                if (s != MICRO_OK) return s;
+            }
+            const bool vec4 = ((reinterpret_cast<uintptr_t>(grad) ^ reinterpret_cast<uintptr_t>(residual)) & 15u) == 0;
+            micro_status s = topk_plan(ctx, grad, residual, start, len, density, vec4, &plan);
+            if (s != MICRO_OK) return s;
+            thf[1] = plan.found ? float_from_bits(plan.key) : none;
+        }
         int64_t kk[3];
         double sq[3];
         const micro_status st =
@@ -312,8 +417,32 @@ micro_status execute_step(micro_ctx* ctx, const float* grad, float* residual, in
             ctx->needs_reset = true;
             return MICRO_EHIP;
         }
-        *k = kk[1];
-        *theta = next_threshold(ctx->cfg, density, len, kk[1], *theta);
+        if (topk) {
+            const int64_t selected = plan.found ? plan.greater + plan.equal : 0;
+            if (kk[1] != selected) {
+                set_error(ctx, "top-k step selected %lld, the select found %lld", static_cast<long long>(kk[1]),
+                          static_cast<long long>(selected));
+                ctx->needs_reset = true;
+                return MICRO_EHIP;
+            }
+            if (plan.found && plan.keep < plan.equal) {
+                hipError_t e = micro::launch_topk_trim(out_idx, out_val, residual, selected, plan.key, plan.keep,
+                                                       ctx->h_topk_dev, ctx->stream);
+                if (e != hipSuccess) return hip_fail(ctx, e, "top-k trim launch");
+                if ((e = hipStreamSynchronize(ctx->stream)) != hipSuccess)
+                    return hip_fail(ctx, e, "hipStreamSynchronize");
+                double returned;
+                const int64_t bits = ctx->h_topk[6];
+                std::memcpy(&returned, &bits, sizeof returned);
+                sq[1] += returned;  // the values the trim returned to the residual
+                kk[1] = plan.greater + plan.keep;
+            }
+            *k = kk[1];
+            if (plan.found) *theta = static_cast<double>(float_from_bits(plan.key));
+        } else {
+            *k = kk[1];
+            *theta = next_threshold(ctx->cfg, density, len, kk[1], *theta);
+        }
         *sumsq = sq[0] + sq[1] + sq[2];
         return MICRO_OK;
     }
@@ -395,6 +524,14 @@ micro_status execute_step(micro_ctx* ctx, const float* grad, float* residual, in
     ctx->stats.redone_tiles = 0;
     if (timed && (e = hipEventRecord(ctx->ev[0], ctx->stream)) != hipSuccess)
         return hip_fail(ctx, e, "hipEventRecord");
+    // The top-k comparator: the exact k-th largest magnitude first (waited
+    // for), then the step at that magnitude (NaN: nothing selected).
+    TopkPlan plan;
+    if (topk && len > 0) {
+        micro_status s = topk_plan(ctx, grad, residual, start, len, density, vec4, &plan);
+        if (s != MICRO_OK) return s;
+        a.theta_f = plan.found ? float_from_bits(plan.key) : std::numeric_limits<float>::quiet_NaN();
+    }
     volatile int64_t* host_count = ctx->h_count;  // stored by the last kernel of the step
     host_count[0] = len > 0 ? -1 : 0;
     host_count[1] = len > 0 ? -1 : 0;
@@ -410,15 +547,31 @@ micro_status execute_step(micro_ctx* ctx, const float* grad, float* residual, in
                     : micro::launch_staged(a, vec4, ctx->stream);
         if (e != hipSuccess) return hip_fail(ctx, e, "sparsify kernel launch");
     }
+    // The step selected every value of the k-th magnitude; the trim keeps the
+    // lowest `keep` of them (the count is known from the select).
+    const bool trim = topk && plan.found && plan.keep < plan.equal;
+    if (trim && (e = micro::launch_topk_trim(out_idx, out_val, residual, plan.greater + plan.equal, plan.key,
+                                             plan.keep, ctx->h_topk_dev, ctx->stream)) != hipSuccess)
+        return hip_fail(ctx, e, "top-k trim launch");
     if (timed && (e = hipEventRecord(ctx->ev[1], ctx->stream)) != hipSuccess)
         return hip_fail(ctx, e, "hipEventRecord");
     if ((e = hipStreamSynchronize(ctx->stream)) != hipSuccess) return hip_fail(ctx, e, "hipStreamSynchronize");
-    const int64_t selected = host_count[0];
+    int64_t selected = host_count[0];
     if (selected < 0 || selected > len) {
         set_error(ctx, "device reported %lld selected of %lld", static_cast<long long>(selected),
                   static_cast<long long>(len));
         ctx->needs_reset = true;
         return MICRO_EHIP;
+    }
+    if (topk) {
+        const int64_t expected = plan.found ? plan.greater + plan.equal : 0;
+        if (selected != expected) {
+            set_error(ctx, "top-k step selected %lld, the select found %lld", static_cast<long long>(selected),
+                      static_cast<long long>(expected));
+            ctx->needs_reset = true;
+            return MICRO_EHIP;
+        }
+        if (trim) selected = plan.greater + plan.keep;
     }
     if (timed && (e = hipEventElapsedTime(&ctx->stats.kernel_ms, ctx->ev[0], ctx->ev[1])) != hipSuccess)
         return hip_fail(ctx, e, "hipEventElapsedTime");
@@ -426,7 +579,10 @@ micro_status execute_step(micro_ctx* ctx, const float* grad, float* residual, in
     ctx->stats.variant = staged ? MICRO_VARIANT_STAGED : MICRO_VARIANT_TICKET;
     ctx->stats.fused = len > 0 && fused ? 1 : 0;
     *k = selected;
-    *theta = next_threshold(ctx->cfg, density, len, selected, *theta);
+    if (!topk)
+        *theta = next_threshold(ctx->cfg, density, len, selected, *theta);
+    else if (plan.found)
+        *theta = static_cast<double>(float_from_bits(plan.key));
     return MICRO_OK;
 }
 
@@ -566,6 +722,10 @@ micro_status execute_sweep(micro_ctx* ctx, const float* grad, float* residual, i
         set_error(ctx, "the sweep needs the staged schedule");
         return MICRO_EINVAL;
     }
+    if (ctx->cfg.rule == MICRO_RULE_TOPK) {
+        set_error(ctx, "the top-k comparator runs through micro_sparsify_step and micro_ef_step, not the sweep");
+        return MICRO_EINVAL;
+    }
     if (!density_valid(density)) {
         set_error(ctx, "density %g outside (0, 1]", density);
         return MICRO_EINVAL;
@@ -666,6 +826,10 @@ micro_status micro_sparsify_step_noalloc(const float* grad, float* residual, int
     if (cfg) c = *cfg;
     if (n_total < 0 || !config_valid(c)) {
         set_error(nullptr, "invalid n_total or configuration");
+        return MICRO_EINVAL;
+    }
+    if (c.rule == MICRO_RULE_TOPK) {
+        set_error(nullptr, "the top-k comparator needs a context (micro_sparsify_step)");
         return MICRO_EINVAL;
     }
     if (n_total > std::numeric_limits<int32_t>::max()) {
@@ -774,7 +938,7 @@ micro_status micro_estimate_threshold(const micro_config* cfg, double density, i
     micro_config_default(&c);
     if (cfg) c = *cfg;
     if (!theta || !config_valid(c) || !density_valid(density) || part_len < 0 || k < 0 ||
-        k > part_len)
+        k > part_len || c.rule == MICRO_RULE_TOPK)  // the top-k threshold comes from the values
         return MICRO_EINVAL;
     *theta = next_threshold(c, density, part_len, k, *theta);
     return MICRO_OK;
@@ -840,7 +1004,11 @@ micro_status micro_sparsify_init(micro_ctx** out, int64_t n_total, void* hip_str
               hipMalloc(&ctx->d_count, 2 * sizeof(int64_t)) == hipSuccess &&
               hipHostMalloc(&ctx->h_count, (2 + micro::kMaxSweep) * sizeof(int64_t),
                             hipHostMallocMapped | hipHostMallocCoherent) == hipSuccess &&
-              hipHostGetDevicePointer(reinterpret_cast<void**>(&ctx->h_count_dev), ctx->h_count, 0) == hipSuccess;
+              hipHostGetDevicePointer(reinterpret_cast<void**>(&ctx->h_count_dev), ctx->h_count, 0) == hipSuccess &&
+              hipMalloc(&ctx->d_topk, sizeof(uint32_t) * (micro::kTopkBins + micro::kTopkStateWords)) == hipSuccess &&
+              hipHostMalloc(&ctx->h_topk, micro::kTopkHostWords * sizeof(int64_t),
+                            hipHostMallocMapped | hipHostMallocCoherent) == hipSuccess &&
+              hipHostGetDevicePointer(reinterpret_cast<void**>(&ctx->h_topk_dev), ctx->h_topk, 0) == hipSuccess;
     if (ok && ctx->has_staged) {
         // a sweep's segments each add at most one tile (alignment) and one chunk
         ctx->tile_capacity = n_total / micro::kStreamTile + 2 + micro::kMaxSweep;

@@ -1,0 +1,276 @@
+// gfx950 kernels of the exact top-k comparator (the sorting-based sparsifier
+// of Sec. 1 that keeps the k largest accumulated gradients; Sec. 2's error
+// feedback supplies the values): a radix select of the k-th largest
+// magnitude, and the trim of equal magnitudes.  See topk_kernel.h.
+#include "topk_kernel.h"
+
+namespace micro {
+namespace {
+
+using f32x4 = float __attribute__((ext_vector_type(4)));
+
+constexpr int kWave = 64;
+
+// Inclusive sum over the workgroup of one value per thread, in thread order;
+// *total receives the workgroup's sum.  Contains two barriers.
+template <int BLOCK>
+__device__ __forceinline__ uint32_t block_inclusive_sum(uint32_t v, uint32_t* s_wave, uint32_t* total) {
+    constexpr int WAVES = BLOCK / kWave;
+    const int lane = threadIdx.x & (kWave - 1);
+    const int wave = threadIdx.x / kWave;
+#pragma unroll
+    for (int off = 1; off < kWave; off <<= 1) {
+        const uint32_t o = __shfl_up(v, off, kWave);
+        if (lane >= off) v += o;
+    }
+    if (lane == kWave - 1) s_wave[wave] = v;
+    __syncthreads();
+    uint32_t before = 0, sum = 0;
+#pragma unroll
+    for (int w = 0; w < WAVES; ++w) {
+        const uint32_t t = s_wave[w];
+        if (w < wave) before += t;
+        sum += t;
+    }
+    *total = sum;
+    __syncthreads();  // s_wave is free again
+    return before + v;
+}
+
+// Pass `pass` of the radix select: a histogram of one digit of the keys of
+// acc = grad + residual over [start, end) (binary32 addition, as in the step)
+// that match the digits fixed by the earlier passes.  Digits: bits 30..20,
+// 19..9 and 8..0 of the key (the bit pattern with the sign cleared); NaN keys
+// are not counted.  Each workgroup counts in LDS, then adds its nonzero
+// counters to the global ones.
+template <bool VEC4>
+__global__ __launch_bounds__(kTopkHistBlock) void topk_hist_kernel(TopkArgs a, uint32_t pass) {
+    __shared__ uint32_t s_hist[kTopkBins];
+    const uint32_t* state = a.words + kTopkBins;
+    uint32_t prefix = 0, mask = 0;
+    if (pass > 0) {
+        if (state[kTopkStatus] != 0) return;  // uniform: nothing left to find
+        prefix = state[kTopkPrefix];
+        mask = state[kTopkMask];
+    }
+    const uint32_t shift = pass == 0 ? 20u : pass == 1 ? 9u : 0u;
+    const uint32_t digit = pass == 2 ? 511u : 2047u;
+    for (int b = threadIdx.x; b < kTopkBins; b += kTopkHistBlock) s_hist[b] = 0u;
+    __syncthreads();
+    auto count = [&](float g, float r) {
+        const float acc = g + r;
+        const uint32_t key = __float_as_uint(acc) & 0x7FFFFFFFu;
+        if (key <= kTopkKeyMax && (key & mask) == prefix) atomicAdd(&s_hist[(key >> shift) & digit], 1u);
+    };
+    const int64_t gtid = static_cast<int64_t>(blockIdx.x) * kTopkHistBlock + threadIdx.x;
+    const int64_t stride = static_cast<int64_t>(gridDim.x) * kTopkHistBlock;
+    if constexpr (VEC4) {
+        // the 16-byte groups of the body, two per thread in flight; fewer
+        // than four values before and after it
+        const f32x4* g4 = reinterpret_cast<const f32x4*>(a.grad + a.body_first);
+        const f32x4* r4 = reinterpret_cast<const f32x4*>(a.residual + a.body_first);
+        const int64_t groups = (a.body_end - a.body_first) / 4;
+        int64_t q = gtid;
+        for (; q + stride < groups; q += 2 * stride) {
+            const f32x4 g0 = __builtin_nontemporal_load(g4 + q);
+            const f32x4 g1 = __builtin_nontemporal_load(g4 + q + stride);
+            const f32x4 r0 = __builtin_nontemporal_load(r4 + q);
+            const f32x4 r1 = __builtin_nontemporal_load(r4 + q + stride);
+#pragma unroll
+            for (int c = 0; c < 4; ++c) count(g0[c], r0[c]);
+#pragma unroll
+            for (int c = 0; c < 4; ++c) count(g1[c], r1[c]);
+        }
+        if (q < groups) {
+            const f32x4 g0 = __builtin_nontemporal_load(g4 + q);
+            const f32x4 r0 = __builtin_nontemporal_load(r4 + q);
+#pragma unroll
+            for (int c = 0; c < 4; ++c) count(g0[c], r0[c]);
+        }
+        if (gtid < a.body_first - a.start) count(a.grad[a.start + gtid], a.residual[a.start + gtid]);
+        if (gtid < a.end - a.body_end) count(a.grad[a.body_end + gtid], a.residual[a.body_end + gtid]);
+    } else {
+        for (int64_t i = a.start + gtid; i < a.end; i += stride) count(a.grad[i], a.residual[i]);
+    }
+    __syncthreads();
+    for (int b = threadIdx.x; b < kTopkBins; b += kTopkHistBlock) {
+        const uint32_t c = s_hist[b];
+        if (c != 0u) atomicAdd(&a.words[b], c);
+    }
+}
+
+// The select after pass `pass`, one workgroup: finds the digit value whose
+// counter holds the wanted key (counting from the largest digit down), fixes
+// it in the prefix and leaves the counters zero for the next pass.  Pass 0
+// also counts the keys that are not NaN and caps the wanted rank by that
+// count; after pass 2 the prefix is the k-th key itself and the result goes to
+// the host words.
+__global__ __launch_bounds__(kTopkSelectBlock) void topk_select_kernel(TopkArgs a, uint32_t pass) {
+    constexpr int PER = kTopkBins / kTopkSelectBlock;
+    __shared__ uint32_t s_wave[kTopkSelectBlock / kWave];
+    uint32_t* state = a.words + kTopkBins;
+    const int tid = threadIdx.x;
+    if (pass > 0 && state[kTopkStatus] != 0) return;  // uniform
+    const uint32_t bins = pass == 2 ? 512u : static_cast<uint32_t>(kTopkBins);
+    const uint32_t per = bins / kTopkSelectBlock;  // 8, or 2 for the last digit
+    const uint32_t shift = pass == 0 ? 20u : pass == 1 ? 9u : 0u;
+    const uint32_t digit = bins - 1;
+    // thread t holds digits bins-1-t*per down to bins-(t+1)*per: thread order
+    // is decreasing digit order
+    uint32_t c[PER];
+    uint32_t mine = 0;
+#pragma unroll
+    for (int i = 0; i < PER; ++i) {
+        c[i] = static_cast<uint32_t>(i) < per ? a.words[bins - 1 - (tid * per + i)] : 0u;
+        mine += c[i];
+    }
+    uint32_t total;
+    const uint32_t above_mine = block_inclusive_sum<kTopkSelectBlock>(mine, s_wave, &total) - mine;
+    // every counter of this pass has been read (the sum's barriers): clear them
+#pragma unroll
+    for (int i = 0; i < PER; ++i)
+        if (static_cast<uint32_t>(i) < per) a.words[bins - 1 - (tid * per + i)] = 0u;
+    uint32_t remaining, prefix = 0, mask = 0, greater = 0;
+    if (pass == 0) {
+        remaining = total < a.k ? total : a.k;
+        if (tid == 0) {
+            state[kTopkValid] = total;
+            state[kTopkStatus] = remaining == 0 ? 2u : 0u;
+        }
+        if (remaining == 0) {  // uniform: every value is NaN
+            if (tid == 0) {
+                a.host[4] = total;
+                a.host[5] = 2;
+            }
+            return;
+        }
+    } else {
+        remaining = state[kTopkRemaining];
+        prefix = state[kTopkPrefix];
+        mask = state[kTopkMask];
+        greater = state[kTopkGreater];
+    }
+    if (above_mine < remaining && remaining <= above_mine + mine) {
+        uint32_t above = above_mine;
+#pragma unroll
+        for (int i = 0; i < PER; ++i) {
+            if (static_cast<uint32_t>(i) >= per) break;
+            if (above + c[i] >= remaining) {
+                const uint32_t d = bins - 1 - (tid * per + i);
+                prefix |= d << shift;
+                mask |= digit << shift;
+                greater += above;
+                remaining -= above;
+                state[kTopkPrefix] = prefix;
+                state[kTopkMask] = mask;
+                state[kTopkGreater] = greater;
+                state[kTopkRemaining] = remaining;
+                if (pass == 2) {
+                    state[kTopkEqual] = c[i];
+                    state[kTopkStatus] = 1u;
+                    a.host[0] = prefix;
+                    a.host[1] = greater;
+                    a.host[2] = c[i];
+                    a.host[3] = remaining;
+                    a.host[4] = state[kTopkValid];
+                    a.host[5] = 1;
+                }
+                break;
+            }
+            above += c[i];
+        }
+    }
+}
+
+// One workgroup walks the index-ordered list in chunks of kTopkTrimBlock * 4
+// entries, in order.  An entry whose value has key `key` is the r-th such
+// entry (r counted from 0 over the list); those with r >= m leave the list and
+// their values return to the residual.  Every other entry moves left by the
+// number of entries that left before it.  A chunk's entries are all read
+// before any of its stores (the scan's barriers), and no store reaches a
+// position beyond its entry's own, so the later chunks still find their
+// entries in place.
+__global__ __launch_bounds__(kTopkTrimBlock) void topk_trim_kernel(int32_t* out_idx, float* out_val, float* residual,
+                                                                   int64_t n, uint32_t key, int64_t m,
+                                                                   int64_t* host) {
+    constexpr int PER = 4;
+    constexpr int64_t CHUNK = static_cast<int64_t>(kTopkTrimBlock) * PER;
+    constexpr int WAVES = kTopkTrimBlock / kWave;
+    __shared__ uint32_t s_wave[WAVES];
+    __shared__ double s_sq[WAVES];
+    const int tid = threadIdx.x;
+    int64_t ties_seen = 0;
+    double sq = 0.0;
+    for (int64_t base = 0; base < n; base += CHUNK) {  // uniform
+        int32_t idx[PER];
+        float val[PER];
+        bool tie[PER];
+        uint32_t mine = 0;
+#pragma unroll
+        for (int i = 0; i < PER; ++i) {
+            const int64_t pos = base + tid * PER + i;
+            const bool live = pos < n;
+            idx[i] = live ? out_idx[pos] : 0;
+            val[i] = live ? out_val[pos] : 0.0f;
+            tie[i] = live && (__float_as_uint(val[i]) & 0x7FFFFFFFu) == key;
+            mine += tie[i] ? 1u : 0u;
+        }
+        uint32_t chunk_ties;
+        const uint32_t incl = block_inclusive_sum<kTopkTrimBlock>(mine, s_wave, &chunk_ties);
+        int64_t rank = ties_seen + (incl - mine);
+#pragma unroll
+        for (int i = 0; i < PER; ++i) {
+            const int64_t pos = base + tid * PER + i;
+            if (pos >= n) break;
+            const int64_t before = rank;
+            if (tie[i]) ++rank;
+            if (tie[i] && before >= m) {
+                residual[idx[i]] = val[i];
+                sq += static_cast<double>(val[i]) * static_cast<double>(val[i]);
+            } else if (before > m) {
+                const int64_t to = pos - (before - m);
+                out_idx[to] = idx[i];
+                out_val[to] = val[i];
+            }
+        }
+        ties_seen += chunk_ties;
+    }
+    // the returned values' squares: each thread's in list order, then the
+    // wavefronts' sums in order
+#pragma unroll
+    for (int off = kWave / 2; off > 0; off >>= 1) sq += __shfl_xor(sq, off, kWave);
+    if ((tid & (kWave - 1)) == 0) s_sq[tid / kWave] = sq;
+    __syncthreads();
+    if (tid == 0) {
+        double total = 0.0;
+        for (int w = 0; w < WAVES; ++w) total += s_sq[w];
+        host[6] = static_cast<int64_t>(__double_as_longlong(total));
+    }
+}
+
+}  // namespace
+
+hipError_t launch_topk_select(const TopkArgs& a, hipStream_t stream) {
+    if (!a.grad || !a.residual || !a.words || !a.host || a.blocks == 0 || a.end <= a.start || a.k == 0 ||
+        (a.vec4 && (a.body_first < a.start || a.body_end < a.body_first || a.body_end > a.end ||
+                    (a.body_end - a.body_first) % 4 != 0 || a.body_first - a.start > 3 || a.end - a.body_end > 3)))
+        return hipErrorInvalidValue;
+    for (uint32_t pass = 0; pass < 3; ++pass) {
+        if (a.vec4)
+            hipLaunchKernelGGL(topk_hist_kernel<true>, dim3(a.blocks), dim3(kTopkHistBlock), 0, stream, a, pass);
+        else
+            hipLaunchKernelGGL(topk_hist_kernel<false>, dim3(a.blocks), dim3(kTopkHistBlock), 0, stream, a, pass);
+        hipLaunchKernelGGL(topk_select_kernel, dim3(1), dim3(kTopkSelectBlock), 0, stream, a, pass);
+    }
+    return hipGetLastError();
+}
+
+hipError_t launch_topk_trim(int32_t* out_idx, float* out_val, float* residual, int64_t n, uint32_t key, int64_t m,
+                            int64_t* host, hipStream_t stream) {
+    if (!out_idx || !out_val || !residual || !host || n <= 0 || m < 0 || m > n) return hipErrorInvalidValue;
+    hipLaunchKernelGGL(topk_trim_kernel, dim3(1), dim3(kTopkTrimBlock), 0, stream, out_idx, out_val, residual, n,
+                       key, m, host);
+    return hipGetLastError();
+}
+
+}  // namespace micro

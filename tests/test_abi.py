@@ -97,6 +97,20 @@ def test_hard_threshold_rule_keeps_the_threshold():
         assert got == oracle.estimate(d, P, k, th, rule)
 
 
+def test_topk_rule_has_no_threshold_update():
+    """MICRO_RULE_TOPK is a valid configuration, but its threshold comes from
+    the values, so the host-only update refuses it; an unknown rule is
+    refused too."""
+    cfg = _lib.default_config()
+    cfg.rule = _lib.MICRO_RULE_TOPK
+    with pytest.raises(_lib.MicroError) as e:
+        _lib.micro_estimate_threshold(0.01, 1000, 10, 1.0, cfg)
+    assert e.value.status == _lib.MICRO_EINVAL
+    cfg.rule = 4
+    with pytest.raises(_lib.MicroError):
+        _lib.micro_estimate_threshold(0.01, 1000, 10, 1.0, cfg)
+
+
 def test_threshold_update_rejects_bad_arguments():
     for args in [(0.0, 10, 1, 1.0), (1.5, 10, 1, 1.0), (float("nan"), 10, 1, 1.0),
                  (0.1, -1, 0, 1.0), (0.1, 10, 11, 1.0), (0.1, 10, -1, 1.0)]:
@@ -221,6 +235,10 @@ def test_noalloc_step_argument_errors_without_device_work():
     cfg = _lib.default_config()
     cfg.beta = -1.0
     assert call(100, 0, 1, cfg=ctypes.byref(cfg)) == _lib.MICRO_EINVAL
+    topk = _lib.default_config()
+    topk.rule = _lib.MICRO_RULE_TOPK  # the top-k comparator needs a context
+    assert call(100, 0, 1, cfg=ctypes.byref(topk)) == _lib.MICRO_EINVAL
+    assert "context" in _lib.last_error()
     assert th.value == 1.5 and k.value == -3
     # 3 values over 5 partitions: partition 0 is empty
     assert call(3, 0, 5) == _lib.MICRO_OK

@@ -1,0 +1,267 @@
+"""The exact top-k comparator (MICRO_RULE_TOPK) against the CPU oracle (GPU).
+
+Every call goes through the C ABI via the ctypes binding.  Indices, values,
+the selected count, the returned k-th magnitude and the residual must equal
+the oracle's (oracle.topk_step / oracle.topk_ef_step) bit for bit.  At the
+GPT-1.3B size, where the oracle's sort would take minutes, the result is
+checked against the properties that define the top k: the count, strictly
+increasing indices inside the partition, the values and residual equal to the
+accumulation, every selected magnitude at least every other one, and equal
+magnitudes taken by lower index.
+"""
+import math
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import paper_2310_00967_amd as micro
+from paper_2310_00967_amd import synth
+
+from gpu_harness import note
+
+pytestmark = pytest.mark.gpu
+
+DEV = "cuda"
+AUTO, STAGED, TICKET = micro.MICRO_VARIANT_AUTO, micro.MICRO_VARIANT_STAGED, micro.MICRO_VARIANT_TICKET
+SEPARATE = -STAGED
+VARIANTS = pytest.mark.parametrize("variant", [STAGED, SEPARATE, TICKET], ids=["staged", "separate", "ticket"])
+
+
+def make(n, variant=AUTO, **kw):
+    if variant == SEPARATE:
+        return micro.Sparsifier(n, device=DEV, rule=micro.MICRO_RULE_TOPK, variant=STAGED, separate_scan=True, **kw)
+    return micro.Sparsifier(n, device=DEV, rule=micro.MICRO_RULE_TOPK, variant=variant, **kw)
+
+
+def same_bits(a, b):
+    """Bitwise equality of two float32 arrays, any NaN matching any NaN."""
+    a = np.ascontiguousarray(a, np.float32)
+    b = np.ascontiguousarray(b, np.float32)
+    both = np.isnan(a) & np.isnan(b)
+    return a.shape == b.shape and np.array_equal(a.view(np.uint32)[~both], b.view(np.uint32)[~both])
+
+
+def topk_vs_oracle(g, res, rank, world, density, variant=AUTO, phase_shift=0, sp=None, theta=1.0):
+    """One call on both sides; g/res are host float32 arrays."""
+    N = g.size
+    own = sp is None
+    if own:
+        sp = make(N, variant)
+    gbuf = torch.empty(N + 4, dtype=torch.float32, device=DEV)
+    g_dev = gbuf[phase_shift:phase_shift + N]
+    g_dev.copy_(torch.from_numpy(g))
+    r_dev = torch.from_numpy(res).to(DEV)
+    s, ln = oracle.partition(N, rank, world)
+    sentinel = -12345
+    out_idx = torch.full((max(1, ln) + 8,), sentinel, dtype=torch.int32, device=DEV)
+    out_val = torch.full((max(1, ln) + 8,), float(sentinel), dtype=torch.float32, device=DEV)
+    k, th, idx, val = sp.step(g_dev, r_dev, rank, world, density, theta, out_idx, out_val)
+    r_or = res.copy()
+    o_idx, o_val, k_or, th_or = oracle.topk_step(g, r_or, rank, world, density, theta)
+    where = f"N={N} rank {rank}/{world} d={density} variant {variant} shift {phase_shift}"
+    assert k == k_or, f"{where}: k {k} oracle {k_or}"
+    assert th == th_or, f"{where}: kth {th!r} oracle {th_or!r}"
+    assert np.array_equal(idx.cpu().numpy(), o_idx), f"{where}: indices differ"
+    assert same_bits(val.cpu().numpy(), o_val), f"{where}: values differ"
+    assert same_bits(r_dev.cpu().numpy(), r_or), f"{where}: residual differs"
+    # the step writes the pairs of every value of magnitude >= the k-th; past
+    # them nothing is written
+    acc = (g[s:s + ln] + res[s:s + ln]).astype(np.float32)
+    reach = int(np.sum(np.abs(acc) >= np.float32(th_or))) if k_or else 0
+    assert np.all(out_idx.cpu().numpy()[reach:] == sentinel), f"{where}: written past the selection"
+    if own:
+        sp.close()
+    return k
+
+
+def gen(rng, n, kind):
+    if kind == "normal":
+        return rng.standard_normal(n).astype(np.float32), (0.5 * rng.standard_normal(n)).astype(np.float32)
+    if kind == "quantised":  # few magnitudes: many values share the k-th
+        return (np.round(rng.standard_normal(n) * 4) / 4).astype(np.float32), np.zeros(n, np.float32)
+    if kind == "laplace":
+        return rng.laplace(0, 1e-3, n).astype(np.float32), rng.laplace(0, 1e-3, n).astype(np.float32)
+    raise ValueError(kind)
+
+
+@pytest.mark.parametrize("N,world,rank", [
+    (1, 1, 0), (3, 1, 0), (1023, 1, 0), (1024, 1, 0), (1025, 1, 0), (4099, 3, 1),
+    (12289, 3, 2), (100003, 16, 5), (262144 + 5, 4, 3), (1000, 2000, 1999),
+])
+@pytest.mark.parametrize("density", [1e-4, 0.01, 0.5, 1.0])
+@VARIANTS
+def test_ragged_sizes_and_densities(N, world, rank, density, variant):
+    rng = np.random.default_rng(N * 3 + rank + int(density * 1e4))
+    g, res = gen(rng, N, "normal")
+    topk_vs_oracle(g, res, rank, world, density, variant)
+
+
+@pytest.mark.parametrize("N", [5000, 1 << 20, (1 << 20) + 3, 3_000_017])
+@pytest.mark.parametrize("density", [0.01, 0.3])
+@pytest.mark.parametrize("kind", ["quantised", "laplace"])
+@pytest.mark.parametrize("phase_shift", [0, 1])
+def test_equal_magnitudes_and_phases(N, density, kind, phase_shift):
+    """Quantised values put thousands of values at the k-th magnitude, so the
+    trim pass runs over long lists; phase 1 takes the scalar-load passes."""
+    note(f"top-k ties N={N} d={density} {kind} shift {phase_shift}")
+    rng = np.random.default_rng(N + int(density * 100) + len(kind))
+    g, res = gen(rng, N, kind)
+    topk_vs_oracle(g, res, 0, 1, density, AUTO, phase_shift)
+
+
+@VARIANTS
+def test_all_values_equal(variant):
+    """Every value ties: the k lowest indices, the rest returned to the residual."""
+    for N, d in [(10, 0.3), (4097, 0.01), (2_000_003, 0.25)]:
+        g = np.full(N, -0.5, np.float32)
+        res = np.zeros(N, np.float32)
+        k = topk_vs_oracle(g, res, 0, 1, d, variant)
+        assert k == oracle.topk_count(d, N)
+
+
+@VARIANTS
+def test_special_values(variant):
+    f = np.float32
+    tiny = f(2.0) ** -149
+    base = np.array([np.nan, np.inf, -np.inf, -0.0, 0.0, tiny, 1.0, -1.0, tiny, 3.0], dtype=np.float32)
+    g = np.tile(base, 1000)
+    res = np.tile(np.array([0.0, 0.0, 0.0, -0.0, 0.0, tiny, 0.0, 0.0, -tiny, np.nan], np.float32), 1000)
+    for d in [1e-4, 0.05, 0.2, 0.35, 0.7, 1.0]:  # infinities only, then magnitude 3 ... up to every non-NaN value
+        topk_vs_oracle(g, res, 0, 1, d, variant)
+    # more NaN than the selection leaves: fewer than k selected
+    g2 = g.copy()
+    g2[::3] = np.nan
+    topk_vs_oracle(g2, res, 0, 1, 1.0, variant)
+    # every value NaN: nothing selected, theta unchanged, residual = acc
+    g3 = np.full(5000, np.nan, np.float32)
+    k = topk_vs_oracle(g3, np.zeros(5000, np.float32), 0, 1, 0.5, variant, theta=7.25)
+    assert k == 0
+    # zeros only: the k-th magnitude is 0, the lowest indices win
+    k = topk_vs_oracle(np.zeros(3000, np.float32), np.zeros(3000, np.float32), 0, 1, 0.1, variant)
+    assert k == 300
+
+
+def test_one_context_many_calls():
+    """The radix-select counters and state are left clean by every call: a
+    context alternating sizes, partitions, densities and the nothing-selected
+    case stays exact."""
+    N = 300_007
+    sp = make(N)
+    rng = np.random.default_rng(99)
+    for t in range(24):
+        kind = ["normal", "quantised", "laplace"][t % 3]
+        g, res = gen(rng, N, kind)
+        world = [1, 3, 8][t % 3]
+        rank = t % world
+        d = [0.001, 0.02, 0.5, 1.0][t % 4]
+        if t % 7 == 6:
+            g[:] = np.nan
+        topk_vs_oracle(g, res, rank, world, d, sp=sp)
+    sp.close()
+
+
+@pytest.mark.parametrize("N,world", [(100_003, 4), (3_000_017, 8)])
+def test_ef_step_with_local_error(N, world):
+    rng = np.random.default_rng(N)
+    sp = make(N)
+    g_dev = torch.empty(N, dtype=torch.float32, device=DEV)
+    r_dev = torch.zeros(N, dtype=torch.float32, device=DEV)
+    r_host = np.zeros(N, np.float32)
+    theta = 1.0
+    for t in range(3):
+        g = (np.round(rng.standard_normal(N) * 8) / 8).astype(np.float32)  # ties at the k-th magnitude
+        g_dev.copy_(torch.from_numpy(g))
+        k, th, c, idx, val, sq = sp.ef_step(g_dev, r_dev, t, 1, world, 0.01, theta, local_error=True)
+        o_idx, o_val, k_or, th_or, c_or = oracle.topk_ef_step(g, r_host, t, 1, world, 0.01, theta)
+        assert (k, th, c) == (k_or, th_or, c_or)
+        assert np.array_equal(idx.cpu().numpy(), o_idx)
+        assert same_bits(val.cpu().numpy(), o_val)
+        assert same_bits(r_dev.cpu().numpy(), r_host)
+        exact = math.fsum(float(x) * float(x) for x in r_host.astype(np.float64))
+        ties = int(np.sum(np.abs(r_host) == np.float32(th_or)))
+        assert abs(sq - exact) <= (N + ties) * 2.0 ** -53 * exact
+        theta = th_or
+    sp.close()
+
+
+def test_sweep_rejects_topk():
+    sp = make(1000)
+    g = torch.zeros(1000, dtype=torch.float32, device=DEV)
+    r = torch.zeros(1000, dtype=torch.float32, device=DEV)
+    with pytest.raises(micro.MicroError) as e:
+        sp.sweep(g, r, 2, 0.1, [1.0, 1.0])
+    assert e.value.status == 1
+    sp.close()
+
+
+def test_bert_large_rank3_full_partition():
+    """BERT-large rank 3 of 8 (41,892,736 values) at d = 0.01, the whole
+    partition against the oracle, two steps of error feedback."""
+    w = synth.get("bert_large")
+    sp = make(w.n_total)
+    g_dev = torch.empty(w.n_total, dtype=torch.float32, device=DEV)
+    r_dev = torch.zeros(w.n_total, dtype=torch.float32, device=DEV)
+    s, ln = oracle.partition(w.n_total, 3, w.world)
+    r_host = np.zeros(ln, np.float32)
+    theta = 1.0
+    for t in range(2):
+        synth.gradient(w, t, DEV, out=g_dev)
+        g_host = g_dev[s:s + ln].cpu().numpy()
+        note(f"top-k bert_large rank 3 step {t}")
+        k, th, idx, val = sp.step(g_dev, r_dev, 3, w.world, 0.01, theta)
+        o_idx, o_val, k_or, th_or = oracle.topk_select(g_host, r_host, 0, ln, 0.01, kth=theta)
+        assert k == k_or == oracle.topk_count(0.01, ln) and th == th_or
+        assert np.array_equal(idx.cpu().numpy(), o_idx + s)
+        assert same_bits(val.cpu().numpy(), o_val)
+        assert same_bits(r_dev[s:s + ln].cpu().numpy(), r_host)
+        theta = th
+    sp.close()
+
+
+def check_topk_properties(g, before, after, s, ln, idx, val, k, th, density):
+    """The top k of [s, s + ln), checked from its definition with torch."""
+    acc = g[s:s + ln] + before[s:s + ln]
+    valid = ~torch.isnan(acc)
+    want = min(oracle.topk_count(density, ln), int(valid.sum()))
+    assert k == want
+    loc = idx.long() - s
+    assert int(loc[0]) >= 0 and int(loc[-1]) < ln
+    assert bool((loc[1:] > loc[:-1]).all())
+    assert torch.equal(val.view(torch.int32), acc[loc].view(torch.int32))
+    sel = torch.zeros(ln, dtype=torch.bool, device=acc.device)
+    sel[loc] = True
+    part_after = after[s:s + ln]
+    assert bool((part_after[sel].view(torch.int32) == 0).all())
+    assert torch.equal(part_after[~sel].view(torch.int32), acc[~sel].view(torch.int32))
+    assert torch.equal(after[:s].view(torch.int32), before[:s].view(torch.int32))
+    assert torch.equal(after[s + ln:].view(torch.int32), before[s + ln:].view(torch.int32))
+    mag = acc.abs()
+    kth = mag[loc].min()
+    assert th == float(kth)
+    others = ~sel & valid
+    if bool(others.any()):
+        assert float(mag[others].max()) <= float(kth)
+        tied_out = torch.nonzero(others & (mag == kth))
+        if tied_out.numel():
+            assert int(torch.nonzero(sel & (mag == kth)).max()) < int(tied_out.min())
+
+
+@pytest.mark.parametrize("density", [0.01, 0.001])
+def test_gpt_1p3b_full_size_properties(density):
+    w = synth.get("gpt_1p3b")
+    sp = make(w.n_total)
+    g = torch.empty(w.n_total, dtype=torch.float32, device=DEV)
+    res = torch.zeros(w.n_total, dtype=torch.float32, device=DEV)
+    theta = 1.0
+    for t in range(2):
+        synth.gradient(w, t, DEV, out=g)
+        before = res.clone()
+        note(f"top-k gpt_1p3b d={density} step {t}")
+        k, th, idx, val = sp.step(g, res, 0, 1, density, theta)
+        check_topk_properties(g, before, res, 0, w.n_total, idx, val, k, th, density)
+        theta = th
+        del before
+    sp.close()
+    torch.cuda.empty_cache()
