@@ -73,12 +73,13 @@ def parse_args():
                          "million values)")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only run a plain device copy of known size (HBM counter scaling)")
-    ap.add_argument("--path", default="step", choices=["step", "ef", "union", "sweep", "ceiling"],
+    ap.add_argument("--path", default="step", choices=["step", "ef", "union", "sweep", "ceiling", "topk"],
                     help="step: the partition-only sparsify step (default); ef: the full error-feedback "
                          "pass with cyclic partitions; union: the gather/reset and model update around "
                          "the exchange; sweep: every partition in one set of launches, with the "
                          "local-error norms; ceiling: vendor streams (torch's in-place add, a device "
-                         "copy) beside the step on the same vector")
+                         "copy) beside the step on the same vector; topk: the exact top-k comparator "
+                         "beside the threshold step and the hard-threshold rule on the same gradients")
     ap.add_argument("--local-error", action="store_true",
                     help="with --path ef: also return the squared norm of the whole residual (Eq. 1)")
     args = ap.parse_args()
@@ -363,6 +364,90 @@ def measure_ef(w, density, pool, sp, warmup, steps, local_error=False):
             "kernel_gbs": alg / kernel_s / 1e9, "kernel_ms_avg": kernel_s * 1e3 / len(log),
             "alg_bytes_per_launch": alg / len(log), "ms_per_step": elapsed * 1e3 / steps,
             "k_avg": sum(k for _, k, _ in log) / len(log), "worker": worker, "fused": fused}
+
+
+TOPK_PASS_BYTES = 36  # per value: three histogram passes reading grad and residual, then the step's 12
+
+
+def measure_topk(w, density, pool, warmup, steps):
+    """The exact top-k comparator (MICRO_RULE_TOPK) on partition w.ranks[0],
+    beside the threshold step (the default rule) and the hard-threshold rule
+    (Sec. 1's comparators) on the same gradients, each with its own residual
+    under error feedback: device time per step from the library's events
+    (for top-k they include the wait for the k-th magnitude between its
+    passes and the step's launches), and the density each rule selects at
+    every step, warm-up included.  Algorithmic bytes: top-k 36 B per value of
+    the partition (three histogram passes of 8 B, the step's 12 B) plus 8 B
+    per selected value; the threshold rules 12 B per value plus 8 B per
+    selected value."""
+    import torch
+    import paper_2310_00967_amd as micro
+    from paper_2310_00967_amd import synth
+    rank = w.ranks[0]
+    N = w.n_total
+    start, ln = micro.micro_partition(N, rank, w.world)
+    theta0 = synth.initial_theta(w, pool[0], start, start + ln, density)
+    rules = {"topk": micro.MICRO_RULE_TOPK, "threshold": micro.MICRO_RULE_PROPORTIONAL,
+             "hard_threshold": micro.MICRO_RULE_HARD_THRESHOLD}
+    out = {}
+    for name, rule in rules.items():
+        sp = micro.Sparsifier(N, device="cuda", time_kernel=True, rule=rule)
+        res = torch.zeros(N, dtype=torch.float32, device="cuda")
+        out_idx, out_val = sp.outputs(ln)
+        theta = theta0
+        ks, ms = [], []
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        for t in range(warmup + steps):
+            if t == warmup:
+                torch.cuda.synchronize()
+                t0 = time.perf_counter()
+            k, theta, _, _ = sp.step(pool[t % len(pool)], res, rank, w.world, density, theta, out_idx, out_val)
+            ks.append(k)
+            if t >= warmup:
+                ms.append(sp.last_stats()[0])
+        torch.cuda.synchronize()
+        elapsed = time.perf_counter() - t0
+        sp.close()
+        del res
+        kernel_ms = sum(ms) / len(ms)
+        k_avg = sum(ks[warmup:]) / steps
+        per_value = TOPK_PASS_BYTES if rule == micro.MICRO_RULE_TOPK else 12
+        alg = per_value * ln + 8 * k_avg
+        dens = [k / ln for k in ks]
+        half = dens[len(dens) // 2:]
+        out[name] = {"kernel_ms_avg": kernel_ms, "ms_per_step": elapsed * 1e3 / steps,
+                     "g_elem_s": ln * steps / elapsed / 1e9, "alg_bytes_per_launch": alg,
+                     "kernel_gbs": alg / (kernel_ms * 1e-3) / 1e9,
+                     "frac": alg / (kernel_ms * 1e-3) / 1e9 / HBM_PEAK_GBS, "k_avg": k_avg,
+                     "density_series": dens,
+                     "density_error_last_half": sum(abs(x - density) / density for x in half) / len(half)}
+    out["partition"] = (rank, start, ln)
+    return out
+
+
+def cpu_baseline_topk(w, density, pool, target_s):
+    """The oracle's top-k selection, single-threaded on one pinned core, on
+    the worker's partition (a prefix of 2^25 values where the partition is
+    longer: its sort is O(P log P)), repeated for about target_s seconds."""
+    import oracle
+    import paper_2310_00967_amd as micro
+    start, ln = micro.micro_partition(w.n_total, w.ranks[0], w.world)
+    n = min(ln, 1 << 25)
+    g = pool[0][start:start + n].cpu().numpy()
+    res0 = pool[1 % len(pool)][start:start + n].cpu().numpy() * 0.5
+    done, elapsed = 0, 0.0
+    with OneCore() as core:
+        while elapsed < target_s or done == 0:
+            res = res0.copy()
+            t0 = time.perf_counter()
+            oracle.topk_select(g, res, 0, n, density)
+            elapsed += time.perf_counter() - t0
+            done += 1
+    what = "the partition" if n == ln else f"the first {n} values of the partition"
+    return {"value": done * n / elapsed / 1e9, "unit": "G elem/s", "cores": 1, "kind": "oracle",
+            "sample": f"{done} top-k selection(s) of {what} of {w.name} rank {w.ranks[0]} ({n} values, "
+                      f"d={density}, {elapsed:.1f} s of single-threaded oracle time), {core.describe()}"}
 
 
 def measure_sweep(w, density, pool, sp, warmup, steps):
@@ -733,6 +818,26 @@ def main_path(args, w, head, pool, n_pool, sp):
     cfg = {"workload": w.name, "n_total": w.n_total, "world": w.world, "worker": w.ranks[0],
            "density": head, "distribution": w.dist, "gradient_pool": n_pool,
            "parallelism": "one worker on one GPU", "path": args.path}
+    if args.path == "topk":
+        r = measure_topk(w, head, pool, args.warmup, args.steps)
+        cpu = cpu_baseline_topk(w, head, pool, args.cpu_seconds) if args.cpu_seconds > 0 else None
+        rank, start, ln = r.pop("partition")
+        cfg.update({"rank": rank, "partition_len": ln, "parallelism": "one worker's partition on one GPU"})
+        tk = r["topk"]
+        line = {"metric": "exact top-k comparator throughput (G elem/s of the partition), beside the threshold step",
+                "value": tk["g_elem_s"], "unit": "G elem/s", "ms_per_step": tk["ms_per_step"], **common,
+                "config": cfg, "k_avg": tk["k_avg"],
+                "roofline": {"bound": "hbm", "achieved": tk["kernel_gbs"], "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                             "frac": tk["frac"], "traffic": None,
+                             "kernel": "3 x (topk_hist_kernel + topk_select_kernel), the wait for the k-th "
+                                       "magnitude, then the step's launches (+ topk_trim_kernel when magnitudes "
+                                       "tie); event-timed together",
+                             "kernel_ms_avg": tk["kernel_ms_avg"], "alg_bytes_per_launch": tk["alg_bytes_per_launch"]},
+                "topk_over_threshold_step_time": tk["kernel_ms_avg"] / r["threshold"]["kernel_ms_avg"],
+                "rules": r,
+                "cpu_baseline": cpu}
+        print(json.dumps(line), flush=True)
+        return
     if args.path == "sweep":
         r = measure_sweep(w, head, pool, sp, args.warmup, args.steps)
         cpu = cpu_baseline_sweep(w, head, pool, args.cpu_seconds) if args.cpu_seconds > 0 else None

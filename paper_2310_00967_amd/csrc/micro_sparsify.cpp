@@ -314,6 +314,18 @@ struct TopkPlan {
     int64_t keep = 0;
 };
 
+// The parallel trim's scratch: the staged schedule's staging pairs (free once
+// the step's kernels are done), tile counts and tile norms, when they hold a
+// list of n entries; else none (the one-workgroup trim).
+micro::TopkTrimScratch trim_scratch(const micro_ctx* ctx, int64_t n) {
+    micro::TopkTrimScratch t{nullptr, nullptr, nullptr};
+    const int64_t chunks = (n + micro::kTopkTrimChunk - 1) / micro::kTopkTrimChunk;
+    if (ctx->has_staged && ctx->d_stage && ctx->d_tile_counts && ctx->d_tile_sumsq &&
+        n <= ctx->tile_capacity * static_cast<int64_t>(micro::kStageCap) && chunks <= ctx->tile_capacity)
+        t = {ctx->d_stage, ctx->d_tile_counts, ctx->d_tile_sumsq};
+    return t;
+}
+
 // Radix select on the device (three histogram passes and selects over
 // acc = grad + residual of [start, start + len)), waited for.
 micro_status topk_plan(micro_ctx* ctx, const float* grad, const float* residual, int64_t start, int64_t len,
@@ -426,8 +438,10 @@ micro_status execute_step(micro_ctx* ctx, const float* grad, float* residual, in
                 return MICRO_EHIP;
             }
             if (plan.found && plan.keep < plan.equal) {
-                hipError_t e = micro::launch_topk_trim(out_idx, out_val, residual, selected, plan.key, plan.keep,
-                                                       ctx->h_topk_dev, ctx->stream);
+                const micro::TopkTrimScratch scratch = trim_scratch(ctx, selected);
+                hipError_t e = micro::launch_topk_trim(out_idx, out_val, residual, selected,
+                                                       plan.greater + plan.keep, plan.key, plan.keep,
+                                                       ctx->h_topk_dev, &scratch, ctx->stream);
                 if (e != hipSuccess) return hip_fail(ctx, e, "top-k trim launch");
                 if ((e = hipStreamSynchronize(ctx->stream)) != hipSuccess)
                     return hip_fail(ctx, e, "hipStreamSynchronize");
@@ -550,9 +564,13 @@ micro_status execute_step(micro_ctx* ctx, const float* grad, float* residual, in
     // The step selected every value of the k-th magnitude; the trim keeps the
     // lowest `keep` of them (the count is known from the select).
     const bool trim = topk && plan.found && plan.keep < plan.equal;
-    if (trim && (e = micro::launch_topk_trim(out_idx, out_val, residual, plan.greater + plan.equal, plan.key,
-                                             plan.keep, ctx->h_topk_dev, ctx->stream)) != hipSuccess)
-        return hip_fail(ctx, e, "top-k trim launch");
+    if (trim) {
+        const int64_t listed = plan.greater + plan.equal;
+        const micro::TopkTrimScratch scratch = trim_scratch(ctx, listed);
+        if ((e = micro::launch_topk_trim(out_idx, out_val, residual, listed, plan.greater + plan.keep, plan.key,
+                                         plan.keep, ctx->h_topk_dev, &scratch, ctx->stream)) != hipSuccess)
+            return hip_fail(ctx, e, "top-k trim launch");
+    }
     if (timed && (e = hipEventRecord(ctx->ev[1], ctx->stream)) != hipSuccess)
         return hip_fail(ctx, e, "hipEventRecord");
     if ((e = hipStreamSynchronize(ctx->stream)) != hipSuccess) return hip_fail(ctx, e, "hipStreamSynchronize");

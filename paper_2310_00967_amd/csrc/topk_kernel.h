@@ -58,9 +58,20 @@ hipError_t launch_topk_select(const TopkArgs& args, hipStream_t stream);
 
 // Drops from the index-ordered output list [0, n) the equal keys `key` after
 // the first m of them, returning their values to the residual and compacting
-// the list in place (one workgroup, the list in order); host[6] receives the
-// binary64 sum of squares of the returned values.
-hipError_t launch_topk_trim(int32_t* out_idx, float* out_val, float* residual, int64_t n, uint32_t key, int64_t m,
-                            int64_t* host, hipStream_t stream);
+// the list; host[6] receives the binary64 sum of squares of the returned
+// values.  With scratch (temp: n pairs, counts and partial: one entry per
+// kTopkTrimChunk list entries) the list is compacted by the whole device in
+// four launches: ties counted per chunk, the counts scanned, every kept entry
+// placed in temp and the dropped ones returned, temp copied back.  Without
+// it (a null temp) one workgroup compacts the list in place, in order.
+constexpr int kTopkTrimChunk = 4096;  // list entries per workgroup of the parallel trim
+struct TopkTrimScratch {
+    uint2* temp;       // >= n pairs
+    uint32_t* counts;  // >= ceil(n / kTopkTrimChunk)
+    double* partial;   // >= ceil(n / kTopkTrimChunk)
+};
+// kept: the entries that stay (n less the key-`key` entries after the first m).
+hipError_t launch_topk_trim(int32_t* out_idx, float* out_val, float* residual, int64_t n, int64_t kept, uint32_t key,
+                            int64_t m, int64_t* host, const TopkTrimScratch* scratch, hipStream_t stream);
 
 }  // namespace micro

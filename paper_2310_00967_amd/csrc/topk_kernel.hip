@@ -248,6 +248,139 @@ __global__ __launch_bounds__(kTopkTrimBlock) void topk_trim_kernel(int32_t* out_
     }
 }
 
+constexpr int kTrimBlock = 256;
+constexpr int kTrimPer = kTopkTrimChunk / kTrimBlock;  // entries per thread, row j at j * kTrimBlock + thread
+constexpr int kTrimWaves = kTrimBlock / kWave;
+
+__device__ __forceinline__ bool has_key(float v, uint32_t key) {
+    return (__float_as_uint(v) & 0x7FFFFFFFu) == key;
+}
+
+// Sum of one binary64 per thread over the workgroup in a fixed order (a
+// butterfly in each wavefront, then the wavefronts in order); valid in
+// thread 0.  Contains one barrier.
+template <int WAVES>
+__device__ __forceinline__ double block_sum_f64(double v, double* s_part) {
+#pragma unroll
+    for (int off = kWave / 2; off > 0; off >>= 1) v += __shfl_xor(v, off, kWave);
+    if ((threadIdx.x & (kWave - 1)) == 0) s_part[threadIdx.x / kWave] = v;
+    __syncthreads();
+    double total = 0.0;
+    if (threadIdx.x == 0)
+        for (int w = 0; w < WAVES; ++w) total += s_part[w];
+    return total;
+}
+
+// Parallel trim, launch 1: the entries of key `key` in each chunk of
+// kTopkTrimChunk list entries.
+__global__ __launch_bounds__(kTrimBlock) void topk_trim_count_kernel(const float* out_val, int64_t n, uint32_t key,
+                                                                     uint32_t* counts) {
+    __shared__ uint32_t s_wave[kTrimWaves];
+    const int64_t base = static_cast<int64_t>(blockIdx.x) * kTopkTrimChunk;
+    uint32_t c = 0;
+#pragma unroll
+    for (int j = 0; j < kTrimPer; ++j) {
+        const int64_t p = base + j * kTrimBlock + threadIdx.x;
+        if (p < n && has_key(out_val[p], key)) ++c;
+    }
+    uint32_t total;
+    block_inclusive_sum<kTrimBlock>(c, s_wave, &total);
+    if (threadIdx.x == 0) counts[blockIdx.x] = total;
+}
+
+// Launch 2, one workgroup: counts[0, chunks) become exclusive prefix sums.
+__global__ __launch_bounds__(kTopkTrimBlock) void topk_trim_scan_kernel(uint32_t* counts, uint32_t chunks) {
+    __shared__ uint32_t s_wave[kTopkTrimBlock / kWave];
+    uint32_t carry = 0;
+    for (uint32_t base = 0; base < chunks; base += kTopkTrimBlock) {  // uniform
+        const uint32_t i = base + threadIdx.x;
+        const uint32_t c = i < chunks ? counts[i] : 0u;
+        uint32_t total;
+        const uint32_t incl = block_inclusive_sum<kTopkTrimBlock>(c, s_wave, &total);
+        if (i < chunks) counts[i] = carry + incl - c;
+        carry += total;
+    }
+}
+
+// Launch 3: each entry's count of key-`key` entries before it (its chunk's
+// prefix, then rows in order and lanes in order inside the chunk) decides:
+// an entry of that key at rank >= m is returned to the residual, every other
+// entry goes to temp at its position less the entries dropped before it.
+// partial[chunk] receives the binary64 sum of squares of the returned values.
+__global__ __launch_bounds__(kTrimBlock) void topk_trim_scatter_kernel(const int32_t* out_idx, const float* out_val,
+                                                                       float* residual, int64_t n, uint32_t key,
+                                                                       int64_t m, const uint32_t* chunk_before,
+                                                                       uint2* temp, double* partial) {
+    __shared__ uint32_t s_row_wave[kTrimPer * kTrimWaves];
+    __shared__ double s_sq[kTrimWaves];
+    const int lane = threadIdx.x & (kWave - 1);
+    const int wave = threadIdx.x / kWave;
+    const int64_t base = static_cast<int64_t>(blockIdx.x) * kTopkTrimChunk;
+    const uint64_t below = lane ? (~0ull >> (kWave - lane)) : 0ull;
+    uint32_t lane_rank[kTrimPer];
+    bool tie[kTrimPer];
+#pragma unroll
+    for (int j = 0; j < kTrimPer; ++j) {
+        const int64_t p = base + j * kTrimBlock + threadIdx.x;
+        tie[j] = p < n && has_key(out_val[p], key);
+        const uint64_t mask = __ballot(tie[j]);
+        lane_rank[j] = static_cast<uint32_t>(__popcll(mask & below));
+        if (lane == 0) s_row_wave[j * kTrimWaves + wave] = static_cast<uint32_t>(__popcll(mask));
+    }
+    __syncthreads();
+    if (wave == 0) {  // exclusive prefix of the kTrimPer * kTrimWaves counts, in list order
+        static_assert(kTrimPer * kTrimWaves == kWave, "one count per lane of wavefront 0");
+        uint32_t v = s_row_wave[lane];
+        const uint32_t own = v;
+#pragma unroll
+        for (int off = 1; off < kWave; off <<= 1) {
+            const uint32_t o = __shfl_up(v, off, kWave);
+            if (lane >= off) v += o;
+        }
+        s_row_wave[lane] = v - own;
+    }
+    __syncthreads();
+    const int64_t chunk_ties = chunk_before[blockIdx.x];
+    double sq = 0.0;
+#pragma unroll
+    for (int j = 0; j < kTrimPer; ++j) {
+        const int64_t p = base + j * kTrimBlock + threadIdx.x;
+        if (p >= n) continue;
+        const int64_t before = chunk_ties + s_row_wave[j * kTrimWaves + wave] + lane_rank[j];
+        const int32_t idx = out_idx[p];
+        const float val = out_val[p];
+        if (tie[j] && before >= m) {
+            residual[idx] = val;
+            sq += static_cast<double>(val) * static_cast<double>(val);
+        } else {
+            const int64_t to = p - (before > m ? before - m : 0);
+            temp[to] = make_uint2(static_cast<uint32_t>(idx), __float_as_uint(val));
+        }
+    }
+    const double total = block_sum_f64<kTrimWaves>(sq, s_sq);
+    if (threadIdx.x == 0) partial[blockIdx.x] = total;
+}
+
+// Launch 4: temp[0, kept) back into the output lists; workgroup 0 also adds
+// the chunks' partial sums in a fixed order into host[6].
+__global__ __launch_bounds__(kTrimBlock) void topk_trim_copy_kernel(const uint2* temp, int64_t kept, int32_t* out_idx,
+                                                                    float* out_val, const double* partial,
+                                                                    uint32_t chunks, int64_t* host) {
+    __shared__ double s_sq[kTrimWaves];
+    const int64_t stride = static_cast<int64_t>(gridDim.x) * kTrimBlock;
+    for (int64_t p = static_cast<int64_t>(blockIdx.x) * kTrimBlock + threadIdx.x; p < kept; p += stride) {
+        const uint2 e = temp[p];
+        out_idx[p] = static_cast<int32_t>(e.x);
+        out_val[p] = __uint_as_float(e.y);
+    }
+    if (blockIdx.x == 0) {  // uniform
+        double sq = 0.0;
+        for (uint32_t c = threadIdx.x; c < chunks; c += kTrimBlock) sq += partial[c];
+        const double total = block_sum_f64<kTrimWaves>(sq, s_sq);
+        if (threadIdx.x == 0) host[6] = static_cast<int64_t>(__double_as_longlong(total));
+    }
+}
+
 }  // namespace
 
 hipError_t launch_topk_select(const TopkArgs& a, hipStream_t stream) {
@@ -265,11 +398,27 @@ hipError_t launch_topk_select(const TopkArgs& a, hipStream_t stream) {
     return hipGetLastError();
 }
 
-hipError_t launch_topk_trim(int32_t* out_idx, float* out_val, float* residual, int64_t n, uint32_t key, int64_t m,
-                            int64_t* host, hipStream_t stream) {
-    if (!out_idx || !out_val || !residual || !host || n <= 0 || m < 0 || m > n) return hipErrorInvalidValue;
-    hipLaunchKernelGGL(topk_trim_kernel, dim3(1), dim3(kTopkTrimBlock), 0, stream, out_idx, out_val, residual, n,
-                       key, m, host);
+hipError_t launch_topk_trim(int32_t* out_idx, float* out_val, float* residual, int64_t n, int64_t kept, uint32_t key,
+                            int64_t m, int64_t* host, const TopkTrimScratch* scratch, hipStream_t stream) {
+    if (!out_idx || !out_val || !residual || !host || n <= 0 || m < 0 || m > n || kept < m || kept > n)
+        return hipErrorInvalidValue;
+    if (!scratch || !scratch->temp) {
+        hipLaunchKernelGGL(topk_trim_kernel, dim3(1), dim3(kTopkTrimBlock), 0, stream, out_idx, out_val, residual, n,
+                           key, m, host);
+        return hipGetLastError();
+    }
+    if (!scratch->counts || !scratch->partial) return hipErrorInvalidValue;
+    const int64_t chunks = (n + kTopkTrimChunk - 1) / kTopkTrimChunk;
+    if (chunks > 0xFFFFFFFFll) return hipErrorInvalidValue;
+    const uint32_t nc = static_cast<uint32_t>(chunks);
+    hipLaunchKernelGGL(topk_trim_count_kernel, dim3(nc), dim3(kTrimBlock), 0, stream, out_val, n, key,
+                       scratch->counts);
+    hipLaunchKernelGGL(topk_trim_scan_kernel, dim3(1), dim3(kTopkTrimBlock), 0, stream, scratch->counts, nc);
+    hipLaunchKernelGGL(topk_trim_scatter_kernel, dim3(nc), dim3(kTrimBlock), 0, stream, out_idx, out_val, residual,
+                       n, key, m, scratch->counts, scratch->temp, scratch->partial);
+    const uint32_t copy_blocks = nc < 2048u ? nc : 2048u;
+    hipLaunchKernelGGL(topk_trim_copy_kernel, dim3(copy_blocks), dim3(kTrimBlock), 0, stream, scratch->temp,
+                       kept, out_idx, out_val, scratch->partial, nc, host);
     return hipGetLastError();
 }
 
