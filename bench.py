@@ -43,6 +43,9 @@ TRAFFIC_FILE_EF = os.path.join(ROOT, "profiles", "ef_pass_bert_large_worker3_tra
 TRAFFIC_FILE_SWEEP = os.path.join(ROOT, "profiles", "sweep_resnet18_16_partitions_traffic.txt")
 TRAFFIC_FILE_UNION = os.path.join(ROOT, "profiles", "union_gather_update_bert_large_traffic.txt")
 UNION_SRC = os.path.join(ROOT, "paper_2310_00967_amd", "csrc", "union_kernel.hip")
+TRAFFIC_FILE_TOPK = os.path.join(ROOT, "profiles", "topk_comparator_bert_large_rank3_traffic.txt")
+TOPK_SOURCES = (os.path.join(ROOT, "paper_2310_00967_amd", "csrc", "topk_kernel.hip"),
+                os.path.join(ROOT, "paper_2310_00967_amd", "csrc", "topk_kernel.h"), KERNEL_SRC, KERNEL_HDR)
 
 
 def parse_args():
@@ -80,6 +83,8 @@ def parse_args():
                          "local-error norms; ceiling: vendor streams (torch's in-place add, a device "
                          "copy) beside the step on the same vector; topk: the exact top-k comparator "
                          "beside the threshold step and the hard-threshold rule on the same gradients")
+    ap.add_argument("--topk-only", action="store_true",
+                    help="with --path topk: the top-k rule alone (its HBM counters then cover only its kernels)")
     ap.add_argument("--local-error", action="store_true",
                     help="with --path ef: also return the squared norm of the whole residual (Eq. 1)")
     args = ap.parse_args()
@@ -369,7 +374,7 @@ def measure_ef(w, density, pool, sp, warmup, steps, local_error=False):
 TOPK_PASS_BYTES = 36  # per value: three histogram passes reading grad and residual, then the step's 12
 
 
-def measure_topk(w, density, pool, warmup, steps):
+def measure_topk(w, density, pool, warmup, steps, only_topk=False):
     """The exact top-k comparator (MICRO_RULE_TOPK) on partition w.ranks[0],
     beside the threshold step (the default rule) and the hard-threshold rule
     (Sec. 1's comparators) on the same gradients, each with its own residual
@@ -389,6 +394,8 @@ def measure_topk(w, density, pool, warmup, steps):
     theta0 = synth.initial_theta(w, pool[0], start, start + ln, density)
     rules = {"topk": micro.MICRO_RULE_TOPK, "threshold": micro.MICRO_RULE_PROPORTIONAL,
              "hard_threshold": micro.MICRO_RULE_HARD_THRESHOLD}
+    if only_topk:
+        rules = {"topk": micro.MICRO_RULE_TOPK}
     out = {}
     for name, rule in rules.items():
         sp = micro.Sparsifier(N, device="cuda", time_kernel=True, rule=rule)
@@ -819,7 +826,7 @@ def main_path(args, w, head, pool, n_pool, sp):
            "density": head, "distribution": w.dist, "gradient_pool": n_pool,
            "parallelism": "one worker on one GPU", "path": args.path}
     if args.path == "topk":
-        r = measure_topk(w, head, pool, args.warmup, args.steps)
+        r = measure_topk(w, head, pool, args.warmup, args.steps, args.topk_only)
         cpu = cpu_baseline_topk(w, head, pool, args.cpu_seconds) if args.cpu_seconds > 0 else None
         rank, start, ln = r.pop("partition")
         cfg.update({"rank": rank, "partition_len": ln, "parallelism": "one worker's partition on one GPU"})
@@ -828,12 +835,15 @@ def main_path(args, w, head, pool, n_pool, sp):
                 "value": tk["g_elem_s"], "unit": "G elem/s", "ms_per_step": tk["ms_per_step"], **common,
                 "config": cfg, "k_avg": tk["k_avg"],
                 "roofline": {"bound": "hbm", "achieved": tk["kernel_gbs"], "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                             "frac": tk["frac"], "traffic": None,
+                             "frac": tk["frac"],
+                             "traffic": read_traffic(TRAFFIC_FILE_TOPK, f"{w.name} world {w.world} rank {rank} topk d={head}",
+                                                     sources=TOPK_SOURCES),
                              "kernel": "3 x (topk_hist_kernel + topk_select_kernel), the wait for the k-th "
                                        "magnitude, then the step's launches (+ topk_trim_kernel when magnitudes "
                                        "tie); event-timed together",
                              "kernel_ms_avg": tk["kernel_ms_avg"], "alg_bytes_per_launch": tk["alg_bytes_per_launch"]},
-                "topk_over_threshold_step_time": tk["kernel_ms_avg"] / r["threshold"]["kernel_ms_avg"],
+                "topk_over_threshold_step_time": (tk["kernel_ms_avg"] / r["threshold"]["kernel_ms_avg"]
+                                                  if "threshold" in r else None),
                 "rules": r,
                 "cpu_baseline": cpu}
         print(json.dumps(line), flush=True)
