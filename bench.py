@@ -371,9 +371,6 @@ def measure_ef(w, density, pool, sp, warmup, steps, local_error=False):
             "k_avg": sum(k for _, k, _ in log) / len(log), "worker": worker, "fused": fused}
 
 
-TOPK_PASS_BYTES = 36  # per value: three histogram passes reading grad and residual, then the step's 12
-
-
 def measure_topk(w, density, pool, warmup, steps, only_topk=False):
     """The exact top-k comparator (MICRO_RULE_TOPK) on partition w.ranks[0],
     beside the threshold step (the default rule) and the hard-threshold rule
@@ -381,10 +378,10 @@ def measure_topk(w, density, pool, warmup, steps, only_topk=False):
     under error feedback: device time per step from the library's events
     (for top-k they include the wait for the k-th magnitude between its
     passes and the step's launches), and the density each rule selects at
-    every step, warm-up included.  Algorithmic bytes: top-k 36 B per value of
-    the partition (three histogram passes of 8 B, the step's 12 B) plus 8 B
-    per selected value; the threshold rules 12 B per value plus 8 B per
-    selected value."""
+    every step, warm-up included.  Algorithmic bytes for every rule: what any
+    selection of the partition has to move, 12 B per value (grad and residual
+    read, residual written) plus 8 B per selected value; the top-k rule's
+    extra passes show in a lower fraction."""
     import torch
     import paper_2310_00967_amd as micro
     from paper_2310_00967_amd import synth
@@ -419,8 +416,7 @@ def measure_topk(w, density, pool, warmup, steps, only_topk=False):
         del res
         kernel_ms = sum(ms) / len(ms)
         k_avg = sum(ks[warmup:]) / steps
-        per_value = TOPK_PASS_BYTES if rule == micro.MICRO_RULE_TOPK else 12
-        alg = per_value * ln + 8 * k_avg
+        alg = 12 * ln + 8 * k_avg
         dens = [k / ln for k in ks]
         half = dens[len(dens) // 2:]
         out[name] = {"kernel_ms_avg": kernel_ms, "ms_per_step": elapsed * 1e3 / steps,
@@ -838,9 +834,10 @@ def main_path(args, w, head, pool, n_pool, sp):
                              "frac": tk["frac"],
                              "traffic": read_traffic(TRAFFIC_FILE_TOPK, f"{w.name} world {w.world} rank {rank} topk d={head}",
                                                      sources=TOPK_SOURCES),
-                             "kernel": "3 x (topk_hist_kernel + topk_select_kernel), the wait for the k-th "
-                                       "magnitude, then the step's launches (+ topk_trim_kernel when magnitudes "
-                                       "tie); event-timed together",
+                             "kernel": "topk_hist_kernel + topk_select_kernel over the partition, the wait, the "
+                                       "step's launches, then two more histogram passes and selects over its "
+                                       "output list and the trim (or, where that list would be long, the two "
+                                       "passes over the partition before the step); event-timed together",
                              "kernel_ms_avg": tk["kernel_ms_avg"], "alg_bytes_per_launch": tk["alg_bytes_per_launch"]},
                 "topk_over_threshold_step_time": (tk["kernel_ms_avg"] / r["threshold"]["kernel_ms_avg"]
                                                   if "threshold" in r else None),

@@ -302,16 +302,22 @@ float float_from_bits(uint32_t b) {
     return f;
 }
 
-// The exact k-th largest magnitude of a partition's accumulated values and
-// how the threshold step at that magnitude has to be trimmed: it selects the
-// `greater` larger magnitudes and all `equal` values of that magnitude, of
-// which the `keep` lowest indices belong to the top k.
+// How a top-k step runs.  Every route starts with the first histogram pass
+// (waited for).  The full route runs the other two passes over the partition
+// too (waited for), then the threshold step at the exact k-th magnitude,
+// then the trim if values equal to it must be dropped.  The list route runs
+// the threshold step at the floor of the first digit's bin instead, then the
+// other two passes over the step's output list, then the trim; it is taken
+// when that list is at most a quarter of the partition and the staging pairs
+// can hold it.  None: every value is NaN, nothing is selected.
+enum class TopkRoute { kNone, kFull, kList };
+
 struct TopkPlan {
-    bool found = false;  // false: every value is NaN, nothing is selected
-    uint32_t key = 0;    // the k-th largest magnitude's binary32 bits
-    int64_t greater = 0;
-    int64_t equal = 0;
-    int64_t keep = 0;
+    TopkRoute route = TopkRoute::kNone;
+    uint32_t threshold_key = 0;  // the step selects the keys >= this one
+    int64_t kept = 0;            // the values selected in the end: min(k, values not NaN)
+    int64_t listed = 0;          // the entries of the step's output list
+    bool trim = false;
 };
 
 // The parallel trim's scratch: the staged schedule's staging pairs (free once
@@ -321,15 +327,34 @@ micro::TopkTrimScratch trim_scratch(const micro_ctx* ctx, int64_t n) {
     micro::TopkTrimScratch t{nullptr, nullptr, nullptr};
     const int64_t chunks = (n + micro::kTopkTrimChunk - 1) / micro::kTopkTrimChunk;
     if (ctx->has_staged && ctx->d_stage && ctx->d_tile_counts && ctx->d_tile_sumsq &&
-        n <= ctx->tile_capacity * static_cast<int64_t>(micro::kStageCap) && chunks <= ctx->tile_capacity)
+        n <= ctx->tile_capacity * static_cast<int64_t>(micro::kStageCap) && 2 * chunks <= ctx->tile_capacity)
         t = {ctx->d_stage, ctx->d_tile_counts, ctx->d_tile_sumsq};
     return t;
 }
 
-// Radix select on the device (three histogram passes and selects over
-// acc = grad + residual of [start, start + len)), waited for.
+// Workgroups of a histogram pass over n values: enough for the device, at
+// most four per compute unit (each thread loops).
+uint32_t topk_blocks(const micro_ctx* ctx, int64_t n, int64_t values_per_thread) {
+    const int64_t per_block = static_cast<int64_t>(micro::kTopkHistBlock) * values_per_thread;
+    const int64_t blocks = std::min<int64_t>((n + per_block - 1) / per_block, 4 * ctx->compute_units);
+    return static_cast<uint32_t>(std::max<int64_t>(blocks, 1));
+}
+
+micro_status topk_inconsistent(micro_ctx* ctx, const char* where) {
+    const volatile int64_t* h = ctx->h_topk;
+    set_error(ctx, "top-k select (%s) reported status %lld, key %lld, %lld above, %lld at it, %lld remaining, %lld valid",
+              where, static_cast<long long>(h[5]), static_cast<long long>(h[0]), static_cast<long long>(h[1]),
+              static_cast<long long>(h[2]), static_cast<long long>(h[3]), static_cast<long long>(h[4]));
+    ctx->needs_reset = true;
+    return MICRO_EHIP;
+}
+
+// The radix select's first pass over acc = grad + residual of
+// [start, start + len) and the choice of the route; on the full route also
+// its other two passes.  Waits for the device.
 micro_status topk_plan(micro_ctx* ctx, const float* grad, const float* residual, int64_t start, int64_t len,
                        double density, bool vec4, TopkPlan* plan) {
+    *plan = TopkPlan{};
     micro::TopkArgs t{};
     t.grad = grad;
     t.residual = residual;
@@ -347,32 +372,97 @@ micro_status topk_plan(micro_ctx* ctx, const float* grad, const float* residual,
     t.k = static_cast<uint32_t>(k);
     t.words = ctx->d_topk;
     t.host = ctx->h_topk_dev;
-    const int64_t per_block = static_cast<int64_t>(micro::kTopkHistBlock) * 8;  // two 16-byte groups a thread
-    const int64_t blocks = std::min<int64_t>((len + per_block - 1) / per_block, 4 * ctx->compute_units);
-    t.blocks = static_cast<uint32_t>(std::max<int64_t>(blocks, 1));
+    t.blocks = topk_blocks(ctx, len, 8);  // two 16-byte groups a thread
     volatile int64_t* h = ctx->h_topk;
     h[5] = 0;
-    hipError_t e = micro::launch_topk_select(t, ctx->stream);
-    if (e != hipSuccess) return hip_fail(ctx, e, "top-k select launch");
+    hipError_t e = micro::launch_topk_first(t, ctx->stream);
+    if (e != hipSuccess) return hip_fail(ctx, e, "top-k first pass launch");
     if ((e = hipStreamSynchronize(ctx->stream)) != hipSuccess) return hip_fail(ctx, e, "hipStreamSynchronize");
-    const int64_t status = h[5];
-    *plan = TopkPlan{};
-    if (status == 2) return MICRO_OK;
-    const int64_t key = h[0], greater = h[1], equal = h[2], keep = h[3], valid = h[4];
-    const int64_t want = std::min(k, valid);
-    if (status != 1 || key < 0 || key > micro::kTopkKeyMax || equal < 1 || keep < 1 || keep > equal ||
-        greater < 0 || greater + keep != want || greater + equal > len) {
-        set_error(ctx, "top-k select reported status %lld, key %lld, %lld above, %lld equal, %lld kept of %lld",
-                  static_cast<long long>(status), static_cast<long long>(key), static_cast<long long>(greater),
-                  static_cast<long long>(equal), static_cast<long long>(keep), static_cast<long long>(want));
+    if (h[5] == 2) return MICRO_OK;  // every value is NaN
+    const int64_t bin = h[0], greater0 = h[1], in_bin = h[2], remaining = h[3], valid = h[4];
+    const int64_t kept = std::min(k, valid);
+    const int64_t bin_width = int64_t(1) << micro::kTopkFirstShift;
+    if (h[5] != 3 || bin < 0 || bin > micro::kTopkKeyMax || bin % bin_width != 0 || remaining < 1 ||
+        remaining > in_bin || greater0 < 0 || greater0 + remaining != kept || greater0 + in_bin > len)
+        return topk_inconsistent(ctx, "first pass");
+    plan->kept = kept;
+    const int64_t listed = greater0 + in_bin;
+    if (listed <= len / 4 && trim_scratch(ctx, listed).temp) {
+        plan->route = TopkRoute::kList;
+        plan->threshold_key = static_cast<uint32_t>(bin);
+        plan->listed = listed;
+        plan->trim = true;
+        return MICRO_OK;
+    }
+    h[5] = 0;
+    if ((e = micro::launch_topk_rest(t, false, ctx->stream)) != hipSuccess) return hip_fail(ctx, e, "top-k pass launch");
+    if ((e = hipStreamSynchronize(ctx->stream)) != hipSuccess) return hip_fail(ctx, e, "hipStreamSynchronize");
+    const int64_t key = h[0], greater = h[1], equal = h[2], keep = h[3];
+    if (h[5] != 1 || key < bin || key >= bin + bin_width || key > micro::kTopkKeyMax || keep < 1 || keep > equal ||
+        greater < 0 || greater + keep != kept || greater + equal > len)
+        return topk_inconsistent(ctx, "last pass");
+    plan->route = TopkRoute::kFull;
+    plan->threshold_key = static_cast<uint32_t>(key);
+    plan->listed = greater + equal;
+    plan->trim = keep < equal;
+    return MICRO_OK;
+}
+
+// Enqueued after the step's launches: on the list route the radix select's
+// last two passes over the step's output values, then the trim if the plan
+// has one.
+hipError_t topk_after_step(micro_ctx* ctx, const TopkPlan& plan, int32_t* out_idx, float* out_val, float* residual) {
+    hipError_t e = hipSuccess;
+    if (plan.route == TopkRoute::kList) {
+        micro::TopkArgs t{};
+        t.list = out_val;
+        t.list_n = plan.listed;
+        t.words = ctx->d_topk;
+        t.host = ctx->h_topk_dev;
+        t.blocks = topk_blocks(ctx, plan.listed, 4);
+        ctx->h_topk[5] = 0;  // the device last wrote it in the first pass's select, which has been waited for
+        if ((e = micro::launch_topk_rest(t, true, ctx->stream)) != hipSuccess) return e;
+    }
+    if (plan.trim) {
+        const micro::TopkTrimScratch scratch = trim_scratch(ctx, plan.listed);
+        e = micro::launch_topk_trim(out_idx, out_val, residual, plan.listed, plan.kept, ctx->d_topk, ctx->h_topk_dev,
+                                    &scratch, ctx->stream);
+    }
+    return e;
+}
+
+// After the wait: the step must have listed what the plan expects; the
+// selected count, the k-th magnitude and (returned_sq) the squares of the
+// values the trim returned to the residual.
+micro_status topk_finish(micro_ctx* ctx, const TopkPlan& plan, int64_t listed_by_step, int64_t* selected,
+                         double* theta, double* returned_sq) {
+    if (returned_sq) *returned_sq = 0.0;
+    const int64_t expected = plan.route == TopkRoute::kNone ? 0 : plan.listed;
+    if (listed_by_step != expected) {
+        set_error(ctx, "top-k step listed %lld values, the select expected %lld", static_cast<long long>(listed_by_step),
+                  static_cast<long long>(expected));
         ctx->needs_reset = true;
         return MICRO_EHIP;
     }
-    plan->found = true;
-    plan->key = static_cast<uint32_t>(key);
-    plan->greater = greater;
-    plan->equal = equal;
-    plan->keep = keep;
+    *selected = 0;
+    if (plan.route == TopkRoute::kNone) return MICRO_OK;
+    const volatile int64_t* h = ctx->h_topk;
+    uint32_t key = plan.threshold_key;
+    if (plan.route == TopkRoute::kList) {
+        const int64_t k_key = h[0], greater = h[1], equal = h[2], keep = h[3];
+        if (h[5] != 1 || k_key < plan.threshold_key ||
+            k_key >= static_cast<int64_t>(plan.threshold_key) + (int64_t(1) << micro::kTopkFirstShift) ||
+            k_key > micro::kTopkKeyMax || keep < 1 || keep > equal || greater < 0 || greater + keep != plan.kept ||
+            greater + equal > plan.listed)
+            return topk_inconsistent(ctx, "output list");
+        key = static_cast<uint32_t>(k_key);
+    }
+    if (plan.trim && returned_sq) {
+        const int64_t bits = h[6];
+        std::memcpy(returned_sq, &bits, sizeof *returned_sq);
+    }
+    *selected = plan.kept;
+    *theta = static_cast<double>(float_from_bits(key));
     return MICRO_OK;
 }
 
@@ -416,7 +506,7 @@ micro_status execute_step(micro_ctx* ctx, const float* grad, float* residual, in
             const bool vec4 = ((reinterpret_cast<uintptr_t>(grad) ^ reinterpret_cast<uintptr_t>(residual)) & 15u) == 0;
             micro_status s = topk_plan(ctx, grad, residual, start, len, density, vec4, &plan);
             if (s != MICRO_OK) return s;
-            thf[1] = plan.found ? float_from_bits(plan.key) : none;
+            thf[1] = plan.route == TopkRoute::kNone ? none : float_from_bits(plan.threshold_key);
         }
         int64_t kk[3];
         double sq[3];
@@ -430,29 +520,17 @@ micro_status execute_step(micro_ctx* ctx, const float* grad, float* residual, in
             return MICRO_EHIP;
         }
         if (topk) {
-            const int64_t selected = plan.found ? plan.greater + plan.equal : 0;
-            if (kk[1] != selected) {
-                set_error(ctx, "top-k step selected %lld, the select found %lld", static_cast<long long>(kk[1]),
-                          static_cast<long long>(selected));
-                ctx->needs_reset = true;
-                return MICRO_EHIP;
-            }
-            if (plan.found && plan.keep < plan.equal) {
-                const micro::TopkTrimScratch scratch = trim_scratch(ctx, selected);
-                hipError_t e = micro::launch_topk_trim(out_idx, out_val, residual, selected,
-                                                       plan.greater + plan.keep, plan.key, plan.keep,
-                                                       ctx->h_topk_dev, &scratch, ctx->stream);
-                if (e != hipSuccess) return hip_fail(ctx, e, "top-k trim launch");
+            if (plan.route == TopkRoute::kList || plan.trim) {
+                hipError_t e = topk_after_step(ctx, plan, out_idx, out_val, residual);
+                if (e != hipSuccess) return hip_fail(ctx, e, "top-k launch after the step");
                 if ((e = hipStreamSynchronize(ctx->stream)) != hipSuccess)
                     return hip_fail(ctx, e, "hipStreamSynchronize");
-                double returned;
-                const int64_t bits = ctx->h_topk[6];
-                std::memcpy(&returned, &bits, sizeof returned);
-                sq[1] += returned;  // the values the trim returned to the residual
-                kk[1] = plan.greater + plan.keep;
             }
+            double returned;
+            const micro_status s = topk_finish(ctx, plan, kk[1], &kk[1], theta, &returned);
+            if (s != MICRO_OK) return s;
+            sq[1] += returned;  // the values the trim returned to the residual
             *k = kk[1];
-            if (plan.found) *theta = static_cast<double>(float_from_bits(plan.key));
         } else {
             *k = kk[1];
             *theta = next_threshold(ctx->cfg, density, len, kk[1], *theta);
@@ -544,7 +622,8 @@ micro_status execute_step(micro_ctx* ctx, const float* grad, float* residual, in
     if (topk && len > 0) {
         micro_status s = topk_plan(ctx, grad, residual, start, len, density, vec4, &plan);
         if (s != MICRO_OK) return s;
-        a.theta_f = plan.found ? float_from_bits(plan.key) : std::numeric_limits<float>::quiet_NaN();
+        a.theta_f = plan.route == TopkRoute::kNone ? std::numeric_limits<float>::quiet_NaN()
+                                                   : float_from_bits(plan.threshold_key);
     }
     volatile int64_t* host_count = ctx->h_count;  // stored by the last kernel of the step
     host_count[0] = len > 0 ? -1 : 0;
@@ -561,16 +640,10 @@ micro_status execute_step(micro_ctx* ctx, const float* grad, float* residual, in
                     : micro::launch_staged(a, vec4, ctx->stream);
         if (e != hipSuccess) return hip_fail(ctx, e, "sparsify kernel launch");
     }
-    // The step selected every value of the k-th magnitude; the trim keeps the
-    // lowest `keep` of them (the count is known from the select).
-    const bool trim = topk && plan.found && plan.keep < plan.equal;
-    if (trim) {
-        const int64_t listed = plan.greater + plan.equal;
-        const micro::TopkTrimScratch scratch = trim_scratch(ctx, listed);
-        if ((e = micro::launch_topk_trim(out_idx, out_val, residual, listed, plan.greater + plan.keep, plan.key,
-                                         plan.keep, ctx->h_topk_dev, &scratch, ctx->stream)) != hipSuccess)
-            return hip_fail(ctx, e, "top-k trim launch");
-    }
+    // The top-k comparator's work after the step: the list route's last
+    // passes over the step's output list, and the trim to the top k.
+    if (topk && (e = topk_after_step(ctx, plan, out_idx, out_val, residual)) != hipSuccess)
+        return hip_fail(ctx, e, "top-k launch after the step");
     if (timed && (e = hipEventRecord(ctx->ev[1], ctx->stream)) != hipSuccess)
         return hip_fail(ctx, e, "hipEventRecord");
     if ((e = hipStreamSynchronize(ctx->stream)) != hipSuccess) return hip_fail(ctx, e, "hipStreamSynchronize");
@@ -582,14 +655,8 @@ micro_status execute_step(micro_ctx* ctx, const float* grad, float* residual, in
         return MICRO_EHIP;
     }
     if (topk) {
-        const int64_t expected = plan.found ? plan.greater + plan.equal : 0;
-        if (selected != expected) {
-            set_error(ctx, "top-k step selected %lld, the select found %lld", static_cast<long long>(selected),
-                      static_cast<long long>(expected));
-            ctx->needs_reset = true;
-            return MICRO_EHIP;
-        }
-        if (trim) selected = plan.greater + plan.keep;
+        const micro_status s = topk_finish(ctx, plan, selected, &selected, theta, nullptr);
+        if (s != MICRO_OK) return s;
     }
     if (timed && (e = hipEventElapsedTime(&ctx->stats.kernel_ms, ctx->ev[0], ctx->ev[1])) != hipSuccess)
         return hip_fail(ctx, e, "hipEventElapsedTime");
@@ -597,10 +664,7 @@ micro_status execute_step(micro_ctx* ctx, const float* grad, float* residual, in
     ctx->stats.variant = staged ? MICRO_VARIANT_STAGED : MICRO_VARIANT_TICKET;
     ctx->stats.fused = len > 0 && fused ? 1 : 0;
     *k = selected;
-    if (!topk)
-        *theta = next_threshold(ctx->cfg, density, len, selected, *theta);
-    else if (plan.found)
-        *theta = static_cast<double>(float_from_bits(plan.key));
+    if (!topk) *theta = next_threshold(ctx->cfg, density, len, selected, *theta);
     return MICRO_OK;
 }
 

@@ -5,11 +5,15 @@
 // partition (equal magnitudes: lower index first; NaN never).  Its k-th
 // largest magnitude is found exactly by a radix select over the 31 magnitude
 // bits of binary32 (for values that are not NaN, the bit pattern with the sign
-// cleared orders like the magnitude): three histogram passes over
-// acc = grad + residual, of 11, 11 and 9 bits, each followed by a
-// one-workgroup select that fixes the digit holding the k-th key.  The
-// selection itself is then the threshold step at that magnitude, and a trim
-// pass drops the surplus of equal magnitudes from its output list.
+// cleared orders like the magnitude), digits of 11, 11 and 9 bits, each digit
+// by a histogram pass and a one-workgroup select.  The first digit always
+// comes from a pass over acc = grad + residual of the partition.  The other
+// two come either from two more such passes (the full route), or (the list
+// route) from passes over the output list of the threshold step run at the
+// lower bound of the first digit's bin: that list holds every value of the
+// bin and above, usually a small multiple of k.  A trim then drops from the
+// step's output list the values below the k-th magnitude and the surplus of
+// values equal to it.
 #pragma once
 
 #include <hip/hip_runtime.h>
@@ -24,54 +28,67 @@ constexpr int kTopkHistBlock = 256;
 constexpr int kTopkSelectBlock = 256;
 constexpr int kTopkTrimBlock = 1024;
 constexpr uint32_t kTopkKeyMax = 0x7F800000u;  // +inf with the sign cleared: larger keys are NaN
+constexpr uint32_t kTopkFirstShift = 20;       // the first digit: key bits 30..20
 
 // Device state words (after the kTopkBins counters):
 enum TopkState : int {
-    kTopkPrefix = 0,     // key bits fixed so far
+    kTopkPrefix = 0,     // key bits fixed so far (the k-th key after the last pass)
     kTopkMask = 1,       // which key bits are fixed
-    kTopkRemaining = 2,  // rank of the wanted key among the keys matching the prefix (1-based)
+    kTopkRemaining = 2,  // rank of the wanted key among the keys matching the prefix (1-based);
+                         // after the last pass, the values equal to the k-th key that are kept
     kTopkValid = 3,      // values of the range that are not NaN
     kTopkGreater = 4,    // keys above the prefix's digit range so far: above the k-th key at the end
     kTopkEqual = 5,      // keys equal to the k-th key (after the last pass)
     kTopkStatus = 6,     // 0 searching, 1 found, 2 nothing to select
 };
 
-// Host words (mapped pinned memory) written by the last select:
-// [0] the k-th key, [1] greater, [2] equal, [3] m = the equal keys to keep,
-// [4] valid, [5] status (1 found, 2 nothing).  The trim kernel writes
-// [6] the bit pattern of the binary64 sum of squares of the values it
-// returns to the residual.
+// Host words (mapped pinned memory), written by the select after the first
+// pass with status 3 and after the last pass with status 1 (status 2:
+// nothing to select): [0] the prefix (after the first pass: the first digit's
+// bin, shifted in place; at the end the k-th key), [1] greater, [2] the
+// count at the prefix (the first digit's bin, or the values equal to the
+// k-th key), [3] remaining (at the end: the equal values kept), [4] valid,
+// [5] status.  The trim writes [6], the bit pattern of the binary64 sum of
+// squares of the values it returns to the residual.
 struct TopkArgs {
     const float* grad;
     const float* residual;
-    int64_t start, end;          // the partition
+    int64_t start, end;            // the partition
     int64_t body_first, body_end;  // vec4: [body_first, body_end) in whole 16-byte groups of both vectors
     bool vec4;
-    uint32_t k;                  // the wanted count, 1 <= k <= end - start
-    uint32_t* words;             // kTopkBins counters (zero between passes), then kTopkStateWords
-    int64_t* host;               // kTopkHostWords mapped host words (device address)
-    uint32_t blocks;             // grid of the histogram passes
+    uint32_t k;                    // the wanted count, 1 <= k <= end - start
+    const float* list;             // list route: the step's output values
+    int64_t list_n;                // and their count
+    uint32_t* words;               // kTopkBins counters (zero between passes), then kTopkStateWords
+    int64_t* host;                 // kTopkHostWords mapped host words (device address)
+    uint32_t blocks;               // grid of the histogram passes
 };
 
-// The three passes and selects (pass 0, 1, 2), enqueued on `stream`.
-hipError_t launch_topk_select(const TopkArgs& args, hipStream_t stream);
+// The first pass and its select over the partition.
+hipError_t launch_topk_first(const TopkArgs& args, hipStream_t stream);
+// The second and third passes and their selects: over the partition, or
+// (over_list) over args.list[0, list_n).
+hipError_t launch_topk_rest(const TopkArgs& args, bool over_list, hipStream_t stream);
 
-// Drops from the index-ordered output list [0, n) the equal keys `key` after
-// the first m of them, returning their values to the residual and compacting
-// the list; host[6] receives the binary64 sum of squares of the returned
-// values.  With scratch (temp: n pairs, counts and partial: one entry per
-// kTopkTrimChunk list entries) the list is compacted by the whole device in
-// four launches: ties counted per chunk, the counts scanned, every kept entry
-// placed in temp and the dropped ones returned, temp copied back.  Without
-// it (a null temp) one workgroup compacts the list in place, in order.
+// Drops from the index-ordered output list [0, n) the values whose key is
+// below the k-th key, and those equal to it after the first `kept equal` of
+// them (both read from the state words, after the last select), returning
+// their values to the residual and compacting the list, of which `kept`
+// entries stay; host[6] receives the binary64 sum of squares of the returned
+// values.  With scratch (temp: n pairs; counts: two per kTopkTrimChunk list
+// entries; partial: one per chunk) the whole device compacts the list in
+// four launches: per chunk the equal and the lower keys counted, both counts
+// scanned, every kept entry placed in temp and the dropped ones returned,
+// temp copied back.  Without it (a null temp) one workgroup compacts the
+// list in place, in order.
 constexpr int kTopkTrimChunk = 4096;  // list entries per workgroup of the parallel trim
 struct TopkTrimScratch {
     uint2* temp;       // >= n pairs
-    uint32_t* counts;  // >= ceil(n / kTopkTrimChunk)
+    uint32_t* counts;  // >= 2 * ceil(n / kTopkTrimChunk)
     double* partial;   // >= ceil(n / kTopkTrimChunk)
 };
-// kept: the entries that stay (n less the key-`key` entries after the first m).
-hipError_t launch_topk_trim(int32_t* out_idx, float* out_val, float* residual, int64_t n, int64_t kept, uint32_t key,
-                            int64_t m, int64_t* host, const TopkTrimScratch* scratch, hipStream_t stream);
+hipError_t launch_topk_trim(int32_t* out_idx, float* out_val, float* residual, int64_t n, int64_t kept,
+                            const uint32_t* words, int64_t* host, const TopkTrimScratch* scratch,
+                            hipStream_t stream);
 
 }  // namespace micro

@@ -1,7 +1,8 @@
 // gfx950 kernels of the exact top-k comparator (the sorting-based sparsifier
 // of Sec. 1 that keeps the k largest accumulated gradients; Sec. 2's error
 // feedback supplies the values): a radix select of the k-th largest
-// magnitude, and the trim of equal magnitudes.  See topk_kernel.h.
+// magnitude, and the trim of the threshold step's output list.  See
+// topk_kernel.h.
 #include "topk_kernel.h"
 
 namespace micro {
@@ -10,6 +11,15 @@ namespace {
 using f32x4 = float __attribute__((ext_vector_type(4)));
 
 constexpr int kWave = 64;
+
+// Where a histogram pass reads its keys.
+constexpr int kSrcVec4 = 0;    // acc = grad + residual, 16-byte groups
+constexpr int kSrcScalar = 1;  // acc = grad + residual, one value per load
+constexpr int kSrcList = 2;    // the values of the step's output list
+
+__device__ __forceinline__ uint32_t key_of(float v) {
+    return __float_as_uint(v) & 0x7FFFFFFFu;
+}
 
 // Inclusive sum over the workgroup of one value per thread, in thread order;
 // *total receives the workgroup's sum.  Contains two barriers.
@@ -37,13 +47,28 @@ __device__ __forceinline__ uint32_t block_inclusive_sum(uint32_t v, uint32_t* s_
     return before + v;
 }
 
-// Pass `pass` of the radix select: a histogram of one digit of the keys of
-// acc = grad + residual over [start, end) (binary32 addition, as in the step)
-// that match the digits fixed by the earlier passes.  Digits: bits 30..20,
-// 19..9 and 8..0 of the key (the bit pattern with the sign cleared); NaN keys
-// are not counted.  Each workgroup counts in LDS, then adds its nonzero
-// counters to the global ones.
-template <bool VEC4>
+// Sum of one binary64 per thread over the workgroup in a fixed order (a
+// butterfly in each wavefront, then the wavefronts in order); valid in
+// thread 0.  Contains one barrier.
+template <int WAVES>
+__device__ __forceinline__ double block_sum_f64(double v, double* s_part) {
+#pragma unroll
+    for (int off = kWave / 2; off > 0; off >>= 1) v += __shfl_xor(v, off, kWave);
+    if ((threadIdx.x & (kWave - 1)) == 0) s_part[threadIdx.x / kWave] = v;
+    __syncthreads();
+    double total = 0.0;
+    if (threadIdx.x == 0)
+        for (int w = 0; w < WAVES; ++w) total += s_part[w];
+    return total;
+}
+
+// Pass `pass` of the radix select: a histogram of one digit (bits 30..20,
+// 19..9 or 8..0) of the keys that match the digits fixed by the earlier
+// passes; NaN keys are not counted.  The keys are those of
+// acc = grad + residual over [start, end) (binary32 addition, as in the
+// step) or of the output list's values.  Each workgroup counts in LDS, then
+// adds its nonzero counters to the global ones.
+template <int SRC>
 __global__ __launch_bounds__(kTopkHistBlock) void topk_hist_kernel(TopkArgs a, uint32_t pass) {
     __shared__ uint32_t s_hist[kTopkBins];
     const uint32_t* state = a.words + kTopkBins;
@@ -53,18 +78,17 @@ __global__ __launch_bounds__(kTopkHistBlock) void topk_hist_kernel(TopkArgs a, u
         prefix = state[kTopkPrefix];
         mask = state[kTopkMask];
     }
-    const uint32_t shift = pass == 0 ? 20u : pass == 1 ? 9u : 0u;
+    const uint32_t shift = pass == 0 ? kTopkFirstShift : pass == 1 ? 9u : 0u;
     const uint32_t digit = pass == 2 ? 511u : 2047u;
     for (int b = threadIdx.x; b < kTopkBins; b += kTopkHistBlock) s_hist[b] = 0u;
     __syncthreads();
-    auto count = [&](float g, float r) {
-        const float acc = g + r;
-        const uint32_t key = __float_as_uint(acc) & 0x7FFFFFFFu;
+    auto count_key = [&](uint32_t key) {
         if (key <= kTopkKeyMax && (key & mask) == prefix) atomicAdd(&s_hist[(key >> shift) & digit], 1u);
     };
+    auto count = [&](float g, float r) { count_key(key_of(g + r)); };
     const int64_t gtid = static_cast<int64_t>(blockIdx.x) * kTopkHistBlock + threadIdx.x;
     const int64_t stride = static_cast<int64_t>(gridDim.x) * kTopkHistBlock;
-    if constexpr (VEC4) {
+    if constexpr (SRC == kSrcVec4) {
         // the 16-byte groups of the body, two per thread in flight; fewer
         // than four values before and after it
         const f32x4* g4 = reinterpret_cast<const f32x4*>(a.grad + a.body_first);
@@ -89,8 +113,10 @@ __global__ __launch_bounds__(kTopkHistBlock) void topk_hist_kernel(TopkArgs a, u
         }
         if (gtid < a.body_first - a.start) count(a.grad[a.start + gtid], a.residual[a.start + gtid]);
         if (gtid < a.end - a.body_end) count(a.grad[a.body_end + gtid], a.residual[a.body_end + gtid]);
-    } else {
+    } else if constexpr (SRC == kSrcScalar) {
         for (int64_t i = a.start + gtid; i < a.end; i += stride) count(a.grad[i], a.residual[i]);
+    } else {
+        for (int64_t i = gtid; i < a.list_n; i += stride) count_key(key_of(a.list[i]));
     }
     __syncthreads();
     for (int b = threadIdx.x; b < kTopkBins; b += kTopkHistBlock) {
@@ -102,9 +128,9 @@ __global__ __launch_bounds__(kTopkHistBlock) void topk_hist_kernel(TopkArgs a, u
 // The select after pass `pass`, one workgroup: finds the digit value whose
 // counter holds the wanted key (counting from the largest digit down), fixes
 // it in the prefix and leaves the counters zero for the next pass.  Pass 0
-// also counts the keys that are not NaN and caps the wanted rank by that
-// count; after pass 2 the prefix is the k-th key itself and the result goes to
-// the host words.
+// also counts the keys that are not NaN, caps the wanted rank by that count
+// and reports its bin to the host; after pass 2 the prefix is the k-th key
+// itself and the result goes to the host words.
 __global__ __launch_bounds__(kTopkSelectBlock) void topk_select_kernel(TopkArgs a, uint32_t pass) {
     constexpr int PER = kTopkBins / kTopkSelectBlock;
     __shared__ uint32_t s_wave[kTopkSelectBlock / kWave];
@@ -113,7 +139,7 @@ __global__ __launch_bounds__(kTopkSelectBlock) void topk_select_kernel(TopkArgs 
     if (pass > 0 && state[kTopkStatus] != 0) return;  // uniform
     const uint32_t bins = pass == 2 ? 512u : static_cast<uint32_t>(kTopkBins);
     const uint32_t per = bins / kTopkSelectBlock;  // 8, or 2 for the last digit
-    const uint32_t shift = pass == 0 ? 20u : pass == 1 ? 9u : 0u;
+    const uint32_t shift = pass == 0 ? kTopkFirstShift : pass == 1 ? 9u : 0u;
     const uint32_t digit = bins - 1;
     // thread t holds digits bins-1-t*per down to bins-(t+1)*per: thread order
     // is decreasing digit order
@@ -168,12 +194,14 @@ __global__ __launch_bounds__(kTopkSelectBlock) void topk_select_kernel(TopkArgs 
                 if (pass == 2) {
                     state[kTopkEqual] = c[i];
                     state[kTopkStatus] = 1u;
+                }
+                if (pass == 0 || pass == 2) {
                     a.host[0] = prefix;
                     a.host[1] = greater;
                     a.host[2] = c[i];
                     a.host[3] = remaining;
-                    a.host[4] = state[kTopkValid];
-                    a.host[5] = 1;
+                    a.host[4] = pass == 0 ? total : state[kTopkValid];
+                    a.host[5] = pass == 0 ? 3 : 1;
                 }
                 break;
             }
@@ -182,178 +210,198 @@ __global__ __launch_bounds__(kTopkSelectBlock) void topk_select_kernel(TopkArgs 
     }
 }
 
-// One workgroup walks the index-ordered list in chunks of kTopkTrimBlock * 4
-// entries, in order.  An entry whose value has key `key` is the r-th such
-// entry (r counted from 0 over the list); those with r >= m leave the list and
-// their values return to the residual.  Every other entry moves left by the
-// number of entries that left before it.  A chunk's entries are all read
-// before any of its stores (the scan's barriers), and no store reaches a
-// position beyond its entry's own, so the later chunks still find their
-// entries in place.
+// The trim's rule for an entry of the output list, given the k-th key `key`
+// and the number `keep` of entries equal to it that stay: an entry with a
+// lower key leaves; an entry equal to it leaves if `keep` equal entries come
+// before it; every other entry moves left by the entries that left before it.
+
+// One workgroup walks the list in chunks of kTopkTrimBlock * 4 entries, in
+// order.  A chunk's entries are all read before any of its stores (the
+// scans' barriers), and no store reaches beyond its entry's own position, so
+// the later chunks still find their entries in place.
 __global__ __launch_bounds__(kTopkTrimBlock) void topk_trim_kernel(int32_t* out_idx, float* out_val, float* residual,
-                                                                   int64_t n, uint32_t key, int64_t m,
+                                                                   int64_t n, const uint32_t* words,
                                                                    int64_t* host) {
     constexpr int PER = 4;
     constexpr int64_t CHUNK = static_cast<int64_t>(kTopkTrimBlock) * PER;
     constexpr int WAVES = kTopkTrimBlock / kWave;
     __shared__ uint32_t s_wave[WAVES];
     __shared__ double s_sq[WAVES];
+    const uint32_t* state = words + kTopkBins;
+    if (state[kTopkStatus] != 1u) return;  // uniform: no k-th key
+    const uint32_t key = state[kTopkPrefix];
+    const int64_t keep = state[kTopkRemaining];
     const int tid = threadIdx.x;
-    int64_t ties_seen = 0;
+    int64_t ties_seen = 0, below_seen = 0;
     double sq = 0.0;
     for (int64_t base = 0; base < n; base += CHUNK) {  // uniform
         int32_t idx[PER];
         float val[PER];
-        bool tie[PER];
-        uint32_t mine = 0;
+        bool tie[PER], below[PER];
+        uint32_t mine_t = 0, mine_b = 0;
 #pragma unroll
         for (int i = 0; i < PER; ++i) {
             const int64_t pos = base + tid * PER + i;
             const bool live = pos < n;
             idx[i] = live ? out_idx[pos] : 0;
             val[i] = live ? out_val[pos] : 0.0f;
-            tie[i] = live && (__float_as_uint(val[i]) & 0x7FFFFFFFu) == key;
-            mine += tie[i] ? 1u : 0u;
+            tie[i] = live && key_of(val[i]) == key;
+            below[i] = live && key_of(val[i]) < key;
+            mine_t += tie[i] ? 1u : 0u;
+            mine_b += below[i] ? 1u : 0u;
         }
-        uint32_t chunk_ties;
-        const uint32_t incl = block_inclusive_sum<kTopkTrimBlock>(mine, s_wave, &chunk_ties);
-        int64_t rank = ties_seen + (incl - mine);
+        uint32_t chunk_t, chunk_b;
+        const uint32_t incl_t = block_inclusive_sum<kTopkTrimBlock>(mine_t, s_wave, &chunk_t);
+        const uint32_t incl_b = block_inclusive_sum<kTopkTrimBlock>(mine_b, s_wave, &chunk_b);
+        int64_t rank = ties_seen + (incl_t - mine_t);
+        int64_t lower = below_seen + (incl_b - mine_b);
 #pragma unroll
         for (int i = 0; i < PER; ++i) {
             const int64_t pos = base + tid * PER + i;
             if (pos >= n) break;
-            const int64_t before = rank;
+            const int64_t before_t = rank, before_b = lower;
             if (tie[i]) ++rank;
-            if (tie[i] && before >= m) {
+            if (below[i]) ++lower;
+            if (below[i] || (tie[i] && before_t >= keep)) {
                 residual[idx[i]] = val[i];
                 sq += static_cast<double>(val[i]) * static_cast<double>(val[i]);
-            } else if (before > m) {
-                const int64_t to = pos - (before - m);
-                out_idx[to] = idx[i];
-                out_val[to] = val[i];
+            } else {
+                const int64_t shift = before_b + (before_t > keep ? before_t - keep : 0);
+                if (shift > 0) {
+                    out_idx[pos - shift] = idx[i];
+                    out_val[pos - shift] = val[i];
+                }
             }
         }
-        ties_seen += chunk_ties;
+        ties_seen += chunk_t;
+        below_seen += chunk_b;
     }
-    // the returned values' squares: each thread's in list order, then the
-    // wavefronts' sums in order
-#pragma unroll
-    for (int off = kWave / 2; off > 0; off >>= 1) sq += __shfl_xor(sq, off, kWave);
-    if ((tid & (kWave - 1)) == 0) s_sq[tid / kWave] = sq;
-    __syncthreads();
-    if (tid == 0) {
-        double total = 0.0;
-        for (int w = 0; w < WAVES; ++w) total += s_sq[w];
-        host[6] = static_cast<int64_t>(__double_as_longlong(total));
-    }
+    const double total = block_sum_f64<WAVES>(sq, s_sq);
+    if (tid == 0) host[6] = static_cast<int64_t>(__double_as_longlong(total));
 }
 
 constexpr int kTrimBlock = 256;
 constexpr int kTrimPer = kTopkTrimChunk / kTrimBlock;  // entries per thread, row j at j * kTrimBlock + thread
 constexpr int kTrimWaves = kTrimBlock / kWave;
 
-__device__ __forceinline__ bool has_key(float v, uint32_t key) {
-    return (__float_as_uint(v) & 0x7FFFFFFFu) == key;
-}
-
-// Sum of one binary64 per thread over the workgroup in a fixed order (a
-// butterfly in each wavefront, then the wavefronts in order); valid in
-// thread 0.  Contains one barrier.
-template <int WAVES>
-__device__ __forceinline__ double block_sum_f64(double v, double* s_part) {
-#pragma unroll
-    for (int off = kWave / 2; off > 0; off >>= 1) v += __shfl_xor(v, off, kWave);
-    if ((threadIdx.x & (kWave - 1)) == 0) s_part[threadIdx.x / kWave] = v;
-    __syncthreads();
-    double total = 0.0;
-    if (threadIdx.x == 0)
-        for (int w = 0; w < WAVES; ++w) total += s_part[w];
-    return total;
-}
-
-// Parallel trim, launch 1: the entries of key `key` in each chunk of
-// kTopkTrimChunk list entries.
-__global__ __launch_bounds__(kTrimBlock) void topk_trim_count_kernel(const float* out_val, int64_t n, uint32_t key,
-                                                                     uint32_t* counts) {
+// Parallel trim, launch 1: per chunk of kTopkTrimChunk list entries, the
+// entries equal to the k-th key (counts[chunk]) and below it
+// (counts[chunks + chunk]).
+__global__ __launch_bounds__(kTrimBlock) void topk_trim_count_kernel(const float* out_val, int64_t n,
+                                                                     const uint32_t* words, uint32_t* counts,
+                                                                     uint32_t chunks) {
     __shared__ uint32_t s_wave[kTrimWaves];
+    const uint32_t* state = words + kTopkBins;
+    if (state[kTopkStatus] != 1u) return;  // uniform
+    const uint32_t key = state[kTopkPrefix];
     const int64_t base = static_cast<int64_t>(blockIdx.x) * kTopkTrimChunk;
-    uint32_t c = 0;
+    uint32_t t = 0, b = 0;
 #pragma unroll
     for (int j = 0; j < kTrimPer; ++j) {
         const int64_t p = base + j * kTrimBlock + threadIdx.x;
-        if (p < n && has_key(out_val[p], key)) ++c;
+        if (p < n) {
+            const uint32_t kv = key_of(out_val[p]);
+            t += kv == key ? 1u : 0u;
+            b += kv < key ? 1u : 0u;
+        }
     }
-    uint32_t total;
-    block_inclusive_sum<kTrimBlock>(c, s_wave, &total);
-    if (threadIdx.x == 0) counts[blockIdx.x] = total;
+    uint32_t total_t, total_b;
+    block_inclusive_sum<kTrimBlock>(t, s_wave, &total_t);
+    block_inclusive_sum<kTrimBlock>(b, s_wave, &total_b);
+    if (threadIdx.x == 0) {
+        counts[blockIdx.x] = total_t;
+        counts[chunks + blockIdx.x] = total_b;
+    }
 }
 
-// Launch 2, one workgroup: counts[0, chunks) become exclusive prefix sums.
+// Launch 2, one workgroup: both count arrays become exclusive prefix sums.
 __global__ __launch_bounds__(kTopkTrimBlock) void topk_trim_scan_kernel(uint32_t* counts, uint32_t chunks) {
     __shared__ uint32_t s_wave[kTopkTrimBlock / kWave];
-    uint32_t carry = 0;
-    for (uint32_t base = 0; base < chunks; base += kTopkTrimBlock) {  // uniform
-        const uint32_t i = base + threadIdx.x;
-        const uint32_t c = i < chunks ? counts[i] : 0u;
-        uint32_t total;
-        const uint32_t incl = block_inclusive_sum<kTopkTrimBlock>(c, s_wave, &total);
-        if (i < chunks) counts[i] = carry + incl - c;
-        carry += total;
+    for (uint32_t half = 0; half < 2; ++half) {
+        uint32_t* c = counts + half * chunks;
+        uint32_t carry = 0;
+        for (uint32_t base = 0; base < chunks; base += kTopkTrimBlock) {  // uniform
+            const uint32_t i = base + threadIdx.x;
+            const uint32_t v = i < chunks ? c[i] : 0u;
+            uint32_t total;
+            const uint32_t incl = block_inclusive_sum<kTopkTrimBlock>(v, s_wave, &total);
+            if (i < chunks) c[i] = carry + incl - v;
+            carry += total;
+        }
     }
 }
 
-// Launch 3: each entry's count of key-`key` entries before it (its chunk's
-// prefix, then rows in order and lanes in order inside the chunk) decides:
-// an entry of that key at rank >= m is returned to the residual, every other
-// entry goes to temp at its position less the entries dropped before it.
-// partial[chunk] receives the binary64 sum of squares of the returned values.
+// Launch 3: each entry's counts of equal and lower entries before it (its
+// chunk's prefixes, then rows in order and lanes in order inside the chunk)
+// decide it: a dropped entry returns to the residual, a kept one goes to
+// temp at its position less the entries dropped before it.  partial[chunk]
+// receives the binary64 sum of squares of the returned values.
 __global__ __launch_bounds__(kTrimBlock) void topk_trim_scatter_kernel(const int32_t* out_idx, const float* out_val,
-                                                                       float* residual, int64_t n, uint32_t key,
-                                                                       int64_t m, const uint32_t* chunk_before,
+                                                                       float* residual, int64_t n,
+                                                                       const uint32_t* words,
+                                                                       const uint32_t* counts, uint32_t chunks,
                                                                        uint2* temp, double* partial) {
-    __shared__ uint32_t s_row_wave[kTrimPer * kTrimWaves];
+    constexpr int ROWS = kTrimPer * kTrimWaves;
+    static_assert(ROWS == kWave, "one (row, wavefront) count per lane of wavefront 0");
+    __shared__ uint32_t s_t[ROWS], s_b[ROWS];
     __shared__ double s_sq[kTrimWaves];
+    const uint32_t* state = words + kTopkBins;
+    if (state[kTopkStatus] != 1u) return;  // uniform
+    const uint32_t key = state[kTopkPrefix];
+    const int64_t keep = state[kTopkRemaining];
     const int lane = threadIdx.x & (kWave - 1);
     const int wave = threadIdx.x / kWave;
     const int64_t base = static_cast<int64_t>(blockIdx.x) * kTopkTrimChunk;
-    const uint64_t below = lane ? (~0ull >> (kWave - lane)) : 0ull;
-    uint32_t lane_rank[kTrimPer];
-    bool tie[kTrimPer];
+    const uint64_t lower_lanes = lane ? (~0ull >> (kWave - lane)) : 0ull;
+    uint32_t rank_t[kTrimPer], rank_b[kTrimPer];
+    bool tie[kTrimPer], below[kTrimPer];
 #pragma unroll
     for (int j = 0; j < kTrimPer; ++j) {
         const int64_t p = base + j * kTrimBlock + threadIdx.x;
-        tie[j] = p < n && has_key(out_val[p], key);
-        const uint64_t mask = __ballot(tie[j]);
-        lane_rank[j] = static_cast<uint32_t>(__popcll(mask & below));
-        if (lane == 0) s_row_wave[j * kTrimWaves + wave] = static_cast<uint32_t>(__popcll(mask));
+        const uint32_t kv = p < n ? key_of(out_val[p]) : 0xFFFFFFFFu;
+        tie[j] = kv == key;
+        below[j] = kv < key;
+        const uint64_t mt = __ballot(tie[j]);
+        const uint64_t mb = __ballot(below[j]);
+        rank_t[j] = static_cast<uint32_t>(__popcll(mt & lower_lanes));
+        rank_b[j] = static_cast<uint32_t>(__popcll(mb & lower_lanes));
+        if (lane == 0) {
+            s_t[j * kTrimWaves + wave] = static_cast<uint32_t>(__popcll(mt));
+            s_b[j * kTrimWaves + wave] = static_cast<uint32_t>(__popcll(mb));
+        }
     }
     __syncthreads();
-    if (wave == 0) {  // exclusive prefix of the kTrimPer * kTrimWaves counts, in list order
-        static_assert(kTrimPer * kTrimWaves == kWave, "one count per lane of wavefront 0");
-        uint32_t v = s_row_wave[lane];
-        const uint32_t own = v;
+    if (wave == 0) {  // exclusive prefixes of the (row, wavefront) counts, in list order
+        uint32_t vt = s_t[lane], vb = s_b[lane];
+        const uint32_t own_t = vt, own_b = vb;
 #pragma unroll
         for (int off = 1; off < kWave; off <<= 1) {
-            const uint32_t o = __shfl_up(v, off, kWave);
-            if (lane >= off) v += o;
+            const uint32_t ot = __shfl_up(vt, off, kWave);
+            const uint32_t ob = __shfl_up(vb, off, kWave);
+            if (lane >= off) {
+                vt += ot;
+                vb += ob;
+            }
         }
-        s_row_wave[lane] = v - own;
+        s_t[lane] = vt - own_t;
+        s_b[lane] = vb - own_b;
     }
     __syncthreads();
-    const int64_t chunk_ties = chunk_before[blockIdx.x];
+    const int64_t chunk_t = counts[blockIdx.x], chunk_b = counts[chunks + blockIdx.x];
     double sq = 0.0;
 #pragma unroll
     for (int j = 0; j < kTrimPer; ++j) {
         const int64_t p = base + j * kTrimBlock + threadIdx.x;
         if (p >= n) continue;
-        const int64_t before = chunk_ties + s_row_wave[j * kTrimWaves + wave] + lane_rank[j];
+        const int64_t before_t = chunk_t + s_t[j * kTrimWaves + wave] + rank_t[j];
+        const int64_t before_b = chunk_b + s_b[j * kTrimWaves + wave] + rank_b[j];
         const int32_t idx = out_idx[p];
         const float val = out_val[p];
-        if (tie[j] && before >= m) {
+        if (below[j] || (tie[j] && before_t >= keep)) {
             residual[idx] = val;
             sq += static_cast<double>(val) * static_cast<double>(val);
         } else {
-            const int64_t to = p - (before > m ? before - m : 0);
+            const int64_t to = p - before_b - (before_t > keep ? before_t - keep : 0);
             temp[to] = make_uint2(static_cast<uint32_t>(idx), __float_as_uint(val));
         }
     }
@@ -364,9 +412,11 @@ __global__ __launch_bounds__(kTrimBlock) void topk_trim_scatter_kernel(const int
 // Launch 4: temp[0, kept) back into the output lists; workgroup 0 also adds
 // the chunks' partial sums in a fixed order into host[6].
 __global__ __launch_bounds__(kTrimBlock) void topk_trim_copy_kernel(const uint2* temp, int64_t kept, int32_t* out_idx,
-                                                                    float* out_val, const double* partial,
-                                                                    uint32_t chunks, int64_t* host) {
+                                                                    float* out_val, const uint32_t* words,
+                                                                    const double* partial, uint32_t chunks,
+                                                                    int64_t* host) {
     __shared__ double s_sq[kTrimWaves];
+    if (words[kTopkBins + kTopkStatus] != 1u) return;  // uniform
     const int64_t stride = static_cast<int64_t>(gridDim.x) * kTrimBlock;
     for (int64_t p = static_cast<int64_t>(blockIdx.x) * kTrimBlock + threadIdx.x; p < kept; p += stride) {
         const uint2 e = temp[p];
@@ -381,44 +431,66 @@ __global__ __launch_bounds__(kTrimBlock) void topk_trim_copy_kernel(const uint2*
     }
 }
 
+bool partition_args_ok(const TopkArgs& a) {
+    return a.grad && a.residual && a.words && a.host && a.blocks > 0 && a.end > a.start && a.k > 0 &&
+           (!a.vec4 || (a.body_first >= a.start && a.body_end >= a.body_first && a.body_end <= a.end &&
+                        (a.body_end - a.body_first) % 4 == 0 && a.body_first - a.start <= 3 &&
+                        a.end - a.body_end <= 3));
+}
+
+void launch_partition_pass(const TopkArgs& a, uint32_t pass, hipStream_t stream) {
+    if (a.vec4)
+        hipLaunchKernelGGL(topk_hist_kernel<kSrcVec4>, dim3(a.blocks), dim3(kTopkHistBlock), 0, stream, a, pass);
+    else
+        hipLaunchKernelGGL(topk_hist_kernel<kSrcScalar>, dim3(a.blocks), dim3(kTopkHistBlock), 0, stream, a, pass);
+    hipLaunchKernelGGL(topk_select_kernel, dim3(1), dim3(kTopkSelectBlock), 0, stream, a, pass);
+}
+
 }  // namespace
 
-hipError_t launch_topk_select(const TopkArgs& a, hipStream_t stream) {
-    if (!a.grad || !a.residual || !a.words || !a.host || a.blocks == 0 || a.end <= a.start || a.k == 0 ||
-        (a.vec4 && (a.body_first < a.start || a.body_end < a.body_first || a.body_end > a.end ||
-                    (a.body_end - a.body_first) % 4 != 0 || a.body_first - a.start > 3 || a.end - a.body_end > 3)))
-        return hipErrorInvalidValue;
-    for (uint32_t pass = 0; pass < 3; ++pass) {
-        if (a.vec4)
-            hipLaunchKernelGGL(topk_hist_kernel<true>, dim3(a.blocks), dim3(kTopkHistBlock), 0, stream, a, pass);
-        else
-            hipLaunchKernelGGL(topk_hist_kernel<false>, dim3(a.blocks), dim3(kTopkHistBlock), 0, stream, a, pass);
-        hipLaunchKernelGGL(topk_select_kernel, dim3(1), dim3(kTopkSelectBlock), 0, stream, a, pass);
-    }
+hipError_t launch_topk_first(const TopkArgs& a, hipStream_t stream) {
+    if (!partition_args_ok(a)) return hipErrorInvalidValue;
+    launch_partition_pass(a, 0, stream);
     return hipGetLastError();
 }
 
-hipError_t launch_topk_trim(int32_t* out_idx, float* out_val, float* residual, int64_t n, int64_t kept, uint32_t key,
-                            int64_t m, int64_t* host, const TopkTrimScratch* scratch, hipStream_t stream) {
-    if (!out_idx || !out_val || !residual || !host || n <= 0 || m < 0 || m > n || kept < m || kept > n)
+hipError_t launch_topk_rest(const TopkArgs& a, bool over_list, hipStream_t stream) {
+    if (over_list) {
+        if (!a.list || a.list_n < 1 || !a.words || !a.host || a.blocks == 0) return hipErrorInvalidValue;
+        for (uint32_t pass = 1; pass < 3; ++pass) {
+            hipLaunchKernelGGL(topk_hist_kernel<kSrcList>, dim3(a.blocks), dim3(kTopkHistBlock), 0, stream, a,
+                               pass);
+            hipLaunchKernelGGL(topk_select_kernel, dim3(1), dim3(kTopkSelectBlock), 0, stream, a, pass);
+        }
+        return hipGetLastError();
+    }
+    if (!partition_args_ok(a)) return hipErrorInvalidValue;
+    for (uint32_t pass = 1; pass < 3; ++pass) launch_partition_pass(a, pass, stream);
+    return hipGetLastError();
+}
+
+hipError_t launch_topk_trim(int32_t* out_idx, float* out_val, float* residual, int64_t n, int64_t kept,
+                            const uint32_t* words, int64_t* host, const TopkTrimScratch* scratch,
+                            hipStream_t stream) {
+    if (!out_idx || !out_val || !residual || !words || !host || n <= 0 || kept < 1 || kept > n)
         return hipErrorInvalidValue;
     if (!scratch || !scratch->temp) {
         hipLaunchKernelGGL(topk_trim_kernel, dim3(1), dim3(kTopkTrimBlock), 0, stream, out_idx, out_val, residual, n,
-                           key, m, host);
+                           words, host);
         return hipGetLastError();
     }
     if (!scratch->counts || !scratch->partial) return hipErrorInvalidValue;
     const int64_t chunks = (n + kTopkTrimChunk - 1) / kTopkTrimChunk;
-    if (chunks > 0xFFFFFFFFll) return hipErrorInvalidValue;
+    if (chunks > 0x7FFFFFFFll) return hipErrorInvalidValue;
     const uint32_t nc = static_cast<uint32_t>(chunks);
-    hipLaunchKernelGGL(topk_trim_count_kernel, dim3(nc), dim3(kTrimBlock), 0, stream, out_val, n, key,
-                       scratch->counts);
+    hipLaunchKernelGGL(topk_trim_count_kernel, dim3(nc), dim3(kTrimBlock), 0, stream, out_val, n, words,
+                       scratch->counts, nc);
     hipLaunchKernelGGL(topk_trim_scan_kernel, dim3(1), dim3(kTopkTrimBlock), 0, stream, scratch->counts, nc);
     hipLaunchKernelGGL(topk_trim_scatter_kernel, dim3(nc), dim3(kTrimBlock), 0, stream, out_idx, out_val, residual,
-                       n, key, m, scratch->counts, scratch->temp, scratch->partial);
+                       n, words, scratch->counts, nc, scratch->temp, scratch->partial);
     const uint32_t copy_blocks = nc < 2048u ? nc : 2048u;
-    hipLaunchKernelGGL(topk_trim_copy_kernel, dim3(copy_blocks), dim3(kTrimBlock), 0, stream, scratch->temp,
-                       kept, out_idx, out_val, scratch->partial, nc, host);
+    hipLaunchKernelGGL(topk_trim_copy_kernel, dim3(copy_blocks), dim3(kTrimBlock), 0, stream, scratch->temp, kept,
+                       out_idx, out_val, words, scratch->partial, nc, host);
     return hipGetLastError();
 }
 

@@ -66,10 +66,13 @@ def topk_vs_oracle(g, res, rank, world, density, variant=AUTO, phase_shift=0, sp
     assert np.array_equal(idx.cpu().numpy(), o_idx), f"{where}: indices differ"
     assert same_bits(val.cpu().numpy(), o_val), f"{where}: values differ"
     assert same_bits(r_dev.cpu().numpy(), r_or), f"{where}: residual differs"
-    # the step writes the pairs of every value of magnitude >= the k-th; past
-    # them nothing is written
+    # the step lists at most every value from the floor of the k-th
+    # magnitude's first radix bin (its top 11 magnitude bits) up; past them
+    # nothing is written
     acc = (g[s:s + ln] + res[s:s + ln]).astype(np.float32)
-    reach = int(np.sum(np.abs(acc) >= np.float32(th_or))) if k_or else 0
+    keys = acc.view(np.uint32) & np.uint32(0x7FFFFFFF)
+    floor = np.uint32(np.float32(th_or).view(np.uint32) & np.uint32(0x7FF00000))
+    reach = int(np.sum((keys >= floor) & (keys <= np.uint32(0x7F800000)))) if k_or else 0
     assert np.all(out_idx.cpu().numpy()[reach:] == sentinel), f"{where}: written past the selection"
     if own:
         sp.close()
