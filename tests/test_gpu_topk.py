@@ -268,3 +268,23 @@ def test_gpt_1p3b_full_size_properties(density):
         del before
     sp.close()
     torch.cuda.empty_cache()
+
+
+def test_largest_vector_the_index_type_allows():
+    """n_total = 2^31 - 1, the largest vector int32 indices address: one
+    partition-wide top-k step at d = 0.001, checked against the definition
+    (at this size many values share the k-th magnitude, so the trim runs
+    over a long list).  About 50 GB of device memory."""
+    N = 2**31 - 1
+    note(f"top-k largest vector N={N}")
+    gen = torch.Generator(device=DEV).manual_seed(2025)
+    g = torch.randn(N, generator=gen, device=DEV, dtype=torch.float32)
+    res = torch.randn(N, generator=gen, device=DEV, dtype=torch.float32) * 0.5
+    before = res.clone()
+    sp = make(N)
+    k, th, idx, val = sp.step(g, res, 0, 1, 0.001, 1.0)
+    check_topk_properties(g, before, res, 0, N, idx, val, k, th, 0.001)
+    assert int(idx[-1]) > 2**31 - 2**20  # indices near the top of the range were selected
+    sp.close()
+    del g, res, before, idx, val
+    torch.cuda.empty_cache()
