@@ -74,6 +74,8 @@ static int check_partition(const float *g, const float *res0, const float *res1,
     return q == k;
 }
 
+static int res1_nonzero(float v) { return v != 0.0f || signbit(v); }
+
 static int run_case(int64_t n, int32_t world, int regime, double theta) {
     micro_oracle_rule rule;
     micro_oracle_default_rule(&rule);
@@ -166,6 +168,56 @@ static int run_case(int64_t n, int32_t world, int regime, double theta) {
         free(u);
         free(out);
         free(x);
+    }
+
+    /* the exact top-k comparator on every partition, outputs sized to it */
+    static const double densities[] = {1e-9, 0.01, 0.5, 1.0};
+    for (size_t di = 0; di < sizeof densities / sizeof *densities && !bad; ++di) {
+        for (int32_t r = 0; r < world && !bad; ++r) {
+            int64_t s, len, k;
+            micro_oracle_partition(n, r, world, &s, &len);
+            int32_t *idx = alloc((size_t)len, sizeof(int32_t));
+            float *val = alloc((size_t)len, sizeof(float));
+            memcpy(res0, res, (size_t)n * sizeof(float));
+            double kth = -1.0;
+            if (micro_oracle_topk_select(g, res, s, len, densities[di], idx, val, &k, &kth) != 0) {
+                bad = fail("topk_select", n, world);
+            } else {
+                /* the count, the order, conservation, and every selected
+                 * magnitude at least every other value's that is not NaN */
+                int64_t valid = 0;
+                for (int64_t j = s; j < s + len; ++j) valid += !isnan(g[j] + res0[j]);
+                const int64_t want = micro_oracle_topk_count(densities[di], len);
+                if (k != (want < valid ? want : valid)) bad = fail("topk count", n, world);
+                if (!bad && k > 0 && !check_partition(g, res0, res, s, len, kth, idx, val, k)) {
+                    /* equal magnitudes at the k-th may stay: check by selection flags instead */
+                    int64_t q = 0;
+                    for (int64_t j = s; j < s + len && !bad; ++j) {
+                        const float acc = g[j] + res0[j];
+                        const int sel = q < k && idx[q] == j;
+                        if (sel) {
+                            if (memcmp(&val[q], &acc, 4) != 0 || res1_nonzero(res[j])) bad = fail("topk selected", n, world);
+                            if (!(fabs((double)acc) >= kth)) bad = fail("topk below kth", n, world);
+                            ++q;
+                        } else {
+                            if (memcmp(&res[j], &acc, 4) != 0) bad = fail("topk residual", n, world);
+                            if (!isnan(acc) && fabs((double)acc) > kth) bad = fail("topk above kth left", n, world);
+                        }
+                    }
+                    if (!bad && q != k) bad = fail("topk order", n, world);
+                }
+                if (!bad && k == 0 && kth != -1.0) bad = fail("topk kth untouched", n, world);
+            }
+            free(idx);
+            free(val);
+        }
+    }
+    if (!bad) {
+        int64_t k = -5;
+        double kth = 3.0;
+        if (micro_oracle_topk_select(g, res, 0, n, 0.0, NULL, NULL, &k, &kth) != -1 || k != -5 || kth != 3.0)
+            bad = fail("topk_select rejects density 0", n, world);
+        if (micro_oracle_topk_count(0.5, 0) != 0) bad = fail("topk_count of nothing", n, world);
     }
 
     /* invalid arguments write nothing */
