@@ -86,6 +86,26 @@ int main() {
         CHECK(micro_estimate_threshold(c, 0.5, 100, 1, nullptr) == MICRO_EINVAL);
     }
 
+    // the comparators: hard threshold keeps theta; the top-k threshold comes
+    // from the values, so the host-only update and the allocation-free step
+    // refuse that rule before any device work
+    {
+        micro_config hard = cfg, topk = cfg;
+        hard.rule = MICRO_RULE_HARD_THRESHOLD;
+        topk.rule = MICRO_RULE_TOPK;
+        double th = 2.0;
+        CHECK(micro_estimate_threshold(&hard, 0.01, 100000, 5000, &th) == MICRO_OK && th == 2.0);
+        CHECK(micro_estimate_threshold(&topk, 0.01, 100000, 5000, &th) == MICRO_EINVAL && th == 2.0);
+        float gg[8] = {1, 2, 3, 4, 5, 6, 7, 8}, rr[8] = {0}, vv[8];
+        int32_t ii[8];
+        int64_t kk = -4;
+        CHECK(micro_sparsify_step_noalloc(gg, rr, 8, 0, 1, 0.5, &th, ii, vv, &kk, nullptr, &topk) == MICRO_EINVAL);
+        CHECK(kk == -4 && th == 2.0 && rr[0] == 0.0f);
+        micro_config unknown = cfg;
+        unknown.rule = 4;
+        CHECK(micro_estimate_threshold(&unknown, 0.01, 100000, 5000, &th) == MICRO_EINVAL);
+    }
+
     // binary32 threshold: the smallest float not below theta
     for (double th : {1e-45, 1e-40, 0.1, 1.0, 2.33, 3.4028234663852886e38, 1e300}) {
         float f = -1.0f;
