@@ -1150,34 +1150,38 @@ __device__ __forceinline__ void move_pieces(const LaunchArgs& a, const SweepTabl
     const longlong2 counts = *reinterpret_cast<const longlong2*>(a.count_out);
     const int64_t k = counts.x;
     const uint32_t flagged = flagged_count(a, counts.y);
-    // What goes to the host (the counts; in a sweep also each segment's
-    // count and each chunk's squared norm) is stored after this workgroup's
-    // pieces: a store to mapped host memory takes a bus round trip, and a wait
-    // for any later load would include it.
-    int64_t seg_k = 0;
-    if constexpr (SWEEP) {
-        // Each segment's count: the difference of the global offsets of its
-        // first tile and of the next segment's first tile.
-        if (blockIdx.x == 0 && tid < static_cast<int>(tbl->count)) {
-            const uint32_t t0 = tbl->seg[tid].tile_first, t1 = tbl->seg[tid + 1].tile_first;
-            const int64_t e0 = t0 < a.num_tiles ? (a.tile_excl[t0] & ~kOverflow) : k;
-            const int64_t e1 = t1 < a.num_tiles ? (a.tile_excl[t1] & ~kOverflow) : k;
-            seg_k = t1 > t0 ? e1 - e0 : 0;
+    // What goes to mapped host memory (the counts; in a sweep also each
+    // segment's count and each chunk's squared norm) is stored by the grid's
+    // last workgroups, which have the fewest pieces (none when the grid
+    // exceeds the pieces), as early as they can: each such store is a bus
+    // round trip, which then overlaps the other workgroups' moves instead of
+    // following them.  (Measured: ResNet-50 rank 0 step 17.0-17.1 against
+    // 17.4-17.5 us, ResNet-18 sweep 41.6-42.3 against 43.1-43.8 us.)
+    const uint32_t host_wg = gridDim.x - 1;
+    if (blockIdx.x == host_wg) {
+        if (tid == 0) {  // the scan kernel has finished both counts
+            a.host_count[0] = k;
+            a.host_count[1] = flagged;
+        }
+        if constexpr (SWEEP) {
+            // Each segment's count: the difference of the global offsets of
+            // its first tile and of the next segment's first tile.
+            if (tid < static_cast<int>(tbl->count)) {
+                const uint32_t t0 = tbl->seg[tid].tile_first, t1 = tbl->seg[tid + 1].tile_first;
+                const int64_t e0 = t0 < a.num_tiles ? (a.tile_excl[t0] & ~kOverflow) : k;
+                const int64_t e1 = t1 < a.num_tiles ? (a.tile_excl[t1] & ~kOverflow) : k;
+                a.host_count[2 + tid] = t1 > t0 ? e1 - e0 : 0;
+            }
         }
     }
     if (k != 0) move_work<VEC, SWEEP>(a, tbl, k, flagged, first_t0, first_t1);
-    if (blockIdx.x == 0 && tid == 0) {  // the scan kernel has finished both counts
-        a.host_count[0] = k;
-        a.host_count[1] = flagged;
-    }
     if constexpr (SWEEP) {
-        if (blockIdx.x == 0 && tid < static_cast<int>(tbl->count)) a.host_count[2 + tid] = seg_k;
         // Each chunk's squared norm, its tiles' norms added in a fixed order
         // (each thread its tiles in increasing order, then the workgroup sum);
         // the host adds a segment's chunks in increasing order.  The stream
         // workgroups stored the tile norms in an earlier launch, so they are
         // read here, not by the scan workgroups of a fused launch.
-        for (uint32_t c = blockIdx.x; c < a.num_chunks; c += gridDim.x) {  // uniform
+        for (uint32_t c = host_wg - blockIdx.x; c < a.num_chunks; c += gridDim.x) {  // uniform: from the grid's end
             uint32_t first, end;
             chunk_tiles<true>(a, tbl, c, first, end);
             double sq = 0.0;
