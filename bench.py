@@ -429,6 +429,72 @@ def measure_topk(w, density, pool, warmup, steps, only_topk=False):
     return out
 
 
+def build_up(w, density, steps, rho=0.5):
+    """Sec. 5.2's gradient build-up on synthetic data: `world` simulated
+    workers, each with its own residual and its own gradient per step
+    (sqrt(rho) * a draw shared by all workers + sqrt(1 - rho) * its own draw,
+    so the per-tensor scale is kept), select under three rules; the density of
+    the union of their selections is what the all-reduce would carry.  Top-k
+    and the hard threshold search the whole vector on every worker (the
+    paper's comparators); MiCRO's workers each search partition
+    ((t mod n) + i) mod n of Algorithm 1 (micro_ef_step), so their selections
+    never overlap.  Returns the per-step union densities and the mean of the
+    workers' own densities."""
+    import torch
+    import paper_2310_00967_amd as micro
+    from paper_2310_00967_amd import synth
+    n, N = w.world, w.n_total
+    a, b = rho ** 0.5, (1.0 - rho) ** 0.5
+
+    def grad(t, i):
+        g = synth.gradient(w, t, "cuda")
+        g.mul_(a).add_(synth.gradient(w, 100_000 + t * n + i, "cuda"), alpha=b)
+        return g
+
+    g0 = grad(0, 0)
+    theta_hard = synth.initial_theta(w, g0, 0, N, density)
+    theta_part = {p: synth.initial_theta(w, g0, s, s + ln, density)
+                  for p, (s, ln) in ((p, micro.micro_partition(N, p, n)) for p in range(n))}
+    del g0
+    rules = {"topk": micro.Sparsifier(N, device="cuda", rule=micro.MICRO_RULE_TOPK),
+             "hard_threshold": micro.Sparsifier(N, device="cuda", rule=micro.MICRO_RULE_HARD_THRESHOLD),
+             "micro": micro.Sparsifier(N, device="cuda")}
+    res = {r: [torch.zeros(N, dtype=torch.float32, device="cuda") for _ in range(n)] for r in rules}
+    out_idx = torch.empty(N, dtype=torch.int32, device="cuda")
+    out_val = torch.empty(N, dtype=torch.float32, device="cuda")
+    theta_topk = [1.0] * n
+    union = {r: [] for r in rules}
+    own = {r: [] for r in rules}
+    for t in range(steps):
+        picked = {r: [] for r in rules}
+        dens = {r: 0.0 for r in rules}
+        for i in range(n):
+            g = grad(t, i)
+            k, theta_topk[i], idx, _ = rules["topk"].step(g, res["topk"][i], 0, 1, density, theta_topk[i],
+                                                          out_idx, out_val)
+            picked["topk"].append(idx.clone())
+            dens["topk"] += k / N / n
+            k, _, idx, _ = rules["hard_threshold"].step(g, res["hard_threshold"][i], 0, 1, density, theta_hard,
+                                                        out_idx, out_val)
+            picked["hard_threshold"].append(idx.clone())
+            dens["hard_threshold"] += k / N / n
+            part = micro.micro_cycle(t, i, n)
+            k, theta_part[part], _, idx, _ = rules["micro"].ef_step(g, res["micro"][i], t, i, n, density,
+                                                                    theta_part[part], out_idx, out_val)
+            picked["micro"].append(idx.clone())
+            dens["micro"] += k / (N / n) / n
+            del g
+        for r in rules:
+            union[r].append(int(torch.unique(torch.cat(picked[r])).numel()) / N)
+            own[r].append(dens[r])
+    for sp in rules.values():
+        sp.close()
+    half = steps // 2
+    return {"workers": n, "rho": rho, "steps": steps,
+            "union_density": union, "worker_density": own,
+            "union_over_target_last_half": {r: sum(v[half:]) / len(v[half:]) / density for r, v in union.items()}}
+
+
 def cpu_baseline_topk(w, density, pool, target_s):
     """The oracle's top-k selection, single-threaded on one pinned core, on
     the worker's partition (a prefix of 2^25 values where the partition is
@@ -842,6 +908,7 @@ def main_path(args, w, head, pool, n_pool, sp):
                 "topk_over_threshold_step_time": (tk["kernel_ms_avg"] / r["threshold"]["kernel_ms_avg"]
                                                   if "threshold" in r else None),
                 "rules": r,
+                "build_up": (build_up(w, head, 24) if not args.topk_only and w.world > 1 else None),
                 "cpu_baseline": cpu}
         print(json.dumps(line), flush=True)
         return

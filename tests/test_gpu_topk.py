@@ -288,3 +288,22 @@ def test_largest_vector_the_index_type_allows():
     sp.close()
     del g, res, before, idx, val
     torch.cuda.empty_cache()
+
+
+def test_build_up_of_the_comparators_and_its_absence_under_micro():
+    """bench.build_up on the toy workload (4 workers): MiCRO's exclusive
+    partitions make the union of the workers' selections exactly their sum;
+    the top-k workers' selections overlap but stay distinct, so their union
+    lies between one worker's density and n times it."""
+    import bench
+    w = synth.get("toy")
+    d = w.densities[0]
+    b = bench.build_up(w, d, 3)
+    n = b["workers"]
+    assert n == w.world
+    for t in range(3):
+        assert abs(b["union_density"]["micro"][t] - b["worker_density"]["micro"][t]) < 1e-12
+        k_frac = oracle.topk_count(d, w.n_total) / w.n_total
+        assert abs(b["worker_density"]["topk"][t] - k_frac) < 1e-12
+        assert k_frac < b["union_density"]["topk"][t] <= n * k_frac + 1e-12
+        assert b["union_density"]["hard_threshold"][t] <= n * b["worker_density"]["hard_threshold"][t] + 1e-12
