@@ -376,9 +376,11 @@ def measure_topk(w, density, pool, warmup, steps, only_topk=False):
     beside the threshold step (the default rule) and the hard-threshold rule
     (Sec. 1's comparators) on the same gradients, each with its own residual
     under error feedback: device time per step from the library's events
-    (for top-k they include the wait for the k-th magnitude between its
-    passes and the step's launches), and the density each rule selects at
-    every step, warm-up included.  Algorithmic bytes for every rule: what any
+    (for top-k they include the host's wait between the step and the passes
+    over its list), and the density each rule selects at every step, warm-up
+    included.  Each top-k call gets the k-th magnitude the last one returned
+    as its hint, as a training loop passes theta on; the first gets the
+    calibrated initial threshold.  Algorithmic bytes for every rule: what any
     selection of the partition has to move, 12 B per value (grad and residual
     read, residual written) plus 8 B per selected value; the top-k rule's
     extra passes show in a lower fraction."""
@@ -399,7 +401,7 @@ def measure_topk(w, density, pool, warmup, steps, only_topk=False):
         res = torch.zeros(N, dtype=torch.float32, device="cuda")
         out_idx, out_val = sp.outputs(ln)
         theta = theta0
-        ks, ms = [], []
+        ks, ms, routes = [], [], []
         torch.cuda.synchronize()
         t0 = time.perf_counter()
         for t in range(warmup + steps):
@@ -410,6 +412,8 @@ def measure_topk(w, density, pool, warmup, steps, only_topk=False):
             ks.append(k)
             if t >= warmup:
                 ms.append(sp.last_stats()[0])
+            if rule == micro.MICRO_RULE_TOPK:
+                routes.append(sp.last_topk_route())
         torch.cuda.synchronize()
         elapsed = time.perf_counter() - t0
         sp.close()
@@ -425,6 +429,8 @@ def measure_topk(w, density, pool, warmup, steps, only_topk=False):
                      "frac": alg / (kernel_ms * 1e-3) / 1e9 / HBM_PEAK_GBS, "k_avg": k_avg,
                      "density_series": dens,
                      "density_error_last_half": sum(abs(x - density) / density for x in half) / len(half)}
+        if routes:
+            out[name]["route_series"] = routes
     out["partition"] = (rank, start, ln)
     return out
 
@@ -900,10 +906,11 @@ def main_path(args, w, head, pool, n_pool, sp):
                              "frac": tk["frac"],
                              "traffic": read_traffic(TRAFFIC_FILE_TOPK, f"{w.name} world {w.world} rank {rank} topk d={head}",
                                                      sources=TOPK_SOURCES),
-                             "kernel": "topk_hist_kernel + topk_select_kernel over the partition, the wait, the "
-                                       "step's launches, then two more histogram passes and selects over its "
-                                       "output list and the trim (or, where that list would be long, the two "
-                                       "passes over the partition before the step); event-timed together",
+                             "kernel": "the threshold step at 7/8 of the incoming theta (the last step's k-th "
+                                       "magnitude), the wait, three topk_hist_kernel + topk_select_kernel passes "
+                                       "over its output list and the trim (route_series 3; 4: the list fell short "
+                                       "and the passes and the pick ran over the residual; 1 and 2: no hint, the "
+                                       "passes over the partition first); event-timed together",
                              "kernel_ms_avg": tk["kernel_ms_avg"], "alg_bytes_per_launch": tk["alg_bytes_per_launch"]},
                 "topk_over_threshold_step_time": (tk["kernel_ms_avg"] / r["threshold"]["kernel_ms_avg"]
                                                   if "threshold" in r else None),

@@ -78,19 +78,35 @@ typedef enum micro_status {
                              of [s, e) whose accumulated magnitude is largest,
                              equal magnitudes by lower index, NaN never (so
                              fewer than k when fewer than k are not NaN).  The
-                             incoming theta is neither checked nor used;
-                             theta receives the smallest selected magnitude
-                             (0 or +inf possible; unchanged when nothing is
-                             selected).  Through
+                             incoming theta is not checked and does not change
+                             the result: when it is positive and finite it is
+                             a hint for the k-th magnitude (pass on the theta
+                             the last step returned) and sets where the step
+                             looks first.  theta receives the smallest
+                             selected magnitude (0 or +inf possible; unchanged
+                             when nothing is selected).  Through
                              micro_sparsify_step and micro_ef_step only
                              (MICRO_EINVAL in micro_sweep_step,
                              micro_sparsify_step_noalloc and
                              micro_estimate_threshold).  The k-th magnitude is
-                             found by a radix select (three histogram passes
-                             over the partition and a wait for their result)
-                             before the step's own launches at that magnitude;
-                             when several values share it, a final pass drops
-                             the surplus from the output list.             */
+                             found by a radix select: three histogram passes
+                             over the keys and a one-workgroup select after
+                             each.  With a hint (and k <= P / 8, STAGED or
+                             AUTO) the threshold step runs first at 7/8 of it
+                             and the passes run over its output list, which
+                             a trim then cuts to the top k; if that list holds
+                             fewer than k values, they go back into the
+                             residual and the passes and a pick of the top k
+                             run over the partition's residual.  Without one
+                             the passes run over the partition first (waited
+                             for), then the step at the k-th magnitude or at
+                             the floor of its first digit, then the passes
+                             left and the trim over its list.               */
+#define MICRO_TOPK_ROUTE_FULL 1      /* micro_step_stats.topk_route: three passes over the partition, then the step */
+#define MICRO_TOPK_ROUTE_LIST 2      /* one pass over the partition, the step, two passes over its list */
+#define MICRO_TOPK_ROUTE_HINT_LIST 3 /* the step at the hint's bound, three passes over its list */
+#define MICRO_TOPK_ROUTE_HINT_PICK 4 /* the step at the hint's bound listed fewer than k: the passes and
+                                        the pick over the residual */
 
 /* Kernel schedules (both compute the same result). */
 #define MICRO_VARIANT_AUTO 0   /* per call, the faster measured schedule: TICKET
@@ -134,6 +150,9 @@ typedef struct micro_step_stats {
                                MICRO_VARIANT_TICKET or MICRO_VARIANT_STAGED    */
     int32_t fused;          /* 1 if its streaming and scan passes ran as one
                                launch (micro_sparsify_step, STAGED), else 0    */
+    int32_t topk_route;     /* MICRO_RULE_TOPK: how the step found the k-th
+                               magnitude (MICRO_TOPK_ROUTE_*); 0 for the other
+                               rules, or when nothing was selectable           */
 } micro_step_stats;
 
 /* Fills *cfg with the defaults listed above. */
@@ -166,7 +185,8 @@ MICRO_API micro_status micro_sparsify_init(micro_ctx **ctx, int64_t n_total,
  *   density   the user-set density d, 0 < d <= 1; the target count is d*P.
  *   theta     host, in/out: the threshold of this step in, the threshold of
  *             the next step out.  Must be finite and > 0.  (MICRO_RULE_TOPK:
- *             the selection is the top k instead and theta is only written,
+ *             the selection is the top k instead; theta in is unchecked and
+ *             only a hint for where to look, theta out the k-th magnitude,
  *             see there.)
  *   out_idx   device int32, capacity >= P = e - s: the first k entries
  *             receive the selected global indices, strictly increasing.

@@ -18,8 +18,8 @@ import ctypes
 from . import _lib
 from ._lib import (MICRO_FLAG_SEPARATE_SCAN, MICRO_FLAG_TIME_KERNEL, MICRO_RULE_FIXED_STEP,
                    MICRO_RULE_HARD_THRESHOLD, MICRO_RULE_PROPORTIONAL, MICRO_RULE_TOPK, MICRO_VARIANT_AUTO,
-                   MICRO_VARIANT_STAGED,
-                   MICRO_VARIANT_TICKET, MicroError, default_config, micro_cycle, micro_estimate_threshold,
+                   MICRO_TOPK_ROUTE_FULL, MICRO_TOPK_ROUTE_HINT_LIST, MICRO_TOPK_ROUTE_HINT_PICK,
+                   MICRO_TOPK_ROUTE_LIST, MICRO_VARIANT_STAGED, MICRO_VARIANT_TICKET, MicroError, default_config, micro_cycle, micro_estimate_threshold,
                    micro_partition, micro_threshold_f32)
 
 __all__ = ["Sparsifier", "MicroError", "default_config", "micro_partition", "micro_cycle",
@@ -27,7 +27,8 @@ __all__ = ["Sparsifier", "MicroError", "default_config", "micro_partition", "mic
            "MICRO_RULE_FIXED_STEP", "MICRO_RULE_HARD_THRESHOLD", "MICRO_RULE_TOPK", "MICRO_VARIANT_AUTO",
            "MICRO_VARIANT_TICKET",
            "MICRO_VARIANT_STAGED",
-           "MICRO_FLAG_TIME_KERNEL", "MICRO_FLAG_SEPARATE_SCAN"]
+           "MICRO_FLAG_TIME_KERNEL", "MICRO_FLAG_SEPARATE_SCAN", "MICRO_TOPK_ROUTE_FULL", "MICRO_TOPK_ROUTE_LIST",
+           "MICRO_TOPK_ROUTE_HINT_LIST", "MICRO_TOPK_ROUTE_HINT_PICK"]
 
 
 class Sparsifier:
@@ -251,6 +252,12 @@ class Sparsifier:
             _lib.check(st, self._ctx)
         s = self._stats_c
         return s.kernel_ms, s.redone_tiles, s.variant, s.fused
+
+    def last_topk_route(self):
+        """MICRO_RULE_TOPK: how the last step found the k-th magnitude
+        (MICRO_TOPK_ROUTE_*), else 0."""
+        self.last_stats()
+        return self._stats_c.topk_route
 
     def last_kernel_ms(self):
         return self.last_stats()[0]

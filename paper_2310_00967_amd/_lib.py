@@ -15,6 +15,7 @@ MICRO_RULE_PROPORTIONAL, MICRO_RULE_FIXED_STEP, MICRO_RULE_HARD_THRESHOLD, MICRO
 MICRO_VARIANT_AUTO, MICRO_VARIANT_TICKET, MICRO_VARIANT_STAGED = 0, 1, 2
 MICRO_FLAG_TIME_KERNEL = 1
 MICRO_FLAG_SEPARATE_SCAN = 2
+MICRO_TOPK_ROUTE_FULL, MICRO_TOPK_ROUTE_LIST, MICRO_TOPK_ROUTE_HINT_LIST, MICRO_TOPK_ROUTE_HINT_PICK = 1, 2, 3, 4
 
 # Every function the header declares, with (restype, argtypes).
 _i64p = ctypes.POINTER(ctypes.c_int64)
@@ -30,7 +31,7 @@ class micro_config(ctypes.Structure):
 
 class micro_step_stats(ctypes.Structure):
     _fields_ = [("kernel_ms", ctypes.c_float), ("redone_tiles", ctypes.c_int64),
-                ("variant", ctypes.c_int32), ("fused", ctypes.c_int32)]
+                ("variant", ctypes.c_int32), ("fused", ctypes.c_int32), ("topk_route", ctypes.c_int32)]
 
 
 _cfgp = ctypes.POINTER(micro_config)

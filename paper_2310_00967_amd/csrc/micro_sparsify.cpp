@@ -302,23 +302,45 @@ float float_from_bits(uint32_t b) {
     return f;
 }
 
-// How a top-k step runs.  Every route starts with the first histogram pass
-// (waited for).  The full route runs the other two passes over the partition
-// too (waited for), then the threshold step at the exact k-th magnitude,
-// then the trim if values equal to it must be dropped.  The list route runs
-// the threshold step at the floor of the first digit's bin instead, then the
-// other two passes over the step's output list, then the trim; it is taken
-// when that list is at most a quarter of the partition and the staging pairs
-// can hold it.  None: every value is NaN, nothing is selected.
-enum class TopkRoute { kNone, kFull, kList };
+// How a top-k step runs.  With a usable hint (the incoming theta, normally
+// the k-th magnitude the last step returned) the threshold step runs first,
+// at 7/8 of the hint rounded down to binary32 (kHint); under the staged
+// schedule it sets the residual to +0 only from the hint itself up (rounded
+// down to binary32), where the k-th magnitude is expected, so the trim has
+// few residual values to change.  When it lists at least k values (and the
+// staging pairs hold them), the three histogram passes run over that list and
+// the trim cuts it to the top k (kHintList); else the list goes back into the
+// residual, which then holds acc over the partition, and the passes and the
+// pick run over the residual (kHintPick).
+// Without a hint every route starts with the first histogram pass over the
+// partition (waited for).  The full route runs the other two passes over the
+// partition too (waited for), then the threshold step at the exact k-th
+// magnitude, then the trim if values equal to it must be dropped.  The list
+// route runs the threshold step at the floor of the first digit's bin
+// instead, then the other two passes over the step's output list, then the
+// trim; it is taken when that list is at most a quarter of the partition and
+// the staging pairs can hold it.  None: every value is NaN, nothing is
+// selected.
+enum class TopkRoute { kNone, kFull, kList, kHint, kHintList, kHintPick };
 
 struct TopkPlan {
     TopkRoute route = TopkRoute::kNone;
     uint32_t threshold_key = 0;  // the step selects the keys >= this one
-    int64_t kept = 0;            // the values selected in the end: min(k, values not NaN)
+    uint32_t zero_key = 0;       // and sets the residual of the keys >= this one to +0
+    int64_t kept = 0;            // the values selected in the end: min(k, values not NaN); kHintPick: k
     int64_t listed = 0;          // the entries of the step's output list
     bool trim = false;
 };
+
+int32_t topk_route_code(TopkRoute r) {
+    switch (r) {
+        case TopkRoute::kFull: return MICRO_TOPK_ROUTE_FULL;
+        case TopkRoute::kList: return MICRO_TOPK_ROUTE_LIST;
+        case TopkRoute::kHintList: return MICRO_TOPK_ROUTE_HINT_LIST;
+        case TopkRoute::kHintPick: return MICRO_TOPK_ROUTE_HINT_PICK;
+        default: return 0;
+    }
+}
 
 // The parallel trim's scratch: the staged schedule's staging pairs (free once
 // the step's kernels are done), tile counts and tile norms, when they hold a
@@ -338,6 +360,34 @@ uint32_t topk_blocks(const micro_ctx* ctx, int64_t n, int64_t values_per_thread)
     const int64_t per_block = static_cast<int64_t>(micro::kTopkHistBlock) * values_per_thread;
     const int64_t blocks = std::min<int64_t>((n + per_block - 1) / per_block, 4 * ctx->compute_units);
     return static_cast<uint32_t>(std::max<int64_t>(blocks, 1));
+}
+
+// The incoming theta as a hint for this step's k-th magnitude: the step
+// first runs at kTopkHintScale times it, rounded down to binary32 (*key: its
+// bits).  Taken when theta is positive and finite, the bound a positive
+// binary32, k at most an eighth of the partition, and the staged scratch
+// there for the trim and the pick.
+constexpr double kTopkHintScale = 0.875;
+
+// The largest binary32 at or below x (x >= 0): FLT_MAX above it.
+float f32_at_or_below(double x) {
+    if (x >= static_cast<double>(std::numeric_limits<float>::max())) return std::numeric_limits<float>::max();
+    float f = static_cast<float>(x);
+    if (static_cast<double>(f) > x) f = std::nextafter(f, 0.0f);
+    return f;
+}
+
+bool topk_hint_key(const micro_ctx* ctx, double theta, int64_t k, int64_t len, uint32_t* key) {
+    if (!ctx->has_staged || !ctx->d_stage || !ctx->d_tile_counts || !ctx->d_tile_sumsq) return false;
+    if (!(theta > 0.0) || !std::isfinite(theta) || k > len / 8) return false;
+    const int64_t chunks = (len + micro::kTopkTrimChunk - 1) / micro::kTopkTrimChunk;
+    if (2 * chunks > ctx->tile_capacity) return false;
+    const double b = theta * kTopkHintScale;
+    if (b > static_cast<double>(std::numeric_limits<float>::max())) return false;
+    const float f = f32_at_or_below(b);
+    if (!(f > 0.0f)) return false;
+    std::memcpy(key, &f, sizeof *key);
+    return true;
 }
 
 micro_status topk_inconsistent(micro_ctx* ctx, const char* where) {
@@ -375,7 +425,7 @@ micro_status topk_plan(micro_ctx* ctx, const float* grad, const float* residual,
     t.blocks = topk_blocks(ctx, len, 8);  // two 16-byte groups a thread
     volatile int64_t* h = ctx->h_topk;
     h[5] = 0;
-    hipError_t e = micro::launch_topk_first(t, ctx->stream);
+    hipError_t e = micro::launch_topk_passes(t, micro::TopkSource::kAcc, 0, 0, ctx->stream);
     if (e != hipSuccess) return hip_fail(ctx, e, "top-k first pass launch");
     if ((e = hipStreamSynchronize(ctx->stream)) != hipSuccess) return hip_fail(ctx, e, "hipStreamSynchronize");
     if (h[5] == 2) return MICRO_OK;  // every value is NaN
@@ -390,12 +440,14 @@ micro_status topk_plan(micro_ctx* ctx, const float* grad, const float* residual,
     if (listed <= len / 4 && trim_scratch(ctx, listed).temp) {
         plan->route = TopkRoute::kList;
         plan->threshold_key = static_cast<uint32_t>(bin);
+        plan->zero_key = plan->threshold_key;
         plan->listed = listed;
         plan->trim = true;
         return MICRO_OK;
     }
     h[5] = 0;
-    if ((e = micro::launch_topk_rest(t, false, ctx->stream)) != hipSuccess) return hip_fail(ctx, e, "top-k pass launch");
+    if ((e = micro::launch_topk_passes(t, micro::TopkSource::kAcc, 1, 2, ctx->stream)) != hipSuccess)
+        return hip_fail(ctx, e, "top-k pass launch");
     if ((e = hipStreamSynchronize(ctx->stream)) != hipSuccess) return hip_fail(ctx, e, "hipStreamSynchronize");
     const int64_t key = h[0], greater = h[1], equal = h[2], keep = h[3];
     if (h[5] != 1 || key < bin || key >= bin + bin_width || key > micro::kTopkKeyMax || keep < 1 || keep > equal ||
@@ -403,6 +455,7 @@ micro_status topk_plan(micro_ctx* ctx, const float* grad, const float* residual,
         return topk_inconsistent(ctx, "last pass");
     plan->route = TopkRoute::kFull;
     plan->threshold_key = static_cast<uint32_t>(key);
+    plan->zero_key = plan->threshold_key;
     plan->listed = greater + equal;
     plan->trim = keep < equal;
     return MICRO_OK;
@@ -417,18 +470,80 @@ hipError_t topk_after_step(micro_ctx* ctx, const TopkPlan& plan, int32_t* out_id
         micro::TopkArgs t{};
         t.list = out_val;
         t.list_n = plan.listed;
+        t.k = static_cast<uint32_t>(plan.kept);  // read by pass 0 only
         t.words = ctx->d_topk;
         t.host = ctx->h_topk_dev;
         t.blocks = topk_blocks(ctx, plan.listed, 4);
         ctx->h_topk[5] = 0;  // the device last wrote it in the first pass's select, which has been waited for
-        if ((e = micro::launch_topk_rest(t, true, ctx->stream)) != hipSuccess) return e;
+        if ((e = micro::launch_topk_passes(t, micro::TopkSource::kList, 1, 2, ctx->stream)) != hipSuccess) return e;
     }
     if (plan.trim) {
         const micro::TopkTrimScratch scratch = trim_scratch(ctx, plan.listed);
-        e = micro::launch_topk_trim(out_idx, out_val, residual, plan.listed, plan.kept, ctx->d_topk, ctx->h_topk_dev,
-                                    &scratch, ctx->stream);
+        e = micro::launch_topk_trim(out_idx, out_val, residual, plan.listed, plan.kept, plan.zero_key, ctx->d_topk,
+                                    ctx->h_topk_dev, &scratch, ctx->stream);
     }
     return e;
+}
+
+// After the step at the hint's bound listed `listed` values (waited for):
+// with at least k of them, and room for the trim, the three passes run over
+// that list and the trim cuts it to the top k; else the list goes back into
+// the residual and the passes and the pick run over the partition's
+// residual, which then holds acc.  Enqueues only.
+micro_status topk_after_hint(micro_ctx* ctx, TopkPlan* plan, int64_t listed, float* residual, int64_t start,
+                             int64_t len, double density, int32_t* out_idx, float* out_val) {
+    const int64_t k = topk_count(density, len);
+    micro::TopkArgs t{};
+    t.k = static_cast<uint32_t>(k);
+    t.words = ctx->d_topk;
+    t.host = ctx->h_topk_dev;
+    ctx->h_topk[5] = 0;
+    plan->listed = listed;
+    plan->kept = k;
+    hipError_t e;
+    if (listed >= k && trim_scratch(ctx, listed).temp) {
+        plan->route = TopkRoute::kHintList;
+        plan->trim = listed > k;
+        t.list = out_val;
+        t.list_n = listed;
+        t.blocks = topk_blocks(ctx, listed, 4);
+        if ((e = micro::launch_topk_passes(t, micro::TopkSource::kList, 0, 2, ctx->stream)) != hipSuccess)
+            return hip_fail(ctx, e, "top-k pass launch");
+        if (plan->trim) {
+            const micro::TopkTrimScratch scratch = trim_scratch(ctx, listed);
+            if ((e = micro::launch_topk_trim(out_idx, out_val, residual, listed, k, plan->zero_key, ctx->d_topk,
+                                             ctx->h_topk_dev, &scratch, ctx->stream)) != hipSuccess)
+                return hip_fail(ctx, e, "top-k trim launch");
+        }
+        return MICRO_OK;
+    }
+    plan->route = TopkRoute::kHintPick;
+    plan->trim = false;
+    const int64_t chunks = (len + micro::kTopkTrimChunk - 1) / micro::kTopkTrimChunk;
+    if (2 * chunks > ctx->tile_capacity) {  // topk_hint_key checked it
+        set_error(ctx, "top-k pick needs %lld count words, scratch holds %lld", static_cast<long long>(2 * chunks),
+                  static_cast<long long>(ctx->tile_capacity));
+        return MICRO_ECAPACITY;
+    }
+    if ((e = micro::launch_topk_restore(out_idx, out_val, listed, residual, start, start + len, ctx->stream)) !=
+        hipSuccess)
+        return hip_fail(ctx, e, "top-k restore launch");
+    t.residual = residual;
+    t.start = start;
+    t.end = start + len;
+    t.vec4 = true;  // the residual's own 16-byte groups
+    const uintptr_t addr = reinterpret_cast<uintptr_t>(residual + start);
+    int64_t head = static_cast<int64_t>(((16u - (addr & 15u)) & 15u) / sizeof(float));
+    if (head > len) head = len;
+    t.body_first = start + head;
+    t.body_end = t.body_first + ((t.end - t.body_first) / 4) * 4;
+    t.blocks = topk_blocks(ctx, len, 8);
+    if ((e = micro::launch_topk_passes(t, micro::TopkSource::kResidual, 0, 2, ctx->stream)) != hipSuccess)
+        return hip_fail(ctx, e, "top-k pass launch");
+    if ((e = micro::launch_topk_pick(residual, start, start + len, out_idx, out_val, ctx->d_topk, ctx->d_tile_counts,
+                                     ctx->stream)) != hipSuccess)
+        return hip_fail(ctx, e, "top-k pick launch");
+    return MICRO_OK;
 }
 
 // After the wait: the step must have listed what the plan expects; the
@@ -448,6 +563,24 @@ micro_status topk_finish(micro_ctx* ctx, const TopkPlan& plan, int64_t listed_by
     if (plan.route == TopkRoute::kNone) return MICRO_OK;
     const volatile int64_t* h = ctx->h_topk;
     uint32_t key = plan.threshold_key;
+    if (plan.route == TopkRoute::kHintPick) {
+        if (h[5] == 2 && plan.listed == 0 && h[4] == 0) return MICRO_OK;  // every value is NaN
+        const int64_t k_key = h[0], greater = h[1], equal = h[2], keep = h[3], valid = h[4];
+        const int64_t kept = std::min(plan.kept, valid);
+        if (h[5] != 1 || k_key < 0 || k_key > micro::kTopkKeyMax || valid < plan.listed || keep < 1 ||
+            keep > equal || greater < 0 || greater + keep != kept || greater + equal > valid)
+            return topk_inconsistent(ctx, "residual");
+        *selected = kept;
+        *theta = static_cast<double>(float_from_bits(static_cast<uint32_t>(k_key)));
+        return MICRO_OK;
+    }
+    if (plan.route == TopkRoute::kHintList) {
+        const int64_t k_key = h[0], greater = h[1], equal = h[2], keep = h[3];
+        if (h[5] != 1 || k_key < plan.threshold_key || k_key > micro::kTopkKeyMax || keep < 1 || keep > equal ||
+            greater < 0 || greater + keep != plan.kept || greater + equal > plan.listed)
+            return topk_inconsistent(ctx, "hinted list");
+        key = static_cast<uint32_t>(k_key);
+    }
     if (plan.route == TopkRoute::kList) {
         const int64_t k_key = h[0], greater = h[1], equal = h[2], keep = h[3];
         if (h[5] != 1 || k_key < plan.threshold_key ||
@@ -531,6 +664,7 @@ micro_status execute_step(micro_ctx* ctx, const float* grad, float* residual, in
             if (s != MICRO_OK) return s;
             sq[1] += returned;  // the values the trim returned to the residual
             *k = kk[1];
+            ctx->stats.topk_route = topk_route_code(plan.route);
         } else {
             *k = kk[1];
             *theta = next_threshold(ctx->cfg, density, len, kk[1], *theta);
@@ -616,12 +750,24 @@ micro_status execute_step(micro_ctx* ctx, const float* grad, float* residual, in
     ctx->stats.redone_tiles = 0;
     if (timed && (e = hipEventRecord(ctx->ev[0], ctx->stream)) != hipSuccess)
         return hip_fail(ctx, e, "hipEventRecord");
-    // The top-k comparator: the exact k-th largest magnitude first (waited
-    // for), then the step at that magnitude (NaN: nothing selected).
+    // The top-k comparator: with a hint the step runs at the hint's bound;
+    // else the exact k-th largest magnitude, or its first digit's bin, first
+    // (waited for), then the step there (NaN: nothing selected).
     TopkPlan plan;
     if (topk && len > 0) {
-        micro_status s = topk_plan(ctx, grad, residual, start, len, density, vec4, &plan);
-        if (s != MICRO_OK) return s;
+        uint32_t hint_key;
+        if (topk_hint_key(ctx, *theta, topk_count(density, len), len, &hint_key)) {
+            plan.route = TopkRoute::kHint;
+            plan.threshold_key = hint_key;
+            plan.zero_key = hint_key;
+            if (staged) {  // the staged kernels leave acc in the residual below theta_zero
+                a.theta_zero = f32_at_or_below(*theta);
+                std::memcpy(&plan.zero_key, &a.theta_zero, sizeof plan.zero_key);
+            }
+        } else {
+            micro_status s = topk_plan(ctx, grad, residual, start, len, density, vec4, &plan);
+            if (s != MICRO_OK) return s;
+        }
         a.theta_f = plan.route == TopkRoute::kNone ? std::numeric_limits<float>::quiet_NaN()
                                                    : float_from_bits(plan.threshold_key);
     }
@@ -640,10 +786,23 @@ micro_status execute_step(micro_ctx* ctx, const float* grad, float* residual, in
                     : micro::launch_staged(a, vec4, ctx->stream);
         if (e != hipSuccess) return hip_fail(ctx, e, "sparsify kernel launch");
     }
-    // The top-k comparator's work after the step: the list route's last
-    // passes over the step's output list, and the trim to the top k.
-    if (topk && (e = topk_after_step(ctx, plan, out_idx, out_val, residual)) != hipSuccess)
+    // The top-k comparator's work after the step: on the hint's route, what
+    // the step's count calls for; else the list route's last passes over the
+    // step's output list, and the trim to the top k.
+    if (topk && plan.route == TopkRoute::kHint) {
+        if ((e = hipStreamSynchronize(ctx->stream)) != hipSuccess) return hip_fail(ctx, e, "hipStreamSynchronize");
+        const int64_t listed = host_count[0];
+        if (listed < 0 || listed > len) {
+            set_error(ctx, "device reported %lld listed of %lld", static_cast<long long>(listed),
+                      static_cast<long long>(len));
+            ctx->needs_reset = true;
+            return MICRO_EHIP;
+        }
+        const micro_status s = topk_after_hint(ctx, &plan, listed, residual, start, len, density, out_idx, out_val);
+        if (s != MICRO_OK) return s;
+    } else if (topk && (e = topk_after_step(ctx, plan, out_idx, out_val, residual)) != hipSuccess) {
         return hip_fail(ctx, e, "top-k launch after the step");
+    }
     if (timed && (e = hipEventRecord(ctx->ev[1], ctx->stream)) != hipSuccess)
         return hip_fail(ctx, e, "hipEventRecord");
     if ((e = hipStreamSynchronize(ctx->stream)) != hipSuccess) return hip_fail(ctx, e, "hipStreamSynchronize");
@@ -663,6 +822,7 @@ micro_status execute_step(micro_ctx* ctx, const float* grad, float* residual, in
     ctx->stats.redone_tiles = staged ? host_count[1] : 0;
     ctx->stats.variant = staged ? MICRO_VARIANT_STAGED : MICRO_VARIANT_TICKET;
     ctx->stats.fused = len > 0 && fused ? 1 : 0;
+    ctx->stats.topk_route = topk ? topk_route_code(plan.route) : 0;
     *k = selected;
     if (!topk) *theta = next_threshold(ctx->cfg, density, len, selected, *theta);
     return MICRO_OK;
@@ -777,6 +937,7 @@ micro_status run_segments(micro_ctx* ctx, const float* grad, float* residual, in
     ctx->stats.redone_tiles = host_count[1];
     ctx->stats.variant = MICRO_VARIANT_STAGED;
     ctx->stats.fused = fused ? 1 : 0;
+    ctx->stats.topk_route = 0;
     for (int32_t r = 0; r < count; ++r) {
         k[r] = host_count[2 + r];
         // the segment's chunks in increasing order
@@ -1134,6 +1295,7 @@ micro_status micro_sparsify_init(micro_ctx** out, int64_t n_total, void* hip_str
     ctx->stats.redone_tiles = 0;
     ctx->stats.variant = ctx->has_staged ? MICRO_VARIANT_STAGED : MICRO_VARIANT_TICKET;
     ctx->stats.fused = 0;
+    ctx->stats.topk_route = 0;
     if (reset_scratch(ctx) != MICRO_OK) {
         set_error(nullptr, "%s", ctx->last_error.c_str());
         release(ctx);

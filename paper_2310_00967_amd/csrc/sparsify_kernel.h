@@ -126,6 +126,10 @@ struct LaunchArgs {
     // ticket schedule
     uint64_t* status;                   // >= num_tiles look-back words
     unsigned long long* ticket;         // 0 at launch, rearmed by the kernel
+    // staged schedule, theta_zero > theta_f: of the selected values only those
+    // with |acc| >= theta_zero have their residual set to +0; the others keep
+    // acc there (the top-k comparator's step at a hint's bound)
+    float theta_zero;
 };
 
 // Error-feedback accumulation outside the searched partition (Algorithm 1,
@@ -147,7 +151,9 @@ struct AccumulateArgs {
 int64_t tile_base_for(const float* grad, int64_t start, bool vec4);
 
 // vec4: grad and residual share their 16-byte phase (dwordx4 kernels), else
-// the scalar-load kernels.  Each returns the launch status.
+// the scalar-load kernels.  Each returns the launch status.  launch_staged and
+// launch_fused take the kernels that honour theta_zero when it is above
+// theta_f.
 hipError_t launch_staged(const LaunchArgs& args, bool vec4, hipStream_t stream);
 // The staged schedule with its stream and scan kernels fused into one launch
 // (num_tiles + num_chunks workgroups, roles from fused_role).  Its waits end

@@ -248,11 +248,21 @@ __device__ __forceinline__ void load_tile(const LaunchArgs& a, int64_t base, int
 
 // acc = grad + residual (one binary32 add) and the threshold test; values
 // outside [start, end) are never selected.  Leaves acc in t.v and returns the
-// lane's selection bits: bit r * VEC + c for value (r, lane, c).
-template <int VEC, int ROWS, int LANES>
-__device__ __forceinline__ uint32_t compute_tile(const LaunchArgs& a, int lane, Tile<VEC, ROWS, LANES>& t) {
+// lane's selection bits: bit r * VEC + c for value (r, lane, c).  HINT: *zero
+// receives the selected values whose residual becomes +0, those with
+// |acc| >= theta_zero.
+template <int VEC, int ROWS, int LANES, bool HINT = false>
+__device__ __forceinline__ uint32_t compute_tile(const LaunchArgs& a, int lane, Tile<VEC, ROWS, LANES>& t,
+                                                 uint32_t* zero = nullptr) {
     static_assert(VEC * ROWS <= 32, "selection bits");
-    uint32_t sel = 0;
+    uint32_t sel = 0, z = 0;
+    float theta_zero = 0.0f;
+    if constexpr (HINT) {
+        // read with the other arguments, not where the mask is used: a load
+        // sunk to its use is a wait of its own in every workgroup
+        theta_zero = a.theta_zero;
+        asm volatile("" : "+s"(theta_zero));
+    }
 #pragma unroll
     for (int r = 0; r < ROWS; ++r)
 #pragma unroll
@@ -265,7 +275,9 @@ __device__ __forceinline__ uint32_t compute_tile(const LaunchArgs& a, int lane, 
                 s = s && i >= a.start && i < a.end;
             }
             sel |= static_cast<uint32_t>(s) << (r * VEC + c);
+            if constexpr (HINT) z |= static_cast<uint32_t>(__builtin_fabsf(acc) >= theta_zero) << (r * VEC + c);
         }
+    if constexpr (HINT) *zero = sel & z;
     return sel;
 }
 
@@ -469,7 +481,7 @@ __device__ __forceinline__ void publish_tile(const LaunchArgs& a, uint32_t tile,
 // segment supplies range and threshold, and the tile also stores the squared
 // norm of its new residual (also for a tile left to the move kernel, whose
 // new residual is fixed by its selection bits all the same).
-template <int VEC, int ROWS, bool SWEEP, bool FUSED = false>
+template <int VEC, int ROWS, bool SWEEP, bool FUSED = false, bool HINT = false>
 __device__ __forceinline__ void stream_tile(LaunchArgs a, const SweepTable* tbl, uint32_t tile) {
     constexpr int WAVES = kStreamBlock / kWaveSize;
     static_assert(VEC * ROWS * kStreamBlock == kStreamTile, "tile size");
@@ -485,7 +497,8 @@ __device__ __forceinline__ void stream_tile(LaunchArgs a, const SweepTable* tbl,
     Tile<VEC, ROWS, kStreamBlock> t;
     uint32_t lane_rank[ROWS], row_count[ROWS], row_base[ROWS];
     load_tile<VEC, ROWS, kStreamBlock, true>(a, tile_base, tid, t);
-    const uint32_t sel = compute_tile(a, tid, t);
+    uint32_t zero = 0;
+    const uint32_t sel = compute_tile<VEC, ROWS, kStreamBlock, HINT>(a, tid, t, &zero);
     if constexpr (SWEEP) {
         double sq = 0.0;
 #pragma unroll
@@ -505,7 +518,7 @@ __device__ __forceinline__ void stream_tile(LaunchArgs a, const SweepTable* tbl,
         if (tid == 0) publish_tile<FUSED>(a, tile, count | kOverflow);
         return;
     }
-    store_residual<VEC, ROWS, kStreamBlock, true>(a, tid, t, sel);
+    store_residual<VEC, ROWS, kStreamBlock, true>(a, tid, t, HINT ? zero : sel);
 #pragma unroll
     for (int r = 0; r < ROWS; ++r) {
         uint32_t pos = row_base[r] + lane_rank[r];
@@ -532,6 +545,13 @@ __global__ __launch_bounds__(kStreamBlock) void stream_kernel(LaunchArgs a) {
     stream_tile<VEC, ROWS, false>(a, nullptr, blockIdx.x);
 }
 
+// The stream pass that sets only the residual of values at or above
+// theta_zero to +0.
+template <int VEC, int ROWS>
+__global__ __launch_bounds__(kStreamBlock) void stream_hint_kernel(LaunchArgs a) {
+    stream_tile<VEC, ROWS, false, false, true>(a, nullptr, blockIdx.x);
+}
+
 template <int VEC, int ROWS>
 __global__ __launch_bounds__(kStreamBlock) void stream_sweep_kernel(LaunchArgs a, SweepTable tbl) {
     stream_tile<VEC, ROWS, true>(a, &tbl, blockIdx.x);
@@ -541,7 +561,7 @@ __global__ __launch_bounds__(kStreamBlock) void stream_sweep_kernel(LaunchArgs a
 // position out_base on: the tile's values in index order, 256 at a time (one
 // part in registers keeps the move kernel's register budget).  a carries the
 // tile's range and threshold; tile_base is its first value's global index.
-template <int VEC>
+template <int VEC, bool HINT = false>
 __device__ void redo_tile(const LaunchArgs& a, int64_t tile_base, int lane, uint32_t out_base) {
     constexpr int ROWS = 4 / VEC;
     using T = Tile<VEC, ROWS, kWaveSize>;
@@ -552,7 +572,8 @@ __device__ void redo_tile(const LaunchArgs& a, int64_t tile_base, int lane, uint
         T t;
         uint32_t lane_rank[ROWS], row_count[ROWS], row_base[ROWS];
         load_tile<VEC, ROWS, kWaveSize, false>(a, tile_base + part * T::kElems, lane, t);
-        const uint32_t sel = compute_tile(a, lane, t);
+        uint32_t zero = 0;
+        const uint32_t sel = compute_tile<VEC, ROWS, kWaveSize, HINT>(a, lane, t, &zero);
         wave_ranks<VEC, ROWS>(sel, lane_rank, row_count);
         uint32_t sub = 0;
 #pragma unroll
@@ -560,7 +581,7 @@ __device__ void redo_tile(const LaunchArgs& a, int64_t tile_base, int lane, uint
             row_base[r] = sub;
             sub += row_count[r];
         }
-        store_residual<VEC, ROWS, kWaveSize, false>(a, lane, t, sel);
+        store_residual<VEC, ROWS, kWaveSize, false>(a, lane, t, HINT ? zero : sel);
         scatter_pairs(a, lane, t, sel, run, row_base, lane_rank);
         run += sub;
     }
@@ -918,6 +939,18 @@ __global__ __launch_bounds__(kStreamBlock) void stream_scan_kernel(LaunchArgs a)
         stream_tile<VEC, ROWS, false, true>(a, nullptr, role.item);
 }
 
+// The fused launch whose stream pass sets only the residual of values at or
+// above theta_zero to +0.
+template <int VEC, int ROWS>
+__global__ __launch_bounds__(kStreamBlock) void stream_scan_hint_kernel(LaunchArgs a) {
+    static_assert(kStreamBlock == kScanBlock, "one workgroup size for both parts");
+    const FusedRole role = fused_role(blockIdx.x, a.num_tiles, a.num_chunks);
+    if (role.scan)
+        scan_chunk<false, true>(a, nullptr, role.item);
+    else
+        stream_tile<VEC, ROWS, false, true, true>(a, nullptr, role.item);
+}
+
 __global__ __launch_bounds__(kScanBlock) void scan_sweep_kernel(LaunchArgs a, SweepTable tbl) {
     scan_chunk<true>(a, &tbl, blockIdx.x);
 }
@@ -1004,7 +1037,7 @@ __device__ __forceinline__ void block_max_scan(uint16_t* v, int tid, uint32_t* s
 // The move kernel's work once the count k > 0 is known: the flagged tiles,
 // then this workgroup's pieces (first_t0 / first_t1: the split words of its
 // first piece, loaded with the counts).
-template <int VEC, bool SWEEP>
+template <int VEC, bool SWEEP, bool HINT = false>
 __device__ __forceinline__ void move_work(const LaunchArgs& a, const SweepTable* tbl, int64_t k, uint32_t flagged,
                                           uint32_t first_t0, uint32_t first_t1) {
     constexpr uint32_t kWindow = kMoveSpan + 1;
@@ -1026,7 +1059,7 @@ __device__ __forceinline__ void move_work(const LaunchArgs& a, const SweepTable*
             const int64_t tile_base = enter_segment(seg_args, tbl, tile);
             redo_tile<VEC>(seg_args, tile_base, lane, out_base);
         } else {
-            redo_tile<VEC>(a, a.base + static_cast<int64_t>(tile) * kStreamTile, lane, out_base);
+            redo_tile<VEC, HINT>(a, a.base + static_cast<int64_t>(tile) * kStreamTile, lane, out_base);
         }
     }
     const uint64_t total = static_cast<uint64_t>(a.num_tiles) + static_cast<uint64_t>(k);
@@ -1133,7 +1166,7 @@ __device__ __forceinline__ void move_work(const LaunchArgs& a, const SweepTable*
 // coalesced write.  Before its pieces, every workgroup redoes its share of the
 // flagged tiles, so a dense region of the partition costs the whole grid a
 // second pass over it rather than one workgroup a serial one.
-template <int VEC, bool SWEEP>
+template <int VEC, bool SWEEP, bool HINT = false>
 __device__ __forceinline__ void move_pieces(const LaunchArgs& a, const SweepTable* tbl) {
     constexpr int WAVES = kMoveBlock / kWaveSize;
     __shared__ double s_sq[WAVES];
@@ -1174,7 +1207,7 @@ __device__ __forceinline__ void move_pieces(const LaunchArgs& a, const SweepTabl
             }
         }
     }
-    if (k != 0) move_work<VEC, SWEEP>(a, tbl, k, flagged, first_t0, first_t1);
+    if (k != 0) move_work<VEC, SWEEP, HINT>(a, tbl, k, flagged, first_t0, first_t1);
     if constexpr (SWEEP) {
         // Each chunk's squared norm, its tiles' norms added in a fixed order
         // (each thread its tiles in increasing order, then the workgroup sum);
@@ -1196,6 +1229,13 @@ __device__ __forceinline__ void move_pieces(const LaunchArgs& a, const SweepTabl
 template <int VEC>
 __global__ __launch_bounds__(kMoveBlock) void move_kernel(LaunchArgs a) {
     move_pieces<VEC, false>(a, nullptr);
+}
+
+// The move kernel after the hint kernels' stream pass: a flagged tile it redoes
+// also sets only the residual of values at or above theta_zero to +0.
+template <int VEC>
+__global__ __launch_bounds__(kMoveBlock) void move_hint_kernel(LaunchArgs a) {
+    move_pieces<VEC, false, true>(a, nullptr);
 }
 
 template <int VEC>
@@ -1321,11 +1361,24 @@ hipError_t launch_staged(const LaunchArgs& args, bool vec4, hipStream_t stream) 
     if (!staged_args_set(args) || !args.tile_counts) return hipErrorInvalidValue;
     const dim3 grid_stream(args.num_tiles), grid_scan(args.num_chunks), grid_move(args.move_blocks);
     const dim3 bs(kStreamBlock);
+    const bool hint = args.theta_zero > args.theta_f;
     if (vec4) {
+        if (hint) {
+            hipLaunchKernelGGL((stream_hint_kernel<4, 1>), grid_stream, bs, 0, stream, args);
+            hipLaunchKernelGGL(scan_kernel, grid_scan, dim3(kScanBlock), 0, stream, args);
+            hipLaunchKernelGGL(move_hint_kernel<4>, grid_move, dim3(kMoveBlock), 0, stream, args);
+            return hipGetLastError();
+        }
         hipLaunchKernelGGL((stream_kernel<4, 1>), grid_stream, bs, 0, stream, args);
         hipLaunchKernelGGL(scan_kernel, grid_scan, dim3(kScanBlock), 0, stream, args);
         hipLaunchKernelGGL(move_kernel<4>, grid_move, dim3(kMoveBlock), 0, stream, args);
     } else {
+        if (hint) {
+            hipLaunchKernelGGL((stream_hint_kernel<1, 4>), grid_stream, bs, 0, stream, args);
+            hipLaunchKernelGGL(scan_kernel, grid_scan, dim3(kScanBlock), 0, stream, args);
+            hipLaunchKernelGGL(move_hint_kernel<1>, grid_move, dim3(kMoveBlock), 0, stream, args);
+            return hipGetLastError();
+        }
         hipLaunchKernelGGL((stream_kernel<1, 4>), grid_stream, bs, 0, stream, args);
         hipLaunchKernelGGL(scan_kernel, grid_scan, dim3(kScanBlock), 0, stream, args);
         hipLaunchKernelGGL(move_kernel<1>, grid_move, dim3(kMoveBlock), 0, stream, args);
@@ -1336,10 +1389,21 @@ hipError_t launch_staged(const LaunchArgs& args, bool vec4, hipStream_t stream) 
 hipError_t launch_fused(const LaunchArgs& args, bool vec4, hipStream_t stream) {
     if (!staged_args_set(args) || !args.tile_words) return hipErrorInvalidValue;
     const dim3 grid_fused(args.num_tiles + args.num_chunks), grid_move(args.move_blocks);
+    const bool hint = args.theta_zero > args.theta_f;
     if (vec4) {
+        if (hint) {
+            hipLaunchKernelGGL((stream_scan_hint_kernel<4, 1>), grid_fused, dim3(kStreamBlock), 0, stream, args);
+            hipLaunchKernelGGL(move_hint_kernel<4>, grid_move, dim3(kMoveBlock), 0, stream, args);
+            return hipGetLastError();
+        }
         hipLaunchKernelGGL((stream_scan_kernel<4, 1>), grid_fused, dim3(kStreamBlock), 0, stream, args);
         hipLaunchKernelGGL(move_kernel<4>, grid_move, dim3(kMoveBlock), 0, stream, args);
     } else {
+        if (hint) {
+            hipLaunchKernelGGL((stream_scan_hint_kernel<1, 4>), grid_fused, dim3(kStreamBlock), 0, stream, args);
+            hipLaunchKernelGGL(move_hint_kernel<1>, grid_move, dim3(kMoveBlock), 0, stream, args);
+            return hipGetLastError();
+        }
         hipLaunchKernelGGL((stream_scan_kernel<1, 4>), grid_fused, dim3(kStreamBlock), 0, stream, args);
         hipLaunchKernelGGL(move_kernel<1>, grid_move, dim3(kMoveBlock), 0, stream, args);
     }

@@ -6,14 +6,13 @@
 // largest magnitude is found exactly by a radix select over the 31 magnitude
 // bits of binary32 (for values that are not NaN, the bit pattern with the sign
 // cleared orders like the magnitude), digits of 11, 11 and 9 bits, each digit
-// by a histogram pass and a one-workgroup select.  The first digit always
-// comes from a pass over acc = grad + residual of the partition.  The other
-// two come either from two more such passes (the full route), or (the list
-// route) from passes over the output list of the threshold step run at the
-// lower bound of the first digit's bin: that list holds every value of the
-// bin and above, usually a small multiple of k.  A trim then drops from the
-// step's output list the values below the k-th magnitude and the surplus of
-// values equal to it.
+// by a histogram pass and a one-workgroup select.  The passes read their keys
+// from acc = grad + residual over the partition, from the residual alone
+// (once it holds acc), or from the values of the threshold step's output
+// list, which holds every value at or above the step's threshold.  A trim
+// then drops from that list the values below the k-th magnitude and the
+// surplus of values equal to it; a pick instead takes the top k straight from
+// a residual that holds acc.
 #pragma once
 
 #include <hip/hip_runtime.h>
@@ -51,31 +50,39 @@ enum TopkState : int {
 // [5] status.  The trim writes [6], the bit pattern of the binary64 sum of
 // squares of the values it returns to the residual.
 struct TopkArgs {
-    const float* grad;
+    const float* grad;             // kAcc only
     const float* residual;
     int64_t start, end;            // the partition
-    int64_t body_first, body_end;  // vec4: [body_first, body_end) in whole 16-byte groups of both vectors
+    int64_t body_first, body_end;  // vec4: [body_first, body_end) in whole 16-byte groups of the vectors read
     bool vec4;
-    uint32_t k;                    // the wanted count, 1 <= k <= end - start
-    const float* list;             // list route: the step's output values
+    uint32_t k;                    // the wanted count, 1 <= k <= the keys read
+    const float* list;             // kList: the step's output values
     int64_t list_n;                // and their count
     uint32_t* words;               // kTopkBins counters (zero between passes), then kTopkStateWords
     int64_t* host;                 // kTopkHostWords mapped host words (device address)
     uint32_t blocks;               // grid of the histogram passes
 };
 
-// The first pass and its select over the partition.
-hipError_t launch_topk_first(const TopkArgs& args, hipStream_t stream);
-// The second and third passes and their selects: over the partition, or
-// (over_list) over args.list[0, list_n).
-hipError_t launch_topk_rest(const TopkArgs& args, bool over_list, hipStream_t stream);
+// Where the histogram passes read their keys.
+enum class TopkSource : int {
+    kAcc = 0,       // acc = grad + residual over [start, end) (binary32 addition, as in the step)
+    kResidual = 1,  // the residual alone over [start, end): it holds acc already
+    kList = 2,      // list[0, list_n)
+};
+
+// Passes first .. last (0, 1, 2) of the radix select, each with its select.
+// Pass 0 starts a new search: it reads no state of an earlier one.
+hipError_t launch_topk_passes(const TopkArgs& args, TopkSource src, uint32_t first, uint32_t last,
+                              hipStream_t stream);
 
 // Drops from the index-ordered output list [0, n) the values whose key is
 // below the k-th key, and those equal to it after the first `kept equal` of
-// them (both read from the state words, after the last select), returning
-// their values to the residual and compacting the list, of which `kept`
-// entries stay; host[6] receives the binary64 sum of squares of the returned
-// values.  With scratch (temp: n pairs; counts: two per kTopkTrimChunk list
+// them (both read from the state words, after the last select), compacting
+// the list, of which `kept` entries stay.  The step set the residual of the
+// listed values with a key at or above zero_key to +0 and left acc in the
+// others: a dropped value of the former returns to the residual, a kept value
+// of the latter gets +0 there.  host[6] receives the binary64 sum of squares
+// of the returned values.  With scratch (temp: n pairs; counts: two per kTopkTrimChunk list
 // entries; partial: one per chunk) the whole device compacts the list in
 // four launches: per chunk the equal and the lower keys counted, both counts
 // scanned, every kept entry placed in temp and the dropped ones returned,
@@ -88,7 +95,25 @@ struct TopkTrimScratch {
     double* partial;   // >= ceil(n / kTopkTrimChunk)
 };
 hipError_t launch_topk_trim(int32_t* out_idx, float* out_val, float* residual, int64_t n, int64_t kept,
-                            const uint32_t* words, int64_t* host, const TopkTrimScratch* scratch,
-                            hipStream_t stream);
+                            uint32_t zero_key, const uint32_t* words, int64_t* host,
+                            const TopkTrimScratch* scratch, hipStream_t stream);
+
+// Writes the output list [0, n) back into the residual: residual[idx[j]] =
+// val[j] for every idx[j] in [start, end) (the rest is skipped).  After the
+// threshold step the residual then holds acc over the whole partition (the
+// values the step did not set to +0 hold it already).
+hipError_t launch_topk_restore(const int32_t* out_idx, const float* out_val, int64_t n, float* residual,
+                               int64_t start, int64_t end, hipStream_t stream);
+
+// Takes the top k straight from a residual holding acc over [start, end),
+// after the last select: the values whose key is above the k-th key (NaN
+// aside) and the first `kept equal` of those equal to it, in index order, into
+// out_idx / out_val [0, kept), each replaced by +0 in the residual.  Three
+// launches: per chunk of kTopkTrimChunk values the equal and the higher keys
+// counted (counts: 2 * ceil((end - start) / kTopkTrimChunk) words), both
+// counts scanned, every picked value placed.  Nothing is written without a
+// k-th key (status other than 1).
+hipError_t launch_topk_pick(float* residual, int64_t start, int64_t end, int32_t* out_idx, float* out_val,
+                            const uint32_t* words, uint32_t* counts, hipStream_t stream);
 
 }  // namespace micro

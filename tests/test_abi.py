@@ -46,6 +46,37 @@ def test_library_exports_nothing_else():
     assert micro_syms == set(declared_functions())
 
 
+def test_binding_layouts_and_constants_match_the_header(tmp_path):
+    """The ctypes structures and constants of the binding against the header,
+    as a C compiler reads it: sizes and field offsets of micro_config and
+    micro_step_stats, and the value of every MICRO_* macro the binding
+    names."""
+    import subprocess
+    macros = sorted(n for n in dir(_lib) if re.fullmatch(r"MICRO_(RULE|VARIANT|FLAG|TOPK_ROUTE)_\w+", n))
+    assert "MICRO_TOPK_ROUTE_HINT_PICK" in macros
+    lines = ['#include <stdio.h>', '#include <stddef.h>', '#include "micro_sparsify.h"', "int main(void) {"]
+    for st, fields in (("micro_config", _lib.micro_config._fields_), ("micro_step_stats", _lib.micro_step_stats._fields_)):
+        lines.append(f'printf("{st} %zu\\n", sizeof({st}));')
+        for name, _ in fields:
+            lines.append(f'printf("{st}.{name} %zu\\n", offsetof({st}, {name}));')
+    for m in macros:
+        lines.append(f'printf("{m} %d\\n", (int)({m}));')
+    lines.append("return 0; }")
+    src = tmp_path / "layout.c"
+    src.write_text("\n".join(lines) + "\n")
+    exe = tmp_path / "layout"
+    subprocess.run(["gcc", "-std=c11", "-Wall", "-Werror", "-I", os.path.join(ROOT, "include"), str(src), "-o",
+                    str(exe)], check=True)
+    got = dict(ln.split() for ln in subprocess.run([str(exe)], capture_output=True, text=True,
+                                                   check=True).stdout.splitlines())
+    for st in (_lib.micro_config, _lib.micro_step_stats):
+        assert int(got[st.__name__]) == ctypes.sizeof(st), st.__name__
+        for name, _ in st._fields_:
+            assert int(got[f"{st.__name__}.{name}"]) == getattr(st, name).offset, (st.__name__, name)
+    for m in macros:
+        assert int(got[m]) == getattr(_lib, m), m
+
+
 def test_partition_matches_oracle():
     rng = np.random.default_rng(0)
     cases = [(0, 0, 1), (7, 3, 16), (11_689_512, 15, 16), (335_141_888, 3, 8), (2**31 - 1, 6, 7)]

@@ -2,12 +2,17 @@
 
 Every call goes through the C ABI via the ctypes binding.  Indices, values,
 the selected count, the returned k-th magnitude and the residual must equal
-the oracle's (oracle.topk_step / oracle.topk_ef_step) bit for bit.  At the
-GPT-1.3B size, where the oracle's sort would take minutes, the result is
-checked against the properties that define the top k: the count, strictly
-increasing indices inside the partition, the values and residual equal to the
-accumulation, every selected magnitude at least every other one, and equal
-magnitudes taken by lower index.
+the oracle's (oracle.topk_step / oracle.topk_ef_step) bit for bit, whatever
+the incoming theta: none (NaN: the radix select's passes over the partition
+first), the exact k-th magnitude (the step at 7/8 of it lists at least k
+values: the passes over that list), one far above it (the step lists fewer
+than k: the list returns to the residual and the passes and the pick run
+over it) or far below it (a long list).  At the GPT-1.3B size, where the
+oracle's sort would take minutes, the result is checked against the
+properties that define the top k: the count, strictly increasing indices
+inside the partition, the values and residual equal to the accumulation,
+every selected magnitude at least every other one, and equal magnitudes
+taken by lower index.
 """
 import math
 
@@ -43,12 +48,45 @@ def same_bits(a, b):
     return a.shape == b.shape and np.array_equal(a.view(np.uint32)[~both], b.view(np.uint32)[~both])
 
 
-def topk_vs_oracle(g, res, rank, world, density, variant=AUTO, phase_shift=0, sp=None, theta=1.0):
-    """One call on both sides; g/res are host float32 arrays."""
+HINT_ROUTES = (micro.MICRO_TOPK_ROUTE_HINT_LIST, micro.MICRO_TOPK_ROUTE_HINT_PICK)
+HINTS = pytest.mark.parametrize("hint", ["none", "exact", "high", "low"])
+
+
+def hint_bound(theta):
+    """The step's first threshold under a hint: the largest binary32 at or
+    below 7/8 of theta."""
+    b = float(theta) * 0.875
+    f = np.float32(b)
+    if float(f) > b:
+        f = np.nextafter(f, np.float32(0))
+    return f
+
+
+def topk_k(density, ln):
+    return oracle.topk_count(density, ln)
+
+
+def theta_for(hint, kth):
+    """The incoming theta for a hint kind, given the oracle's k-th magnitude."""
+    if not isinstance(hint, str):
+        return float(hint)
+    if hint == "none" or not (0.0 < kth < math.inf):
+        return math.nan
+    return {"exact": kth, "high": 8.0 * kth, "low": kth / 1024.0}[hint]
+
+
+def topk_vs_oracle(g, res, rank, world, density, variant=AUTO, phase_shift=0, sp=None, hint="none"):
+    """One call on both sides; g/res are host float32 arrays.  `hint` picks
+    the incoming theta (theta_for) or is the theta itself."""
     N = g.size
     own = sp is None
     if own:
         sp = make(N, variant)
+    r_or = res.copy()
+    o_idx, o_val, k_or, th_or = oracle.topk_step(g, r_or, rank, world, density, 1.0)
+    theta = theta_for(hint, th_or if k_or else math.nan)
+    if k_or == 0:
+        th_or = theta  # nothing selected: theta comes back unchanged
     gbuf = torch.empty(N + 4, dtype=torch.float32, device=DEV)
     g_dev = gbuf[phase_shift:phase_shift + N]
     g_dev.copy_(torch.from_numpy(g))
@@ -58,21 +96,33 @@ def topk_vs_oracle(g, res, rank, world, density, variant=AUTO, phase_shift=0, sp
     out_idx = torch.full((max(1, ln) + 8,), sentinel, dtype=torch.int32, device=DEV)
     out_val = torch.full((max(1, ln) + 8,), float(sentinel), dtype=torch.float32, device=DEV)
     k, th, idx, val = sp.step(g_dev, r_dev, rank, world, density, theta, out_idx, out_val)
-    r_or = res.copy()
-    o_idx, o_val, k_or, th_or = oracle.topk_step(g, r_or, rank, world, density, theta)
-    where = f"N={N} rank {rank}/{world} d={density} variant {variant} shift {phase_shift}"
+    route = sp.last_topk_route()
+    where = f"N={N} rank {rank}/{world} d={density} variant {variant} shift {phase_shift} hint {hint} route {route}"
     assert k == k_or, f"{where}: k {k} oracle {k_or}"
-    assert th == th_or, f"{where}: kth {th!r} oracle {th_or!r}"
+    assert th == th_or or (math.isnan(th) and math.isnan(th_or)), f"{where}: kth {th!r} oracle {th_or!r}"
     assert np.array_equal(idx.cpu().numpy(), o_idx), f"{where}: indices differ"
     assert same_bits(val.cpu().numpy(), o_val), f"{where}: values differ"
     assert same_bits(r_dev.cpu().numpy(), r_or), f"{where}: residual differs"
-    # the step lists at most every value from the floor of the k-th
-    # magnitude's first radix bin (its top 11 magnitude bits) up; past them
-    # nothing is written
+    # Without a hint the step lists at most every value from the floor of
+    # the k-th magnitude's first radix bin (its top 11 magnitude bits) up;
+    # with one, every value from the hint's bound up, and the pick then
+    # writes the top k.  Past that nothing is written.
     acc = (g[s:s + ln] + res[s:s + ln]).astype(np.float32)
     keys = acc.view(np.uint32) & np.uint32(0x7FFFFFFF)
-    floor = np.uint32(np.float32(th_or).view(np.uint32) & np.uint32(0x7FF00000))
-    reach = int(np.sum((keys >= floor) & (keys <= np.uint32(0x7F800000)))) if k_or else 0
+    finite = keys <= np.uint32(0x7F800000)
+    usable = (variant != TICKET and ln >= 8 and topk_k(density, ln) <= ln // 8 and 0 < theta < math.inf
+              and float(theta) * 0.875 <= float(np.finfo(np.float32).max) and hint_bound(theta) > 0)
+    assert (route in HINT_ROUTES) == usable, where
+    if route in HINT_ROUTES:
+        low = np.uint32(hint_bound(theta).view(np.uint32))
+        reach = max(int(np.sum((keys >= low) & finite)), k_or)
+        if route == micro.MICRO_TOPK_ROUTE_HINT_LIST:
+            assert int(np.sum((keys >= low) & finite)) >= k_or, where
+    else:
+        floor = np.uint32(np.float32(th_or).view(np.uint32) & np.uint32(0x7FF00000))
+        reach = int(np.sum((keys >= floor) & finite)) if k_or else 0
+    if hint == "high" and route in HINT_ROUTES:
+        assert route == micro.MICRO_TOPK_ROUTE_HINT_PICK, where
     assert np.all(out_idx.cpu().numpy()[reach:] == sentinel), f"{where}: written past the selection"
     if own:
         sp.close()
@@ -95,33 +145,38 @@ def gen(rng, n, kind):
 ])
 @pytest.mark.parametrize("density", [1e-4, 0.01, 0.5, 1.0])
 @VARIANTS
-def test_ragged_sizes_and_densities(N, world, rank, density, variant):
+@HINTS
+def test_ragged_sizes_and_densities(N, world, rank, density, variant, hint):
     rng = np.random.default_rng(N * 3 + rank + int(density * 1e4))
     g, res = gen(rng, N, "normal")
-    topk_vs_oracle(g, res, rank, world, density, variant)
+    topk_vs_oracle(g, res, rank, world, density, variant, hint=hint)
 
 
 @pytest.mark.parametrize("N", [5000, 1 << 20, (1 << 20) + 3, 3_000_017])
 @pytest.mark.parametrize("density", [0.01, 0.3])
 @pytest.mark.parametrize("kind", ["quantised", "laplace"])
 @pytest.mark.parametrize("phase_shift", [0, 1])
-def test_equal_magnitudes_and_phases(N, density, kind, phase_shift):
+@pytest.mark.parametrize("hint", ["none", "exact", "high"])
+def test_equal_magnitudes_and_phases(N, density, kind, phase_shift, hint):
     """Quantised values put thousands of values at the k-th magnitude, so the
-    trim pass runs over long lists; phase 1 takes the scalar-load passes."""
-    note(f"top-k ties N={N} d={density} {kind} shift {phase_shift}")
+    trim pass runs over long lists; phase 1 takes the scalar-load passes (and
+    a residual of another 16-byte phase than the gradient's for the pick's
+    passes)."""
+    note(f"top-k ties N={N} d={density} {kind} shift {phase_shift} hint {hint}")
     rng = np.random.default_rng(N + int(density * 100) + len(kind))
     g, res = gen(rng, N, kind)
-    topk_vs_oracle(g, res, 0, 1, density, AUTO, phase_shift)
+    topk_vs_oracle(g, res, 0, 1, density, AUTO, phase_shift, hint=hint)
 
 
 @VARIANTS
 def test_all_values_equal(variant):
     """Every value ties: the k lowest indices, the rest returned to the residual."""
-    for N, d in [(10, 0.3), (4097, 0.01), (2_000_003, 0.25)]:
+    for N, d in [(10, 0.3), (4097, 0.01), (2_000_003, 0.25), (2_000_003, 0.01)]:
         g = np.full(N, -0.5, np.float32)
         res = np.zeros(N, np.float32)
-        k = topk_vs_oracle(g, res, 0, 1, d, variant)
-        assert k == oracle.topk_count(d, N)
+        for hint in ["none", "exact", "high", "low"]:
+            k = topk_vs_oracle(g, res, 0, 1, d, variant, hint=hint)
+            assert k == oracle.topk_count(d, N)
 
 
 @VARIANTS
@@ -132,36 +187,112 @@ def test_special_values(variant):
     g = np.tile(base, 1000)
     res = np.tile(np.array([0.0, 0.0, 0.0, -0.0, 0.0, tiny, 0.0, 0.0, -tiny, np.nan], np.float32), 1000)
     for d in [1e-4, 0.05, 0.2, 0.35, 0.7, 1.0]:  # infinities only, then magnitude 3 ... up to every non-NaN value
-        topk_vs_oracle(g, res, 0, 1, d, variant)
+        for hint in ["none", "exact", "high", "low", 1e-45, 3e38, -1.0, 0.0, math.inf]:
+            topk_vs_oracle(g, res, 0, 1, d, variant, hint=hint)
     # more NaN than the selection leaves: fewer than k selected
     g2 = g.copy()
     g2[::3] = np.nan
     topk_vs_oracle(g2, res, 0, 1, 1.0, variant)
     # every value NaN: nothing selected, theta unchanged, residual = acc
     g3 = np.full(5000, np.nan, np.float32)
-    k = topk_vs_oracle(g3, np.zeros(5000, np.float32), 0, 1, 0.5, variant, theta=7.25)
-    assert k == 0
+    for d, theta in [(0.5, 7.25), (0.01, 7.25), (0.01, 1e-30)]:
+        k = topk_vs_oracle(g3, np.zeros(5000, np.float32), 0, 1, d, variant, hint=theta)
+        assert k == 0
     # zeros only: the k-th magnitude is 0, the lowest indices win
-    k = topk_vs_oracle(np.zeros(3000, np.float32), np.zeros(3000, np.float32), 0, 1, 0.1, variant)
-    assert k == 300
+    for hint in ["none", 1.0]:
+        k = topk_vs_oracle(np.zeros(3000, np.float32), np.zeros(3000, np.float32), 0, 1, 0.1, variant, hint=hint)
+        assert k == 300
 
 
 def test_one_context_many_calls():
     """The radix-select counters and state are left clean by every call: a
-    context alternating sizes, partitions, densities and the nothing-selected
-    case stays exact."""
+    context alternating sizes, partitions, densities, hints and the
+    nothing-selected case stays exact."""
     N = 300_007
     sp = make(N)
     rng = np.random.default_rng(99)
-    for t in range(24):
+    for t in range(48):
         kind = ["normal", "quantised", "laplace"][t % 3]
         g, res = gen(rng, N, kind)
         world = [1, 3, 8][t % 3]
         rank = t % world
-        d = [0.001, 0.02, 0.5, 1.0][t % 4]
+        d = [0.001, 0.02, 0.5, 1.0, 0.01][t % 5]
         if t % 7 == 6:
             g[:] = np.nan
-        topk_vs_oracle(g, res, rank, world, d, sp=sp)
+        topk_vs_oracle(g, res, rank, world, d, sp=sp, hint=["exact", "none", "high", "low"][t % 4])
+    sp.close()
+
+
+@pytest.mark.parametrize("hint", ["exact", "high", "low"])
+def test_hint_routes_are_taken(hint):
+    """A 2M-value partition at d = 0.01 (k = 20,000): with the exact k-th
+    magnitude as the hint the step at 7/8 of it lists at least k values and the
+    passes run over that list; with 8 times it the step lists fewer than k
+    and the pick runs over the residual; with 1/1024 of it the step lists
+    about half the partition, more than the staging pairs hold, and the pick
+    runs too."""
+    N = 2_000_003
+    rng = np.random.default_rng(7)
+    g, res = gen(rng, N, "normal")
+    sp = make(N)
+    topk_vs_oracle(g, res, 0, 1, 0.01, sp=sp, hint=hint)
+    want = {"exact": micro.MICRO_TOPK_ROUTE_HINT_LIST, "high": micro.MICRO_TOPK_ROUTE_HINT_PICK,
+            "low": micro.MICRO_TOPK_ROUTE_HINT_PICK}[hint]
+    assert sp.last_topk_route() == want
+    topk_vs_oracle(g, res, 0, 1, 0.01, sp=sp, hint="none")
+    assert sp.last_topk_route() == micro.MICRO_TOPK_ROUTE_LIST
+    sp.close()
+
+
+@VARIANTS
+@HINTS
+def test_hint_with_dense_tiles(variant, hint):
+    """A block of 100,000 large values in a 1M-value partition, k = 40,000:
+    at the hint's bound most values of the block are listed, so its tiles
+    overflow their staging slots and the move kernel redoes them, with the
+    residual set to +0 only from the hint up."""
+    N = 1_000_003
+    rng = np.random.default_rng(31)
+    g = (0.01 * rng.standard_normal(N)).astype(np.float32)
+    g[200_000:300_000] = rng.uniform(1.0, 2.0, 100_000).astype(np.float32) * np.where(
+        rng.random(100_000) < 0.5, -1, 1).astype(np.float32)
+    res = (0.001 * rng.standard_normal(N)).astype(np.float32)
+    sp = make(N, variant)
+    topk_vs_oracle(g, res, 0, 1, 40_000 / N, variant, sp=sp, hint=hint)
+    if variant != TICKET:
+        _, redone, _, _ = sp.last_stats()
+        if hint in ("exact", "low"):
+            assert redone > 0
+    sp.close()
+
+
+@pytest.mark.parametrize("N,world", [(100_003, 4), (3_000_017, 8)])
+def test_ef_steps_passing_theta_on(N, world):
+    """Algorithm 1's pass with the top-k comparator over several iterations,
+    each call given the k-th magnitude the last one returned (the hint), on
+    both sides."""
+    rng = np.random.default_rng(N + 1)
+    sp = make(N)
+    g_dev = torch.empty(N, dtype=torch.float32, device=DEV)
+    r_dev = torch.zeros(N, dtype=torch.float32, device=DEV)
+    r_host = np.zeros(N, np.float32)
+    theta = 1.0
+    routes = []
+    for t in range(6):
+        g = (rng.laplace(0, 1e-3, N) * (1.0 + 0.5 * t)).astype(np.float32)
+        g_dev.copy_(torch.from_numpy(g))
+        k, th, c, idx, val = sp.ef_step(g_dev, r_dev, t, 2, world, 0.01, theta)
+        routes.append(sp.last_topk_route())
+        o_idx, o_val, k_or, th_or, c_or = oracle.topk_ef_step(g, r_host, t, 2, world, 0.01, theta)
+        assert (k, th, c) == (k_or, th_or, c_or)
+        assert np.array_equal(idx.cpu().numpy(), o_idx)
+        assert same_bits(val.cpu().numpy(), o_val)
+        assert same_bits(r_dev.cpu().numpy(), r_host)
+        theta = th_or
+    # 1.0 is far above the k-th magnitude at first: the pick; then the last
+    # k-th magnitude is a hint the step's list covers
+    assert routes[0] == micro.MICRO_TOPK_ROUTE_HINT_PICK
+    assert micro.MICRO_TOPK_ROUTE_HINT_LIST in routes[1:]
     sp.close()
 
 
