@@ -355,7 +355,11 @@ micro::TopkTrimScratch trim_scratch(const micro_ctx* ctx, int64_t n) {
 }
 
 // Workgroups of a histogram pass over n values: enough for the device, at
-// most four per compute unit (each thread loops).
+// most four per compute unit (each thread loops).  Each workgroup adds its
+// nonzero counters (up to 2048) to the global ones, so a pass over a short
+// list takes fewer workgroups with more values each (kTopkListPerThread).
+constexpr int64_t kTopkListPerThread = 16;
+
 uint32_t topk_blocks(const micro_ctx* ctx, int64_t n, int64_t values_per_thread) {
     const int64_t per_block = static_cast<int64_t>(micro::kTopkHistBlock) * values_per_thread;
     const int64_t blocks = std::min<int64_t>((n + per_block - 1) / per_block, 4 * ctx->compute_units);
@@ -473,7 +477,7 @@ hipError_t topk_after_step(micro_ctx* ctx, const TopkPlan& plan, int32_t* out_id
         t.k = static_cast<uint32_t>(plan.kept);  // read by pass 0 only
         t.words = ctx->d_topk;
         t.host = ctx->h_topk_dev;
-        t.blocks = topk_blocks(ctx, plan.listed, 4);
+        t.blocks = topk_blocks(ctx, plan.listed, kTopkListPerThread);
         ctx->h_topk[5] = 0;  // the device last wrote it in the first pass's select, which has been waited for
         if ((e = micro::launch_topk_passes(t, micro::TopkSource::kList, 1, 2, ctx->stream)) != hipSuccess) return e;
     }
@@ -506,7 +510,7 @@ micro_status topk_after_hint(micro_ctx* ctx, TopkPlan* plan, int64_t listed, flo
         plan->trim = listed > k;
         t.list = out_val;
         t.list_n = listed;
-        t.blocks = topk_blocks(ctx, listed, 4);
+        t.blocks = topk_blocks(ctx, listed, kTopkListPerThread);
         if ((e = micro::launch_topk_passes(t, micro::TopkSource::kList, 0, 2, ctx->stream)) != hipSuccess)
             return hip_fail(ctx, e, "top-k pass launch");
         if (plan->trim) {
