@@ -123,7 +123,12 @@ class Sparsifier:
                 and t.get_device() == self.device.index and t.is_contiguous())
 
     def step(self, grad, residual, rank, world, density, theta, out_idx=None, out_val=None):
-        """One sparsify step; returns (k, theta_next, idx[:k], val[:k])."""
+        """One sparsify step; returns (k, theta_next, idx[:k], val[:k]).
+
+        idx and val are views of out_idx / out_val; without them, of this
+        Sparsifier's own output buffers, which the next call overwrites: pass
+        buffers of your own (or clone the views) to keep a step's selection
+        while the next one runs."""
         if self._ctx is None:
             raise RuntimeError("Sparsifier is closed")
         length = self._length(rank, world)
@@ -158,7 +163,8 @@ class Sparsifier:
         value accumulates, the partition of the worker's cycle is searched.
         Returns (k, theta_next, cycle, idx[:k], val[:k]); with local_error,
         (k, theta_next, cycle, idx[:k], val[:k], sumsq) where sumsq is the
-        squared norm of the whole new residual."""
+        squared norm of the whole new residual.  idx and val are views of the
+        output buffers, as in step."""
         if self._ctx is None:
             raise RuntimeError("Sparsifier is closed")
         length = self._length(_lib.micro_cycle(t, worker, world), world)
