@@ -23,7 +23,9 @@ constexpr int kUnionBlock = 256;
 // nothing.  The contiguous streams (the union indices, the sums, the outputs)
 // and the scattered stores are non-temporal, since nothing here reads them
 // again; that took another 3-5% off both kernels.  The scattered reads stay
-// ordinary loads: non-temporal ones were 25% slower.
+// ordinary loads: non-temporal ones were 25% slower.  The gather's reset store
+// follows its read at once instead of the output store that waits for the
+// read's value (81.2 against 77.5-79.4 us on that union).
 constexpr int kUnionPerThread = 1;
 
 // The worker's own selection occupies union positions [own_first,
@@ -49,12 +51,15 @@ __global__ __launch_bounds__(kUnionBlock) void union_gather_kernel(float* residu
     for (int u = 0; u < kUnionPerThread; ++u) {
         const int64_t q = first + static_cast<int64_t>(u) * kUnionBlock;
         v[u] = own[u] ? own_val[q - own_first] : (j[u] >= 0 ? residual[j[u]] : __builtin_nanf(""));
+        // the reset goes out right behind the read of the same value (one
+        // thread's accesses to one address are performed in order), without
+        // waiting for the value to come back
+        if (j[u] >= 0) __builtin_nontemporal_store(0.0f, residual + j[u]);
     }
 #pragma unroll
     for (int u = 0; u < kUnionPerThread; ++u) {
         const int64_t q = first + static_cast<int64_t>(u) * kUnionBlock;
         if (q < m) __builtin_nontemporal_store(v[u], out + q);
-        if (j[u] >= 0) __builtin_nontemporal_store(0.0f, residual + j[u]);
     }
 }
 
