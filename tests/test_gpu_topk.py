@@ -244,6 +244,29 @@ def test_hint_routes_are_taken(hint):
     sp.close()
 
 
+@pytest.mark.parametrize("seed", range(64))
+def test_fuzz_sizes_densities_and_hints(seed):
+    """Random partition sizes and ranks, densities from 1e-4 to 0.3, value
+    kinds, schedules, grad phases and hints (the kinds above or any positive
+    number), each case bit for bit against the oracle."""
+    rng = np.random.default_rng(1000 + seed)
+    N = int(rng.integers(1, 3_000_000))
+    world = int(rng.choice([1, 2, 3, 8, 16]))
+    rank = int(rng.integers(0, world))
+    density = float(10 ** rng.uniform(-4, np.log10(0.3)))
+    kind = str(rng.choice(["normal", "quantised", "laplace"]))
+    variant = int(rng.choice([AUTO, STAGED, SEPARATE, TICKET]))
+    hint = rng.choice(["none", "exact", "high", "low", "random"])
+    if hint == "random":
+        hint = float(10 ** rng.uniform(-6, 2))
+    g, res = gen(rng, N, kind)
+    if rng.random() < 0.2:  # a sprinkle of special values
+        pos = rng.integers(0, N, size=max(1, N // 1000))
+        g[pos] = rng.choice(np.array([np.nan, np.inf, -np.inf, 0.0, -0.0], np.float32), size=pos.size)
+    note(f"top-k fuzz seed {seed}: N={N} rank {rank}/{world} d={density:.3g} {kind} variant {variant} hint {hint}")
+    topk_vs_oracle(g, res, rank, world, density, variant, phase_shift=int(rng.integers(0, 4)), hint=hint)
+
+
 @VARIANTS
 @HINTS
 def test_hint_with_dense_tiles(variant, hint):
