@@ -316,6 +316,28 @@ def test_ef_local_error_ragged(N, world, phase_shift):
             ef_norm_vs_oracle(g, res, t, worker, world, 0.05, 1.5, phase_shift)
 
 
+@pytest.mark.parametrize("seed", range(24))
+def test_ef_fuzz(seed):
+    """Random vector lengths up to 3M, worlds up to 16, iterations and
+    workers (so any cyclic partition), thresholds, densities and phases, with
+    and without the local error."""
+    rng = np.random.default_rng(7000 + seed)
+    N = int(rng.integers(1, 3_000_000))
+    world = int(rng.integers(1, 17))
+    t = int(rng.integers(0, 3 * world))
+    worker = int(rng.integers(0, world))
+    g = (rng.standard_normal(N) * rng.uniform(0.1, 3)).astype(np.float32)
+    res = (rng.standard_normal(N) * rng.uniform(0.0, 2)).astype(np.float32)
+    theta = float(np.exp(rng.uniform(-3, 2)))
+    density = float(rng.choice([0.001, 0.01, 0.1]))
+    phase = int(rng.integers(0, 4))
+    note(f"ef fuzz seed {seed}: N={N} t={t} worker {worker}/{world} theta {theta:.4g} d={density} phase {phase}")
+    if seed % 2:
+        ef_norm_vs_oracle(g, res, t, worker, world, density, theta, phase)
+    else:
+        ef_gpu_vs_oracle(g, res, t, worker, world, density, theta, phase)
+
+
 def test_ef_local_error_special_values():
     """Infinities outside the partition are accumulated, never selected; the
     norm is then infinite; a NaN makes it NaN."""

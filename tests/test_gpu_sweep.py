@@ -114,6 +114,23 @@ def test_sweep_ragged_sizes_worlds_and_phases(N, world, phase_shift):
     check_sweep(g, res, world, 0.02, thetas, phase_shift, where=f"N={N} world={world}")
 
 
+@pytest.mark.parametrize("seed", range(24))
+def test_sweep_fuzz(seed):
+    """Random vector lengths up to 3M, worlds up to 64 (segments of every
+    size, empty ones included), thresholds per partition spread over two
+    decades (from near-empty to dense selections), densities and phases."""
+    rng = np.random.default_rng(5000 + seed)
+    N = int(rng.integers(1, 3_000_000))
+    world = int(rng.integers(1, 65))
+    g = (rng.standard_normal(N) * np.exp(rng.uniform(-1.5, 1.5, N))).astype(np.float32)
+    res = (rng.standard_normal(N) * rng.uniform(0.0, 1.0)).astype(np.float32)
+    thetas = list(np.exp(rng.uniform(-1.5, 3.0, world)))
+    density = float(rng.choice([0.001, 0.01, 0.1]))
+    phase = int(rng.integers(0, 4))
+    note(f"sweep fuzz seed {seed}: N={N} world={world} d={density} phase {phase}")
+    check_sweep(g, res, world, density, thetas, phase, where=f"seed {seed} N={N} world={world}")
+
+
 def test_sweep_dense_partitions_and_specials():
     """Some partitions select almost everything (tiles redone by the move
     kernel inside several segments), one holds NaN (its norm is NaN), one
