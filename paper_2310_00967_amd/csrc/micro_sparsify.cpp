@@ -507,7 +507,9 @@ micro_status topk_after_hint(micro_ctx* ctx, TopkPlan* plan, int64_t listed, flo
     hipError_t e;
     if (listed >= k && trim_scratch(ctx, listed).temp) {
         plan->route = TopkRoute::kHintList;
-        plan->trim = listed > k;
+        // with nothing to drop (listed == k) the trim still sets to +0 the
+        // residual of kept values the step left at acc (below zero_key)
+        plan->trim = listed > k || plan->zero_key > plan->threshold_key;
         t.list = out_val;
         t.list_n = listed;
         t.blocks = topk_blocks(ctx, listed, kTopkListPerThread);

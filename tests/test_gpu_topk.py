@@ -267,6 +267,24 @@ def test_fuzz_sizes_densities_and_hints(seed):
     topk_vs_oracle(g, res, rank, world, density, variant, phase_shift=int(rng.integers(0, 4)), hint=hint)
 
 
+@pytest.mark.parametrize("variant", [AUTO, STAGED, SEPARATE], ids=["auto", "staged", "separate"])
+def test_hint_list_of_exactly_k_below_the_hint(variant):
+    """k values of 9.0 among small ones and a hint of 10: the step lists from
+    8.75 up, exactly the k values, all of them below the hint, so the staged
+    step left acc in their residual; with nothing to drop, the trim still has
+    to set their residual to +0."""
+    N = (1 << 20) + 5003
+    rng = np.random.default_rng(77)
+    g = (0.1 * rng.standard_normal(N)).astype(np.float32)
+    k = oracle.topk_count(0.01, N)
+    g[rng.choice(N, size=k, replace=False)] = np.float32(9.0)
+    res = np.zeros(N, np.float32)
+    sp = make(N, variant)
+    topk_vs_oracle(g, res, 0, 1, 0.01, variant, sp=sp, hint=10.0)
+    assert sp.last_topk_route() == micro.MICRO_TOPK_ROUTE_HINT_LIST
+    sp.close()
+
+
 @VARIANTS
 @HINTS
 def test_hint_with_dense_tiles(variant, hint):
