@@ -285,6 +285,45 @@ def test_hint_list_of_exactly_k_below_the_hint(variant):
     sp.close()
 
 
+@pytest.mark.parametrize("seed", range(40))
+def test_hint_bounds_adversarial(seed):
+    """Magnitudes just below, at and just above the step's two bounds for a
+    hint of 1 (7/8, where it lists from, and 1, where it zeroes from), with
+    random multiplicities and signs; k falls on, next to or between the
+    groups, so the k-th magnitude meets either bound, the list holds exactly
+    k values or far more, and ties at the k-th magnitude straddle the
+    bounds."""
+    rng = np.random.default_rng(9000 + seed)
+    f = np.float32
+    b, z = f(0.875), f(1.0)
+    mags = np.array([f(0.5), np.nextafter(b, f(0)), b, f(0.9), np.nextafter(z, f(0)), z,
+                     np.nextafter(z, f(2)), f(1.5), f(3.0)], np.float32)
+    counts = rng.integers(1, 3000, size=mags.size)
+    counts[0] += 200_000  # the bulk below both bounds (k stays within an eighth of the partition)
+    if seed % 7 == 6:
+        counts[rng.integers(1, mags.size - 1)] = 0
+    vals = np.repeat(mags, counts)
+    vals *= np.where(rng.random(vals.size) < 0.5, f(-1), f(1))
+    rng.shuffle(vals)
+    N = vals.size
+    # k on the boundary of group `edge` (counting from the largest
+    # magnitudes: k takes the groups above it whole), one below or above it,
+    # or anywhere
+    tops = np.cumsum(counts[::-1])[:-1]
+    edge, choice = seed % tops.size, (seed // tops.size) % 4
+    k = int(tops[edge]) + (0, -1, 1, 0)[choice]
+    if choice == 3:
+        k = int(rng.integers(1, N // 8 + 1))
+    k = max(1, min(N // 8, k))
+    density = (k + 0.5) / N
+    assert oracle.topk_count(density, N) == k
+    g = vals.astype(np.float32)
+    res = np.zeros(N, np.float32)
+    variant = [STAGED, SEPARATE, AUTO][seed % 3]
+    note(f"top-k bounds seed {seed}: N={N} k={k} counts {counts.tolist()} variant {variant}")
+    topk_vs_oracle(g, res, 0, 1, density, variant, hint=1.0)
+
+
 @VARIANTS
 @HINTS
 def test_hint_with_dense_tiles(variant, hint):
