@@ -83,6 +83,10 @@ def parse_args():
                          "local-error norms; ceiling: vendor streams (torch's in-place add, a device "
                          "copy) beside the step on the same vector; topk: the exact top-k comparator "
                          "beside the threshold step and the hard-threshold rule on the same gradients")
+    ap.add_argument("--topk-hint", choices=["last", "none", "high"], default="last",
+                    help="with --path topk: the theta each top-k call gets: the k-th magnitude the last call "
+                         "returned (default), NaN (no hint: the passes over the partition first), or 8 times the "
+                         "last one (too high: the step lists fewer than k and the pick runs over the residual)")
     ap.add_argument("--topk-only", action="store_true",
                     help="with --path topk: the top-k rule alone (its HBM counters then cover only its kernels)")
     ap.add_argument("--local-error", action="store_true",
@@ -371,7 +375,7 @@ def measure_ef(w, density, pool, sp, warmup, steps, local_error=False):
             "k_avg": sum(k for _, k, _ in log) / len(log), "worker": worker, "fused": fused}
 
 
-def measure_topk(w, density, pool, warmup, steps, only_topk=False):
+def measure_topk(w, density, pool, warmup, steps, only_topk=False, hint="last"):
     """The exact top-k comparator (MICRO_RULE_TOPK) on partition w.ranks[0],
     beside the threshold step (the default rule) and the hard-threshold rule
     (Sec. 1's comparators) on the same gradients, each with its own residual
@@ -408,7 +412,14 @@ def measure_topk(w, density, pool, warmup, steps, only_topk=False):
             if t == warmup:
                 torch.cuda.synchronize()
                 t0 = time.perf_counter()
-            k, theta, _, _ = sp.step(pool[t % len(pool)], res, rank, w.world, density, theta, out_idx, out_val)
+            theta_in = theta
+            if rule == micro.MICRO_RULE_TOPK and hint != "last":
+                theta_in = float("nan") if hint == "none" else 8.0 * theta
+            k, theta_out, _, _ = sp.step(pool[t % len(pool)], res, rank, w.world, density, theta_in, out_idx,
+                                         out_val)
+            # a top-k call with no hint hands back the theta it got when it
+            # selects nothing; keep the last k-th magnitude for the next call
+            theta = theta_out if not (rule == micro.MICRO_RULE_TOPK and theta_out != theta_out) else theta
             ks.append(k)
             if t >= warmup:
                 ms.append(sp.last_stats()[0])
@@ -894,18 +905,21 @@ def main_path(args, w, head, pool, n_pool, sp):
            "density": head, "distribution": w.dist, "gradient_pool": n_pool,
            "parallelism": "one worker on one GPU", "path": args.path}
     if args.path == "topk":
-        r = measure_topk(w, head, pool, args.warmup, args.steps, args.topk_only)
+        r = measure_topk(w, head, pool, args.warmup, args.steps, args.topk_only, args.topk_hint)
         cpu = cpu_baseline_topk(w, head, pool, args.cpu_seconds) if args.cpu_seconds > 0 else None
         rank, start, ln = r.pop("partition")
-        cfg.update({"rank": rank, "partition_len": ln, "parallelism": "one worker's partition on one GPU"})
+        cfg.update({"rank": rank, "partition_len": ln, "parallelism": "one worker's partition on one GPU",
+                    "topk_hint": args.topk_hint})
         tk = r["topk"]
         line = {"metric": "exact top-k comparator throughput (G elem/s of the partition), beside the threshold step",
                 "value": tk["g_elem_s"], "unit": "G elem/s", "ms_per_step": tk["ms_per_step"], **common,
                 "config": cfg, "k_avg": tk["k_avg"],
                 "roofline": {"bound": "hbm", "achieved": tk["kernel_gbs"], "peak": HBM_PEAK_GBS, "unit": "GB/s",
                              "frac": tk["frac"],
-                             "traffic": read_traffic(TRAFFIC_FILE_TOPK, f"{w.name} world {w.world} rank {rank} topk d={head}",
-                                                     sources=TOPK_SOURCES),
+                             "traffic": (read_traffic(TRAFFIC_FILE_TOPK,
+                                                      f"{w.name} world {w.world} rank {rank} topk d={head}",
+                                                      sources=TOPK_SOURCES)
+                                         if args.topk_hint == "last" else None),
                              "kernel": "the threshold step at 7/8 of the incoming theta (the last step's k-th "
                                        "magnitude), the wait, three topk_hist_kernel + topk_select_kernel passes "
                                        "over its output list and the trim (route_series 3; 4: the list fell short "
