@@ -96,8 +96,8 @@ typedef enum micro_status {
                              and the passes run over its output list, which
                              a trim then cuts to the top k; if that list holds
                              fewer than k values, they go back into the
-                             residual and the passes and a pick of the top k
-                             run over the partition's residual.  Without one
+                             residual and the select starts over on the
+                             partition's residual.  Without one
                              the passes run over the partition first (waited
                              for), then the step at the k-th magnitude or at
                              the floor of its first digit, then the passes
@@ -105,8 +105,10 @@ typedef enum micro_status {
 #define MICRO_TOPK_ROUTE_FULL 1      /* micro_step_stats.topk_route: three passes over the partition, then the step */
 #define MICRO_TOPK_ROUTE_LIST 2      /* one pass over the partition, the step, two passes over its list */
 #define MICRO_TOPK_ROUTE_HINT_LIST 3 /* the step at the hint's bound, three passes over its list */
-#define MICRO_TOPK_ROUTE_HINT_PICK 4 /* the step at the hint's bound listed fewer than k: the passes and
-                                        the pick over the residual */
+#define MICRO_TOPK_ROUTE_HINT_PICK 4 /* the step at the hint's bound listed fewer than k: one pass over the
+                                        residual, then the values from the k-th magnitude's first-digit bin
+                                        up extracted and two passes over them (or the passes and a pick
+                                        over the residual) */
 
 /* Kernel schedules (both compute the same result). */
 #define MICRO_VARIANT_AUTO 0   /* per call, the faster measured schedule: TICKET

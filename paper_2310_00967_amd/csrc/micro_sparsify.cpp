@@ -310,8 +310,10 @@ float float_from_bits(uint32_t b) {
 // few residual values to change.  When it lists at least k values (and the
 // staging pairs hold them), the three histogram passes run over that list and
 // the trim cuts it to the top k (kHintList); else the list goes back into the
-// residual, which then holds acc over the partition, and the passes and the
-// pick run over the residual (kHintPick).
+// residual, which then holds acc over the partition, a first pass runs over
+// the residual and either the values from the k-th magnitude's first-digit
+// bin up are extracted into the list for the other passes and the trim, or
+// (a long list) the passes and the pick run over the residual (kHintPick).
 // Without a hint every route starts with the first histogram pass over the
 // partition (waited for).  The full route runs the other two passes over the
 // partition too (waited for), then the threshold step at the exact k-th
@@ -491,9 +493,9 @@ hipError_t topk_after_step(micro_ctx* ctx, const TopkPlan& plan, int32_t* out_id
 
 // After the step at the hint's bound listed `listed` values (waited for):
 // with at least k of them, and room for the trim, the three passes run over
-// that list and the trim cuts it to the top k; else the list goes back into
-// the residual and the passes and the pick run over the partition's
-// residual, which then holds acc.  Enqueues only.
+// that list and the trim cuts it to the top k (enqueued only); else the list
+// goes back into the residual, which then holds acc over the partition, and
+// the select starts over on it (one more wait).
 micro_status topk_after_hint(micro_ctx* ctx, TopkPlan* plan, int64_t listed, float* residual, int64_t start,
                              int64_t len, double density, int32_t* out_idx, float* out_val) {
     const int64_t k = topk_count(density, len);
@@ -544,7 +546,45 @@ micro_status topk_after_hint(micro_ctx* ctx, TopkPlan* plan, int64_t listed, flo
     t.body_first = start + head;
     t.body_end = t.body_first + ((t.end - t.body_first) / 4) * 4;
     t.blocks = topk_blocks(ctx, len, 8);
-    if ((e = micro::launch_topk_passes(t, micro::TopkSource::kResidual, 0, 2, ctx->stream)) != hipSuccess)
+    // The first pass over the residual (waited for) gives the k-th
+    // magnitude's first-digit bin.  If everything from the bin's floor up is
+    // short, it is extracted into the output list and the other two passes
+    // and the trim run over that list; else they and the pick run over the
+    // residual.
+    volatile int64_t* h = ctx->h_topk;
+    if ((e = micro::launch_topk_passes(t, micro::TopkSource::kResidual, 0, 0, ctx->stream)) != hipSuccess)
+        return hip_fail(ctx, e, "top-k pass launch");
+    if ((e = hipStreamSynchronize(ctx->stream)) != hipSuccess) return hip_fail(ctx, e, "hipStreamSynchronize");
+    if (h[5] == 2) return MICRO_OK;  // every value is NaN
+    const int64_t bin = h[0], greater0 = h[1], in_bin = h[2], remaining = h[3], valid = h[4];
+    const int64_t kept = std::min(k, valid);
+    const int64_t bin_width = int64_t(1) << micro::kTopkFirstShift;
+    if (h[5] != 3 || bin < 0 || bin > micro::kTopkKeyMax || bin % bin_width != 0 || remaining < 1 ||
+        remaining > in_bin || greater0 < 0 || greater0 + remaining != kept || greater0 + in_bin > len)
+        return topk_inconsistent(ctx, "first pass over the residual");
+    const int64_t extracted = greater0 + in_bin;
+    h[5] = 0;
+    if (extracted <= len / 4 && trim_scratch(ctx, extracted).temp) {
+        if ((e = micro::launch_topk_extract(residual, start, start + len, static_cast<uint32_t>(bin), out_idx, out_val,
+                                            ctx->d_tile_counts, ctx->stream)) != hipSuccess)
+            return hip_fail(ctx, e, "top-k extract launch");
+        micro::TopkArgs l{};
+        l.k = static_cast<uint32_t>(k);
+        l.words = ctx->d_topk;
+        l.host = ctx->h_topk_dev;
+        l.list = out_val;
+        l.list_n = extracted;
+        l.blocks = topk_blocks(ctx, extracted, kTopkListPerThread);
+        if ((e = micro::launch_topk_passes(l, micro::TopkSource::kList, 1, 2, ctx->stream)) != hipSuccess)
+            return hip_fail(ctx, e, "top-k pass launch");
+        // every extracted value had its residual set to +0
+        const micro::TopkTrimScratch scratch = trim_scratch(ctx, extracted);
+        if ((e = micro::launch_topk_trim(out_idx, out_val, residual, extracted, kept, static_cast<uint32_t>(bin),
+                                         ctx->d_topk, ctx->h_topk_dev, &scratch, ctx->stream)) != hipSuccess)
+            return hip_fail(ctx, e, "top-k trim launch");
+        return MICRO_OK;
+    }
+    if ((e = micro::launch_topk_passes(t, micro::TopkSource::kResidual, 1, 2, ctx->stream)) != hipSuccess)
         return hip_fail(ctx, e, "top-k pass launch");
     if ((e = micro::launch_topk_pick(residual, start, start + len, out_idx, out_val, ctx->d_topk, ctx->d_tile_counts,
                                      ctx->stream)) != hipSuccess)

@@ -11,8 +11,9 @@
 // (once it holds acc), or from the values of the threshold step's output
 // list, which holds every value at or above the step's threshold.  A trim
 // then drops from that list the values below the k-th magnitude and the
-// surplus of values equal to it; a pick instead takes the top k straight from
-// a residual that holds acc.
+// surplus of values equal to it; a pick instead takes the top k (or an
+// extract every value from a bound up) straight from a residual that holds
+// acc.
 #pragma once
 
 #include <hip/hip_runtime.h>
@@ -115,5 +116,12 @@ hipError_t launch_topk_restore(const int32_t* out_idx, const float* out_val, int
 // k-th key (status other than 1).
 hipError_t launch_topk_pick(float* residual, int64_t start, int64_t end, int32_t* out_idx, float* out_val,
                             const uint32_t* words, uint32_t* counts, hipStream_t stream);
+
+// The same three launches with a fixed rule: every value of [start, end)
+// whose key is at least key_floor (NaN aside) goes to out_idx / out_val in
+// index order and its residual becomes +0 (the output holds at most
+// end - start entries).
+hipError_t launch_topk_extract(float* residual, int64_t start, int64_t end, uint32_t key_floor, int32_t* out_idx,
+                               float* out_val, uint32_t* counts, hipStream_t stream);
 
 }  // namespace micro

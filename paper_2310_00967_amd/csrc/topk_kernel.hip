@@ -561,16 +561,39 @@ __global__ __launch_bounds__(kTrimBlock) void topk_restore_kernel(const int32_t*
     }
 }
 
+// What a pick takes: the values whose key is above `key`, and the first
+// `keep` of those equal to it, NaN aside.  With `words` the key and keep are
+// the last select's (nothing is taken without a k-th key); without, they are
+// the fixed ones here.
+struct PickRule {
+    const uint32_t* words;
+    uint32_t key;
+    int64_t keep;
+};
+
+__device__ __forceinline__ bool pick_rule(const PickRule& r, uint32_t& key, int64_t& keep) {
+    if (r.words) {
+        const uint32_t* state = r.words + kTopkBins;
+        if (state[kTopkStatus] != 1u) return false;
+        key = state[kTopkPrefix];
+        keep = state[kTopkRemaining];
+    } else {
+        key = r.key;
+        keep = r.keep;
+    }
+    return true;
+}
+
 // The pick, launch 1: per chunk of kTopkTrimChunk values of [start, end) of
 // the residual, the values equal to the k-th key (counts[chunk]) and above it,
 // NaN aside (counts[chunks + chunk]).
 __global__ __launch_bounds__(kTrimBlock) void topk_pick_count_kernel(const float* residual, int64_t start,
-                                                                     int64_t end, const uint32_t* words,
+                                                                     int64_t end, PickRule rule,
                                                                      uint32_t* counts, uint32_t chunks) {
     __shared__ uint32_t s_wave[kTrimWaves];
-    const uint32_t* state = words + kTopkBins;
-    if (state[kTopkStatus] != 1u) return;  // uniform
-    const uint32_t key = state[kTopkPrefix];
+    uint32_t key;
+    int64_t keep;
+    if (!pick_rule(rule, key, keep)) return;  // uniform
     const int64_t base = start + static_cast<int64_t>(blockIdx.x) * kTopkTrimChunk;
     float v[kTrimPer];
     load_rows<0>(residual, base, end, __uint_as_float(0xFFFFFFFFu), v);  // padding: a NaN key, neither count
@@ -597,16 +620,15 @@ __global__ __launch_bounds__(kTrimBlock) void topk_pick_count_kernel(const float
 // output at the number of values picked before it, and its residual becomes
 // +0.  The placement never reaches past end - start entries.
 __global__ __launch_bounds__(kTrimBlock) void topk_pick_scatter_kernel(float* residual, int64_t start, int64_t end,
-                                                                       const uint32_t* words,
+                                                                       PickRule rule,
                                                                        const uint32_t* counts, uint32_t chunks,
                                                                        int32_t* out_idx, float* out_val) {
     constexpr int ROWS = kTrimPer * kTrimWaves;
     static_assert(ROWS == kWave, "one (row, wavefront) count per lane of wavefront 0");
     __shared__ uint32_t s_t[ROWS], s_h[ROWS];
-    const uint32_t* state = words + kTopkBins;
-    if (state[kTopkStatus] != 1u) return;  // uniform
-    const uint32_t key = state[kTopkPrefix];
-    const int64_t keep = state[kTopkRemaining];
+    uint32_t key;
+    int64_t keep;
+    if (!pick_rule(rule, key, keep)) return;  // uniform
     const int lane = threadIdx.x & (kWave - 1);
     const int wave = threadIdx.x / kWave;
     const int64_t base = start + static_cast<int64_t>(blockIdx.x) * kTopkTrimChunk;
@@ -743,19 +765,36 @@ hipError_t launch_topk_restore(const int32_t* out_idx, const float* out_val, int
     return hipGetLastError();
 }
 
-hipError_t launch_topk_pick(float* residual, int64_t start, int64_t end, int32_t* out_idx, float* out_val,
-                            const uint32_t* words, uint32_t* counts, hipStream_t stream) {
-    if (!residual || !out_idx || !out_val || !words || !counts || start < 0 || end <= start)
-        return hipErrorInvalidValue;
+namespace {
+
+hipError_t launch_pick(float* residual, int64_t start, int64_t end, int32_t* out_idx, float* out_val,
+                       const PickRule& rule, uint32_t* counts, hipStream_t stream) {
+    if (!residual || !out_idx || !out_val || !counts || start < 0 || end <= start) return hipErrorInvalidValue;
     const int64_t chunks = (end - start + kTopkTrimChunk - 1) / kTopkTrimChunk;
     if (chunks > 0x7FFFFFFFll) return hipErrorInvalidValue;
     const uint32_t nc = static_cast<uint32_t>(chunks);
-    hipLaunchKernelGGL(topk_pick_count_kernel, dim3(nc), dim3(kTrimBlock), 0, stream, residual, start, end, words,
+    hipLaunchKernelGGL(topk_pick_count_kernel, dim3(nc), dim3(kTrimBlock), 0, stream, residual, start, end, rule,
                        counts, nc);
     hipLaunchKernelGGL(topk_trim_scan_kernel, dim3(1), dim3(kTopkTrimBlock), 0, stream, counts, nc);
-    hipLaunchKernelGGL(topk_pick_scatter_kernel, dim3(nc), dim3(kTrimBlock), 0, stream, residual, start, end, words,
+    hipLaunchKernelGGL(topk_pick_scatter_kernel, dim3(nc), dim3(kTrimBlock), 0, stream, residual, start, end, rule,
                        counts, nc, out_idx, out_val);
     return hipGetLastError();
+}
+
+}  // namespace
+
+hipError_t launch_topk_pick(float* residual, int64_t start, int64_t end, int32_t* out_idx, float* out_val,
+                            const uint32_t* words, uint32_t* counts, hipStream_t stream) {
+    if (!words) return hipErrorInvalidValue;
+    return launch_pick(residual, start, end, out_idx, out_val, PickRule{words, 0u, 0}, counts, stream);
+}
+
+hipError_t launch_topk_extract(float* residual, int64_t start, int64_t end, uint32_t key_floor, int32_t* out_idx,
+                               float* out_val, uint32_t* counts, hipStream_t stream) {
+    if (key_floor > kTopkKeyMax) return hipErrorInvalidValue;
+    // every key above the floor, and every one equal to it
+    return launch_pick(residual, start, end, out_idx, out_val,
+                       PickRule{nullptr, key_floor, static_cast<int64_t>(0x7FFFFFFFFFFFFFFFll)}, counts, stream);
 }
 
 }  // namespace micro

@@ -105,22 +105,25 @@ def topk_vs_oracle(g, res, rank, world, density, variant=AUTO, phase_shift=0, sp
     assert same_bits(r_dev.cpu().numpy(), r_or), f"{where}: residual differs"
     # Without a hint the step lists at most every value from the floor of
     # the k-th magnitude's first radix bin (its top 11 magnitude bits) up;
-    # with one, every value from the hint's bound up, and the pick then
-    # writes the top k.  Past that nothing is written.
+    # with one, every value from the hint's bound up; where that list falls
+    # short, the values from the bin's floor up are extracted (or the top k
+    # picked).  Past that nothing is written.
     acc = (g[s:s + ln] + res[s:s + ln]).astype(np.float32)
     keys = acc.view(np.uint32) & np.uint32(0x7FFFFFFF)
     finite = keys <= np.uint32(0x7F800000)
+    bin_floor = np.uint32(np.float32(th_or).view(np.uint32) & np.uint32(0x7FF00000)) if k_or else None
     usable = (variant != TICKET and ln >= 8 and topk_k(density, ln) <= ln // 8 and 0 < theta < math.inf
               and float(theta) * 0.875 <= float(np.finfo(np.float32).max) and hint_bound(theta) > 0)
     assert (route in HINT_ROUTES) == usable, where
     if route in HINT_ROUTES:
         low = np.uint32(hint_bound(theta).view(np.uint32))
         reach = max(int(np.sum((keys >= low) & finite)), k_or)
+        if route == micro.MICRO_TOPK_ROUTE_HINT_PICK and k_or:
+            reach = max(reach, int(np.sum((keys >= bin_floor) & finite)))
         if route == micro.MICRO_TOPK_ROUTE_HINT_LIST:
             assert int(np.sum((keys >= low) & finite)) >= k_or, where
     else:
-        floor = np.uint32(np.float32(th_or).view(np.uint32) & np.uint32(0x7FF00000))
-        reach = int(np.sum((keys >= floor) & finite)) if k_or else 0
+        reach = int(np.sum((keys >= bin_floor) & finite)) if k_or else 0
     if hint == "high" and route in HINT_ROUTES:
         assert route == micro.MICRO_TOPK_ROUTE_HINT_PICK, where
     assert np.all(out_idx.cpu().numpy()[reach:] == sentinel), f"{where}: written past the selection"
