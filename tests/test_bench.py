@@ -113,3 +113,22 @@ def test_more_than_one_gpu_is_refused(n):
     assert r.returncode == 2
     assert "not supported" in r.stderr and "one GPU" in r.stderr
     assert r.stdout == ""
+
+
+def test_paths_default_to_their_workloads_and_the_topk_hint_to_the_last_theta(monkeypatch):
+    """--path topk / ef / union / sweep fall back to the workloads they are
+    measured on (world 1 makes them degenerate), and top-k calls get the last
+    k-th magnitude as their hint unless --topk-hint says otherwise."""
+    cases = [(["--path", "topk"], "bert_large", "last"),
+             (["--path", "topk", "--topk-hint", "high"], "bert_large", "high"),
+             (["--path", "topk", "--workload", "gpt_1p3b", "--topk-hint", "none"], "gpt_1p3b", "none"),
+             (["--path", "sweep"], "resnet18", "last"),
+             (["--path", "ef"], "bert_large", "last"),
+             ([], "gpt_1p3b", "last")]
+    for argv, workload, hint in cases:
+        monkeypatch.setattr(sys, "argv", ["bench.py"] + argv)
+        args = bench.parse_args()
+        assert (args.workload, args.topk_hint) == (workload, hint), argv
+    monkeypatch.setattr(sys, "argv", ["bench.py", "--path", "topk", "--topk-hint", "sometimes"])
+    with pytest.raises(SystemExit):
+        bench.parse_args()
