@@ -215,6 +215,19 @@ def test_union_gather_reset_update_parity(N, world):
     simulate_workers(N, world, 4, seed=N + world)
 
 
+@pytest.mark.parametrize("seed", range(12))
+def test_union_fuzz(seed):
+    """Random vector lengths and worker counts (1 to 16, more workers than
+    values included): the union gather, reset and update step by step
+    against the oracle."""
+    rng = np.random.default_rng(3000 + seed)
+    N = int(rng.integers(1, 600_000))
+    world = int(rng.integers(1, 17))
+    steps = int(rng.integers(1, 4))
+    note(f"union fuzz seed {seed}: N={N} world={world} steps {steps}")
+    simulate_workers(N, world, steps, seed=3000 + seed, exact=bool(seed % 2))
+
+
 def test_union_path_loses_nothing():
     """With binary32-exact values (multiples of 1/8, n a power of two) the
     device path keeps Sec. 2's identity exactly: the workers' local errors
